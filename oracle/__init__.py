@@ -1,0 +1,283 @@
+"""Reference oracle for weight-cache hit detection.
+
+TEST INFRASTRUCTURE ONLY. This package is the plain, slow, obviously correct CPU
+definition of what the GPU library computes. Only the test suite, the package's
+smoke check and the benchmark's CPU-baseline leg may import it; the GPU library
+never does, and shares no code with it.
+
+The method (Gleam, Sec. 4.1.2 "Hash-based Weight Chunk Retrieval"): the server
+holds a set of hash identifiers of weight chunks it already has; each incoming
+host-to-device payload is hashed from its source bytes, and only payloads whose
+identifier is not in the set must send their bytes; a hit sends only the
+identifier and size, and the server restores the bytes locally. Sec. 4.1.1 and
+4.1.3 add that chunks later found to be weights are kept for reuse.
+
+The oracle computes, per fixed-size block of each payload:
+  geometry      -- blocks and leaves restart at every payload start
+  digests       -- XXH64 (seed 0) per 4 KiB leaf, bottom-up pairwise tree per
+                   block (gleam_oracle.c)
+  lookup        -- HIT_CACHE if the digest is in the table (value = the table's);
+                   else HIT_BATCH if an earlier block of the same batch has the
+                   same digest (ref = the earliest such block); else MISS
+  compaction    -- the ascending list of MISS blocks, their count and bytes
+  insert        -- set semantics; an existing key is never overwritten; among
+                   equal keys of one insert batch the lowest index's value wins
+
+The fingerprint is C (gleam_oracle.c) because the oracle must digest tens of GB;
+everything after it is numpy.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "gleam_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+MISS, HIT_CACHE, HIT_BATCH = 0, 1, 2
+LEAF_BYTES = 4096
+
+
+def build() -> str:
+    """Compile gleam_oracle.c into liboracle.so next to it (plain gcc, no SIMD flags)."""
+    tmp = _LIB_PATH + ".tmp"
+    subprocess.check_call(["gcc", "-O2", "-std=c99", "-Wall", "-Wextra", "-shared", "-fPIC",
+                           _SRC, "-o", tmp])
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    u64, u32, p = ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p
+    lib.oracle_xxh64.argtypes = [p, u64, u64]
+    lib.oracle_xxh64.restype = u64
+    lib.oracle_node.argtypes = [u64, u64]
+    lib.oracle_node.restype = u64
+    lib.oracle_tree.argtypes = [p, u64]
+    lib.oracle_tree.restype = u64
+    lib.oracle_blocks.argtypes = [p, u64, u32, u32, u64, u64, p, p]
+    lib.oracle_blocks.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _as_u8(data) -> np.ndarray:
+    if isinstance(data, (bytes, bytearray, memoryview)):
+        return np.frombuffer(bytes(data), dtype=np.uint8)
+    arr = np.ascontiguousarray(data)
+    if arr.dtype != np.uint8:
+        arr = arr.view(np.uint8).reshape(-1)
+    return arr.reshape(-1)
+
+
+# --------------------------------------------------------------------------- #
+# Fingerprints (C)
+# --------------------------------------------------------------------------- #
+def xxh64(data, seed: int = 0) -> int:
+    """XXH64 of `data` with `seed` (the xxHash specification's 64-bit algorithm)."""
+    arr = _as_u8(data)
+    return int(_load().oracle_xxh64(arr.ctypes.data if arr.size else None, arr.size, seed))
+
+
+def node(left: int, right: int) -> int:
+    """Tree node: XXH64(LE64(left) || LE64(right), seed 0)."""
+    return int(_load().oracle_node(left, right))
+
+
+def tree(digests) -> int:
+    """Bottom-up pairwise tree over >= 1 leaf digests; an odd last element moves up unchanged."""
+    work = np.array(digests, dtype=np.uint64)
+    if work.size == 0:
+        raise ValueError("a block has at least one leaf")
+    return int(_load().oracle_tree(work.ctypes.data, work.size))
+
+
+def num_blocks(length: int, block_bytes: int) -> int:
+    return (int(length) + block_bytes - 1) // block_bytes
+
+
+def payload_digests(payload, block_bytes: int, leaf_bytes: int = LEAF_BYTES,
+                    with_leaves: bool = False, first_block: int = 0, count: int | None = None):
+    """Block digests (and optionally padded leaf digests) of one payload.
+
+    Returns (block_digests u64[count], leaf_digests u64[count, block/leaf] or None).
+    """
+    arr = _as_u8(payload)
+    nblk = num_blocks(arr.size, block_bytes)
+    if count is None:
+        count = nblk - first_block
+    blk = np.zeros(count, dtype=np.uint64)
+    per = block_bytes // leaf_bytes
+    leaves = np.zeros((count, per), dtype=np.uint64) if with_leaves else None
+    if count:
+        rc = _load().oracle_blocks(arr.ctypes.data, arr.size, leaf_bytes, block_bytes, first_block, count,
+                                   blk.ctypes.data, leaves.ctypes.data if with_leaves else None)
+        if rc != 0:
+            raise ValueError(f"oracle_blocks failed with {rc}")
+    return blk, leaves
+
+
+def geometry(seg_lens, block_bytes: int):
+    """Per-batch geometry: blk_first[S+1] (exclusive prefix of blocks per payload)
+    and blk_len[n_blocks] (bytes of each block; only a payload's last block is short)."""
+    lens = np.asarray(seg_lens, dtype=np.uint64).reshape(-1)
+    nblk = [num_blocks(n, block_bytes) for n in lens.tolist()]
+    blk_first = np.zeros(len(nblk) + 1, dtype=np.uint64)
+    blk_first[1:] = np.cumsum(np.array(nblk, dtype=np.uint64))
+    blk_len = np.full(int(blk_first[-1]), block_bytes, dtype=np.uint64)
+    for s, n in enumerate(lens.tolist()):
+        if nblk[s]:
+            blk_len[int(blk_first[s + 1]) - 1] = n - (nblk[s] - 1) * block_bytes
+    return blk_first, blk_len
+
+
+def batch_digests(payloads, block_bytes: int, with_leaves: bool = False, threads: int = 1,
+                  blocks_per_task: int | None = None):
+    """Digests of every block of a batch, in batch order (payload-major, then offset).
+
+    `threads` > 1 hands independent block ranges to a thread pool; each range is
+    still one plain call of the oracle above.
+    """
+    lens = [int(_as_u8(p).size) for p in payloads]
+    blk_first, _ = geometry(lens, block_bytes)
+    n = int(blk_first[-1])
+    per = block_bytes // LEAF_BYTES
+    blk = np.zeros(n, dtype=np.uint64)
+    leaves = np.zeros((n, per), dtype=np.uint64) if with_leaves else None
+    if blocks_per_task is None:
+        blocks_per_task = max(1, (64 << 20) // block_bytes)
+    tasks = []
+    for s, p in enumerate(payloads):
+        nb = int(blk_first[s + 1] - blk_first[s])
+        for j0 in range(0, nb, blocks_per_task):
+            tasks.append((s, j0, min(blocks_per_task, nb - j0)))
+
+    def run(task):
+        s, j0, cnt = task
+        b, lv = payload_digests(payloads[s], block_bytes, with_leaves=with_leaves, first_block=j0, count=cnt)
+        g0 = int(blk_first[s]) + j0
+        blk[g0:g0 + cnt] = b
+        if with_leaves:
+            leaves[g0:g0 + cnt] = lv
+
+    if threads <= 1:
+        for t in tasks:
+            run(t)
+    else:
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            list(ex.map(run, tasks))
+    return blk, leaves
+
+
+# --------------------------------------------------------------------------- #
+# Table, lookup, compaction (numpy)
+# --------------------------------------------------------------------------- #
+class Table:
+    """The server's identifier set: a map from u64 digest to u64 value.
+
+    Every u64 is a valid key (no reserved value).
+    """
+
+    def __init__(self):
+        self.keys = np.zeros(0, dtype=np.uint64)   # sorted
+        self.vals = np.zeros(0, dtype=np.uint64)
+
+    def __len__(self):
+        return int(self.keys.size)
+
+    def insert(self, keys, vals) -> int:
+        """Insert in batch order: a key already present keeps its value; among equal
+        keys of this batch the lowest index wins. Returns the number of new keys."""
+        keys = np.asarray(keys, dtype=np.uint64).reshape(-1)
+        vals = np.asarray(vals, dtype=np.uint64).reshape(-1)
+        if keys.size != vals.size:
+            raise ValueError("keys and vals differ in length")
+        if keys.size == 0:
+            return 0
+        uniq, first = np.unique(keys, return_index=True)       # first = lowest index per key
+        new = ~self.contains(uniq)
+        add_k, add_v = uniq[new], vals[first[new]]
+        k = np.concatenate([self.keys, add_k])
+        v = np.concatenate([self.vals, add_v])
+        order = np.argsort(k, kind="stable")
+        self.keys, self.vals = k[order], v[order]
+        return int(add_k.size)
+
+    def contains(self, keys) -> np.ndarray:
+        keys = np.asarray(keys, dtype=np.uint64).reshape(-1)
+        if self.keys.size == 0:
+            return np.zeros(keys.size, dtype=bool)
+        pos = np.searchsorted(self.keys, keys)
+        pos_c = np.minimum(pos, self.keys.size - 1)
+        return (pos < self.keys.size) & (self.keys[pos_c] == keys)
+
+    def get(self, keys) -> tuple[np.ndarray, np.ndarray]:
+        """(present mask, value where present else 0)."""
+        keys = np.asarray(keys, dtype=np.uint64).reshape(-1)
+        present = self.contains(keys)
+        out = np.zeros(keys.size, dtype=np.uint64)
+        if present.any():
+            out[present] = self.vals[np.searchsorted(self.keys, keys[present])]
+        return present, out
+
+
+def lookup(digests, table: Table):
+    """status u8[n] and ref u64[n] for a batch of block digests.
+
+    HIT_CACHE (1): digest in the table; ref = its value.
+    HIT_BATCH (2): otherwise, an earlier block g0 < g has the same digest; ref = the
+                   smallest such g0 (itself a MISS).
+    MISS (0):      otherwise; ref = g.
+    The table is not modified.
+    """
+    d = np.asarray(digests, dtype=np.uint64).reshape(-1)
+    n = d.size
+    status = np.zeros(n, dtype=np.uint8)
+    ref = np.zeros(n, dtype=np.uint64)
+    if n == 0:
+        return status, ref
+    present, val = table.get(d)
+    _, first, inverse = np.unique(d, return_index=True, return_inverse=True)
+    g0 = first[inverse.reshape(-1)].astype(np.uint64)
+    g = np.arange(n, dtype=np.uint64)
+    status[present] = HIT_CACHE
+    ref[present] = val[present]
+    batch = ~present & (g0 < g)
+    status[batch] = HIT_BATCH
+    ref[batch] = g0[batch]
+    miss = ~present & (g0 == g)
+    ref[miss] = g[miss]
+    return status, ref
+
+
+def compact(status, blk_len=None):
+    """Ascending MISS block indices, their count, and (given blk_len) their total bytes."""
+    st = np.asarray(status, dtype=np.uint8).reshape(-1)
+    idx = np.flatnonzero(st == MISS).astype(np.uint64)
+    nbytes = None
+    if blk_len is not None:
+        nbytes = int(np.asarray(blk_len, dtype=np.uint64)[idx].sum(dtype=np.uint64))
+    return idx, int(idx.size), nbytes
+
+
+def run(payloads, block_bytes: int, table: Table, threads: int = 1):
+    """The whole path: digests -> lookup -> compaction for one batch."""
+    digests, _ = batch_digests(payloads, block_bytes, threads=threads)
+    _, blk_len = geometry([_as_u8(p).size for p in payloads], block_bytes)
+    status, ref = lookup(digests, table)
+    miss_idx, miss_count, miss_bytes = compact(status, blk_len)
+    return {"digests": digests, "status": status, "ref": ref, "miss_idx": miss_idx,
+            "miss_count": miss_count, "miss_bytes": miss_bytes}
