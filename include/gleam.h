@@ -1,0 +1,209 @@
+/*
+ * gleam.h -- GPU cache-hit detection for host-to-device weight payloads (gfx950).
+ *
+ * The operation (Gleam, Sec. 4.1.2 "Hash-based Weight Chunk Retrieval"): the
+ * server keeps the hash identifiers of the weight chunks it already holds; every
+ * host-to-device copy payload is hashed from its bytes, and only payloads whose
+ * identifier is not held must send their bytes over the network (a hit sends the
+ * identifier and size, and the server restores the bytes locally). Sec. 4.1.1
+ * defines the payload ("chunk") as the bytes of one host-to-device copy, and
+ * Sec. 4.1.3 keeps identified chunks for later reuse.
+ *
+ * This library decides it per fixed-size block of each payload, on the GPU:
+ *   gleam_fp_chunks     -- digest every block (XXH64 per 4 KiB leaf, seed 0,
+ *                          folded by a bottom-up pairwise tree)
+ *   gleam_cache_lookup  -- probe the resident identifier table; detect blocks
+ *                          repeated inside the batch
+ *   gleam_miss_compact  -- list the blocks whose bytes must still travel
+ *   gleam_cache_insert  -- add identifiers to the table
+ *
+ * Conventions for every entry point:
+ *   - C ABI; no exception crosses it; functions are thread-compatible (distinct
+ *     handles and buffers may be used from distinct threads).
+ *   - "device" pointers point to GPU memory (hipMalloc'd or a torch tensor);
+ *     "host" pointers to CPU memory. The CALLER owns all device memory:
+ *     payloads, descriptors, outputs, workspace and table storage. The library
+ *     allocates no device memory; it owns only the small host-side
+ *     gleam_cache handle.
+ *   - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued
+ *     asynchronously on it; outputs are valid once the stream has synchronised.
+ *     The library never synchronises.
+ *   - Arguments are validated on the host before anything is enqueued; on any
+ *     error a negative status is returned and nothing has been enqueued. A HIP
+ *     launch failure returns GLEAM_E_HIP; gleam_last_error() then holds the HIP
+ *     message (thread-local).
+ *   - Device descriptor contents (seg_addr, seg_len, blk_first) are not read on
+ *     the host. The caller guarantees they describe the batch; kernels never read
+ *     payload bytes outside [seg_addr[s], seg_addr[s] + seg_len[s]) whatever they
+ *     hold.
+ */
+#ifndef GLEAM_H
+#define GLEAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t gleam_status;
+enum {
+  GLEAM_OK = 0,
+  GLEAM_E_INVALID = -1,     /* a null required pointer, a bad size or alignment */
+  GLEAM_E_CAPACITY = -2,    /* an insert could push the table past its maximum load */
+  GLEAM_E_WORKSPACE = -3,   /* workspace smaller than gleam_workspace_bytes(n) */
+  GLEAM_E_HIP = -4,         /* a HIP call or kernel launch failed */
+  GLEAM_E_UNSUPPORTED = -5  /* valid, but beyond what this build handles */
+};
+
+/* Per-block status byte written by gleam_cache_lookup. */
+enum {
+  GLEAM_MISS = 0,       /* bytes must travel; ref = the block's own index */
+  GLEAM_HIT_CACHE = 1,  /* digest held by the table; ref = the table's value */
+  GLEAM_HIT_BATCH = 2   /* an earlier block of this batch has the same digest;
+                           ref = the earliest such block (which is a MISS) */
+};
+
+#define GLEAM_LEAF_BYTES 4096u
+#define GLEAM_MIN_BLOCK_BYTES 4096u
+#define GLEAM_MAX_BLOCK_BYTES (4096u << 12) /* 16 MiB */
+
+/*
+ * A batch of host-to-device payloads (Sec. 4.1.1: one payload = the bytes of one
+ * host-to-device copy). Each payload is cut, from its first byte, into 4 KiB
+ * leaves and blocks of block_bytes; a payload's last leaf and last block may be
+ * short. Global block index g = blk_first[s] + j for block j of payload s.
+ *   seg_addr  device u64[n_seg]    device address of payload s (any alignment)
+ *   seg_len   device u64[n_seg]    bytes of payload s (0 allowed)
+ *   blk_first device u64[n_seg+1]  exclusive prefix of ceil(seg_len[s]/block_bytes);
+ *                                  gleam_batch_geometry computes it
+ *   n_seg, n_blocks                host copies; n_blocks == blk_first[n_seg]
+ *   leaf_bytes                     must be GLEAM_LEAF_BYTES
+ *   block_bytes                    4096 << k for 0 <= k <= 12
+ */
+typedef struct {
+  const uint64_t* seg_addr;
+  const uint64_t* seg_len;
+  const uint64_t* blk_first;
+  uint64_t n_seg;
+  uint64_t n_blocks;
+  uint32_t leaf_bytes;
+  uint32_t block_bytes;
+} gleam_batch;
+
+/* Opaque host handle of a device-resident identifier table (the server's set of
+ * identifiers of resident chunks, Sec. 4.1.2). Table storage is caller-owned
+ * device memory that must outlive the handle. */
+typedef struct gleam_cache gleam_cache;
+
+/*
+ * Batch geometry (Sec. 4.1.1: decisions are made per payload, restarting at its
+ * first byte). host_seg_len: host u64[n_seg]; host_blk_first: host u64[n_seg+1]
+ * receives the exclusive prefix of ceil(len/block_bytes); *n_blocks (nullable)
+ * receives the total. Errors: GLEAM_E_INVALID for null arrays with n_seg > 0 or a
+ * bad block_bytes.
+ */
+gleam_status gleam_batch_geometry(const uint64_t* host_seg_len, uint64_t n_seg, uint32_t block_bytes,
+                                  uint64_t* host_blk_first, uint64_t* n_blocks);
+
+/*
+ * Digest every block of a batch (Sec. 4.1.2: the identifier is a hash of the
+ * source bytes). Leaf digest = XXH64(leaf bytes, seed 0) over the actual bytes
+ * (no padding); block digest = bottom-up pairwise tree over the block's leaf
+ * digests, node = XXH64(LE64(left) || LE64(right), seed 0), an odd last element
+ * moving up unchanged; a one-leaf block's digest is its leaf digest.
+ *   b               host pointer to the batch descriptor (device arrays inside)
+ *   d_block_digest  device u64[n_blocks] output
+ *   d_leaf_digest   nullable device u64[n_blocks * block_bytes/4096] output,
+ *                   block-major; slots past a short block's last leaf get 0
+ * Errors: GLEAM_E_INVALID (null b, null descriptor or output with n_blocks > 0,
+ * leaf_bytes != 4096, bad block_bytes, n_blocks > 0 with n_seg == 0),
+ * GLEAM_E_UNSUPPORTED (a grid beyond 2^31 workgroups), GLEAM_E_HIP.
+ * n_blocks == 0 is a no-op.
+ */
+gleam_status gleam_fp_chunks(const gleam_batch* b, uint64_t* d_block_digest, uint64_t* d_leaf_digest,
+                             void* stream);
+
+/* Device bytes of table storage for `capacity` slots (a power of two >= 16);
+ * 0 for an invalid capacity. */
+size_t gleam_cache_bytes(uint64_t capacity);
+
+/*
+ * Create a handle over caller-owned storage and enqueue the table clear.
+ *   d_storage  device memory, 256-byte aligned, >= gleam_cache_bytes(capacity)
+ *   capacity   power of two >= 16
+ *   max_load   in (0, 1): inserts are refused once the number of keys could
+ *              exceed floor(max_load * capacity) (at most capacity - 1)
+ *   out        receives the handle (host memory, freed by gleam_cache_destroy)
+ * Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
+ */
+gleam_status gleam_cache_create(void* d_storage, size_t bytes, uint64_t capacity, double max_load,
+                                gleam_cache** out, void* stream);
+
+/* Free the host handle; the storage is not touched. NULL is allowed. */
+gleam_status gleam_cache_destroy(gleam_cache* c);
+
+/* Host-side upper bound on the keys the table may hold (exact unless inserts
+ * carried keys already present). UINT64_MAX for a NULL handle. */
+uint64_t gleam_cache_key_bound(const gleam_cache* c);
+
+/* Device workspace bytes needed by lookup, insert and compaction of n items. */
+size_t gleam_workspace_bytes(uint64_t n);
+
+/*
+ * Insert identifiers (Sec. 4.1.2 and 4.1.3: a chunk identified as a weight is kept
+ * and its identifier reused by later connections). Set semantics: a key already
+ * present keeps its value; among equal keys of this call the lowest index's value
+ * is stored. Every u64 is a valid key.
+ *   d_keys, d_vals  device u64[n]
+ *   d_n_new         nullable device u64[1]: number of keys that were new
+ *   d_ws, ws_bytes  device workspace, 256-byte aligned, >= gleam_workspace_bytes(n)
+ * Capacity is enforced on the host without a device sync: if key_bound + n could
+ * exceed the maximum load, GLEAM_E_CAPACITY is returned and nothing is inserted.
+ * Errors: GLEAM_E_INVALID, GLEAM_E_CAPACITY, GLEAM_E_WORKSPACE, GLEAM_E_HIP.
+ */
+gleam_status gleam_cache_insert(gleam_cache* c, const uint64_t* d_keys, const uint64_t* d_vals, uint64_t n,
+                                uint64_t* d_n_new, void* d_ws, size_t ws_bytes, void* stream);
+
+/*
+ * Decide each block's fate (Sec. 4.1.2: identifier held -> only metadata travels).
+ *   d_keys    device u64[n] block digests in batch order
+ *   d_status  device u8[n] output: GLEAM_MISS / GLEAM_HIT_CACHE / GLEAM_HIT_BATCH
+ *   d_ref     nullable device u64[n] output (see the status enum)
+ *   d_ws      device workspace, 256-byte aligned, >= gleam_workspace_bytes(n)
+ * The table is only read.
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_HIP. n == 0 is a no-op.
+ */
+gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t* d_keys, uint64_t n, uint8_t* d_status,
+                                uint64_t* d_ref, void* d_ws, size_t ws_bytes, void* stream);
+
+/*
+ * The blocks whose bytes must still cross the network (Sec. 4.1.2: on a miss the
+ * full chunk is sent).
+ *   d_status      device u8[n] (as written by gleam_cache_lookup)
+ *   b             nullable host pointer to the batch the statuses belong to;
+ *                 needed only for d_miss_bytes (b->n_blocks must equal n)
+ *   d_miss_idx    device u64[n] output: ascending indices g with status MISS,
+ *                 in its first *d_miss_count entries
+ *   d_miss_count  device u64[1] output
+ *   d_miss_bytes  nullable device u64[1] output: total bytes of those blocks
+ *   d_ws          device workspace, 256-byte aligned, >= gleam_workspace_bytes(n)
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_HIP. With n == 0 the
+ * counters are still set to 0.
+ */
+gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam_batch* b, uint64_t* d_miss_idx,
+                                uint64_t* d_miss_count, uint64_t* d_miss_bytes, void* d_ws, size_t ws_bytes,
+                                void* stream);
+
+/* Static text for a status code. */
+const char* gleam_status_string(gleam_status s);
+
+/* Thread-local detail of the last error on this thread ("" if none). */
+const char* gleam_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GLEAM_H */

@@ -1,0 +1,260 @@
+"""Python binding of libgleam: GPU cache-hit detection for host-to-device weight payloads.
+
+Argument marshalling only: every step of the path runs in the library's gfx950
+kernels (include/gleam.h documents each call). PyTorch supplies device memory
+(tensors) and streams. Importing this module fails loudly if libgleam.so has not
+been built (python -m paper_2607_23115_amd.build).
+
+    batch = Batch.from_tensors([t0, t1, ...], block_bytes=1 << 20)
+    digests = fp_chunks(batch)
+    table = Cache(capacity=1 << 15)
+    status, ref = table.lookup(digests)
+    miss_idx, miss_count, miss_bytes = miss_compact(status, batch)
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libgleam.so")
+
+OK, E_INVALID, E_CAPACITY, E_WORKSPACE, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+MISS, HIT_CACHE, HIT_BATCH = 0, 1, 2
+LEAF_BYTES = 4096
+
+EXPORTS = (
+    "gleam_batch_geometry", "gleam_fp_chunks", "gleam_cache_bytes", "gleam_cache_create", "gleam_cache_destroy",
+    "gleam_cache_key_bound", "gleam_workspace_bytes", "gleam_cache_insert", "gleam_cache_lookup",
+    "gleam_miss_compact", "gleam_status_string", "gleam_last_error",
+)
+
+
+class GleamError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+class _Batch(ctypes.Structure):
+    _fields_ = [("seg_addr", ctypes.c_void_p), ("seg_len", ctypes.c_void_p), ("blk_first", ctypes.c_void_p),
+                ("n_seg", ctypes.c_uint64), ("n_blocks", ctypes.c_uint64), ("leaf_bytes", ctypes.c_uint32),
+                ("block_bytes", ctypes.c_uint32)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libgleam.so is not built at {LIB_PATH}; run python -m paper_2607_23115_amd.build")
+    lib = ctypes.CDLL(LIB_PATH)
+    u64, u32, vp, st = ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_int32
+    sz = ctypes.c_size_t
+    sigs = {
+        "gleam_batch_geometry": ([vp, u64, u32, vp, vp], st),
+        "gleam_fp_chunks": ([ctypes.POINTER(_Batch), vp, vp, vp], st),
+        "gleam_cache_bytes": ([u64], sz),
+        "gleam_cache_create": ([vp, sz, u64, ctypes.c_double, ctypes.POINTER(vp), vp], st),
+        "gleam_cache_destroy": ([vp], st),
+        "gleam_cache_key_bound": ([vp], u64),
+        "gleam_workspace_bytes": ([u64], sz),
+        "gleam_cache_insert": ([vp, vp, vp, u64, vp, vp, sz, vp], st),
+        "gleam_cache_lookup": ([vp, vp, u64, vp, vp, vp, sz, vp], st),
+        "gleam_miss_compact": ([vp, u64, ctypes.POINTER(_Batch), vp, vp, vp, vp, sz, vp], st),
+        "gleam_status_string": ([st], ctypes.c_char_p),
+        "gleam_last_error": ([], ctypes.c_char_p),
+    }
+    for name, (args, res) in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+lib = _load()
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        detail = lib.gleam_last_error().decode() or lib.gleam_status_string(status).decode()
+        raise GleamError(status, detail)
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _u64_device(a: np.ndarray, device) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint64).view(np.int64)).to(device)
+
+
+def workspace_bytes(n: int) -> int:
+    return int(lib.gleam_workspace_bytes(n))
+
+
+def workspace(n: int, device="cuda") -> torch.Tensor:
+    """Device workspace for lookup / insert / compaction of n items."""
+    return torch.empty(max(workspace_bytes(n), 256), dtype=torch.uint8, device=device)
+
+
+def geometry(seg_len, block_bytes: int) -> np.ndarray:
+    """blk_first[S+1] for the given payload lengths (the library's host geometry)."""
+    lens = np.ascontiguousarray(seg_len, dtype=np.uint64).reshape(-1)
+    first = np.zeros(lens.size + 1, dtype=np.uint64)
+    _check(lib.gleam_batch_geometry(lens.ctypes.data if lens.size else None, lens.size, block_bytes,
+                                    first.ctypes.data, None))
+    return first
+
+
+class Batch:
+    """A batch of payloads in device memory: addresses, lengths and block geometry."""
+
+    def __init__(self, seg_addr, seg_len, block_bytes: int, device="cuda", keepalive=None):
+        addr = np.ascontiguousarray(seg_addr, dtype=np.uint64).reshape(-1)
+        lens = np.ascontiguousarray(seg_len, dtype=np.uint64).reshape(-1)
+        if addr.size != lens.size:
+            raise ValueError("seg_addr and seg_len differ in length")
+        self.block_bytes = int(block_bytes)
+        self.host_len = lens
+        self.host_first = geometry(lens, block_bytes)
+        self.n_seg = int(lens.size)
+        self.n_blocks = int(self.host_first[-1])
+        self.d_addr = _u64_device(addr if addr.size else np.zeros(1, np.uint64), device)
+        self.d_len = _u64_device(lens if lens.size else np.zeros(1, np.uint64), device)
+        self.d_first = _u64_device(self.host_first, device)
+        self.keepalive = keepalive
+        self._c = _Batch(self.d_addr.data_ptr(), self.d_len.data_ptr(), self.d_first.data_ptr(), self.n_seg,
+                         self.n_blocks, LEAF_BYTES, self.block_bytes)
+
+    @classmethod
+    def from_arena(cls, arena: torch.Tensor, offsets, lengths, block_bytes: int) -> "Batch":
+        """Payloads at byte offsets of one device u8 tensor."""
+        base = arena.data_ptr()
+        offs = np.asarray(offsets, dtype=np.uint64)
+        return cls(offs + np.uint64(base), lengths, block_bytes, arena.device, keepalive=arena)
+
+    @classmethod
+    def from_tensors(cls, tensors, block_bytes: int) -> "Batch":
+        """One payload per device tensor (its whole storage extent as bytes)."""
+        addr = [t.data_ptr() for t in tensors]
+        lens = [t.numel() * t.element_size() for t in tensors]
+        dev = tensors[0].device if tensors else "cuda"
+        return cls(addr, lens, block_bytes, dev, keepalive=list(tensors))
+
+    @property
+    def leaves_per_block(self) -> int:
+        return self.block_bytes // LEAF_BYTES
+
+    def c_struct(self) -> _Batch:
+        return self._c
+
+
+def fp_chunks(batch: Batch, out: torch.Tensor | None = None, leaf_out: torch.Tensor | None = None,
+              with_leaves: bool = False, stream=None):
+    """Block digests (u64 as int64 tensor); optionally padded leaf digests."""
+    dev = batch.d_first.device
+    if out is None:
+        out = torch.empty(max(batch.n_blocks, 1), dtype=torch.int64, device=dev)
+    if with_leaves and leaf_out is None:
+        leaf_out = torch.empty(max(batch.n_blocks * batch.leaves_per_block, 1), dtype=torch.int64, device=dev)
+    _check(lib.gleam_fp_chunks(ctypes.byref(batch.c_struct()), _ptr(out), _ptr(leaf_out), _stream(stream)))
+    if with_leaves:
+        return out[:batch.n_blocks], leaf_out[:batch.n_blocks * batch.leaves_per_block]
+    return out[:batch.n_blocks]
+
+
+class Cache:
+    """A device-resident identifier table over a torch-allocated storage tensor."""
+
+    def __init__(self, capacity: int, max_load: float = 0.7, device="cuda", stream=None):
+        nbytes = int(lib.gleam_cache_bytes(capacity))
+        if nbytes == 0:
+            raise GleamError(E_INVALID, f"invalid capacity {capacity}")
+        self.capacity = capacity
+        self.storage = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        h = ctypes.c_void_p()
+        _check(lib.gleam_cache_create(_ptr(self.storage), nbytes, capacity, max_load, ctypes.byref(h),
+                                      _stream(stream)))
+        self._h = h
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        if self._h is None:
+            raise GleamError(E_INVALID, "table handle already destroyed")
+        return self._h
+
+    def key_bound(self) -> int:
+        return int(lib.gleam_cache_key_bound(self.handle))
+
+    def insert(self, keys: torch.Tensor, vals: torch.Tensor, ws: torch.Tensor | None = None,
+               n_new: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        n = keys.numel()
+        if vals.numel() != n:
+            raise ValueError("keys and vals differ in length")
+        if ws is None:
+            ws = workspace(n, keys.device)
+        if n_new is None:
+            n_new = torch.empty(1, dtype=torch.int64, device=keys.device)
+        _check(lib.gleam_cache_insert(self.handle, _ptr(keys), _ptr(vals), n, _ptr(n_new), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+        return n_new
+
+    def lookup(self, keys: torch.Tensor, status: torch.Tensor | None = None, ref: torch.Tensor | None = None,
+               ws: torch.Tensor | None = None, want_ref: bool = True, stream=None):
+        n = keys.numel()
+        if status is None:
+            status = torch.empty(max(n, 1), dtype=torch.uint8, device=keys.device)
+        if ref is None and want_ref:
+            ref = torch.empty(max(n, 1), dtype=torch.int64, device=keys.device)
+        if ws is None:
+            ws = workspace(n, keys.device)
+        _check(lib.gleam_cache_lookup(self.handle, _ptr(keys), n, _ptr(status), _ptr(ref), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+        return status[:n], (ref[:n] if ref is not None else None)
+
+    def close(self) -> None:
+        if self._h is not None:
+            lib.gleam_cache_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def miss_compact(status: torch.Tensor, batch: Batch | None = None, miss_idx: torch.Tensor | None = None,
+                 counters: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None):
+    """(miss_idx[n] int64, counters[2] int64 = [miss_count, miss_bytes]) on the device.
+
+    The first counters[0] entries of miss_idx are valid; counters[1] is filled when
+    `batch` is given."""
+    n = status.numel()
+    dev = status.device
+    if miss_idx is None:
+        miss_idx = torch.empty(max(n, 1), dtype=torch.int64, device=dev)
+    if counters is None:
+        counters = torch.zeros(2, dtype=torch.int64, device=dev)
+    if ws is None:
+        ws = workspace(n, dev)
+    cb = ctypes.byref(batch.c_struct()) if batch is not None else None
+    bytes_ptr = ctypes.c_void_p(counters.data_ptr() + 8) if batch is not None else None
+    _check(lib.gleam_miss_compact(_ptr(status), n, cb, _ptr(miss_idx), _ptr(counters), bytes_ptr, _ptr(ws),
+                                  ws.numel(), _stream(stream)))
+    return miss_idx, counters
+
+
+def as_u64(t: torch.Tensor) -> np.ndarray:
+    """Device int64 tensor -> host uint64 array (same bits)."""
+    return t.detach().cpu().numpy().view(np.uint64)

@@ -1,0 +1,97 @@
+// Host-side parts of the libgleam C ABI: status text, error detail, batch geometry
+// and workspace sizing.
+
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "gleam_internal.h"
+
+namespace gleam {
+namespace {
+thread_local char g_last_error[512] = "";
+}
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+}
+
+void clear_error() { g_last_error[0] = '\0'; }
+
+gleam_status launch_status(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e == hipSuccess) return GLEAM_OK;
+  set_error("%s: %s", what, hipGetErrorString(e));
+  return GLEAM_E_HIP;
+}
+
+int log2_exact(uint64_t x) {
+  if (x == 0 || (x & (x - 1)) != 0) return -1;
+  int r = 0;
+  while ((1ull << r) != x) ++r;
+  return r;
+}
+
+bool valid_block_bytes(uint32_t block_bytes) {
+  const int l = log2_exact(block_bytes);
+  return l >= 12 && l <= 24;
+}
+
+bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255) == 0; }
+
+WsLayout ws_layout(uint64_t n) {
+  WsLayout L;
+  uint64_t cap = 64;
+  while (cap < 2 * n) cap <<= 1;
+  L.scratch_cap = cap;
+  L.scratch_off = kHeaderBytes;
+  L.tiles = (n + kTileItems - 1) / kTileItems;
+  L.tiles_off = L.scratch_off + (size_t)cap * 16;
+  L.total = L.tiles_off + (size_t)(L.tiles + 1) * 16;
+  L.total = (L.total + 255) & ~(size_t)255;
+  return L;
+}
+
+}  // namespace gleam
+
+extern "C" const char* gleam_status_string(gleam_status s) {
+  switch (s) {
+    case GLEAM_OK: return "ok";
+    case GLEAM_E_INVALID: return "invalid argument";
+    case GLEAM_E_CAPACITY: return "table capacity exceeded";
+    case GLEAM_E_WORKSPACE: return "workspace too small";
+    case GLEAM_E_HIP: return "HIP error";
+    case GLEAM_E_UNSUPPORTED: return "unsupported";
+    default: return "unknown status";
+  }
+}
+
+extern "C" const char* gleam_last_error(void) { return gleam::g_last_error; }
+
+extern "C" size_t gleam_workspace_bytes(uint64_t n) {
+  if (n > (1ull << 40)) return 0;
+  return gleam::ws_layout(n).total;
+}
+
+extern "C" gleam_status gleam_batch_geometry(const uint64_t* host_seg_len, uint64_t n_seg, uint32_t block_bytes,
+                                             uint64_t* host_blk_first, uint64_t* n_blocks) {
+  gleam::clear_error();
+  if (!gleam::valid_block_bytes(block_bytes)) {
+    gleam::set_error("gleam_batch_geometry: block_bytes must be 4096 << k, k <= 12");
+    return GLEAM_E_INVALID;
+  }
+  if (!host_blk_first || (n_seg > 0 && !host_seg_len)) {
+    gleam::set_error("gleam_batch_geometry: null array");
+    return GLEAM_E_INVALID;
+  }
+  uint64_t total = 0;
+  for (uint64_t s = 0; s < n_seg; ++s) {
+    host_blk_first[s] = total;
+    total += host_seg_len[s] / block_bytes + (host_seg_len[s] % block_bytes != 0);
+  }
+  host_blk_first[n_seg] = total;
+  if (n_blocks) *n_blocks = total;
+  return GLEAM_OK;
+}

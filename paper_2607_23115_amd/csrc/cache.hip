@@ -1,0 +1,330 @@
+// The resident identifier table: create, insert, lookup (Gleam Sec. 4.1.2: the
+// server's set of identifiers of chunks it holds; a held identifier means only
+// metadata travels. Sec. 4.1.3: identified weight chunks are kept for reuse).
+//
+// Layout: open addressing with linear probing over `capacity` 16-byte slots
+// (key u64, value u64), after a 256-byte header. The empty marker is kEmpty; a key
+// equal to kEmpty is kept in the header (flag + value), so every u64 is a key.
+// The table is never fuller than max_load (enforced on the host), so every probe
+// meets an empty slot; probe loops are still bounded by the capacity.
+//
+// Determinism: results never depend on thread timing. Duplicates inside one call
+// are resolved through a workspace scratch table that keeps, per key, the lowest
+// index (atomicMin); only that index inserts (insert) or is the MISS (lookup).
+
+#include <new>
+
+#include "gleam_device.h"
+#include "gleam_internal.h"
+
+namespace gleam {
+namespace {
+
+constexpr int kThreads = 256;
+
+struct TableRef {
+  uint64_t* hdr;    // [0] flag: key kEmpty present, [1] its value
+  uint64_t* slots;  // capacity x {key, value}
+  uint64_t mask;
+  int shift;
+};
+
+struct ScratchRef {
+  uint64_t* hdr;    // [0] min index of key kEmpty, [1] new-key counter
+  uint64_t* slots;  // cap x {key, min index}
+  uint64_t mask;
+  int shift;
+};
+
+__device__ __forceinline__ unsigned long long* ull(uint64_t* p) { return reinterpret_cast<unsigned long long*>(p); }
+
+__global__ void fill_kernel(uint64_t* p, uint64_t n, uint64_t value) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = value;
+}
+
+// Scratch: record index i for key k, keeping the minimum index per key.
+__device__ void scratch_mark(const ScratchRef& sc, uint64_t k, uint64_t i) {
+  if (k == kEmpty) {
+    atomicMin(ull(&sc.hdr[0]), (unsigned long long)i);
+    return;
+  }
+  uint64_t pos = slot_hash(k, sc.shift);
+  for (uint64_t probe = 0; probe <= sc.mask; ++probe) {
+    uint64_t* slot = sc.slots + 2 * pos;
+    const uint64_t prev = atomicCAS(ull(slot), (unsigned long long)kEmpty, (unsigned long long)k);
+    if (prev == kEmpty || prev == k) {
+      atomicMin(ull(slot + 1), (unsigned long long)i);
+      return;
+    }
+    pos = (pos + 1) & sc.mask;
+  }
+}
+
+// Scratch: the minimum index recorded for key k (k was marked earlier).
+__device__ uint64_t scratch_min(const ScratchRef& sc, uint64_t k) {
+  if (k == kEmpty) return sc.hdr[0];
+  uint64_t pos = slot_hash(k, sc.shift);
+  for (uint64_t probe = 0; probe <= sc.mask; ++probe) {
+    const uint64_t* slot = sc.slots + 2 * pos;
+    if (slot[0] == k) return slot[1];
+    pos = (pos + 1) & sc.mask;
+  }
+  return ~0ull;
+}
+
+__global__ void insert_mark_kernel(ScratchRef sc, const uint64_t* keys, uint64_t n) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) scratch_mark(sc, keys[i], i);
+}
+
+__global__ void insert_commit_kernel(TableRef t, ScratchRef sc, const uint64_t* keys, const uint64_t* vals,
+                                     uint64_t n, uint64_t* n_new) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const uint64_t k = keys[i];
+  if (scratch_min(sc, k) != i) return;  // a lower index carries this key
+  if (k == kEmpty) {
+    if (atomicCAS(ull(&t.hdr[0]), 0ull, 1ull) == 0ull) {
+      t.hdr[1] = vals[i];
+      atomicAdd(ull(n_new), 1ull);
+    }
+    return;
+  }
+  uint64_t pos = slot_hash(k, t.shift);
+  for (uint64_t probe = 0; probe <= t.mask; ++probe) {
+    uint64_t* slot = t.slots + 2 * pos;
+    const uint64_t prev = atomicCAS(ull(slot), (unsigned long long)kEmpty, (unsigned long long)k);
+    if (prev == kEmpty) {
+      slot[1] = vals[i];
+      atomicAdd(ull(n_new), 1ull);
+      return;
+    }
+    if (prev == k) return;  // already held: keep the existing value
+    pos = (pos + 1) & t.mask;
+  }
+}
+
+// Lookup pass 1: table probe. Hits are final; the rest are marked in the scratch
+// table and flagged 0xFF for pass 2.
+__global__ void lookup_probe_kernel(TableRef t, ScratchRef sc, const uint64_t* keys, uint64_t n, uint8_t* status,
+                                    uint64_t* ref) {
+  const uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= n) return;
+  const uint64_t k = keys[g];
+  bool hit = false;
+  uint64_t val = 0;
+  if (k == kEmpty) {
+    hit = t.hdr[0] != 0;
+    val = t.hdr[1];
+  } else {
+    uint64_t pos = slot_hash(k, t.shift);
+    for (uint64_t probe = 0; probe <= t.mask; ++probe) {
+      const uint4 e = *reinterpret_cast<const uint4*>(t.slots + 2 * pos);
+      const uint64_t key = lo64(e);
+      if (key == k) {
+        hit = true;
+        val = hi64(e);
+        break;
+      }
+      if (key == kEmpty) break;
+      pos = (pos + 1) & t.mask;
+    }
+  }
+  if (hit) {
+    status[g] = GLEAM_HIT_CACHE;
+    if (ref) ref[g] = val;
+  } else {
+    status[g] = 0xFF;
+    scratch_mark(sc, k, g);
+  }
+}
+
+// Lookup pass 2: the earliest block with a digest is the MISS, later ones HIT_BATCH.
+__global__ void lookup_resolve_kernel(ScratchRef sc, const uint64_t* keys, uint64_t n, uint8_t* status,
+                                      uint64_t* ref) {
+  const uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= n || status[g] != 0xFF) return;
+  const uint64_t g0 = scratch_min(sc, keys[g]);
+  status[g] = g0 == g ? GLEAM_MISS : GLEAM_HIT_BATCH;
+  if (ref) ref[g] = g0;
+}
+
+TableRef table_ref(const gleam_cache* c) {
+  TableRef t;
+  t.hdr = reinterpret_cast<uint64_t*>(c->storage);
+  t.slots = reinterpret_cast<uint64_t*>(c->storage + kHeaderBytes);
+  t.mask = c->capacity - 1;
+  t.shift = c->shift;
+  return t;
+}
+
+ScratchRef scratch_ref(void* ws, const WsLayout& L) {
+  ScratchRef s;
+  s.hdr = reinterpret_cast<uint64_t*>(ws);
+  s.slots = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + L.scratch_off);
+  s.mask = L.scratch_cap - 1;
+  s.shift = 64 - log2_exact(L.scratch_cap);
+  return s;
+}
+
+// Reset the scratch header and slots: keys to kEmpty, min-indices to all-ones.
+gleam_status clear_scratch(void* ws, const WsLayout& L, hipStream_t stream) {
+  gleam_status st = fill_u64(reinterpret_cast<uint64_t*>(ws), 1, ~0ull, stream);
+  if (st == GLEAM_OK) st = fill_u64(reinterpret_cast<uint64_t*>(ws) + 1, 3, 0, stream);
+  if (st == GLEAM_OK)
+    st = fill_u64(reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + L.scratch_off), 2 * L.scratch_cap, ~0ull,
+                  stream);
+  return st;
+}
+
+uint32_t blocks_for(uint64_t n) { return (uint32_t)((n + kThreads - 1) / kThreads); }
+
+}  // namespace
+
+gleam_status fill_u64(uint64_t* p, uint64_t n, uint64_t value, hipStream_t stream) {
+  if (n == 0) return GLEAM_OK;
+  const uint64_t want = (n + kThreads - 1) / kThreads;
+  const uint32_t grid = (uint32_t)(want < 4096 ? want : 4096);
+  hipLaunchKernelGGL(fill_kernel, dim3(grid), dim3(kThreads), 0, stream, p, n, value);
+  return launch_status("fill_kernel");
+}
+
+}  // namespace gleam
+
+extern "C" size_t gleam_cache_bytes(uint64_t capacity) {
+  if (capacity < 16 || gleam::log2_exact(capacity) < 0 || capacity > (1ull << 40)) return 0;
+  return gleam::kHeaderBytes + (size_t)capacity * 16;
+}
+
+extern "C" gleam_status gleam_cache_create(void* d_storage, size_t bytes, uint64_t capacity, double max_load,
+                                           gleam_cache** out, void* stream) {
+  using namespace gleam;
+  clear_error();
+  if (!out) {
+    set_error("gleam_cache_create: null output handle");
+    return GLEAM_E_INVALID;
+  }
+  *out = nullptr;
+  const size_t need = gleam_cache_bytes(capacity);
+  if (need == 0) {
+    set_error("gleam_cache_create: capacity must be a power of two in [16, 2^40]");
+    return GLEAM_E_INVALID;
+  }
+  if (!d_storage || !aligned256(d_storage) || bytes < need) {
+    set_error("gleam_cache_create: storage must be non-null, 256-byte aligned and >= %zu bytes", need);
+    return GLEAM_E_INVALID;
+  }
+  if (!(max_load > 0.0 && max_load < 1.0)) {
+    set_error("gleam_cache_create: max_load must lie in (0, 1)");
+    return GLEAM_E_INVALID;
+  }
+  uint64_t max_keys = (uint64_t)(max_load * (double)capacity);
+  if (max_keys > capacity - 1) max_keys = capacity - 1;
+  gleam_cache* c = new (std::nothrow) gleam_cache;
+  if (!c) {
+    set_error("gleam_cache_create: out of host memory");
+    return GLEAM_E_INVALID;
+  }
+  c->storage = static_cast<uint8_t*>(d_storage);
+  c->capacity = capacity;
+  c->shift = 64 - log2_exact(capacity);
+  c->max_keys = max_keys;
+  c->key_bound = 0;
+  hipStream_t s = (hipStream_t)stream;
+  gleam_status st = fill_u64(reinterpret_cast<uint64_t*>(c->storage), kHeaderBytes / 8, 0, s);
+  if (st == GLEAM_OK)
+    st = fill_u64(reinterpret_cast<uint64_t*>(c->storage + kHeaderBytes), 2 * capacity, kEmpty, s);
+  if (st != GLEAM_OK) {
+    delete c;
+    return st;
+  }
+  *out = c;
+  return GLEAM_OK;
+}
+
+extern "C" gleam_status gleam_cache_destroy(gleam_cache* c) {
+  delete c;
+  return GLEAM_OK;
+}
+
+extern "C" uint64_t gleam_cache_key_bound(const gleam_cache* c) { return c ? c->key_bound : UINT64_MAX; }
+
+extern "C" gleam_status gleam_cache_insert(gleam_cache* c, const uint64_t* d_keys, const uint64_t* d_vals, uint64_t n,
+                                           uint64_t* d_n_new, void* d_ws, size_t ws_bytes, void* stream) {
+  using namespace gleam;
+  clear_error();
+  if (!c) {
+    set_error("gleam_cache_insert: null table");
+    return GLEAM_E_INVALID;
+  }
+  if (n > 0 && (!d_keys || !d_vals)) {
+    set_error("gleam_cache_insert: null keys or values");
+    return GLEAM_E_INVALID;
+  }
+  const WsLayout L = ws_layout(n);
+  if (!d_ws || !aligned256(d_ws)) {
+    set_error("gleam_cache_insert: workspace must be non-null and 256-byte aligned");
+    return GLEAM_E_INVALID;
+  }
+  if (ws_bytes < L.total) {
+    set_error("gleam_cache_insert: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
+    return GLEAM_E_WORKSPACE;
+  }
+  if (n > c->max_keys || c->key_bound > c->max_keys - n) {
+    set_error("gleam_cache_insert: %llu more keys could exceed the maximum load (%llu keys, bound %llu)",
+              (unsigned long long)n, (unsigned long long)c->max_keys, (unsigned long long)c->key_bound);
+    return GLEAM_E_CAPACITY;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  gleam_status st = clear_scratch(d_ws, L, s);
+  uint64_t* counter = d_n_new ? d_n_new : reinterpret_cast<uint64_t*>(d_ws) + 1;
+  if (st == GLEAM_OK && d_n_new) st = fill_u64(d_n_new, 1, 0, s);
+  if (st != GLEAM_OK) return st;
+  if (n == 0) return GLEAM_OK;
+  const ScratchRef sc = scratch_ref(d_ws, L);
+  const TableRef t = table_ref(c);
+  hipLaunchKernelGGL(insert_mark_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s, sc, d_keys, n);
+  if ((st = launch_status("insert_mark_kernel")) != GLEAM_OK) return st;
+  hipLaunchKernelGGL(insert_commit_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s, t, sc, d_keys, d_vals, n,
+                     counter);
+  if ((st = launch_status("insert_commit_kernel")) != GLEAM_OK) return st;
+  c->key_bound += n;
+  return GLEAM_OK;
+}
+
+extern "C" gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t* d_keys, uint64_t n,
+                                           uint8_t* d_status, uint64_t* d_ref, void* d_ws, size_t ws_bytes,
+                                           void* stream) {
+  using namespace gleam;
+  clear_error();
+  if (!c) {
+    set_error("gleam_cache_lookup: null table");
+    return GLEAM_E_INVALID;
+  }
+  if (n == 0) return GLEAM_OK;
+  if (!d_keys || !d_status) {
+    set_error("gleam_cache_lookup: null keys or status");
+    return GLEAM_E_INVALID;
+  }
+  const WsLayout L = ws_layout(n);
+  if (!d_ws || !aligned256(d_ws)) {
+    set_error("gleam_cache_lookup: workspace must be non-null and 256-byte aligned");
+    return GLEAM_E_INVALID;
+  }
+  if (ws_bytes < L.total) {
+    set_error("gleam_cache_lookup: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
+    return GLEAM_E_WORKSPACE;
+  }
+  if (n > 0xFFFFFFFFull * kThreads) return GLEAM_E_UNSUPPORTED;
+  hipStream_t s = (hipStream_t)stream;
+  gleam_status st = clear_scratch(d_ws, L, s);
+  if (st != GLEAM_OK) return st;
+  const ScratchRef sc = scratch_ref(d_ws, L);
+  const TableRef t = table_ref(c);
+  hipLaunchKernelGGL(lookup_probe_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s, t, sc, d_keys, n, d_status, d_ref);
+  if ((st = launch_status("lookup_probe_kernel")) != GLEAM_OK) return st;
+  hipLaunchKernelGGL(lookup_resolve_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s, sc, d_keys, n, d_status,
+                     d_ref);
+  return launch_status("lookup_resolve_kernel");
+}

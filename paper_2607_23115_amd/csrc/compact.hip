@@ -1,0 +1,176 @@
+// gleam_miss_compact: the blocks whose bytes must still travel (Gleam Sec. 4.1.2:
+// on a miss the full chunk is transmitted), as an ascending index list, its length
+// and its byte total.
+//
+// Order-preserving stream compaction in three passes over tiles of 2048 statuses:
+// count per tile (wave ballots), one-workgroup exclusive scan of the tile counts,
+// then each tile writes its MISS indices at its offset using a workgroup scan of
+// per-thread counts. Byte total = count * block_bytes minus, for every payload
+// whose short last block is a MISS, the part of that block that does not exist.
+// All sums are integer, so the results do not depend on thread timing.
+
+#include "gleam_device.h"
+#include "gleam_internal.h"
+
+namespace gleam {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kPerThread = (int)(kTileItems / kThreads);  // 8 statuses per thread
+constexpr int kScanThreads = 1024;
+
+__device__ __forceinline__ uint32_t count_misses(const uint8_t* status, uint64_t n, uint64_t first) {
+  uint32_t c = 0;
+#pragma unroll
+  for (int e = 0; e < kPerThread; ++e) {
+    const uint64_t g = first + e;
+    c += (g < n && status[g] == GLEAM_MISS) ? 1u : 0u;
+  }
+  return c;
+}
+
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x, int lane) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  return x;
+}
+
+// Exclusive scan of one value per thread over a workgroup of `waves` waves.
+// Returns the exclusive prefix; *total receives the workgroup sum.
+template <int kWaves>
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* wave_sums, uint32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t incl = wave_inclusive_scan(x, lane);
+  if (lane == 63) wave_sums[wave] = incl;
+  __syncthreads();
+  uint32_t before = 0, sum = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const uint32_t s = wave_sums[w];
+    before += w < wave ? s : 0u;
+    sum += s;
+  }
+  __syncthreads();
+  *total = sum;
+  return before + incl - x;
+}
+
+__global__ __launch_bounds__(kThreads) void compact_count_kernel(const uint8_t* status, uint64_t n,
+                                                                 uint64_t* tile_counts) {
+  __shared__ uint32_t wave_sums[kThreads / 64];
+  const uint64_t first = (uint64_t)blockIdx.x * kTileItems + (uint64_t)threadIdx.x * kPerThread;
+  const uint32_t c = count_misses(status, n, first);
+  uint32_t total;
+  block_exclusive_scan<kThreads / 64>(c, wave_sums, &total);
+  if (threadIdx.x == 0) tile_counts[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(kScanThreads) void compact_scan_kernel(const uint64_t* tile_counts, uint64_t tiles,
+                                                                    uint64_t* tile_offsets, uint64_t* miss_count,
+                                                                    uint64_t* miss_bytes, uint64_t block_bytes) {
+  __shared__ uint32_t wave_sums[kScanThreads / 64];
+  uint64_t carry = 0;
+  for (uint64_t base = 0; base < tiles; base += kScanThreads) {
+    const uint64_t t = base + threadIdx.x;
+    const uint32_t c = t < tiles ? (uint32_t)tile_counts[t] : 0u;
+    uint32_t total;
+    const uint32_t excl = block_exclusive_scan<kScanThreads / 64>(c, wave_sums, &total);
+    if (t < tiles) tile_offsets[t] = carry + excl;
+    carry += total;
+  }
+  if (threadIdx.x == 0) {
+    *miss_count = carry;
+    if (miss_bytes) *miss_bytes = carry * block_bytes;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void compact_scatter_kernel(const uint8_t* status, uint64_t n,
+                                                                   const uint64_t* tile_offsets,
+                                                                   uint64_t* miss_idx) {
+  __shared__ uint32_t wave_sums[kThreads / 64];
+  const uint64_t first = (uint64_t)blockIdx.x * kTileItems + (uint64_t)threadIdx.x * kPerThread;
+  const uint32_t c = count_misses(status, n, first);
+  uint32_t total;
+  const uint32_t excl = block_exclusive_scan<kThreads / 64>(c, wave_sums, &total);
+  uint64_t out = tile_offsets[blockIdx.x] + excl;
+#pragma unroll
+  for (int e = 0; e < kPerThread; ++e) {
+    const uint64_t g = first + e;
+    if (g < n && status[g] == GLEAM_MISS) miss_idx[out++] = g;
+  }
+}
+
+// Subtract the missing tail of every MISS short last block from the byte total.
+__global__ void compact_short_block_kernel(const uint8_t* status, uint64_t n, const uint64_t* seg_len,
+                                           const uint64_t* blk_first, uint64_t n_seg, uint64_t block_bytes,
+                                           uint64_t* miss_bytes) {
+  const uint64_t s = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= n_seg) return;
+  const uint64_t b0 = blk_first[s], b1 = blk_first[s + 1];
+  if (b1 <= b0 || b1 - 1 >= n) return;
+  const uint64_t g_last = b1 - 1;
+  if (status[g_last] != GLEAM_MISS) return;
+  const uint64_t last_len = seg_len[s] - (b1 - b0 - 1) * block_bytes;
+  if (last_len < block_bytes)
+    atomicAdd(reinterpret_cast<unsigned long long*>(miss_bytes), (unsigned long long)(0 - (block_bytes - last_len)));
+}
+
+}  // namespace
+}  // namespace gleam
+
+extern "C" gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam_batch* b,
+                                           uint64_t* d_miss_idx, uint64_t* d_miss_count, uint64_t* d_miss_bytes,
+                                           void* d_ws, size_t ws_bytes, void* stream) {
+  using namespace gleam;
+  clear_error();
+  if (!d_miss_count || (n > 0 && (!d_status || !d_miss_idx))) {
+    set_error("gleam_miss_compact: null status, index list or count");
+    return GLEAM_E_INVALID;
+  }
+  if (d_miss_bytes) {
+    if (!b || b->n_blocks != n || !valid_block_bytes(b->block_bytes)) {
+      set_error("gleam_miss_compact: miss_bytes needs the batch of these n statuses");
+      return GLEAM_E_INVALID;
+    }
+    if (n > 0 && (b->n_seg == 0 || !b->seg_len || !b->blk_first)) {
+      set_error("gleam_miss_compact: null batch descriptor");
+      return GLEAM_E_INVALID;
+    }
+  }
+  const WsLayout L = ws_layout(n);
+  if (!d_ws || !aligned256(d_ws)) {
+    set_error("gleam_miss_compact: workspace must be non-null and 256-byte aligned");
+    return GLEAM_E_INVALID;
+  }
+  if (ws_bytes < L.total) {
+    set_error("gleam_miss_compact: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
+    return GLEAM_E_WORKSPACE;
+  }
+  if (L.tiles > 0x7fffffffull || (d_miss_bytes && b->n_seg / 256 > 0x7fffffffull)) return GLEAM_E_UNSUPPORTED;
+  hipStream_t s = (hipStream_t)stream;
+  uint64_t* counts = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(d_ws) + L.tiles_off);
+  uint64_t* offsets = counts + L.tiles;
+  const uint64_t block_bytes = d_miss_bytes ? b->block_bytes : 0;
+  gleam_status st;
+  if (n > 0) {
+    hipLaunchKernelGGL(compact_count_kernel, dim3((uint32_t)L.tiles), dim3(kThreads), 0, s, d_status, n, counts);
+    if ((st = launch_status("compact_count_kernel")) != GLEAM_OK) return st;
+  }
+  hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, counts, L.tiles, offsets, d_miss_count,
+                     d_miss_bytes, block_bytes);
+  if ((st = launch_status("compact_scan_kernel")) != GLEAM_OK) return st;
+  if (n == 0) return GLEAM_OK;
+  hipLaunchKernelGGL(compact_scatter_kernel, dim3((uint32_t)L.tiles), dim3(kThreads), 0, s, d_status, n, offsets,
+                     d_miss_idx);
+  if ((st = launch_status("compact_scatter_kernel")) != GLEAM_OK) return st;
+  if (d_miss_bytes) {
+    const uint32_t grid = (uint32_t)((b->n_seg + 255) / 256);
+    hipLaunchKernelGGL(compact_short_block_kernel, dim3(grid), dim3(256), 0, s, d_status, n, b->seg_len,
+                       b->blk_first, b->n_seg, block_bytes, d_miss_bytes);
+    if ((st = launch_status("compact_short_block_kernel")) != GLEAM_OK) return st;
+  }
+  return GLEAM_OK;
+}

@@ -1,0 +1,47 @@
+// Host-side helpers shared by the libgleam translation units (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "gleam.h"
+
+// Host view of a table: storage = [256-byte header][capacity x (key u64, value u64)].
+// Header: u64 flag "the key kEmpty is present", u64 its value.
+struct gleam_cache {
+  uint8_t* storage;
+  uint64_t capacity;
+  int shift;           // 64 - log2(capacity)
+  uint64_t max_keys;   // floor(max_load * capacity), at most capacity - 1
+  uint64_t key_bound;  // upper bound on keys present
+};
+
+namespace gleam {
+
+constexpr size_t kHeaderBytes = 256;
+constexpr uint64_t kTileItems = 2048;  // statuses per compaction workgroup
+
+// Workspace layout for n items: [header 256 B][scratch table][tile counts][tile offsets].
+// Header u64 words: 0 = scratch min-index of the key kEmpty, 1 = new-key counter,
+// 2 = short-block byte deficit.
+struct WsLayout {
+  uint64_t scratch_cap;   // power of two >= max(64, 2n)
+  size_t scratch_off;
+  uint64_t tiles;
+  size_t tiles_off;
+  size_t total;
+};
+WsLayout ws_layout(uint64_t n);
+
+void set_error(const char* fmt, ...);
+void clear_error();
+gleam_status launch_status(const char* what);  // GLEAM_OK, or GLEAM_E_HIP after a failed launch
+bool valid_block_bytes(uint32_t block_bytes);
+int log2_exact(uint64_t x);                    // -1 unless x is a power of two
+bool aligned256(const void* p);
+
+// Fill n u64 words with value on stream (a kernel, so it can live in a captured graph).
+gleam_status fill_u64(uint64_t* p, uint64_t n, uint64_t value, hipStream_t stream);
+
+}  // namespace gleam

@@ -1,0 +1,221 @@
+"""GPU parity: every output of the library's kernels equals the oracle's, bit for
+bit, on the same seeded inputs (integer work: no tolerance).
+
+Sizes span several workgroups and end in ragged tails; edge cases cover empty
+batches, zero-length and one-byte payloads, every tail path of the leaf hash,
+unaligned payload starts, every block size from 4 KiB to 16 MiB (one leaf per
+block up to 4096 leaves per block), keys 0 and 2^64-1, duplicate keys, multi-tile
+compaction and table capacity errors."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_23115_amd as g
+import workloads as W
+from gpu_util import assert_same, host_threads, keys_to_device, run_path, say, to_device, u64
+
+pytestmark = pytest.mark.gpu
+
+TAIL_LENGTHS = [1, 2, 3, 4, 5, 7, 8, 9, 15, 16, 31, 32, 33, 37, 63, 64, 100, 255, 4095, 4096, 4097, 8191, 8192]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a visible GPU")
+    torch.cuda.init()
+
+
+def oracle_path(payloads, block, table):
+    res = oracle.run(payloads, block, table, threads=host_threads())
+    _, leaves = oracle.batch_digests(payloads, block, with_leaves=True, threads=host_threads())
+    res["leaves"] = leaves
+    return res
+
+
+def make_payloads(rng, block, extra=()):
+    lens = TAIL_LENGTHS + [block - 1, block, block + 1, 2 * block + 12345, 3 * block] + list(extra)
+    lens += [0, 0]
+    order = rng.permutation(len(lens))
+    return [np.frombuffer(rng.bytes(int(lens[i])), np.uint8) for i in order]
+
+
+@pytest.mark.parametrize("block", [4096 << k for k in range(13)])
+def test_digests_every_block_size(block):
+    rng = np.random.default_rng(100 + block.bit_length())
+    payloads = make_payloads(rng, block)
+    arena, offs, lens = W.pack(payloads, align=256)
+    say("digests block", block, "payloads", len(payloads), "bytes", int(lens.sum()))
+    d_arena = to_device(arena)
+    batch = g.Batch.from_arena(d_arena, offs, lens, block)
+    table = g.Cache(1 << 10)
+    gpu = run_path(batch, table, with_leaves=True)
+    ref = oracle_path(payloads, block, oracle.Table())
+    assert_same(gpu, ref, f"block {block}")
+    assert np.array_equal(gpu["leaves"], ref["leaves"])
+
+
+@pytest.mark.parametrize("skew", [1, 3, 8, 12])
+@pytest.mark.parametrize("block", [4096, 65536, 1 << 20])
+def test_unaligned_payload_starts(skew, block):
+    rng = np.random.default_rng(200 + skew + block.bit_length())
+    payloads = make_payloads(rng, block)
+    arena, offs, lens = W.pack(payloads, align=256, skew=skew)
+    say("unaligned skew", skew, "block", block)
+    batch = g.Batch.from_arena(to_device(arena), offs, lens, block)
+    gpu = run_path(batch, g.Cache(1 << 10), with_leaves=True)
+    ref = oracle_path(payloads, block, oracle.Table())
+    assert_same(gpu, ref, f"skew {skew}")
+    assert np.array_equal(gpu["leaves"], ref["leaves"])
+
+
+def test_random16_three_passes():
+    block = W.RANDOM16_BLOCK
+    p = W.random16_payload()
+    say("random16 pass 1")
+    d_p = to_device(p)
+    batch = g.Batch.from_arena(d_p, [0], [p.size], block)
+    table = g.Cache(1 << 10)
+    otable = oracle.Table()
+    gpu1 = run_path(batch, table, with_leaves=True)
+    ref1 = oracle_path([p], block, otable)
+    assert_same(gpu1, ref1, "pass 1")
+    assert np.array_equal(gpu1["leaves"], ref1["leaves"])
+    assert gpu1["miss_count"] == 256
+    say("random16 insert")
+    vals = torch.arange(256, dtype=torch.int64, device="cuda")
+    n_new = table.insert(gpu1["_device_digests"], vals)
+    assert int(n_new.item()) == 256 == otable.insert(ref1["digests"], np.arange(256, dtype=np.uint64))
+    say("random16 pass 2a")
+    gpu2 = run_path(batch, table)
+    ref2 = oracle_path([p], block, otable)
+    assert_same(gpu2, ref2, "pass 2a")
+    assert (gpu2["status"] == g.HIT_CACHE).all()
+    q, chosen = W.random16_rerandomized(p)
+    say("random16 pass 2b")
+    batch_q = g.Batch.from_arena(to_device(q), [0], [q.size], block)
+    gpu3 = run_path(batch_q, table)
+    ref3 = oracle_path([q], block, otable)
+    assert_same(gpu3, ref3, "pass 2b")
+    assert gpu3["miss_idx"].tolist() == chosen.tolist()
+
+
+def test_repeated_runs_identical():
+    block = 65536
+    rng = np.random.default_rng(300)
+    pool = [rng.bytes(block) for _ in range(8)]
+    payloads = [np.frombuffer(b"".join(pool[int(i)] for i in rng.integers(0, 8, 40)) + rng.bytes(777), np.uint8)
+                for _ in range(10)]
+    arena, offs, lens = W.pack(payloads)
+    batch = g.Batch.from_arena(to_device(arena), offs, lens, block)
+    table = g.Cache(1 << 12)
+    say("determinism x10")
+    first = run_path(batch, table)
+    for _ in range(9):
+        again = run_path(batch, table)
+        assert_same(again, first, "repeat")
+    ref = oracle_path(payloads, block, oracle.Table())
+    assert_same(first, ref, "vs oracle")
+    assert (first["status"] == g.HIT_BATCH).sum() > 100
+
+
+def test_lookup_special_keys_and_duplicates():
+    rng = np.random.default_rng(400)
+    pool = np.concatenate([rng.integers(0, 2**64, 500, dtype=np.uint64, endpoint=False),
+                           np.array([0, 2**64 - 1, 1, 2**63], np.uint64)])
+    keys = pool[rng.integers(0, pool.size, 20000)]
+    cached = pool[rng.choice(pool.size, 200, replace=False)]
+    cached = np.concatenate([cached, np.array([0, 2**64 - 1], np.uint64)])
+    cvals = rng.integers(0, 2**64, cached.size, dtype=np.uint64, endpoint=False)
+    say("lookup special keys")
+    table = g.Cache(1 << 12)
+    n_new = table.insert(keys_to_device(cached), keys_to_device(cvals))
+    ot = oracle.Table()
+    assert int(n_new.item()) == ot.insert(cached, cvals)
+    status, ref = table.lookup(keys_to_device(keys))
+    torch.cuda.synchronize()
+    est, eref = oracle.lookup(keys, ot)
+    assert np.array_equal(status.cpu().numpy(), est)
+    assert np.array_equal(u64(ref), eref)
+    assert {0, 1, 2} <= set(est.tolist())
+
+
+def test_insert_lowest_index_wins_and_existing_kept():
+    rng = np.random.default_rng(500)
+    table, ot = g.Cache(1 << 12, max_load=0.9), oracle.Table()
+    for rnd in range(5):
+        keys = rng.integers(0, 300, 700).astype(np.uint64)
+        keys[rng.integers(0, 700, 5)] = 2**64 - 1
+        keys[rng.integers(0, 700, 5)] = 0
+        vals = rng.integers(0, 2**64, 700, dtype=np.uint64, endpoint=False)
+        say("insert round", rnd)
+        n_new = table.insert(keys_to_device(keys), keys_to_device(vals))
+        assert int(n_new.item()) == ot.insert(keys, vals)
+        probe = np.concatenate([np.arange(0, 310, dtype=np.uint64), np.array([2**64 - 1], np.uint64)])
+        st, ref = table.lookup(keys_to_device(probe))
+        torch.cuda.synchronize()
+        est, eref = oracle.lookup(probe, ot)
+        assert np.array_equal(st.cpu().numpy(), est)
+        assert np.array_equal(u64(ref), eref)
+
+
+def test_capacity_is_enforced():
+    table = g.Cache(16, max_load=0.5)  # at most 8 keys
+    k = keys_to_device(np.arange(9, dtype=np.uint64))
+    with pytest.raises(g.GleamError) as e:
+        table.insert(k, k)
+    assert e.value.status == g.E_CAPACITY
+    table.insert(k[:8], k[:8])
+    with pytest.raises(g.GleamError):
+        table.insert(k[8:], k[8:])
+    assert table.key_bound() == 8
+    st, ref = table.lookup(k)
+    torch.cuda.synchronize()
+    assert st.cpu().numpy().tolist() == [1] * 8 + [0]
+
+
+@pytest.mark.parametrize("n", [1, 63, 2047, 2048, 2049, 3 * 2048 + 17, 100_003, 2_500_001])
+def test_compaction_tiles(n):
+    rng = np.random.default_rng(600 + n)
+    status = rng.choice(np.array([0, 1, 2], np.uint8), n, p=[0.3, 0.5, 0.2])
+    # a batch whose geometry has n blocks with short last blocks
+    block = 4096
+    lens = []
+    left = n
+    while left:
+        k = int(min(left, rng.integers(1, 6)))
+        lens.append((k - 1) * block + int(rng.integers(1, block + 1)))
+        left -= k
+    batch = g.Batch(np.full(len(lens), 0, np.uint64), lens, block)
+    assert batch.n_blocks == n
+    say("compaction n", n)
+    d_status = to_device(status)
+    miss_idx, counters = g.miss_compact(d_status, batch)
+    torch.cuda.synchronize()
+    c = u64(counters)
+    _, blen = oracle.geometry(lens, block)
+    eidx, ecnt, ebytes = oracle.compact(status, blen)
+    assert int(c[0]) == ecnt and int(c[1]) == ebytes
+    assert np.array_equal(u64(miss_idx)[:ecnt], eidx)
+
+
+def test_empty_inputs():
+    say("empty batch")
+    batch = g.Batch([], [], 65536)
+    assert batch.n_blocks == 0
+    d = g.fp_chunks(batch)
+    assert d.numel() == 0
+    table = g.Cache(64)
+    st, ref = table.lookup(d)
+    miss_idx, counters = g.miss_compact(st, batch)
+    torch.cuda.synchronize()
+    assert u64(counters).tolist() == [0, 0]
+    # zero-length payloads between non-empty ones
+    rng = np.random.default_rng(700)
+    payloads = [np.zeros(0, np.uint8), np.frombuffer(rng.bytes(5000), np.uint8), np.zeros(0, np.uint8)]
+    arena, offs, lens = W.pack(payloads)
+    batch = g.Batch.from_arena(to_device(arena), offs, lens, 4096)
+    gpu = run_path(batch, table)
+    assert_same(gpu, oracle_path(payloads, 4096, oracle.Table()), "zero-length")
