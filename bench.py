@@ -1,0 +1,289 @@
+"""Benchmark: payload GB/s of weight-cache hit detection (fingerprint + table lookup +
+miss compaction) on one MI355X, with the HBM roofline of the fingerprint kernel and
+the reference oracle timed on the host's cores.
+
+Workload (default): the weights of a 7B decoder (32 layers, d_model 4096, FFN 11008,
+vocab 32000; 291 fp16 tensors, 13,476,831,232 bytes) as one batch of host-to-device
+payloads, cut into 1 MiB blocks (12,917 blocks). The resident table holds the digests
+of the base weights; the payload perturbs 3 of the 32 layers with a rank-16 update,
+so 1,158 blocks miss and 11,759 hit. Values are synthetic N(0, 0.02) (no checkpoint).
+
+One step = gleam_fp_chunks -> gleam_cache_lookup -> gleam_miss_compact over the whole
+batch, inputs already resident in HBM. Prints ONE JSON line.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload decoder7b]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD public specification
+PROFILE_PMC = os.path.join(ROOT, "profiles", "fp_kernel_decoder7b_pmc.txt")
+FP_SOURCE = os.path.join(ROOT, "paper_2607_23115_amd", "csrc", "fp_chunks.hip")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def host_threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def source_digest() -> str:
+    with open(FP_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def pmc_traffic(algo_bytes: int):
+    """HBM bytes per fingerprint launch from the committed counter summary, scaled by
+    the copy-kernel calibration in it; None if absent or taken on other source."""
+    if not os.path.exists(PROFILE_PMC):
+        return None
+    kv = {}
+    with open(PROFILE_PMC) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    try:
+        if kv.get("fp_chunks.hip sha256[:16]") != source_digest():
+            return None
+        fetch = float(kv["fp FETCH_SIZE KiB per dispatch"]) * 1024 * float(kv["copy fetch scale"])
+        write = float(kv["fp WRITE_SIZE KiB per dispatch"]) * 1024 * float(kv["copy write scale"])
+    except (KeyError, ValueError):
+        return None
+    return int(fetch + write)
+
+
+# --------------------------------------------------------------------------- #
+# Workloads (device-resident batch + table built through the library)
+# --------------------------------------------------------------------------- #
+def build_decoder7b(g, torch, threads):
+    import workloads as W
+    dec = W.Decoder()
+    t0 = time.time()
+    arena, offs, lens = dec.arena(perturbed=True, threads=threads)
+    log(f"generated payload {arena.size / 1e9:.2f} GB in {time.time() - t0:.1f}s")
+    d_arena = torch.from_numpy(arena).to("cuda")
+    # base versions of the perturbed tensors, for the table
+    side_lens = [dec.nbytes[i] for i in dec.perturbed]
+    side_offs, side_total = W.arena_offsets(side_lens)
+    side = np.empty(side_total, dtype=np.uint8)
+    W.parallel_fill(side, side_offs, [lambda i=i: dec.base(i) for i in dec.perturbed], threads)
+    d_side = torch.from_numpy(side).to("cuda")
+    base_addr = offs + np.uint64(d_arena.data_ptr())
+    for j, i in enumerate(dec.perturbed):
+        base_addr[i] = np.uint64(d_side.data_ptr()) + side_offs[j]
+    block = W.DECODER_BLOCK
+    batch = g.Batch.from_arena(d_arena, offs, lens, block)
+    base_batch = g.Batch(base_addr, lens, block, keepalive=(d_arena, d_side))
+    table = g.Cache(1 << 15, max_load=0.7)
+    base_digests = g.fp_chunks(base_batch)
+    table.insert(base_digests, torch.arange(base_batch.n_blocks, dtype=torch.int64, device="cuda"))
+    torch.cuda.synchronize()
+    del d_side, base_batch, side
+    first = batch.host_first
+    expect_miss = int(sum(int(first[i + 1] - first[i]) for i in dec.perturbed))
+    payloads = [arena[int(o):int(o) + int(n)] for o, n in zip(offs, lens)]
+    desc = ("7B decoder fp16 weights (32 layers, d 4096, ffn 11008, vocab 32000; 291 tensors), "
+            "1 MiB blocks, 3 of 32 layers rank-16 perturbed, table holds the base weights' digests")
+    return batch, table, payloads, expect_miss, desc, d_arena
+
+
+def build_random16(g, torch, threads):
+    import workloads as W
+    p = W.random16_payload()
+    q, chosen = W.random16_rerandomized(p)
+    d_p = torch.from_numpy(p).to("cuda")
+    d_q = torch.from_numpy(q).to("cuda")
+    block = W.RANDOM16_BLOCK
+    table = g.Cache(1 << 10)
+    base = g.Batch.from_arena(d_p, [0], [p.size], block)
+    table.insert(g.fp_chunks(base), torch.arange(base.n_blocks, dtype=torch.int64, device="cuda"))
+    batch = g.Batch.from_arena(d_q, [0], [q.size], block)
+    desc = "16 MiB random payload, 64 KiB blocks, 64 blocks re-randomised, table holds the original"
+    return batch, table, [q], len(chosen), desc, (d_p, d_q)
+
+
+def build_small_copies(g, torch, threads):
+    import workloads as W
+    sc = W.SmallCopies()
+    d_arena = torch.from_numpy(sc.arena).to("cuda")
+    batch = g.Batch.from_arena(d_arena, sc.offsets, sc.sizes, W.SMALL_BLOCK)
+    table = g.Cache(1 << 10)
+    expect_miss = batch.n_blocks - int(sc.targets.size)
+    desc = "100,000 buffers of 256 B..64 KiB (log-uniform), 20% of full leaves planted duplicates, 4 KiB blocks"
+    return batch, table, sc.payloads(), expect_miss, desc, d_arena
+
+
+WORKLOADS = {"decoder7b": build_decoder7b, "random16": build_random16, "small_copies": build_small_copies}
+
+
+def run_cpu_baseline(payloads, block, threads, budget_bytes):
+    """The oracle as it stands, over the leading payloads up to budget_bytes."""
+    import oracle
+    sample, total = [], 0
+    for p in payloads:
+        if sample and total + p.size > budget_bytes:
+            break
+        sample.append(p)
+        total += p.size
+    # table: nothing cached (the oracle's lookup cost does not depend on the hit rate); median of 3
+    times = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        oracle.run(sample, block, oracle.Table(), threads=threads)
+        times.append(time.perf_counter() - t0)
+    dt = float(np.median(times))
+    return {"value": round(total / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(sample)} of {len(payloads)} payloads ({total} bytes), median of 3 runs "
+                      f"{dt:.3f} s, {cpu_model()}"}
+
+
+def copy_calibration(torch, nbytes=4 << 30, reps=3):
+    """A plain device copy of known size, for scaling the HBM byte counters."""
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes, "reps": reps}))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="decoder7b", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-gb", type=float, default=20.0)
+    ap.add_argument("--copy-calibration", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (see DESIGN.md, sharding)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_23115_amd as g
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
+
+    threads = host_threads()
+    batch, table, payloads, expect_miss, desc, keep = WORKLOADS[args.workload](g, torch, threads)
+    n = batch.n_blocks
+    payload_bytes = int(batch.host_len.sum())
+    dev = "cuda"
+    digests = torch.empty(n, dtype=torch.int64, device=dev)
+    status = torch.empty(n, dtype=torch.uint8, device=dev)
+    ref = torch.empty(n, dtype=torch.int64, device=dev)
+    miss_idx = torch.empty(n, dtype=torch.int64, device=dev)
+    counters = torch.zeros(2, dtype=torch.int64, device=dev)
+    ws = g.workspace(n, dev)
+
+    def step(ev_a=None, ev_b=None):
+        if ev_a is not None:
+            ev_a.record()
+        g.fp_chunks(batch, out=digests)
+        if ev_b is not None:
+            ev_b.record()
+        table.lookup(digests, status=status, ref=ref, ws=ws)
+        g.miss_compact(status, batch, miss_idx=miss_idx, counters=counters, ws=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    c = g.as_u64(counters)
+    miss_count, miss_bytes = int(c[0]), int(c[1])
+    if miss_count != expect_miss:
+        raise SystemExit(f"planted truth violated: {miss_count} misses, expected {expect_miss}")
+
+    K = args.steps
+    ev_fp = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for k in range(K):
+        step(*ev_fp[k])
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    fp_ms = [a.elapsed_time(b) for a, b in ev_fp]
+    fp_avg_ms = float(np.mean(fp_ms))
+    ms_per_step = total_ms / K
+    value = payload_bytes / (ms_per_step * 1e-3) / 1e9
+
+    algo_bytes = payload_bytes + 8 * n + 24 * batch.n_seg + 8 * (batch.n_seg + 1)
+    achieved = algo_bytes / (fp_avg_ms * 1e-3) / 1e9
+    traffic = pmc_traffic(algo_bytes) if args.workload == "decoder7b" else None
+    log(f"{desc}: {n} blocks, {miss_count} misses ({miss_bytes} bytes), fp {fp_avg_ms:.3f} ms "
+        f"(min {min(fp_ms):.3f}, max {max(fp_ms):.3f}), step {ms_per_step:.3f} ms")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = run_cpu_baseline(payloads, batch.block_bytes, threads, int(args.cpu_budget_gb * 1e9))
+        log(f"cpu baseline: {cpu}")
+
+    out = {
+        "metric": "payload GB/s for fingerprint+lookup+compact (and % of HBM peak), 1 MI355X",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": desc, "payload_bytes": payload_bytes, "payloads": batch.n_seg, "blocks": n,
+                   "block_bytes": batch.block_bytes, "leaf_bytes": 4096, "misses": miss_count,
+                   "miss_bytes": miss_bytes, "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2)},
+        "roofline": {"bound": "hbm", "kernel": "fp_kernel", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "algorithmic_bytes": algo_bytes, "avg_launch_ms": round(fp_avg_ms, 4)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    del keep
+
+
+if __name__ == "__main__":
+    main()
