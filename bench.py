@@ -144,7 +144,46 @@ def build_small_copies(g, torch, threads):
     return batch, table, sc.payloads(), expect_miss, desc, d_arena
 
 
-WORKLOADS = {"decoder7b": build_decoder7b, "random16": build_random16, "small_copies": build_small_copies}
+def build_resnet50(g, torch, threads):
+    import workloads as W
+    payloads = W.resnet50_payloads()
+    arena, offs, lens = W.pack(payloads)
+    d_arena = torch.from_numpy(arena).to("cuda")
+    block = W.RESNET_BLOCK
+    batch = g.Batch.from_arena(d_arena, offs, lens, block)
+    cached = W.resnet50_cached_tensors()
+    sub = g.Batch.from_arena(d_arena, offs[cached], lens[cached], block)
+    table = g.Cache(1 << 12)
+    table.insert(g.fp_chunks(sub), torch.arange(sub.n_blocks, dtype=torch.int64, device="cuda"))
+    expect_miss = batch.n_blocks - sub.n_blocks
+    desc = "ResNet-50 fp16 weights (161 tensors, 25.6M params), 64 KiB blocks, table holds 80 of the tensors"
+    return batch, table, payloads, expect_miss, desc, d_arena
+
+
+def build_large_bf16(g, torch, threads):
+    import workloads as W
+    ls = W.LargeSet()
+    arena, offs, lens = ls.arena(threads=threads)
+    d_arena = torch.from_numpy(arena).to("cuda")
+    block = W.LARGE_BLOCK
+    batch = g.Batch.from_arena(d_arena, offs, lens, block)
+    rand = torch.from_numpy(ls.random_digests().view(np.int64)).to("cuda")
+    chosen = ls.cached_blocks(batch.n_blocks)
+    digests = g.fp_chunks(batch)
+    sel = torch.from_numpy(chosen.astype(np.int64)).to("cuda")
+    keys = torch.cat([rand, digests[sel]])
+    vals = torch.cat([torch.zeros_like(rand), sel])
+    table = g.Cache(1 << 25, max_load=0.65)
+    table.insert(keys, vals)
+    torch.cuda.synchronize()
+    payloads = [arena[int(o):int(o) + int(n)] for o, n in zip(offs, lens)]
+    desc = ("2,000 bf16 tensors (40 GB, log-uniform sizes), 2 MiB blocks, table holds 20M random digests "
+            "plus 60% of the blocks")
+    return batch, table, payloads, batch.n_blocks - chosen.size, desc, d_arena
+
+
+WORKLOADS = {"decoder7b": build_decoder7b, "random16": build_random16, "small_copies": build_small_copies,
+             "resnet50": build_resnet50, "large_bf16": build_large_bf16}
 
 
 def run_cpu_baseline(payloads, block, threads, budget_bytes):

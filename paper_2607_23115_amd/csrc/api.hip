@@ -2,6 +2,7 @@
 // and workspace sizing.
 
 #include <stdarg.h>
+#include <atomic>
 #include <stdio.h>
 
 #include "gleam_internal.h"
@@ -40,6 +41,32 @@ bool valid_block_bytes(uint32_t block_bytes) {
 }
 
 bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255) == 0; }
+
+gleam_status device_cu_count(int* cus) {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    set_error("hipGetDevice: %s", hipGetErrorString(e));
+    return GLEAM_E_HIP;
+  }
+  if (dev >= 0 && dev < 64) {
+    const int c = cached[dev].load(std::memory_order_relaxed);
+    if (c > 0) {
+      *cus = c;
+      return GLEAM_OK;
+    }
+  }
+  int n = 0;
+  e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess || n <= 0) {
+    set_error("hipDeviceGetAttribute(multiprocessor count): %s", hipGetErrorString(e));
+    return GLEAM_E_HIP;
+  }
+  if (dev >= 0 && dev < 64) cached[dev].store(n, std::memory_order_relaxed);
+  *cus = n;
+  return GLEAM_OK;
+}
 
 WsLayout ws_layout(uint64_t n) {
   WsLayout L;

@@ -168,14 +168,24 @@ ScratchRef scratch_ref(void* ws, const WsLayout& L) {
   return s;
 }
 
-// Reset the scratch header and slots: keys to kEmpty, min-indices to all-ones.
-gleam_status clear_scratch(void* ws, const WsLayout& L, hipStream_t stream) {
-  gleam_status st = fill_u64(reinterpret_cast<uint64_t*>(ws), 1, ~0ull, stream);
-  if (st == GLEAM_OK) st = fill_u64(reinterpret_cast<uint64_t*>(ws) + 1, 3, 0, stream);
-  if (st == GLEAM_OK)
-    st = fill_u64(reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + L.scratch_off), 2 * L.scratch_cap, ~0ull,
-                  stream);
-  return st;
+// One launch resets the scratch table: slot keys to kEmpty and min-indices to all-ones,
+// header word 0 (min index of key kEmpty) to all-ones, words 1..3 and *also_zero to 0.
+__global__ void scratch_clear_kernel(uint64_t* hdr, uint64_t* slots, uint64_t words, uint64_t* also_zero) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < 4) hdr[t] = t == 0 ? ~0ull : 0ull;
+  if (t == 4 && also_zero) *also_zero = 0;
+  for (uint64_t i = t; i < words; i += stride) slots[i] = ~0ull;
+}
+
+gleam_status clear_scratch(void* ws, const WsLayout& L, hipStream_t stream, uint64_t* also_zero = nullptr) {
+  uint64_t* hdr = reinterpret_cast<uint64_t*>(ws);
+  uint64_t* slots = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + L.scratch_off);
+  const uint64_t words = 2 * L.scratch_cap;
+  const uint64_t want = (words + kThreads - 1) / kThreads;
+  const uint32_t grid = (uint32_t)(want < 2048 ? want : 2048);
+  hipLaunchKernelGGL(scratch_clear_kernel, dim3(grid), dim3(kThreads), 0, stream, hdr, slots, words, also_zero);
+  return launch_status("scratch_clear_kernel");
 }
 
 uint32_t blocks_for(uint64_t n) { return (uint32_t)((n + kThreads - 1) / kThreads); }
@@ -277,9 +287,8 @@ extern "C" gleam_status gleam_cache_insert(gleam_cache* c, const uint64_t* d_key
     return GLEAM_E_CAPACITY;
   }
   hipStream_t s = (hipStream_t)stream;
-  gleam_status st = clear_scratch(d_ws, L, s);
+  gleam_status st = clear_scratch(d_ws, L, s, d_n_new);
   uint64_t* counter = d_n_new ? d_n_new : reinterpret_cast<uint64_t*>(d_ws) + 1;
-  if (st == GLEAM_OK && d_n_new) st = fill_u64(d_n_new, 1, 0, s);
   if (st != GLEAM_OK) return st;
   if (n == 0) return GLEAM_OK;
   const ScratchRef sc = scratch_ref(d_ws, L);

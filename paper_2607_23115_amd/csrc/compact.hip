@@ -3,10 +3,11 @@
 // and its byte total.
 //
 // Order-preserving stream compaction in three passes over tiles of 2048 statuses:
-// count per tile (wave ballots), one-workgroup exclusive scan of the tile counts,
+// count per tile, one-workgroup exclusive scan of the tile counts,
 // then each tile writes its MISS indices at its offset using a workgroup scan of
 // per-thread counts. Byte total = count * block_bytes minus, for every payload
-// whose short last block is a MISS, the part of that block that does not exist.
+// whose short last block is a MISS, the part of that block that does not exist
+// (each tile handles the payloads whose last block it holds).
 // All sums are integer, so the results do not depend on thread timing.
 
 #include "gleam_device.h"
@@ -87,9 +88,30 @@ __global__ __launch_bounds__(kScanThreads) void compact_scan_kernel(const uint64
   }
 }
 
+// Number of payloads s with blk_first[s + 1] <= x (blk_first is non-decreasing).
+__device__ __forceinline__ uint64_t segments_ending_by(const uint64_t* blk_first, uint64_t n_seg, uint64_t x) {
+  uint64_t lo = 0, hi = n_seg;
+  while (lo < hi) {
+    const uint64_t mid = (lo + hi) >> 1;
+    if (blk_first[mid + 1] <= x) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+struct ShortBlocks {  // payload geometry for the byte total; seg_len == nullptr: not wanted
+  const uint64_t* seg_len;
+  const uint64_t* blk_first;
+  uint64_t n_seg;
+  uint64_t block_bytes;
+  uint64_t* miss_bytes;
+};
+
+// Writes the tile's MISS indices at its offset; also subtracts, for every payload whose
+// last block lies in this tile, is short and is a MISS, the bytes that block lacks.
 __global__ __launch_bounds__(kThreads) void compact_scatter_kernel(const uint8_t* status, uint64_t n,
                                                                    const uint64_t* tile_offsets,
-                                                                   uint64_t* miss_idx) {
+                                                                   uint64_t* miss_idx, ShortBlocks sb) {
   __shared__ uint32_t wave_sums[kThreads / 64];
   const uint64_t first = (uint64_t)blockIdx.x * kTileItems + (uint64_t)threadIdx.x * kPerThread;
   const uint32_t c = count_misses(status, n, first);
@@ -101,21 +123,27 @@ __global__ __launch_bounds__(kThreads) void compact_scatter_kernel(const uint8_t
     const uint64_t g = first + e;
     if (g < n && status[g] == GLEAM_MISS) miss_idx[out++] = g;
   }
-}
-
-// Subtract the missing tail of every MISS short last block from the byte total.
-__global__ void compact_short_block_kernel(const uint8_t* status, uint64_t n, const uint64_t* seg_len,
-                                           const uint64_t* blk_first, uint64_t n_seg, uint64_t block_bytes,
-                                           uint64_t* miss_bytes) {
-  const uint64_t s = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (s >= n_seg) return;
-  const uint64_t b0 = blk_first[s], b1 = blk_first[s + 1];
-  if (b1 <= b0 || b1 - 1 >= n) return;
-  const uint64_t g_last = b1 - 1;
-  if (status[g_last] != GLEAM_MISS) return;
-  const uint64_t last_len = seg_len[s] - (b1 - b0 - 1) * block_bytes;
-  if (last_len < block_bytes)
-    atomicAdd(reinterpret_cast<unsigned long long*>(miss_bytes), (unsigned long long)(0 - (block_bytes - last_len)));
+  if (!sb.seg_len) return;
+  // payloads whose last block g = blk_first[s + 1] - 1 falls in [lo, hi)
+  const uint64_t lo = (uint64_t)blockIdx.x * kTileItems;
+  const uint64_t hi = min(lo + kTileItems, n);
+  const uint64_t s_begin = segments_ending_by(sb.blk_first, sb.n_seg, lo);
+  const uint64_t s_end = segments_ending_by(sb.blk_first, sb.n_seg, hi);
+  uint64_t deficit = 0;
+  for (uint64_t s = s_begin + threadIdx.x; s < s_end; s += kThreads) {
+    const uint64_t b0 = sb.blk_first[s], b1 = sb.blk_first[s + 1];
+    if (b1 <= b0 || b1 - 1 >= n || status[b1 - 1] != GLEAM_MISS) continue;
+    const uint64_t last_len = sb.seg_len[s] - (b1 - b0 - 1) * sb.block_bytes;
+    if (last_len < sb.block_bytes) deficit += sb.block_bytes - last_len;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const uint32_t lo32 = __shfl_xor((uint32_t)deficit, o, 64);
+    const uint32_t hi32 = __shfl_xor((uint32_t)(deficit >> 32), o, 64);
+    deficit += ((uint64_t)hi32 << 32) | lo32;
+  }
+  if ((threadIdx.x & 63) == 0 && deficit)
+    atomicAdd(reinterpret_cast<unsigned long long*>(sb.miss_bytes), (unsigned long long)(0 - deficit));
 }
 
 }  // namespace
@@ -149,7 +177,7 @@ extern "C" gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, 
     set_error("gleam_miss_compact: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
     return GLEAM_E_WORKSPACE;
   }
-  if (L.tiles > 0x7fffffffull || (d_miss_bytes && b->n_seg / 256 > 0x7fffffffull)) return GLEAM_E_UNSUPPORTED;
+  if (L.tiles > 0x7fffffffull) return GLEAM_E_UNSUPPORTED;
   hipStream_t s = (hipStream_t)stream;
   uint64_t* counts = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(d_ws) + L.tiles_off);
   uint64_t* offsets = counts + L.tiles;
@@ -163,14 +191,9 @@ extern "C" gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, 
                      d_miss_bytes, block_bytes);
   if ((st = launch_status("compact_scan_kernel")) != GLEAM_OK) return st;
   if (n == 0) return GLEAM_OK;
+  ShortBlocks sb{nullptr, nullptr, 0, 0, nullptr};
+  if (d_miss_bytes) sb = ShortBlocks{b->seg_len, b->blk_first, b->n_seg, block_bytes, d_miss_bytes};
   hipLaunchKernelGGL(compact_scatter_kernel, dim3((uint32_t)L.tiles), dim3(kThreads), 0, s, d_status, n, offsets,
-                     d_miss_idx);
-  if ((st = launch_status("compact_scatter_kernel")) != GLEAM_OK) return st;
-  if (d_miss_bytes) {
-    const uint32_t grid = (uint32_t)((b->n_seg + 255) / 256);
-    hipLaunchKernelGGL(compact_short_block_kernel, dim3(grid), dim3(256), 0, s, d_status, n, b->seg_len,
-                       b->blk_first, b->n_seg, block_bytes, d_miss_bytes);
-    if ((st = launch_status("compact_short_block_kernel")) != GLEAM_OK) return st;
-  }
-  return GLEAM_OK;
+                     d_miss_idx, sb);
+  return launch_status("compact_scatter_kernel");
 }

@@ -47,6 +47,7 @@ struct FpArgs {
   uint64_t* block_out;
   uint64_t* leaf_out;
   uint32_t lpb_log2;
+  uint64_t items;  // work items: groups of 256 slots (LPB <= 256) or blocks (LPB > 256)
 };
 
 struct Leaf {
@@ -178,11 +179,83 @@ __device__ uint64_t hash_wave_streamed(const uint8_t* base, uint8_t* tile, int l
   return xxh_avalanche(xxh_converge(v1, v2, v3, v4) + 4096);
 }
 
+// Any 64 leaves whose present ones start 16-byte aligned (lengths 0..4096, anywhere in
+// memory): the full 32-byte stripes stream through the LDS tile as above, with each loader
+// lane holding the addresses of the 16 leaves it loads for; the wave runs as many stages as
+// its longest leaf needs. Each lane then finishes its own tail (< 32 bytes) directly.
+__device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, int lane) {
+  const int wm = lane / kRunLanes, wc = lane % kRunLanes;
+  const int wslot = (wm * kRunLanes + (wc ^ (wm * 4))) * 16;
+  const int rk = lane / kLeavesPerLoad, rm = lane % kLeavesPerLoad;
+  const uint8_t* rp = tile + rk * kSlotStride + rm * kRun;
+  const int rsw = rm * 4;
+  const uint32_t stripes = lf.len >> 5;
+  const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
+
+  const uint8_t* la[kLoads];  // this loader lane's 16-byte chunk of leaf 4k + wm, stage 0
+  uint32_t lim[kLoads];       // that leaf's number of 16-byte chunks in full stripes
+  uint32_t longest = stripes;
+#pragma unroll
+  for (int k = 0; k < kLoads; ++k) {
+    const int src = k * kLeavesPerLoad + wm;
+    la[k] = reinterpret_cast<const uint8_t*>(shfl64(addr, src)) + wc * 16;
+    lim[k] = 2 * (uint32_t)__shfl((int)stripes, src, 64);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) longest = max(longest, (uint32_t)__shfl_xor((int)longest, o, 64));
+  const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 7) / 8);
+
+  uint64_t v1 = kP1 + kP2, v2 = kP2, v3 = 0, v4 = 0 - kP1;
+  uint4 R[kLoads];
+#pragma unroll
+  for (int k = 0; k < kLoads; ++k) R[k] = (uint32_t)wc < lim[k] ? load_stream16(la[k]) : make_uint4(0, 0, 0, 0);
+  for (uint32_t s = 0; s < stages; ++s) {
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) *reinterpret_cast<uint4*>(tile + k * kSlotStride + wslot) = R[k];
+    wave_lds_sync();
+    if (s + 1 < stages) {
+      const uint32_t chunk = (s + 1) * kRunLanes + wc;
+#pragma unroll
+      for (int k = 0; k < kLoads; ++k)
+        R[k] = chunk < lim[k] ? load_stream16(la[k] + (s + 1) * kRun) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      uint4 D[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) D[j] = *reinterpret_cast<const uint4*>(rp + (((half * 8 + j) ^ rsw) * 16));
+#pragma unroll
+      for (int j = 0; j < 8; j += 2) {
+        if (s * 8 + half * 4 + j / 2 < stripes) {
+          v1 = xxh_round(v1, lo64(D[j]));
+          v2 = xxh_round(v2, hi64(D[j]));
+          v3 = xxh_round(v3, lo64(D[j + 1]));
+          v4 = xxh_round(v4, hi64(D[j + 1]));
+        }
+      }
+    }
+    wave_lds_sync();
+  }
+  if (lf.len == 0) return 0;
+  uint64_t h = stripes ? xxh_converge(v1, v2, v3, v4) : kP5;
+  h += lf.len;
+  uint32_t pos = stripes << 5;
+  for (; pos + 8 <= lf.len; pos += 8) h = xxh_tail8(h, *reinterpret_cast<const uint64_t*>(lf.addr + pos));
+  if (pos + 4 <= lf.len) {
+    h = xxh_tail4(h, *reinterpret_cast<const uint32_t*>(lf.addr + pos));
+    pos += 4;
+  }
+  for (; pos < lf.len; ++pos) h = xxh_tail1(h, lf.addr[pos]);
+  return xxh_avalanche(h);
+}
+
 __device__ __forceinline__ uint64_t hash_slot(const Leaf& lf, uint8_t* tile, int lane) {
   const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
   const uint64_t a0 = shfl64(addr, 0);
-  const bool streamable = lf.len == 4096 && addr == a0 + (uint64_t)lane * 4096 && (a0 & 15) == 0;
-  if (__all(streamable)) return hash_wave_streamed(reinterpret_cast<const uint8_t*>(uniform64(a0)), tile, lane);
+  const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)lane * 4096 && (a0 & 15) == 0;
+  if (__all(contiguous)) return hash_wave_streamed(reinterpret_cast<const uint8_t*>(uniform64(a0)), tile, lane);
+  if (!__any(lf.len != 0)) return 0;
+  if (__all(lf.len == 0 || (addr & 15) == 0)) return hash_wave_gathered(lf, tile, lane);
   return lf.len ? hash_leaf_lane(lf.addr, lf.len) : 0;
 }
 
@@ -195,9 +268,12 @@ __global__ __launch_bounds__(kWG) void fp_kernel(FpArgs a) {
   const uint32_t L2 = a.lpb_log2;
   const uint64_t lpb = 1ull << L2;
 
+  // Persistent workgroups: a grid of a few workgroups per CU walks the work items.
+  for (uint64_t item = blockIdx.x; item < a.items; item += gridDim.x) {
+  __syncthreads();  // the previous item's roots have been consumed
   if (L2 <= 8) {
     // 256 consecutive slots: 256 / LPB whole blocks.
-    const uint64_t wave_slot0 = uniform64((uint64_t)blockIdx.x * kWG + (uint64_t)wave * 64);
+    const uint64_t wave_slot0 = uniform64(item * kWG + (uint64_t)wave * 64);
     const uint64_t slot = wave_slot0 + lane;
     const uint64_t g = slot >> L2;
     const uint32_t k = (uint32_t)(slot & (lpb - 1));
@@ -222,7 +298,7 @@ __global__ __launch_bounds__(kWG) void fp_kernel(FpArgs a) {
       if (wave == 0) {
         // 4 group roots = 256 / LPB blocks of G2 = LPB / 64 roots each
         const uint32_t G2 = (uint32_t)(lpb >> 6);
-        const uint64_t g2 = (((uint64_t)blockIdx.x * kWG) >> L2) + (uint64_t)(lane / G2);
+        const uint64_t g2 = ((item * kWG) >> L2) + (uint64_t)(lane / G2);
         uint32_t n2 = 0;
         uint64_t v2 = 0;
         if (lane < 4 && g2 < a.n_blocks) {
@@ -236,7 +312,7 @@ __global__ __launch_bounds__(kWG) void fp_kernel(FpArgs a) {
     }
   } else {
     // One block of LPB > 256 leaves, 256 slots at a time.
-    const uint64_t g = blockIdx.x;
+    const uint64_t g = item;
     const uint64_t s0 = uniform64(find_segment(a.blk_first, a.n_seg, g));
     const uint32_t nleaf = locate(a, g, 0, s0).blk_leaves;
     const uint32_t groups = a.leaf_out ? (uint32_t)(lpb >> 8) : (nleaf + 255) / 256;
@@ -258,6 +334,7 @@ __global__ __launch_bounds__(kWG) void fp_kernel(FpArgs a) {
       const uint64_t r = tree_reduce_lanes(v2, lane & (G2 - 1), (uint32_t)lane < G2 ? n2 : 0, G2);
       if (lane == 0) a.block_out[g] = r;
     }
+  }
   }
 }
 
@@ -283,19 +360,19 @@ extern "C" gleam_status gleam_fp_chunks(const gleam_batch* b, uint64_t* d_block_
   }
   const int lpb_log2 = log2_exact(b->block_bytes) - 12;
   const uint64_t lpb = 1ull << lpb_log2;
-  uint64_t grid;
-  if (lpb_log2 <= 8) {
-    if (b->n_blocks > (UINT64_MAX >> 13)) return GLEAM_E_UNSUPPORTED;
-    grid = (b->n_blocks * lpb + kWG - 1) / kWG;
-  } else {
-    grid = b->n_blocks;
-  }
-  if (grid > 0x7fffffffull) {
-    set_error("gleam_fp_chunks: batch needs more than 2^31 workgroups");
+  if (b->n_blocks > (UINT64_MAX >> 13)) {
+    set_error("gleam_fp_chunks: batch too large");
     return GLEAM_E_UNSUPPORTED;
   }
+  const uint64_t items = lpb_log2 <= 8 ? (b->n_blocks * lpb + kWG - 1) / kWG : b->n_blocks;
+  int cus = 0;
+  gleam_status st = device_cu_count(&cus);
+  if (st != GLEAM_OK) return st;
+  // Four workgroups per CU (two resident at a time, by LDS): measured best on MI355X.
+  const uint64_t cap = 4ull * (uint64_t)cus;
+  const uint64_t grid = items < cap ? items : cap;
   FpArgs a{b->seg_addr, b->seg_len, b->blk_first, b->n_seg, b->n_blocks, d_block_digest, d_leaf_digest,
-           (uint32_t)lpb_log2};
+           (uint32_t)lpb_log2, items};
   hipLaunchKernelGGL(fp_kernel, dim3((uint32_t)grid), dim3(kWG), 0, (hipStream_t)stream, a);
   return launch_status("fp_kernel");
 }

@@ -40,6 +40,7 @@ gleam_status launch_status(const char* what);  // GLEAM_OK, or GLEAM_E_HIP after
 bool valid_block_bytes(uint32_t block_bytes);
 int log2_exact(uint64_t x);                    // -1 unless x is a power of two
 bool aligned256(const void* p);
+gleam_status device_cu_count(int* cus);        // compute units of the current device (cached)
 
 // Fill n u64 words with value on stream (a kernel, so it can live in a captured graph).
 gleam_status fill_u64(uint64_t* p, uint64_t n, uint64_t value, hipStream_t stream);

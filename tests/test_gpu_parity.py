@@ -71,6 +71,29 @@ def test_unaligned_payload_starts(skew, block):
     assert np.array_equal(gpu["leaves"], ref["leaves"])
 
 
+@pytest.mark.parametrize("block", [4096, 65536])
+def test_mixed_alignment_in_one_wave(block):
+    """Aligned and unaligned payloads side by side, so waves mix both kinds."""
+    rng = np.random.default_rng(250 + block.bit_length())
+    payloads = make_payloads(rng, block, extra=[5000, 12000, 4096 * 3])
+    lens = np.array([p.size for p in payloads], np.uint64)
+    offs = np.zeros(len(payloads), np.uint64)
+    pos = 0
+    for i, n in enumerate(lens.tolist()):
+        start = ((pos + 255) // 256) * 256 + (8 if i % 3 == 1 else 0)
+        offs[i] = start
+        pos = start + n
+    arena = np.zeros(pos + 512, np.uint8)
+    for p, o in zip(payloads, offs.tolist()):
+        arena[o:o + p.size] = p
+    say("mixed alignment block", block)
+    batch = g.Batch.from_arena(to_device(arena), offs, lens, block)
+    gpu = run_path(batch, g.Cache(1 << 10), with_leaves=True)
+    ref = oracle_path(payloads, block, oracle.Table())
+    assert_same(gpu, ref, "mixed alignment")
+    assert np.array_equal(gpu["leaves"], ref["leaves"])
+
+
 def test_random16_three_passes():
     block = W.RANDOM16_BLOCK
     p = W.random16_payload()
