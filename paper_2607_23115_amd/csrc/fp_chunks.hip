@@ -368,9 +368,15 @@ extern "C" gleam_status gleam_fp_chunks(const gleam_batch* b, uint64_t* d_block_
   int cus = 0;
   gleam_status st = device_cu_count(&cus);
   if (st != GLEAM_OK) return st;
-  // Four workgroups per CU (two resident at a time, by LDS): measured best on MI355X.
-  const uint64_t cap = 4ull * (uint64_t)cus;
+  // Items of <= 1 MiB: four workgroups per CU (two resident at a time, by LDS) walk
+  // them, which trims the launch tail (measured best on MI355X). Larger blocks
+  // already amortise per-item setup and balance better with one workgroup per item.
+  const uint64_t cap = lpb_log2 <= 8 ? 4ull * (uint64_t)cus : items;
   const uint64_t grid = items < cap ? items : cap;
+  if (grid > 0x7fffffffull) {
+    set_error("gleam_fp_chunks: batch needs more than 2^31 workgroups");
+    return GLEAM_E_UNSUPPORTED;
+  }
   FpArgs a{b->seg_addr, b->seg_len, b->blk_first, b->n_seg, b->n_blocks, d_block_digest, d_leaf_digest,
            (uint32_t)lpb_log2, items};
   hipLaunchKernelGGL(fp_kernel, dim3((uint32_t)grid), dim3(kWG), 0, (hipStream_t)stream, a);
