@@ -110,6 +110,9 @@ def build_decoder7b(g, torch, threads):
     table.insert(base_digests, torch.arange(base_batch.n_blocks, dtype=torch.int64, device="cuda"))
     torch.cuda.synchronize()
     del d_side, base_batch, side
+    global RECORDED
+    RECORDED = (base_digests, np.array([0] + [1 + 9 * l for l in range(33)] + [len(lens)], np.uint64),
+                [dec.base(i) for i in dec.perturbed], list(dec.perturbed))
     first = batch.host_first
     expect_miss = int(sum(int(first[i + 1] - first[i]) for i in dec.perturbed))
     payloads = [arena[int(o):int(o) + int(n)] for o, n in zip(offs, lens)]
@@ -182,6 +185,54 @@ def build_large_bf16(g, torch, threads):
     return batch, table, payloads, batch.n_blocks - chosen.size, desc, d_arena
 
 
+RECORDED = None  # (recorded block digests, allocation boundaries, base tensors, their indices)
+
+
+def identify_path(args, g, torch, threads, batch, payloads, keep):
+    """Free-time weight identification over the 7B decoder: the digests recorded when the
+    base weights were written vs. the device bytes now (3 layers updated in place)."""
+    recorded, region_first, base_tensors, base_idx = RECORDED
+    n_regions = region_first.size - 1
+    rf = torch.from_numpy(region_first.view(np.int64)).to("cuda")
+    ws = g.workspace(batch.n_blocks + batch.n_seg)
+    for _ in range(args.warmup):
+        m, f, w = g.identify_weights(batch, recorded, rf, ws=ws)
+    torch.cuda.synchronize()
+    weights = int(w.sum().item())
+    if weights != n_regions - 3:
+        raise SystemExit(f"identification truth violated: {weights} weight allocations of {n_regions}")
+    K = args.steps
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(K):
+        g.identify_weights(batch, recorded, rf, ws=ws)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / K
+    payload_bytes = int(batch.host_len.sum())
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        rec = g.as_u64(recorded)
+        current = [p for p in payloads]
+        t0 = time.perf_counter()
+        oracle.identify_weights(rec, current, batch.block_bytes, region_first, threads=threads)
+        dt = time.perf_counter() - t0
+        cpu = {"value": round(payload_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+               "sample": f"whole workload ({payload_bytes} bytes), one run {dt:.3f} s, {cpu_model()}"}
+    out = {"metric": "payload GB/s for free-time weight identification (digest + compare), 1 MI355X",
+           "value": round(payload_bytes / (ms * 1e-3) / 1e9, 2), "unit": "GB/s", "n_gpus": 1, "steps": K,
+           "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+           "config": {"workload": "7B decoder fp16 weights as 34 allocations (embedding, 32 layers, head); "
+                                  "3 layers updated in place after the write; 1 MiB blocks",
+                      "payload_bytes": payload_bytes, "blocks": batch.n_blocks, "allocations": n_regions,
+                      "weight_allocations": weights,
+                      "pct_of_hbm_peak": round(100 * payload_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 2)},
+           "cpu_baseline": cpu}
+    print(json.dumps(out), flush=True)
+
+
 WORKLOADS = {"decoder7b": build_decoder7b, "random16": build_random16, "small_copies": build_small_copies,
              "resnet50": build_resnet50, "large_bf16": build_large_bf16}
 
@@ -226,6 +277,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-gb", type=float, default=20.0)
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--path", default="detect", choices=["detect", "identify"],
+                    help="detect: fingerprint+lookup+compact (default); identify: free-time weight identification")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -245,6 +298,12 @@ def main():
         return
 
     threads = host_threads()
+    if args.path == "identify":
+        if args.workload != "decoder7b":
+            raise SystemExit("--path identify runs on the decoder7b workload")
+        batch, table, payloads, expect_miss, desc, keep = build_decoder7b(g, torch, threads)
+        identify_path(args, g, torch, threads, batch, payloads, keep)
+        return
     batch, table, payloads, expect_miss, desc, keep = WORKLOADS[args.workload](g, torch, threads)
     n = batch.n_blocks
     payload_bytes = int(batch.host_len.sum())

@@ -16,6 +16,8 @@
  *                          repeated inside the batch
  *   gleam_miss_compact  -- list the blocks whose bytes must still travel
  *   gleam_cache_insert  -- add identifiers to the table
+ *   gleam_identify_weights -- at free time, decide which allocations still hold
+ *                          exactly what was written to them (Sec. 4.1.1)
  *
  * Conventions for every entry point:
  *   - C ABI; no exception crosses it; functions are thread-compatible (distinct
@@ -195,6 +197,32 @@ gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t* d_keys, ui
 gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam_batch* b, uint64_t* d_miss_idx,
                                 uint64_t* d_miss_count, uint64_t* d_miss_bytes, void* d_ws, size_t ws_bytes,
                                 void* stream);
+
+/*
+ * Weight identification at free time (Sec. 4.1.1 "Weight Block Identification"): an
+ * allocation holds weights only if every payload recorded at its first host-to-device
+ * write still has the same bytes when the allocation is freed (in-place activations or
+ * inputs disqualify it; Appendix, corner cases of weight identification). The digests
+ * recorded at write time (gleam_fp_chunks on the payloads as written) are compared with
+ * digests of the current device bytes.
+ *   b                  the recorded payloads at their device addresses, lengths as recorded
+ *   d_recorded         device u64[b->n_blocks]: block digests recorded at write time
+ *   d_region_first     device u64[n_regions+1]: payloads of allocation r are
+ *                      [region_first[r], region_first[r+1]); non-decreasing, starting at 0
+ *                      and ending at b->n_seg (payloads outside it are ignored)
+ *   d_block_match      nullable device u8[n_blocks]: 1 where the block is unchanged
+ *   d_seg_first_diff   nullable device u64[n_seg]: index, within its payload, of the first
+ *                      changed block; UINT64_MAX if none
+ *   d_region_weight    device u8[n_regions]: 1 iff the allocation has at least one recorded
+ *                      payload and none of them changed
+ *   d_ws, ws_bytes     device workspace, 256-byte aligned,
+ *                      >= gleam_workspace_bytes(n_blocks + n_seg)
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED, GLEAM_E_HIP.
+ */
+gleam_status gleam_identify_weights(const gleam_batch* b, const uint64_t* d_recorded,
+                                    const uint64_t* d_region_first, uint64_t n_regions,
+                                    uint8_t* d_block_match, uint64_t* d_seg_first_diff,
+                                    uint8_t* d_region_weight, void* d_ws, size_t ws_bytes, void* stream);
 
 /* Static text for a status code. */
 const char* gleam_status_string(gleam_status s);

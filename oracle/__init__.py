@@ -281,3 +281,43 @@ def run(payloads, block_bytes: int, table: Table, threads: int = 1):
     miss_idx, miss_count, miss_bytes = compact(status, blk_len)
     return {"digests": digests, "status": status, "ref": ref, "miss_idx": miss_idx,
             "miss_count": miss_count, "miss_bytes": miss_bytes}
+
+
+# --------------------------------------------------------------------------- #
+# Weight identification at free time (Sec. 4.1.1)
+# --------------------------------------------------------------------------- #
+NO_DIFF = 2**64 - 1
+
+
+def identify_weights(recorded_digests, current_payloads, block_bytes: int, region_first, threads: int = 1):
+    """Sec. 4.1.1: an allocation ("block" in the paper) holds weights only if every
+    payload recorded at its first host-to-device write still has the same bytes when
+    the allocation is freed. The recorded payloads are compared block by block through
+    their digests: recorded at write time vs. computed now from the current bytes.
+
+    recorded_digests : u64[n_blocks] block digests of the payloads as written
+    current_payloads : the same payloads' current bytes (same lengths)
+    region_first     : u64[R+1]; payloads of allocation r are [region_first[r], region_first[r+1])
+
+    Returns (block_match u8[n_blocks], first_diff u64[S] = index within the payload of
+    its first differing block or 2^64-1, region_weight u8[R]); an allocation with no
+    recorded payload is not identified as weights.
+    """
+    rec = np.asarray(recorded_digests, dtype=np.uint64).reshape(-1)
+    cur, _ = batch_digests(current_payloads, block_bytes, threads=threads)
+    if cur.size != rec.size:
+        raise ValueError("recorded digests do not match the payloads' geometry")
+    block_match = (cur == rec).astype(np.uint8)
+    lens = [_as_u8(p).size for p in current_payloads]
+    blk_first, _ = geometry(lens, block_bytes)
+    first_diff = np.full(len(lens), NO_DIFF, dtype=np.uint64)
+    for s in range(len(lens)):
+        bad = np.flatnonzero(block_match[int(blk_first[s]):int(blk_first[s + 1])] == 0)
+        if bad.size:
+            first_diff[s] = bad[0]
+    rf = np.asarray(region_first, dtype=np.uint64).reshape(-1)
+    region_weight = np.zeros(rf.size - 1, dtype=np.uint8)
+    for r in range(rf.size - 1):
+        segs = first_diff[int(rf[r]):int(rf[r + 1])]
+        region_weight[r] = 1 if segs.size and (segs == NO_DIFF).all() else 0
+    return block_match, first_diff, region_weight

@@ -30,7 +30,7 @@ LEAF_BYTES = 4096
 EXPORTS = (
     "gleam_batch_geometry", "gleam_fp_chunks", "gleam_cache_bytes", "gleam_cache_create", "gleam_cache_destroy",
     "gleam_cache_key_bound", "gleam_workspace_bytes", "gleam_cache_insert", "gleam_cache_lookup",
-    "gleam_miss_compact", "gleam_status_string", "gleam_last_error",
+    "gleam_miss_compact", "gleam_status_string", "gleam_last_error", "gleam_identify_weights",
 )
 
 
@@ -63,6 +63,7 @@ def _load() -> ctypes.CDLL:
         "gleam_cache_insert": ([vp, vp, vp, u64, vp, vp, sz, vp], st),
         "gleam_cache_lookup": ([vp, vp, u64, vp, vp, vp, sz, vp], st),
         "gleam_miss_compact": ([vp, u64, ctypes.POINTER(_Batch), vp, vp, vp, vp, sz, vp], st),
+        "gleam_identify_weights": ([ctypes.POINTER(_Batch), vp, vp, u64, vp, vp, vp, vp, sz, vp], st),
         "gleam_status_string": ([st], ctypes.c_char_p),
         "gleam_last_error": ([], ctypes.c_char_p),
     }
@@ -253,6 +254,25 @@ def miss_compact(status: torch.Tensor, batch: Batch | None = None, miss_idx: tor
     _check(lib.gleam_miss_compact(_ptr(status), n, cb, _ptr(miss_idx), _ptr(counters), bytes_ptr, _ptr(ws),
                                   ws.numel(), _stream(stream)))
     return miss_idx, counters
+
+
+def identify_weights(batch: Batch, recorded: torch.Tensor, region_first, ws: torch.Tensor | None = None,
+                     stream=None):
+    """Free-time weight identification: (block_match u8[n_blocks], first_diff int64[n_seg],
+    region_weight u8[n_regions]) on the device. `recorded` holds the block digests taken
+    when the payloads were written; `region_first` the allocation boundaries over payloads."""
+    dev = batch.d_first.device
+    rf = region_first if isinstance(region_first, torch.Tensor) else _u64_device(np.asarray(region_first), dev)
+    n_regions = rf.numel() - 1
+    block_match = torch.empty(max(batch.n_blocks, 1), dtype=torch.uint8, device=dev)
+    first_diff = torch.empty(max(batch.n_seg, 1), dtype=torch.int64, device=dev)
+    region_weight = torch.empty(max(n_regions, 1), dtype=torch.uint8, device=dev)
+    if ws is None:
+        ws = workspace(batch.n_blocks + batch.n_seg, dev)
+    _check(lib.gleam_identify_weights(ctypes.byref(batch.c_struct()), _ptr(recorded), _ptr(rf), n_regions,
+                                      _ptr(block_match), _ptr(first_diff), _ptr(region_weight), _ptr(ws),
+                                      ws.numel(), _stream(stream)))
+    return block_match[:batch.n_blocks], first_diff[:batch.n_seg], region_weight[:n_regions]
 
 
 def as_u64(t: torch.Tensor) -> np.ndarray:

@@ -341,29 +341,32 @@ __global__ __launch_bounds__(kWG) void fp_kernel(FpArgs a) {
 }  // namespace
 }  // namespace gleam
 
-extern "C" gleam_status gleam_fp_chunks(const gleam_batch* b, uint64_t* d_block_digest, uint64_t* d_leaf_digest,
-                                        void* stream) {
-  using namespace gleam;
-  clear_error();
+namespace gleam {
+
+gleam_status validate_batch(const gleam_batch* b, const char* who) {
   if (!b) {
-    set_error("gleam_fp_chunks: null batch");
+    set_error("%s: null batch", who);
     return GLEAM_E_INVALID;
   }
   if (b->leaf_bytes != GLEAM_LEAF_BYTES || !valid_block_bytes(b->block_bytes)) {
-    set_error("gleam_fp_chunks: leaf_bytes must be 4096 and block_bytes 4096 << k (k <= 12)");
+    set_error("%s: leaf_bytes must be 4096 and block_bytes 4096 << k (k <= 12)", who);
     return GLEAM_E_INVALID;
   }
-  if (b->n_blocks == 0) return GLEAM_OK;
-  if (b->n_seg == 0 || !b->seg_addr || !b->seg_len || !b->blk_first || !d_block_digest) {
-    set_error("gleam_fp_chunks: null descriptor or output for a non-empty batch");
+  if (b->n_blocks > 0 && (b->n_seg == 0 || !b->seg_addr || !b->seg_len || !b->blk_first)) {
+    set_error("%s: null descriptor for a non-empty batch", who);
     return GLEAM_E_INVALID;
   }
-  const int lpb_log2 = log2_exact(b->block_bytes) - 12;
-  const uint64_t lpb = 1ull << lpb_log2;
   if (b->n_blocks > (UINT64_MAX >> 13)) {
-    set_error("gleam_fp_chunks: batch too large");
+    set_error("%s: batch too large", who);
     return GLEAM_E_UNSUPPORTED;
   }
+  return GLEAM_OK;
+}
+
+gleam_status launch_fp(const gleam_batch* b, uint64_t* d_block_digest, uint64_t* d_leaf_digest, hipStream_t stream) {
+  if (b->n_blocks == 0) return GLEAM_OK;
+  const int lpb_log2 = log2_exact(b->block_bytes) - 12;
+  const uint64_t lpb = 1ull << lpb_log2;
   const uint64_t items = lpb_log2 <= 8 ? (b->n_blocks * lpb + kWG - 1) / kWG : b->n_blocks;
   int cus = 0;
   gleam_status st = device_cu_count(&cus);
@@ -374,11 +377,27 @@ extern "C" gleam_status gleam_fp_chunks(const gleam_batch* b, uint64_t* d_block_
   const uint64_t cap = lpb_log2 <= 8 ? 4ull * (uint64_t)cus : items;
   const uint64_t grid = items < cap ? items : cap;
   if (grid > 0x7fffffffull) {
-    set_error("gleam_fp_chunks: batch needs more than 2^31 workgroups");
+    set_error("fingerprint: batch needs more than 2^31 workgroups");
     return GLEAM_E_UNSUPPORTED;
   }
   FpArgs a{b->seg_addr, b->seg_len, b->blk_first, b->n_seg, b->n_blocks, d_block_digest, d_leaf_digest,
            (uint32_t)lpb_log2, items};
-  hipLaunchKernelGGL(fp_kernel, dim3((uint32_t)grid), dim3(kWG), 0, (hipStream_t)stream, a);
+  hipLaunchKernelGGL(fp_kernel, dim3((uint32_t)grid), dim3(kWG), 0, stream, a);
   return launch_status("fp_kernel");
+}
+
+}  // namespace gleam
+
+extern "C" gleam_status gleam_fp_chunks(const gleam_batch* b, uint64_t* d_block_digest, uint64_t* d_leaf_digest,
+                                        void* stream) {
+  using namespace gleam;
+  clear_error();
+  gleam_status st = validate_batch(b, "gleam_fp_chunks");
+  if (st != GLEAM_OK) return st;
+  if (b->n_blocks == 0) return GLEAM_OK;
+  if (!d_block_digest) {
+    set_error("gleam_fp_chunks: null output for a non-empty batch");
+    return GLEAM_E_INVALID;
+  }
+  return launch_fp(b, d_block_digest, d_leaf_digest, (hipStream_t)stream);
 }

@@ -42,6 +42,11 @@ int log2_exact(uint64_t x);                    // -1 unless x is a power of two
 bool aligned256(const void* p);
 gleam_status device_cu_count(int* cus);        // compute units of the current device (cached)
 
+// Batch checks shared by the entry points that take a batch (nothing enqueued on error).
+gleam_status validate_batch(const gleam_batch* b, const char* who);
+// Block digests of a validated batch (the fingerprint kernel launch).
+gleam_status launch_fp(const gleam_batch* b, uint64_t* d_block_digest, uint64_t* d_leaf_digest, hipStream_t stream);
+
 // Fill n u64 words with value on stream (a kernel, so it can live in a captured graph).
 gleam_status fill_u64(uint64_t* p, uint64_t n, uint64_t value, hipStream_t stream);
 

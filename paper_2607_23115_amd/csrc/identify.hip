@@ -1,0 +1,95 @@
+// gleam_identify_weights: weight identification at free time (Gleam Sec. 4.1.1,
+// "Weight Block Identification"). An allocation holds weights only if every payload
+// recorded at its first host-to-device write still has the same bytes when the
+// allocation is freed; in-place activations or inputs make it non-weights (Appendix,
+// discussion of corner cases). Instead of the recorded bytes, the digests recorded
+// at write time are compared with digests of the current device bytes: the same
+// fingerprint kernel, then a compare pass and two small reductions.
+
+#include "gleam_device.h"
+#include "gleam_internal.h"
+
+namespace gleam {
+namespace {
+
+constexpr int kThreads = 256;
+
+__global__ void identify_init_kernel(uint64_t* first_diff, uint64_t n_seg, const uint64_t* region_first,
+                                     uint64_t n_regions, uint8_t* region_weight) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (uint64_t s = t; s < n_seg; s += stride) first_diff[s] = ~0ull;
+  for (uint64_t r = t; r < n_regions; r += stride) region_weight[r] = region_first[r + 1] > region_first[r] ? 1 : 0;
+}
+
+// Per block: equal digests? The first differing block of each payload by atomicMin.
+__global__ void identify_compare_kernel(const uint64_t* current, const uint64_t* recorded, uint64_t n_blocks,
+                                        const uint64_t* blk_first, uint64_t n_seg, uint8_t* block_match,
+                                        uint64_t* first_diff) {
+  const uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= n_blocks) return;
+  const bool same = current[g] == recorded[g];
+  if (block_match) block_match[g] = same ? 1 : 0;
+  if (!same) {
+    const uint64_t s = find_segment(blk_first, n_seg, g);
+    atomicMin(reinterpret_cast<unsigned long long*>(&first_diff[s]), (unsigned long long)(g - blk_first[s]));
+  }
+}
+
+// Per payload: a difference clears its allocation's weight flag.
+__global__ void identify_region_kernel(const uint64_t* first_diff, uint64_t n_seg, const uint64_t* region_first,
+                                       uint64_t n_regions, uint8_t* region_weight) {
+  const uint64_t s = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= n_seg || first_diff[s] == ~0ull) return;
+  if (s < region_first[0] || s >= region_first[n_regions]) return;
+  const uint64_t r = find_segment(region_first, n_regions, s);
+  region_weight[r] = 0;
+}
+
+uint32_t grid_for(uint64_t n, uint64_t cap = 0x7fffffffull) {
+  const uint64_t g = (n + kThreads - 1) / kThreads;
+  return (uint32_t)(g < cap ? (g ? g : 1) : cap);
+}
+
+}  // namespace
+}  // namespace gleam
+
+extern "C" gleam_status gleam_identify_weights(const gleam_batch* b, const uint64_t* d_recorded,
+                                               const uint64_t* d_region_first, uint64_t n_regions,
+                                               uint8_t* d_block_match, uint64_t* d_seg_first_diff,
+                                               uint8_t* d_region_weight, void* d_ws, size_t ws_bytes, void* stream) {
+  using namespace gleam;
+  clear_error();
+  gleam_status st = validate_batch(b, "gleam_identify_weights");
+  if (st != GLEAM_OK) return st;
+  if ((b->n_blocks > 0 && !d_recorded) || (n_regions > 0 && (!d_region_first || !d_region_weight))) {
+    set_error("gleam_identify_weights: null recorded digests, region list or output");
+    return GLEAM_E_INVALID;
+  }
+  if (b->n_seg > (UINT64_MAX >> 8) || n_regions > (UINT64_MAX >> 8)) return GLEAM_E_UNSUPPORTED;
+  const WsLayout L = ws_layout(b->n_blocks + b->n_seg);
+  if (!d_ws || !aligned256(d_ws)) {
+    set_error("gleam_identify_weights: workspace must be non-null and 256-byte aligned");
+    return GLEAM_E_INVALID;
+  }
+  if (ws_bytes < L.total) {
+    set_error("gleam_identify_weights: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
+    return GLEAM_E_WORKSPACE;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  uint64_t* current = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(d_ws) + L.scratch_off);
+  uint64_t* first_diff = d_seg_first_diff ? d_seg_first_diff : current + b->n_blocks;
+  const uint64_t init_n = b->n_seg > n_regions ? b->n_seg : n_regions;
+  hipLaunchKernelGGL(identify_init_kernel, dim3(grid_for(init_n, 4096)), dim3(kThreads), 0, s, first_diff, b->n_seg,
+                     d_region_first, n_regions, d_region_weight);
+  if ((st = launch_status("identify_init_kernel")) != GLEAM_OK) return st;
+  if (b->n_blocks == 0) return GLEAM_OK;
+  if ((st = launch_fp(b, current, nullptr, s)) != GLEAM_OK) return st;
+  hipLaunchKernelGGL(identify_compare_kernel, dim3(grid_for(b->n_blocks)), dim3(kThreads), 0, s, current,
+                     d_recorded, b->n_blocks, b->blk_first, b->n_seg, d_block_match, first_diff);
+  if ((st = launch_status("identify_compare_kernel")) != GLEAM_OK) return st;
+  if (n_regions == 0) return GLEAM_OK;
+  hipLaunchKernelGGL(identify_region_kernel, dim3(grid_for(b->n_seg)), dim3(kThreads), 0, s, first_diff, b->n_seg,
+                     d_region_first, n_regions, d_region_weight);
+  return launch_status("identify_region_kernel");
+}

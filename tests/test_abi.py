@@ -84,6 +84,17 @@ def test_fp_chunks_validation():
     assert _call_fp(_batch(n_seg=0, n_blocks=0), out=None) == g.OK
 
 
+def test_identify_validation():
+    f = g.lib.gleam_identify_weights
+    assert f(None, 256, 256, 1, None, None, 256, 256, 1 << 20, None) == g.E_INVALID
+    b = _batch()
+    assert f(ctypes.byref(b), None, 256, 1, None, None, 256, 256, 1 << 20, None) == g.E_INVALID
+    assert f(ctypes.byref(b), 256, None, 1, None, None, 256, 256, 1 << 20, None) == g.E_INVALID
+    assert f(ctypes.byref(b), 256, 256, 1, None, None, None, 256, 1 << 20, None) == g.E_INVALID
+    assert f(ctypes.byref(b), 256, 256, 1, None, None, 256, 300, 1 << 20, None) == g.E_INVALID
+    assert f(ctypes.byref(b), 256, 256, 1, None, None, 256, 256, 64, None) == g.E_WORKSPACE
+
+
 def test_cache_create_validation():
     h = ctypes.c_void_p()
     assert g.lib.gleam_cache_create(256, 1 << 20, 100, 0.5, ctypes.byref(h), None) == g.E_INVALID  # not pow2
