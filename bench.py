@@ -233,6 +233,39 @@ def identify_path(args, g, torch, threads, batch, payloads, keep):
     print(json.dumps(out), flush=True)
 
 
+def md5_path(args, g, torch, threads, batch, payloads, desc):
+    """The paper's identifier (MD5 of each payload's first 1024 bits) over a workload's
+    payloads: payloads per second; it reads at most 128 bytes of each."""
+    for _ in range(args.warmup):
+        g.md5_prefix(batch)
+    torch.cuda.synchronize()
+    K = args.steps
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(K):
+        g.md5_prefix(batch)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / K
+    read = int(np.minimum(batch.host_len, 128).sum())
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        t0 = time.perf_counter()
+        oracle.md5_prefix(payloads)
+        dt = time.perf_counter() - t0
+        cpu = {"value": round(len(payloads) / dt, 1), "unit": "payloads/s", "cores": 1, "kind": "oracle",
+               "sample": f"all {len(payloads)} payloads, one run {dt:.3f} s, {cpu_model()}"}
+    out = {"metric": "payloads/s for the MD5-of-first-1024-bits identifier, 1 MI355X",
+           "value": round(batch.n_seg / (ms * 1e-3), 1), "unit": "payloads/s", "n_gpus": 1, "steps": K,
+           "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "u32", "data": "synthetic",
+           "config": {"workload": desc, "payloads": batch.n_seg, "bytes_read": read,
+                      "payload_bytes": int(batch.host_len.sum())},
+           "cpu_baseline": cpu}
+    print(json.dumps(out), flush=True)
+
+
 WORKLOADS = {"decoder7b": build_decoder7b, "random16": build_random16, "small_copies": build_small_copies,
              "resnet50": build_resnet50, "large_bf16": build_large_bf16}
 
@@ -277,8 +310,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-gb", type=float, default=20.0)
     ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--path", default="detect", choices=["detect", "identify"],
-                    help="detect: fingerprint+lookup+compact (default); identify: free-time weight identification")
+    ap.add_argument("--path", default="detect", choices=["detect", "identify", "md5prefix"],
+                    help="detect: fingerprint+lookup+compact (default); identify: free-time weight "
+                         "identification; md5prefix: the paper's MD5-of-first-1024-bits identifier")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -305,6 +339,9 @@ def main():
         identify_path(args, g, torch, threads, batch, payloads, keep)
         return
     batch, table, payloads, expect_miss, desc, keep = WORKLOADS[args.workload](g, torch, threads)
+    if args.path == "md5prefix":
+        md5_path(args, g, torch, threads, batch, payloads, desc)
+        return
     n = batch.n_blocks
     payload_bytes = int(batch.host_len.sum())
     dev = "cuda"

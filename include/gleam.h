@@ -18,6 +18,8 @@
  *   gleam_cache_insert  -- add identifiers to the table
  *   gleam_identify_weights -- at free time, decide which allocations still hold
  *                          exactly what was written to them (Sec. 4.1.1)
+ *   gleam_md5_prefix    -- the paper's own identifier (MD5 of a payload's first
+ *                          1024 bits), as an ablation
  *
  * Conventions for every entry point:
  *   - C ABI; no exception crosses it; functions are thread-compatible (distinct
@@ -223,6 +225,25 @@ gleam_status gleam_identify_weights(const gleam_batch* b, const uint64_t* d_reco
                                     const uint64_t* d_region_first, uint64_t n_regions,
                                     uint8_t* d_block_match, uint64_t* d_seg_first_diff,
                                     uint8_t* d_region_weight, void* d_ws, size_t ws_bytes, void* stream);
+
+/*
+ * The paper's own identifier (Appendix, discussion of hash cost and collisions): an MD5
+ * (RFC 1321) of the first 1024 bits of each host-to-device chunk; chunks of at most 1024
+ * bytes get no cache entry. Kept as an ablation of the full-content block digests.
+ *   b             the payloads (only seg_addr, seg_len and n_seg are used; block_bytes
+ *                 must still be valid)
+ *   prefix_bytes  bytes hashed per payload: min(len, prefix_bytes); 128 in the paper;
+ *                 at most 1 MiB
+ *   min_len       payloads longer than this are eligible for a cache entry (1024)
+ *   d_digest      device u64[2 * n_seg]: the 16-byte MD5 of payload s at [2s, 2s+1]
+ *                 (byte order of the digest, little-endian words)
+ *   d_key         nullable device u64[n_seg]: the digest's first 8 bytes, usable as a
+ *                 gleam_cache key
+ *   d_eligible    nullable device u8[n_seg]: 1 iff seg_len[s] > min_len
+ * Errors: GLEAM_E_INVALID, GLEAM_E_UNSUPPORTED, GLEAM_E_HIP. n_seg == 0 is a no-op.
+ */
+gleam_status gleam_md5_prefix(const gleam_batch* b, uint32_t prefix_bytes, uint64_t min_len, uint64_t* d_digest,
+                              uint64_t* d_key, uint8_t* d_eligible, void* stream);
 
 /* Static text for a status code. */
 const char* gleam_status_string(gleam_status s);

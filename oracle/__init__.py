@@ -49,7 +49,7 @@ def build() -> str:
     """Compile gleam_oracle.c into liboracle.so next to it (plain gcc, no SIMD flags)."""
     tmp = _LIB_PATH + ".tmp"
     subprocess.check_call(["gcc", "-O2", "-std=c99", "-Wall", "-Wextra", "-shared", "-fPIC",
-                           _SRC, "-o", tmp])
+                           _SRC, "-o", tmp, "-lm"])
     os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
@@ -70,6 +70,8 @@ def _load():
     lib.oracle_tree.restype = u64
     lib.oracle_blocks.argtypes = [p, u64, u32, u32, u64, u64, p, p]
     lib.oracle_blocks.restype = ctypes.c_int
+    lib.oracle_md5.argtypes = [p, u64, p]
+    lib.oracle_md5.restype = None
     _lib = lib
     return lib
 
@@ -321,3 +323,29 @@ def identify_weights(recorded_digests, current_payloads, block_bytes: int, regio
         segs = first_diff[int(rf[r]):int(rf[r + 1])]
         region_weight[r] = 1 if segs.size and (segs == NO_DIFF).all() else 0
     return block_match, first_diff, region_weight
+
+
+# --------------------------------------------------------------------------- #
+# The paper's identifier: MD5 of a payload's first 1024 bits (Appendix discussion)
+# --------------------------------------------------------------------------- #
+def md5(data) -> bytes:
+    """MD5 (RFC 1321) of `data`."""
+    arr = _as_u8(data)
+    out = np.zeros(16, dtype=np.uint8)
+    _load().oracle_md5(arr.ctypes.data if arr.size else None, arr.size, out.ctypes.data)
+    return out.tobytes()
+
+
+def md5_prefix(payloads, prefix_bytes: int = 128, min_len: int = 1024):
+    """Per payload: MD5 of its first min(len, prefix_bytes) bytes (u8[S, 16]), the table
+    key = the digest's first 8 bytes as a little-endian u64, and whether the paper would
+    build a cache entry for it (only payloads longer than min_len bytes)."""
+    S = len(payloads)
+    digests = np.zeros((S, 16), dtype=np.uint8)
+    eligible = np.zeros(S, dtype=np.uint8)
+    for s, p in enumerate(payloads):
+        arr = _as_u8(p)
+        digests[s] = np.frombuffer(md5(arr[:prefix_bytes]), np.uint8)
+        eligible[s] = 1 if arr.size > min_len else 0
+    keys = digests[:, :8].copy().view("<u8").reshape(-1).astype(np.uint64)
+    return digests, keys, eligible

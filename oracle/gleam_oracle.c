@@ -23,7 +23,10 @@
  *
  * Nothing here is blocked, fused or reordered: one scalar pass per leaf, one
  * level of the tree at a time.
+ *
+ * It also holds MD5 (RFC 1321) for the paper's own identifier (see oracle_md5).
  */
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -174,4 +177,71 @@ int oracle_blocks(const uint8_t* payload, uint64_t len, uint32_t leaf_bytes, uin
   }
   free(work);
   return 0;
+}
+
+/*
+ * MD5 (RFC 1321), used for the paper's own identifier (Appendix, discussion of hash
+ * cost and collisions: an MD5 string of the first 1024 bits of each host-to-device
+ * chunk). Written from the RFC's description: the message is padded with one 1 bit,
+ * zeros to 56 mod 64 bytes and the 64-bit little-endian bit length; each 64-byte block
+ * runs four rounds of sixteen steps a = b + ((a + fn(b,c,d) + X[k] + T[i]) <<< s)
+ * over the state A, B, C, D. T[i] is the integer part of 2^32 * |sin(i)| (i in radians),
+ * computed here from that definition.
+ */
+
+static uint32_t md5_rotl(uint32_t x, unsigned s) { return (x << s) | (x >> (32u - s)); }
+
+static void md5_block(uint32_t state[4], const uint8_t block[64], const uint32_t T[65]) {
+  static const unsigned S[4][4] = {{7, 12, 17, 22}, {5, 9, 14, 20}, {4, 11, 16, 23}, {6, 10, 15, 21}};
+  uint32_t X[16];
+  for (int j = 0; j < 16; ++j) X[j] = read_le32(block + 4 * j);
+  uint32_t a = state[0], b = state[1], c = state[2], d = state[3];
+  for (int i = 0; i < 64; ++i) {
+    const int round = i / 16;
+    uint32_t f;
+    int k;
+    if (round == 0) {        /* F(X,Y,Z) = XY v not(X) Z */
+      f = (b & c) | (~b & d);
+      k = i;
+    } else if (round == 1) { /* G(X,Y,Z) = XZ v Y not(Z) */
+      f = (b & d) | (c & ~d);
+      k = (5 * i + 1) % 16;
+    } else if (round == 2) { /* H(X,Y,Z) = X xor Y xor Z */
+      f = b ^ c ^ d;
+      k = (3 * i + 5) % 16;
+    } else {                 /* I(X,Y,Z) = Y xor (X v not(Z)) */
+      f = c ^ (b | ~d);
+      k = (7 * i) % 16;
+    }
+    const uint32_t t = a + f + X[k] + T[i + 1];
+    a = d;
+    d = c;
+    c = b;
+    b = b + md5_rotl(t, S[round][i % 4]);
+  }
+  state[0] += a;
+  state[1] += b;
+  state[2] += c;
+  state[3] += d;
+}
+
+/* MD5 of p[0..len); out receives the 16-byte digest (A, B, C, D little-endian). */
+void oracle_md5(const uint8_t* p, uint64_t len, uint8_t out[16]) {
+  uint32_t T[65];
+  for (int i = 1; i <= 64; ++i) T[i] = (uint32_t)floor(4294967296.0 * fabs(sin((double)i)));
+  uint32_t state[4] = {0x67452301u, 0xefcdab89u, 0x98badcfeu, 0x10325476u};
+  uint64_t pos = 0;
+  for (; pos + 64 <= len; pos += 64) md5_block(state, p + pos, T);
+  uint8_t tail[128];
+  const uint64_t rem = len - pos;
+  memset(tail, 0, sizeof tail);
+  if (rem) memcpy(tail, p + pos, rem);
+  tail[rem] = 0x80;
+  const uint64_t tail_len = rem + 1 + 8 <= 64 ? 64 : 128;
+  const uint64_t bits = len * 8;
+  for (int i = 0; i < 8; ++i) tail[tail_len - 8 + i] = (uint8_t)(bits >> (8 * i));
+  md5_block(state, tail, T);
+  if (tail_len == 128) md5_block(state, tail + 64, T);
+  for (int w = 0; w < 4; ++w)
+    for (int i = 0; i < 4; ++i) out[4 * w + i] = (uint8_t)(state[w] >> (8 * i));
 }

@@ -31,6 +31,7 @@ EXPORTS = (
     "gleam_batch_geometry", "gleam_fp_chunks", "gleam_cache_bytes", "gleam_cache_create", "gleam_cache_destroy",
     "gleam_cache_key_bound", "gleam_workspace_bytes", "gleam_cache_insert", "gleam_cache_lookup",
     "gleam_miss_compact", "gleam_status_string", "gleam_last_error", "gleam_identify_weights",
+    "gleam_md5_prefix",
 )
 
 
@@ -64,6 +65,7 @@ def _load() -> ctypes.CDLL:
         "gleam_cache_lookup": ([vp, vp, u64, vp, vp, vp, sz, vp], st),
         "gleam_miss_compact": ([vp, u64, ctypes.POINTER(_Batch), vp, vp, vp, vp, sz, vp], st),
         "gleam_identify_weights": ([ctypes.POINTER(_Batch), vp, vp, u64, vp, vp, vp, vp, sz, vp], st),
+        "gleam_md5_prefix": ([ctypes.POINTER(_Batch), u32, u64, vp, vp, vp, vp], st),
         "gleam_status_string": ([st], ctypes.c_char_p),
         "gleam_last_error": ([], ctypes.c_char_p),
     }
@@ -273,6 +275,19 @@ def identify_weights(batch: Batch, recorded: torch.Tensor, region_first, ws: tor
                                       _ptr(block_match), _ptr(first_diff), _ptr(region_weight), _ptr(ws),
                                       ws.numel(), _stream(stream)))
     return block_match[:batch.n_blocks], first_diff[:batch.n_seg], region_weight[:n_regions]
+
+
+def md5_prefix(batch: Batch, prefix_bytes: int = 128, min_len: int = 1024, stream=None):
+    """The paper's identifier per payload: (digest int64[S, 2], key int64[S], eligible u8[S])."""
+    dev = batch.d_first.device
+    S = max(batch.n_seg, 1)
+    digest = torch.empty(2 * S, dtype=torch.int64, device=dev)
+    key = torch.empty(S, dtype=torch.int64, device=dev)
+    eligible = torch.empty(S, dtype=torch.uint8, device=dev)
+    _check(lib.gleam_md5_prefix(ctypes.byref(batch.c_struct()), prefix_bytes, min_len, _ptr(digest), _ptr(key),
+                                _ptr(eligible), _stream(stream)))
+    n = batch.n_seg
+    return digest[:2 * n].view(n, 2), key[:n], eligible[:n]
 
 
 def as_u64(t: torch.Tensor) -> np.ndarray:

@@ -95,6 +95,15 @@ def test_identify_validation():
     assert f(ctypes.byref(b), 256, 256, 1, None, None, 256, 256, 64, None) == g.E_WORKSPACE
 
 
+def test_md5_prefix_validation():
+    f = g.lib.gleam_md5_prefix
+    b = _batch()
+    assert f(None, 128, 1024, 256, None, None, None) == g.E_INVALID
+    assert f(ctypes.byref(b), (1 << 20) + 1, 1024, 256, None, None, None) == g.E_INVALID
+    assert f(ctypes.byref(b), 128, 1024, None, None, None, None) == g.E_INVALID
+    assert f(ctypes.byref(_batch(n_seg=0, n_blocks=0)), 128, 1024, None, None, None, None) == g.OK
+
+
 def test_cache_create_validation():
     h = ctypes.c_void_p()
     assert g.lib.gleam_cache_create(256, 1 << 20, 100, 0.5, ctypes.byref(h), None) == g.E_INVALID  # not pow2
