@@ -266,6 +266,73 @@ def md5_path(args, g, torch, threads, batch, payloads, desc):
     print(json.dumps(out), flush=True)
 
 
+def lifecycle_path(args, g, torch):
+    """LRU eviction and export of a 20M-entry table (2^25 slots, the 40 GB workload's
+    table size): each step restores the table (untimed), then times evict-to-half and,
+    separately, export."""
+    import workloads as W
+    n, cap = 20_000_000, 1 << 25
+    keys = torch.from_numpy(W.LargeSet().random_digests(n).view(np.int64)).to("cuda")
+    vals = torch.arange(n, dtype=torch.int64, device="cuda")
+    epochs = torch.randint(0, 1 << 20, (n,), dtype=torch.int64, device="cuda",
+                           generator=torch.Generator(device="cuda").manual_seed(5))
+    table = g.Cache(cap, max_load=0.65)
+    ws = table.maint_workspace()
+    ins_ws = g.workspace(n)
+
+    def restore():
+        g.lib.gleam_cache_destroy(table._h)
+        h = g.ctypes.c_void_p()
+        g._check(g.lib.gleam_cache_create(g._ptr(table.storage), table.storage.numel(), cap, 0.65,
+                                          g.ctypes.byref(h), g._stream(None)))
+        table._h = h
+        table.insert(keys, vals, ws=ins_ws)
+        table.touch(keys, epochs=epochs)
+        torch.cuda.synchronize()
+
+    ev_ms, ex_ms = [], []
+    for step in range(args.warmup + args.steps):
+        restore()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        table.export(ws=ws)
+        b.record()
+        torch.cuda.synchronize()
+        c, d = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c.record()
+        _, counts = table.evict(n // 2, ws=ws)
+        d.record()
+        torch.cuda.synchronize()
+        if step >= args.warmup:
+            ex_ms.append(a.elapsed_time(b))
+            ev_ms.append(c.elapsed_time(d))
+    cnt = g.as_u64(counts)
+    if int(cnt[0]) != n - n // 2 or int(cnt[1]) != n // 2:
+        raise SystemExit(f"eviction counts wrong: {cnt}")
+    ev, ex = float(np.median(ev_ms)), float(np.median(ex_ms))
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        ot = oracle.Table()
+        hk, hv, he = g.as_u64(keys), np.arange(n, dtype=np.uint64), g.as_u64(epochs)
+        ot.insert(hk, hv)
+        ot.touch(hk, he)
+        t0 = time.perf_counter()
+        ot.evict(n // 2)
+        dt = time.perf_counter() - t0
+        cpu = {"value": round(n / dt / 1e6, 2), "unit": "M entries/s", "cores": 1, "kind": "oracle",
+               "sample": f"evict {n - n // 2} of {n} entries, one run {dt:.2f} s, {cpu_model()}"}
+    out = {"metric": "M table entries/s for LRU eviction (evict half of a 20M-entry table), 1 MI355X",
+           "value": round(n / (ev * 1e-3) / 1e6, 1), "unit": "M entries/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(ev, 3), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+           "config": {"workload": "20M random digests in 2^25 slots, random stamps, keep the 10M most recent",
+                      "entries": n, "capacity": cap, "evict_ms": round(ev, 3), "export_ms": round(ex, 3),
+                      "export_M_entries_per_s": round(n / (ex * 1e-3) / 1e6, 1)},
+           "cpu_baseline": cpu}
+    print(json.dumps(out), flush=True)
+
+
 WORKLOADS = {"decoder7b": build_decoder7b, "random16": build_random16, "small_copies": build_small_copies,
              "resnet50": build_resnet50, "large_bf16": build_large_bf16}
 
@@ -310,7 +377,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-gb", type=float, default=20.0)
     ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--path", default="detect", choices=["detect", "identify", "md5prefix"],
+    ap.add_argument("--path", default="detect", choices=["detect", "identify", "md5prefix", "lifecycle"],
                     help="detect: fingerprint+lookup+compact (default); identify: free-time weight "
                          "identification; md5prefix: the paper's MD5-of-first-1024-bits identifier")
     args = ap.parse_args()
@@ -332,6 +399,9 @@ def main():
         return
 
     threads = host_threads()
+    if args.path == "lifecycle":
+        lifecycle_path(args, g, torch)
+        return
     if args.path == "identify":
         if args.workload != "decoder7b":
             raise SystemExit("--path identify runs on the decoder7b workload")

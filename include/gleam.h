@@ -16,6 +16,8 @@
  *                          repeated inside the batch
  *   gleam_miss_compact  -- list the blocks whose bytes must still travel
  *   gleam_cache_insert  -- add identifiers to the table
+ *   gleam_cache_touch / _evict / _erase / _export -- the table's lifecycle: last-use
+ *                          stamps, LRU eviction, removal, the identifier set (4.1.3)
  *   gleam_identify_weights -- at free time, decide which allocations still hold
  *                          exactly what was written to them (Sec. 4.1.1)
  *   gleam_md5_prefix    -- the paper's own identifier (MD5 of a payload's first
@@ -129,8 +131,9 @@ gleam_status gleam_batch_geometry(const uint64_t* host_seg_len, uint64_t n_seg, 
 gleam_status gleam_fp_chunks(const gleam_batch* b, uint64_t* d_block_digest, uint64_t* d_leaf_digest,
                              void* stream);
 
-/* Device bytes of table storage for `capacity` slots (a power of two >= 16);
- * 0 for an invalid capacity. */
+/* Device bytes of table storage for `capacity` slots (a power of two >= 16):
+ * 256 + 24 * capacity (key, value and last-use stamp per slot); 0 for an invalid
+ * capacity. */
 size_t gleam_cache_bytes(uint64_t capacity);
 
 /*
@@ -199,6 +202,51 @@ gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t* d_keys, ui
 gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam_batch* b, uint64_t* d_miss_idx,
                                 uint64_t* d_miss_count, uint64_t* d_miss_bytes, void* d_ws, size_t ws_bytes,
                                 void* stream);
+
+/*
+ * Table lifecycle (Sec. 4.1.3: identified weight chunks stay in a shared cache across
+ * tasks and LRU eviction keeps it bounded; Sec. 4.1.2: at connect time the server sends
+ * the identifiers it holds). Every entry has a last-use stamp (0 when inserted). These
+ * calls must not overlap, on any stream, with other calls on the same table.
+ *
+ * gleam_cache_maint_bytes: device workspace bytes for evict, erase and export of this
+ * table (0 for NULL or a table above 2^31 slots).
+ *
+ * gleam_cache_touch: for every key present, stamp = max(stamp, epoch), the epoch being
+ * d_epochs[i] (device u64[n]) or, when d_epochs is NULL, the scalar `epoch`.
+ * d_n_touched (nullable device u64[1]) receives how many of the n keys were present.
+ *
+ * gleam_cache_evict: keep the `keep` most recently used entries. Entries are ordered by
+ * (stamp, key) ascending and the first live - keep of them are removed; d_evicted
+ * (nullable device u64[capacity + 1]) receives their keys in that order; d_counts
+ * (device u64[2]) receives {removed, live after}. The host key bound drops to `keep`.
+ *
+ * gleam_cache_erase: remove the given keys (device u64[n]) that are present; d_counts
+ * (device u64[2]) receives {removed, live after}. The host bound is unchanged; lower
+ * it with gleam_cache_set_key_bound once the live count has been read back.
+ *
+ * gleam_cache_export: every entry sorted by key into device u64[capacity + 1] arrays
+ * d_keys, d_vals and (nullable) d_stamps; *d_count (device u64[1]) = entries written.
+ * Re-inserting the exported pairs (and touching them with their stamps) rebuilds the
+ * table: the export is also its checkpoint.
+ *
+ * gleam_cache_set_key_bound: lower the host key bound to n (a live count read back
+ * from d_counts); raising it is refused.
+ *
+ * Workspace (evict, erase, export): device, 256-byte aligned,
+ * >= gleam_cache_maint_bytes(c). Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE,
+ * GLEAM_E_UNSUPPORTED, GLEAM_E_HIP.
+ */
+size_t gleam_cache_maint_bytes(const gleam_cache* c);
+gleam_status gleam_cache_touch(gleam_cache* c, const uint64_t* d_keys, uint64_t n, const uint64_t* d_epochs,
+                               uint64_t epoch, uint64_t* d_n_touched, void* stream);
+gleam_status gleam_cache_evict(gleam_cache* c, uint64_t keep, uint64_t* d_evicted, uint64_t* d_counts, void* d_ws,
+                               size_t ws_bytes, void* stream);
+gleam_status gleam_cache_erase(gleam_cache* c, const uint64_t* d_keys, uint64_t n, uint64_t* d_counts, void* d_ws,
+                               size_t ws_bytes, void* stream);
+gleam_status gleam_cache_export(const gleam_cache* c, uint64_t* d_keys, uint64_t* d_vals, uint64_t* d_stamps,
+                                uint64_t* d_count, void* d_ws, size_t ws_bytes, void* stream);
+gleam_status gleam_cache_set_key_bound(gleam_cache* c, uint64_t n);
 
 /*
  * Weight identification at free time (Sec. 4.1.1 "Weight Block Identification"): an

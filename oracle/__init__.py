@@ -188,17 +188,23 @@ def batch_digests(payloads, block_bytes: int, with_leaves: bool = False, threads
 # Table, lookup, compaction (numpy)
 # --------------------------------------------------------------------------- #
 class Table:
-    """The server's identifier set: a map from u64 digest to u64 value.
+    """The server's identifier set: a map from u64 digest to u64 value, with a last-use
+    stamp per entry for LRU eviction (Sec. 4.1.3).
 
-    Every u64 is a valid key (no reserved value).
+    Every u64 is a valid key (no reserved value). New entries get stamp 0.
     """
 
     def __init__(self):
         self.keys = np.zeros(0, dtype=np.uint64)   # sorted
         self.vals = np.zeros(0, dtype=np.uint64)
+        self.stamps = np.zeros(0, dtype=np.uint64)
 
     def __len__(self):
         return int(self.keys.size)
+
+    def _set(self, k, v, t):
+        order = np.argsort(k, kind="stable")
+        self.keys, self.vals, self.stamps = k[order], v[order], t[order]
 
     def insert(self, keys, vals) -> int:
         """Insert in batch order: a key already present keeps its value; among equal
@@ -212,10 +218,8 @@ class Table:
         uniq, first = np.unique(keys, return_index=True)       # first = lowest index per key
         new = ~self.contains(uniq)
         add_k, add_v = uniq[new], vals[first[new]]
-        k = np.concatenate([self.keys, add_k])
-        v = np.concatenate([self.vals, add_v])
-        order = np.argsort(k, kind="stable")
-        self.keys, self.vals = k[order], v[order]
+        self._set(np.concatenate([self.keys, add_k]), np.concatenate([self.vals, add_v]),
+                  np.concatenate([self.stamps, np.zeros(add_k.size, np.uint64)]))
         return int(add_k.size)
 
     def contains(self, keys) -> np.ndarray:
@@ -234,6 +238,42 @@ class Table:
         if present.any():
             out[present] = self.vals[np.searchsorted(self.keys, keys[present])]
         return present, out
+
+    # -- lifecycle (Sec. 4.1.3: LRU eviction keeps the cache bounded) --------------- #
+    def touch(self, keys, epochs) -> int:
+        """Stamp present keys with max(stamp, epoch). Returns how many keys (with
+        repetition) were present."""
+        keys = np.asarray(keys, dtype=np.uint64).reshape(-1)
+        epochs = np.broadcast_to(np.asarray(epochs, dtype=np.uint64), keys.shape)
+        present = self.contains(keys)
+        pos = np.searchsorted(self.keys, keys[present])
+        np.maximum.at(self.stamps, pos, epochs[present])
+        return int(present.sum())
+
+    def evict(self, keep: int) -> np.ndarray:
+        """Keep the `keep` most recently used entries: entries are ordered by (stamp, key)
+        ascending and the first len - keep are removed. Returns them in that order."""
+        n_evict = max(0, len(self) - int(keep))
+        order = np.lexsort((self.keys, self.stamps))   # primary: stamp, secondary: key
+        gone = order[:n_evict]
+        evicted = self.keys[gone].copy()
+        mask = np.ones(len(self), dtype=bool)
+        mask[gone] = False
+        self.keys, self.vals, self.stamps = self.keys[mask], self.vals[mask], self.stamps[mask]
+        return evicted
+
+    def erase(self, keys) -> int:
+        """Remove the given keys that are present. Returns how many entries went."""
+        keys = np.unique(np.asarray(keys, dtype=np.uint64).reshape(-1))
+        gone = self.contains(keys)
+        mask = ~np.isin(self.keys, keys[gone])
+        self.keys, self.vals, self.stamps = self.keys[mask], self.vals[mask], self.stamps[mask]
+        return int(gone.sum())
+
+    def export(self):
+        """(keys, vals, stamps) sorted by key: the identifier set a server ships at
+        connect time (Sec. 4.1.2), also a checkpoint of the table."""
+        return self.keys.copy(), self.vals.copy(), self.stamps.copy()
 
 
 def lookup(digests, table: Table):

@@ -31,7 +31,8 @@ EXPORTS = (
     "gleam_batch_geometry", "gleam_fp_chunks", "gleam_cache_bytes", "gleam_cache_create", "gleam_cache_destroy",
     "gleam_cache_key_bound", "gleam_workspace_bytes", "gleam_cache_insert", "gleam_cache_lookup",
     "gleam_miss_compact", "gleam_status_string", "gleam_last_error", "gleam_identify_weights",
-    "gleam_md5_prefix",
+    "gleam_md5_prefix", "gleam_cache_maint_bytes", "gleam_cache_touch", "gleam_cache_evict", "gleam_cache_erase",
+    "gleam_cache_export", "gleam_cache_set_key_bound",
 )
 
 
@@ -66,6 +67,12 @@ def _load() -> ctypes.CDLL:
         "gleam_miss_compact": ([vp, u64, ctypes.POINTER(_Batch), vp, vp, vp, vp, sz, vp], st),
         "gleam_identify_weights": ([ctypes.POINTER(_Batch), vp, vp, u64, vp, vp, vp, vp, sz, vp], st),
         "gleam_md5_prefix": ([ctypes.POINTER(_Batch), u32, u64, vp, vp, vp, vp], st),
+        "gleam_cache_maint_bytes": ([vp], sz),
+        "gleam_cache_touch": ([vp, vp, u64, vp, u64, vp, vp], st),
+        "gleam_cache_evict": ([vp, u64, vp, vp, vp, sz, vp], st),
+        "gleam_cache_erase": ([vp, vp, u64, vp, vp, sz, vp], st),
+        "gleam_cache_export": ([vp, vp, vp, vp, vp, vp, sz, vp], st),
+        "gleam_cache_set_key_bound": ([vp, u64], st),
         "gleam_status_string": ([st], ctypes.c_char_p),
         "gleam_last_error": ([], ctypes.c_char_p),
     }
@@ -224,6 +231,51 @@ class Cache:
         _check(lib.gleam_cache_lookup(self.handle, _ptr(keys), n, _ptr(status), _ptr(ref), _ptr(ws), ws.numel(),
                                       _stream(stream)))
         return status[:n], (ref[:n] if ref is not None else None)
+
+    # -- lifecycle ------------------------------------------------------------------ #
+    def maint_workspace(self) -> torch.Tensor:
+        n = int(lib.gleam_cache_maint_bytes(self.handle))
+        if n == 0:
+            raise GleamError(E_UNSUPPORTED, "no maintenance workspace for this table")
+        return torch.empty(n, dtype=torch.uint8, device=self.storage.device)
+
+    def touch(self, keys: torch.Tensor, epochs: torch.Tensor | None = None, epoch: int = 0, stream=None):
+        """Stamp present keys with max(stamp, epoch); returns the device count of present keys."""
+        n_touched = torch.empty(1, dtype=torch.int64, device=keys.device)
+        _check(lib.gleam_cache_touch(self.handle, _ptr(keys), keys.numel(), _ptr(epochs), epoch, _ptr(n_touched),
+                                     _stream(stream)))
+        return n_touched
+
+    def evict(self, keep: int, ws: torch.Tensor | None = None, stream=None):
+        """Keep the `keep` most recently used entries: (evicted keys [capacity+1], counts[2])."""
+        ws = self.maint_workspace() if ws is None else ws
+        evicted = torch.empty(self.capacity + 1, dtype=torch.int64, device=ws.device)
+        counts = torch.empty(2, dtype=torch.int64, device=ws.device)
+        _check(lib.gleam_cache_evict(self.handle, keep, _ptr(evicted), _ptr(counts), _ptr(ws), ws.numel(),
+                                     _stream(stream)))
+        return evicted, counts
+
+    def erase(self, keys: torch.Tensor, ws: torch.Tensor | None = None, stream=None):
+        ws = self.maint_workspace() if ws is None else ws
+        counts = torch.empty(2, dtype=torch.int64, device=ws.device)
+        _check(lib.gleam_cache_erase(self.handle, _ptr(keys), keys.numel(), _ptr(counts), _ptr(ws), ws.numel(),
+                                     _stream(stream)))
+        return counts
+
+    def export(self, ws: torch.Tensor | None = None, stream=None):
+        """(keys, vals, stamps, count) with the first count entries valid, sorted by key."""
+        ws = self.maint_workspace() if ws is None else ws
+        dev = ws.device
+        keys = torch.empty(self.capacity + 1, dtype=torch.int64, device=dev)
+        vals = torch.empty_like(keys)
+        stamps = torch.empty_like(keys)
+        count = torch.empty(1, dtype=torch.int64, device=dev)
+        _check(lib.gleam_cache_export(self.handle, _ptr(keys), _ptr(vals), _ptr(stamps), _ptr(count), _ptr(ws),
+                                      ws.numel(), _stream(stream)))
+        return keys, vals, stamps, count
+
+    def set_key_bound(self, n: int) -> None:
+        _check(lib.gleam_cache_set_key_bound(self.handle, n))
 
     def close(self) -> None:
         if self._h is not None:

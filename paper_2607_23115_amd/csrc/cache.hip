@@ -22,13 +22,6 @@ namespace {
 
 constexpr int kThreads = 256;
 
-struct TableRef {
-  uint64_t* hdr;    // [0] flag: key kEmpty present, [1] its value
-  uint64_t* slots;  // capacity x {key, value}
-  uint64_t mask;
-  int shift;
-};
-
 struct ScratchRef {
   uint64_t* hdr;    // [0] min index of key kEmpty, [1] new-key counter
   uint64_t* slots;  // cap x {key, min index}
@@ -150,15 +143,6 @@ __global__ void lookup_resolve_kernel(ScratchRef sc, const uint64_t* keys, uint6
   if (ref) ref[g] = g0;
 }
 
-TableRef table_ref(const gleam_cache* c) {
-  TableRef t;
-  t.hdr = reinterpret_cast<uint64_t*>(c->storage);
-  t.slots = reinterpret_cast<uint64_t*>(c->storage + kHeaderBytes);
-  t.mask = c->capacity - 1;
-  t.shift = c->shift;
-  return t;
-}
-
 ScratchRef scratch_ref(void* ws, const WsLayout& L) {
   ScratchRef s;
   s.hdr = reinterpret_cast<uint64_t*>(ws);
@@ -200,11 +184,19 @@ gleam_status fill_u64(uint64_t* p, uint64_t n, uint64_t value, hipStream_t strea
   return launch_status("fill_kernel");
 }
 
+gleam_status clear_table(const gleam_cache* c, hipStream_t stream) {
+  const TableRef t = table_ref(c);
+  gleam_status st = fill_u64(t.hdr, kHeaderBytes / 8, 0, stream);
+  if (st == GLEAM_OK) st = fill_u64(t.slots, 2 * c->capacity, kEmpty, stream);
+  if (st == GLEAM_OK) st = fill_u64(t.stamps, c->capacity, 0, stream);
+  return st;
+}
+
 }  // namespace gleam
 
 extern "C" size_t gleam_cache_bytes(uint64_t capacity) {
   if (capacity < 16 || gleam::log2_exact(capacity) < 0 || capacity > (1ull << 40)) return 0;
-  return gleam::kHeaderBytes + (size_t)capacity * 16;
+  return gleam::kHeaderBytes + (size_t)capacity * 24;
 }
 
 extern "C" gleam_status gleam_cache_create(void* d_storage, size_t bytes, uint64_t capacity, double max_load,
@@ -241,10 +233,7 @@ extern "C" gleam_status gleam_cache_create(void* d_storage, size_t bytes, uint64
   c->shift = 64 - log2_exact(capacity);
   c->max_keys = max_keys;
   c->key_bound = 0;
-  hipStream_t s = (hipStream_t)stream;
-  gleam_status st = fill_u64(reinterpret_cast<uint64_t*>(c->storage), kHeaderBytes / 8, 0, s);
-  if (st == GLEAM_OK)
-    st = fill_u64(reinterpret_cast<uint64_t*>(c->storage + kHeaderBytes), 2 * capacity, kEmpty, s);
+  gleam_status st = clear_table(c, (hipStream_t)stream);
   if (st != GLEAM_OK) {
     delete c;
     return st;

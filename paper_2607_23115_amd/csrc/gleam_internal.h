@@ -7,8 +7,9 @@
 
 #include "gleam.h"
 
-// Host view of a table: storage = [256-byte header][capacity x (key u64, value u64)].
-// Header: u64 flag "the key kEmpty is present", u64 its value.
+// Host view of a table: storage = [256-byte header][capacity x (key u64, value u64)]
+// [capacity x last-use stamp u64]. Header u64 words: 0 flag "the key kEmpty is
+// present", 1 its value, 2 its stamp.
 struct gleam_cache {
   uint8_t* storage;
   uint64_t capacity;
@@ -20,6 +21,28 @@ struct gleam_cache {
 namespace gleam {
 
 constexpr size_t kHeaderBytes = 256;
+
+// Device view of a table (kernel argument).
+struct TableRef {
+  uint64_t* hdr;     // [0] flag: key kEmpty present, [1] its value, [2] its stamp
+  uint64_t* slots;   // capacity x {key, value}
+  uint64_t* stamps;  // capacity last-use stamps
+  uint64_t mask;
+  int shift;
+};
+
+inline TableRef table_ref(const gleam_cache* c) {
+  TableRef t;
+  t.hdr = reinterpret_cast<uint64_t*>(c->storage);
+  t.slots = reinterpret_cast<uint64_t*>(c->storage + kHeaderBytes);
+  t.stamps = t.slots + 2 * c->capacity;
+  t.mask = c->capacity - 1;
+  t.shift = c->shift;
+  return t;
+}
+
+// Enqueue the clear of a table: header zero, keys kEmpty, values and stamps zero.
+gleam_status clear_table(const gleam_cache* c, hipStream_t stream);
 constexpr uint64_t kTileItems = 2048;  // statuses per compaction workgroup
 
 // Workspace layout for n items: [header 256 B][scratch table][tile counts][tile offsets].

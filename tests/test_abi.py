@@ -54,7 +54,7 @@ def test_geometry_rejects_bad_block():
 
 
 def test_sizes():
-    assert g.lib.gleam_cache_bytes(16) == 256 + 16 * 16
+    assert g.lib.gleam_cache_bytes(16) == 256 + 16 * 24
     assert g.lib.gleam_cache_bytes(15) == 0
     assert g.lib.gleam_cache_bytes(8) == 0
     ws = [g.workspace_bytes(n) for n in (0, 1, 1000, 10**6)]
@@ -114,6 +114,12 @@ def test_cache_create_validation():
     assert g.lib.gleam_cache_create(256, 1 << 20, 64, 0.5, None, None) == g.E_INVALID
     assert g.lib.gleam_cache_destroy(None) == g.OK
     assert g.lib.gleam_cache_key_bound(None) == 2**64 - 1
+    assert g.lib.gleam_cache_maint_bytes(None) == 0
+    assert g.lib.gleam_cache_touch(None, 256, 1, None, 0, None, None) == g.E_INVALID
+    assert g.lib.gleam_cache_evict(None, 0, None, 256, 256, 1 << 20, None) == g.E_INVALID
+    assert g.lib.gleam_cache_erase(None, 256, 1, 256, 256, 1 << 20, None) == g.E_INVALID
+    assert g.lib.gleam_cache_export(None, 256, 256, None, 256, 256, 1 << 20, None) == g.E_INVALID
+    assert g.lib.gleam_cache_set_key_bound(None, 0) == g.E_INVALID
 
 
 def test_lookup_insert_compact_validation():

@@ -1,0 +1,121 @@
+"""GPU parity of the table lifecycle (Sec. 4.1.3: LRU eviction of the shared cache;
+Sec. 4.1.2: the identifier set shipped at connect): every export, eviction order,
+count and lookup equals the oracle's after each operation of a random sequence."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_23115_amd as g
+from gpu_util import keys_to_device, say, u64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a visible GPU")
+    torch.cuda.init()
+
+
+def exported(table):
+    k, v, s, c = table.export()
+    torch.cuda.synchronize()
+    n = int(c.item())
+    return u64(k)[:n], u64(v)[:n], u64(s)[:n]
+
+
+def assert_table(table, ot, what):
+    k, v, s = exported(table)
+    ek, ev, es = ot.export()
+    assert np.array_equal(k, ek), f"{what}: keys"
+    assert np.array_equal(v, ev), f"{what}: values"
+    assert np.array_equal(s, es), f"{what}: stamps"
+
+
+def test_random_lifecycle_sequence():
+    rng = np.random.default_rng(1000)
+    table, ot = g.Cache(1024, max_load=0.9), oracle.Table()
+    special = np.array([0, 2**64 - 1], np.uint64)
+    for step in range(80):
+        op = ["insert", "touch", "touch1", "evict", "erase", "lookup"][step % 6]
+        say("lifecycle step", step, op)
+        if op == "insert":
+            keys = np.concatenate([rng.integers(0, 600, 60, dtype=np.uint64), special[rng.integers(0, 2, 2)]])
+            vals = rng.integers(0, 2**64, keys.size, dtype=np.uint64, endpoint=False)
+            try:
+                n_new = table.insert(keys_to_device(keys), keys_to_device(vals))
+            except g.GleamError as e:
+                assert e.status == g.E_CAPACITY
+                continue
+            assert int(n_new.item()) == ot.insert(keys, vals)
+        elif op in ("touch", "touch1"):
+            keys = np.concatenate([rng.integers(0, 650, 90, dtype=np.uint64), special])
+            if op == "touch":
+                ep = rng.integers(1, 10_000, keys.size, dtype=np.uint64)
+                hit = table.touch(keys_to_device(keys), epochs=keys_to_device(ep))
+            else:
+                ep = np.full(keys.size, step * 100 + 7, np.uint64)
+                hit = table.touch(keys_to_device(keys), epoch=int(ep[0]))
+            assert int(hit.item()) == ot.touch(keys, ep)
+        elif op == "evict":
+            keep = int(rng.integers(0, len(ot) + 3))
+            ev, counts = table.evict(keep)
+            torch.cuda.synchronize()
+            want = ot.evict(keep)
+            c = u64(counts)
+            assert int(c[0]) == want.size and int(c[1]) == len(ot)
+            assert np.array_equal(u64(ev)[:want.size], want)
+        elif op == "erase":
+            keys = np.concatenate([rng.integers(0, 650, 40, dtype=np.uint64), special[:1]])
+            counts = table.erase(keys_to_device(keys))
+            torch.cuda.synchronize()
+            c = u64(counts)
+            assert int(c[0]) == ot.erase(keys) and int(c[1]) == len(ot)
+            table.set_key_bound(int(c[1]))
+        else:
+            probe = np.concatenate([np.arange(0, 660, dtype=np.uint64), special])
+            st, ref = table.lookup(keys_to_device(probe))
+            torch.cuda.synchronize()
+            est, eref = oracle.lookup(probe, ot)
+            assert np.array_equal(st.cpu().numpy(), est) and np.array_equal(u64(ref), eref)
+        assert_table(table, ot, f"step {step} {op}")
+
+
+def test_evict_large_table_and_restore():
+    rng = np.random.default_rng(1001)
+    n = 1_000_000
+    keys = rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False)
+    vals = np.arange(n, dtype=np.uint64)
+    table, ot = g.Cache(1 << 21, max_load=0.6), oracle.Table()
+    say("lifecycle large insert")
+    table.insert(keys_to_device(keys), keys_to_device(vals))
+    ot.insert(keys, vals)
+    ep = rng.integers(0, 50, n, dtype=np.uint64)  # many equal stamps: ties go by key
+    table.touch(keys_to_device(keys), epochs=keys_to_device(ep))
+    ot.touch(keys, ep)
+    say("lifecycle large evict")
+    ev, counts = table.evict(n // 2)
+    torch.cuda.synchronize()
+    want = ot.evict(n // 2)
+    assert np.array_equal(u64(ev)[:want.size], want)
+    assert_table(table, ot, "after evict")
+    # checkpoint: export, rebuild a fresh table from it, export again
+    k, v, s = exported(table)
+    fresh = g.Cache(1 << 21, max_load=0.6)
+    fresh.insert(keys_to_device(k), keys_to_device(v))
+    fresh.touch(keys_to_device(k), epochs=keys_to_device(s))
+    k2, v2, s2 = exported(fresh)
+    assert np.array_equal(k, k2) and np.array_equal(v, v2) and np.array_equal(s, s2)
+
+
+def test_maintenance_workspace_checked():
+    table = g.Cache(64)
+    small = torch.empty(256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(g.GleamError) as e:
+        table.evict(1, ws=small)
+    assert e.value.status == g.E_WORKSPACE
+    with pytest.raises(g.GleamError):
+        table.set_key_bound(10)  # cannot raise the bound above 0
