@@ -333,6 +333,78 @@ def lifecycle_path(args, g, torch):
     print(json.dumps(out), flush=True)
 
 
+def transfer_path(args, g, torch, threads):
+    """Sender plan + packing of the MISS bytes, and the receiver's rebuild of the 7B
+    decoder payload from its held base copy plus the packed bytes."""
+    import workloads as W
+    dec = W.Decoder()
+    block = W.DECODER_BLOCK
+    arena, offs, lens = dec.arena(perturbed=True, threads=threads)
+    base_arena, _, _ = dec.arena(perturbed=False, threads=threads)
+    d_pay, d_base = torch.from_numpy(arena).to("cuda"), torch.from_numpy(base_arena).to("cuda")
+    del base_arena
+    src = g.Batch.from_arena(d_pay, offs, lens, block)
+    base = g.Batch.from_arena(d_base, offs, lens, block)
+    addrs = torch.from_numpy(np.array([d_base.data_ptr() + int(o) + j * block for o, n in zip(offs, lens)
+                                       for j in range(-(-int(n) // block))], np.uint64).view(np.int64)).to("cuda")
+    table = g.Cache(1 << 15)
+    table.insert(g.fp_chunks(base), addrs)
+    d = g.fp_chunks(src)
+    status, ref = table.lookup(d)
+    ws = g.workspace(src.n_blocks)
+    records, totals = g.send_plan(src, d, status, ref, ws=ws)
+    torch.cuda.synchronize()
+    tot = g.as_u64(totals)
+    packed = torch.empty(int(tot[3]), dtype=torch.uint8, device="cuda")
+    dst_t = torch.zeros_like(d_pay)
+    dst = g.Batch.from_arena(dst_t, offs, lens, block)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    t_plan, t_pack, t_rest = [], [], []
+    for step in range(args.warmup + args.steps):
+        a, b, c, e = ev(), ev(), ev(), ev()
+        a.record()
+        g.send_plan(src, d, status, ref, ws=ws)
+        b.record()
+        g.pack_misses(src, records, packed)
+        c.record()
+        g.restore_blocks(dst, records, packed, held=ref)
+        e.record()
+        torch.cuda.synchronize()
+        if step >= args.warmup:
+            t_plan.append(a.elapsed_time(b))
+            t_pack.append(b.elapsed_time(c))
+            t_rest.append(c.elapsed_time(e))
+    if not torch.equal(dst_t, d_pay):
+        raise SystemExit("restore did not rebuild the payload")
+    plan_ms, pack_ms, rest_ms = (float(np.median(x)) for x in (t_plan, t_pack, t_rest))
+    payload_bytes = int(lens.sum())
+    rest_gbs = payload_bytes / (rest_ms * 1e-3) / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        payloads = [arena[int(o):int(o) + int(n)] for o, n in zip(offs, lens)]
+        t0 = time.perf_counter()
+        erec, etot = oracle.send_plan(lens, block, g.as_u64(d), status.cpu().numpy(), g.as_u64(ref))
+        oracle.pack_misses(payloads, erec, int(etot[3]))
+        dt = time.perf_counter() - t0
+        cpu = {"value": round(int(etot[3]) / dt / 1e9, 3), "unit": "packed GB/s (plan + pack)", "cores": 1,
+               "kind": "oracle", "sample": f"whole plan and pack, one run {dt:.3f} s, {cpu_model()}"}
+    out = {"metric": "payload GB/s rebuilt by the receiver (restore), with sender plan+pack times, 1 MI355X",
+           "value": round(rest_gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(rest_ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "u8", "data": "synthetic",
+           "config": {"workload": "7B decoder fp16 weights, 1 MiB blocks, 3 of 32 layers rank-16 perturbed; "
+                                  "receiver holds the base weights",
+                      "payload_bytes": payload_bytes, "packed_bytes": int(tot[3]), "plan_ms": round(plan_ms, 4),
+                      "pack_ms": round(pack_ms, 4), "pack_GBps": round(int(tot[3]) / (pack_ms * 1e-3) / 1e9, 1),
+                      "restore_ms": round(rest_ms, 4)},
+           "roofline": {"bound": "hbm", "kernel": "restore_kernel", "achieved": round(2 * rest_gbs, 1),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(2 * rest_gbs / HBM_PEAK_GBS, 4),
+                        "traffic": None, "algorithmic_bytes": 2 * payload_bytes},
+           "cpu_baseline": cpu}
+    print(json.dumps(out), flush=True)
+
+
 WORKLOADS = {"decoder7b": build_decoder7b, "random16": build_random16, "small_copies": build_small_copies,
              "resnet50": build_resnet50, "large_bf16": build_large_bf16}
 
@@ -377,7 +449,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-gb", type=float, default=20.0)
     ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--path", default="detect", choices=["detect", "identify", "md5prefix", "lifecycle"],
+    ap.add_argument("--path", default="detect", choices=["detect", "identify", "md5prefix", "lifecycle", "transfer"],
                     help="detect: fingerprint+lookup+compact (default); identify: free-time weight "
                          "identification; md5prefix: the paper's MD5-of-first-1024-bits identifier")
     args = ap.parse_args()
@@ -401,6 +473,9 @@ def main():
     threads = host_threads()
     if args.path == "lifecycle":
         lifecycle_path(args, g, torch)
+        return
+    if args.path == "transfer":
+        transfer_path(args, g, torch, threads)
         return
     if args.path == "identify":
         if args.workload != "decoder7b":

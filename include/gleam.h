@@ -22,6 +22,8 @@
  *                          exactly what was written to them (Sec. 4.1.1)
  *   gleam_md5_prefix    -- the paper's own identifier (MD5 of a payload's first
  *                          1024 bits), as an ablation
+ *   gleam_send_plan / gleam_pack_misses / gleam_restore_blocks -- the transfer
+ *                          around the decision: what travels, packed, and rebuilt
  *
  * Conventions for every entry point:
  *   - C ABI; no exception crosses it; functions are thread-compatible (distinct
@@ -292,6 +294,63 @@ gleam_status gleam_identify_weights(const gleam_batch* b, const uint64_t* d_reco
  */
 gleam_status gleam_md5_prefix(const gleam_batch* b, uint32_t prefix_bytes, uint64_t min_len, uint64_t* d_digest,
                               uint64_t* d_key, uint8_t* d_eligible, void* stream);
+
+/*
+ * One block of a send plan (Sec. 4.1.2: a chunk whose identifier the server holds sends
+ * only reuse metadata -- its hash and size -- any other chunk sends its bytes).
+ *   block, payload, offset, length  the block's global index, payload, byte offset in
+ *                                   that payload, and bytes
+ *   kind   GLEAM_MISS: the bytes travel; ident = their offset in the packed buffer
+ *          GLEAM_HIT_CACHE: (digest, length) travels; ident = the digest
+ *          GLEAM_HIT_BATCH: (earlier block, length) travels; ident = that block's index
+ */
+typedef struct {
+  uint64_t block;
+  uint64_t payload;
+  uint64_t offset;
+  uint64_t ident;
+  uint32_t length;
+  uint32_t kind;
+} gleam_send_record;
+
+/*
+ * Sender side (Sec. 4.1.2): one record per block from the lookup's results. MISS blocks
+ * are laid out in block order in a packed buffer, each at a multiple of 16 bytes.
+ *   b                     the batch the statuses belong to
+ *   d_digest, d_status, d_ref   device arrays of n_blocks (gleam_fp_chunks and
+ *                         gleam_cache_lookup outputs)
+ *   d_records             device gleam_send_record[n_blocks] output
+ *   d_totals              device u64[4] output: MISS blocks, HIT_CACHE blocks,
+ *                         HIT_BATCH blocks, packed buffer bytes
+ *   d_ws                  device workspace, 256-byte aligned, >= gleam_workspace_bytes(n_blocks)
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED, GLEAM_E_HIP.
+ */
+gleam_status gleam_send_plan(const gleam_batch* b, const uint64_t* d_digest, const uint8_t* d_status,
+                             const uint64_t* d_ref, gleam_send_record* d_records, uint64_t* d_totals, void* d_ws,
+                             size_t ws_bytes, void* stream);
+
+/*
+ * Copy every MISS block's bytes to its planned offset in d_out (device, out_bytes long,
+ * at least the plan's packed total; a block that would not fit is skipped). Padding
+ * bytes between blocks are not written.
+ * Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
+ */
+gleam_status gleam_pack_misses(const gleam_batch* b, const gleam_send_record* d_records, uint8_t* d_out,
+                               uint64_t out_bytes, void* stream);
+
+/*
+ * Receiver side (Sec. 4.1.2: on a hit the server restores the bytes locally): write
+ * every block of the destination payloads `dst` (same geometry as the plan's batch).
+ * MISS blocks come from d_packed (packed_bytes long); HIT_CACHE blocks from the
+ * receiver's own copy at device address d_held[g] (device u64[n_blocks], e.g. the
+ * lookup's ref output when table values are addresses of held blocks; nullable: then
+ * HIT_CACHE blocks are left untouched); HIT_BATCH blocks from the packed bytes of the
+ * block they repeat. Records that point outside the buffers are skipped.
+ * Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
+ */
+gleam_status gleam_restore_blocks(const gleam_batch* dst, const gleam_send_record* d_records,
+                                  const uint8_t* d_packed, uint64_t packed_bytes, const uint64_t* d_held,
+                                  void* stream);
 
 /* Static text for a status code. */
 const char* gleam_status_string(gleam_status s);

@@ -389,3 +389,59 @@ def md5_prefix(payloads, prefix_bytes: int = 128, min_len: int = 1024):
         eligible[s] = 1 if arr.size > min_len else 0
     keys = digests[:, :8].copy().view("<u8").reshape(-1).astype(np.uint64)
     return digests, keys, eligible
+
+
+# --------------------------------------------------------------------------- #
+# Sender-side plan, packing and the receiver's restore (Sec. 4.1.2)
+# --------------------------------------------------------------------------- #
+PLAN_DTYPE = np.dtype([("block", "<u8"), ("payload", "<u8"), ("offset", "<u8"), ("ident", "<u8"),
+                       ("length", "<u4"), ("kind", "<u4")])
+
+
+def _round16(n: int) -> int:
+    return (int(n) + 15) // 16 * 16
+
+
+def send_plan(payload_lens, block_bytes: int, digests, status, ref):
+    """Sec. 4.1.2: a block whose identifier the server holds sends (hash, size); a block
+    repeating an earlier block of the batch sends (that block, size); any other block
+    sends its bytes. One record per block, in batch order:
+        kind MISS      -> ident = offset of its bytes in the packed send buffer, where
+                          every block starts at a multiple of 16 bytes
+        kind HIT_CACHE -> ident = the block digest
+        kind HIT_BATCH -> ident = the earlier block's index
+    Returns (records, totals = [miss blocks, cache-hit blocks, batch-hit blocks, packed bytes])."""
+    blk_first, blk_len = geometry(payload_lens, block_bytes)
+    n = int(blk_first[-1])
+    digests = np.asarray(digests, dtype=np.uint64).reshape(-1)
+    status = np.asarray(status, dtype=np.uint8).reshape(-1)
+    ref = np.asarray(ref, dtype=np.uint64).reshape(-1)
+    rec = np.zeros(n, dtype=PLAN_DTYPE)
+    packed = 0
+    for s in range(len(payload_lens)):
+        for j in range(int(blk_first[s + 1] - blk_first[s])):
+            gidx = int(blk_first[s]) + j
+            r = rec[gidx]
+            r["block"], r["payload"], r["offset"] = gidx, s, j * block_bytes
+            r["length"], r["kind"] = int(blk_len[gidx]), int(status[gidx])
+            if status[gidx] == MISS:
+                r["ident"] = packed
+                packed += _round16(blk_len[gidx])
+            elif status[gidx] == HIT_CACHE:
+                r["ident"] = digests[gidx]
+            else:
+                r["ident"] = ref[gidx]
+            rec[gidx] = r
+    totals = np.array([(status == MISS).sum(), (status == HIT_CACHE).sum(), (status == HIT_BATCH).sum(), packed],
+                      dtype=np.uint64)
+    return rec, totals
+
+
+def pack_misses(payloads, records, packed_bytes: int) -> np.ndarray:
+    """The send buffer: every MISS block's bytes at its planned offset (zero padding)."""
+    out = np.zeros(int(packed_bytes), dtype=np.uint8)
+    for r in records[records["kind"] == MISS]:
+        p = _as_u8(payloads[int(r["payload"])])
+        o, ln = int(r["offset"]), int(r["length"])
+        out[int(r["ident"]):int(r["ident"]) + ln] = p[o:o + ln]
+    return out

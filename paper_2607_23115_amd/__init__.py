@@ -32,7 +32,8 @@ EXPORTS = (
     "gleam_cache_key_bound", "gleam_workspace_bytes", "gleam_cache_insert", "gleam_cache_lookup",
     "gleam_miss_compact", "gleam_status_string", "gleam_last_error", "gleam_identify_weights",
     "gleam_md5_prefix", "gleam_cache_maint_bytes", "gleam_cache_touch", "gleam_cache_evict", "gleam_cache_erase",
-    "gleam_cache_export", "gleam_cache_set_key_bound",
+    "gleam_cache_export", "gleam_cache_set_key_bound", "gleam_send_plan", "gleam_pack_misses",
+    "gleam_restore_blocks",
 )
 
 
@@ -73,6 +74,9 @@ def _load() -> ctypes.CDLL:
         "gleam_cache_erase": ([vp, vp, u64, vp, vp, sz, vp], st),
         "gleam_cache_export": ([vp, vp, vp, vp, vp, vp, sz, vp], st),
         "gleam_cache_set_key_bound": ([vp, u64], st),
+        "gleam_send_plan": ([ctypes.POINTER(_Batch), vp, vp, vp, vp, vp, vp, sz, vp], st),
+        "gleam_pack_misses": ([ctypes.POINTER(_Batch), vp, vp, u64, vp], st),
+        "gleam_restore_blocks": ([ctypes.POINTER(_Batch), vp, vp, u64, vp, vp], st),
         "gleam_status_string": ([st], ctypes.c_char_p),
         "gleam_last_error": ([], ctypes.c_char_p),
     }
@@ -340,6 +344,40 @@ def md5_prefix(batch: Batch, prefix_bytes: int = 128, min_len: int = 1024, strea
                                 _ptr(eligible), _stream(stream)))
     n = batch.n_seg
     return digest[:2 * n].view(n, 2), key[:n], eligible[:n]
+
+
+RECORD_BYTES = 40  # gleam_send_record
+RECORD_DTYPE = np.dtype([("block", "<u8"), ("payload", "<u8"), ("offset", "<u8"), ("ident", "<u8"),
+                         ("length", "<u4"), ("kind", "<u4")])
+
+
+def send_plan(batch: Batch, digests: torch.Tensor, status: torch.Tensor, ref: torch.Tensor,
+              ws: torch.Tensor | None = None, stream=None):
+    """(records as a u8 tensor of n_blocks x 40 bytes, totals int64[4]) on the device."""
+    dev = batch.d_first.device
+    records = torch.empty(max(batch.n_blocks, 1) * RECORD_BYTES, dtype=torch.uint8, device=dev)
+    totals = torch.empty(4, dtype=torch.int64, device=dev)
+    if ws is None:
+        ws = workspace(batch.n_blocks, dev)
+    _check(lib.gleam_send_plan(ctypes.byref(batch.c_struct()), _ptr(digests), _ptr(status), _ptr(ref),
+                               _ptr(records), _ptr(totals), _ptr(ws), ws.numel(), _stream(stream)))
+    return records[:batch.n_blocks * RECORD_BYTES], totals
+
+
+def pack_misses(batch: Batch, records: torch.Tensor, out: torch.Tensor, stream=None) -> torch.Tensor:
+    _check(lib.gleam_pack_misses(ctypes.byref(batch.c_struct()), _ptr(records), _ptr(out), out.numel(),
+                                 _stream(stream)))
+    return out
+
+
+def restore_blocks(dst: Batch, records: torch.Tensor, packed: torch.Tensor, held: torch.Tensor | None = None,
+                   stream=None) -> None:
+    _check(lib.gleam_restore_blocks(ctypes.byref(dst.c_struct()), _ptr(records), _ptr(packed), packed.numel(),
+                                    _ptr(held), _stream(stream)))
+
+
+def records_to_numpy(records: torch.Tensor) -> np.ndarray:
+    return records.cpu().numpy().view(RECORD_DTYPE)
 
 
 def as_u64(t: torch.Tensor) -> np.ndarray:

@@ -104,6 +104,16 @@ def test_md5_prefix_validation():
     assert f(ctypes.byref(_batch(n_seg=0, n_blocks=0)), 128, 1024, None, None, None, None) == g.OK
 
 
+def test_transfer_validation():
+    b = _batch()
+    assert g.lib.gleam_send_plan(None, 256, 256, 256, 256, 256, 256, 1 << 20, None) == g.E_INVALID
+    assert g.lib.gleam_send_plan(ctypes.byref(b), None, 256, 256, 256, 256, 256, 1 << 20, None) == g.E_INVALID
+    assert g.lib.gleam_send_plan(ctypes.byref(b), 256, 256, 256, 256, 256, 256, 16, None) == g.E_WORKSPACE
+    assert g.lib.gleam_pack_misses(ctypes.byref(b), None, 256, 16, None) == g.E_INVALID
+    assert g.lib.gleam_restore_blocks(ctypes.byref(b), None, 256, 16, None, None) == g.E_INVALID
+    assert ctypes.sizeof(ctypes.c_uint64) * 4 + 8 == g.RECORD_BYTES == g.RECORD_DTYPE.itemsize
+
+
 def test_cache_create_validation():
     h = ctypes.c_void_p()
     assert g.lib.gleam_cache_create(256, 1 << 20, 100, 0.5, ctypes.byref(h), None) == g.E_INVALID  # not pow2
