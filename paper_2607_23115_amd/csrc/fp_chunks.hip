@@ -5,23 +5,28 @@
 // tree (node = XXH64 of LE64(left) || LE64(right); an odd last element moves up).
 //
 // Work decomposition. Leaf slot = g * LPB + k (block g, leaf k, LPB = leaves per
-// block). One thread owns one slot: it keeps the four XXH64 accumulators of its
-// leaf in registers, so a 4 KiB leaf is four independent chains of 128 rounds in
-// one lane. A workgroup of 256 threads owns 256 consecutive slots (LPB <= 256), or
-// one whole block walked 256 slots at a time (LPB > 256).
+// block). Two lanes own one slot: the even lane keeps XXH64 accumulators 1 and 2, the
+// odd lane 3 and 4, so each lane runs two independent chains of 128 rounds and a
+// wave covers 32 leaves. A workgroup of W waves owns GROUP = 32 W consecutive slots
+// (LPB <= GROUP), or one whole block walked GROUP slots at a time (LPB > GROUP);
+// W = 4 for blocks up to 512 KiB and 8 for larger blocks, so a 1 MiB block is one
+// work item.
 //
 // Memory path (the kernel is HBM-bound; XXH64 itself runs far above HBM rate).
-// A wave whose 64 leaves are full, contiguous and 16-byte aligned streams them
-// with non-temporal 16-byte loads in which 16 consecutive lanes read one 256-byte
-// run of one leaf (4 leaves per load instruction, 16 loads = 64 leaves x 256 B per
-// stage). The stage goes through a per-wave LDS tile with an XOR swizzle so that
-// each lane then reads its own leaf's 256 bytes conflict-free; the next stage's
-// loads are in flight while the current one is hashed. Other waves (short leaves,
-// unaligned payloads, payload boundaries) hash lane by lane with direct loads.
+// A wave whose 32 leaves are full, contiguous and 16-byte aligned streams them with
+// non-temporal 16-byte loads in which 32 consecutive lanes read one 512-byte run of
+// one leaf (2 leaves per load instruction, 16 loads = 32 leaves x 512 B per stage).
+// Each stage goes through a per-wave LDS tile, 512 B per leaf, whose 32-byte stripes
+// are XOR-swizzled by the leaf index, so both the stores and each lane's 16-byte
+// reads of its own half-stripes are free of bank conflicts; the next stage's loads
+// are in flight while the current one is hashed. Waves of aligned leaves that are
+// not one contiguous full run (payload ends, small payloads) use the same tile with
+// per-instruction leaf addresses from a small LDS table; unaligned waves hash leaf by
+// leaf in the even lanes.
 //
-// Tree: levels inside a 64-lane group use cross-lane shuffles; groups of 64 leaves
-// are combined by wave 0 from LDS. Pairing by aligned position level by level is
-// the same computation as the plain bottom-up definition.
+// Tree: levels inside a wave's 32 leaves use cross-lane shuffles; the roots of
+// 32-leaf groups meet in LDS. Pairing by aligned position level by level is the same
+// computation as the plain bottom-up definition.
 
 #include "gleam_device.h"
 #include "gleam_internal.h"
@@ -29,14 +34,13 @@
 namespace gleam {
 namespace {
 
-constexpr int kWG = 256;
-constexpr int kRunLanes = 16;                       // lanes reading one contiguous run
-constexpr int kRun = kRunLanes * 16;                // 256 B of one leaf per load
-constexpr int kLeavesPerLoad = 64 / kRunLanes;      // 4
-constexpr int kLoads = kRunLanes;                   // 16 loads per stage
-constexpr int kStages = 4096 / kRun;                // 16
-constexpr int kSlotStride = 1024 + 16;              // LDS stride between load slots
-constexpr int kWaveLds = kLoads * kSlotStride;      // 16,640 B per wave
+constexpr int kLeavesPerWave = 32;
+constexpr int kRunLanes = 32;                     // lanes reading one contiguous run
+constexpr int kRun = kRunLanes * 16;              // 512 B of one leaf per load
+constexpr int kLoads = kLeavesPerWave / (64 / kRunLanes);  // 16 loads per stage
+constexpr int kStages = 4096 / kRun;              // 8 stages per leaf
+constexpr int kWaveLds = kLeavesPerWave * kRun;   // 16 KiB tile per wave
+constexpr int kMaxRoots = 128;                    // 32-leaf group roots of a 16 MiB block
 
 struct FpArgs {
   const uint64_t* seg_addr;
@@ -47,7 +51,7 @@ struct FpArgs {
   uint64_t* block_out;
   uint64_t* leaf_out;
   uint32_t lpb_log2;
-  uint64_t items;  // work items: groups of 256 slots (LPB <= 256) or blocks (LPB > 256)
+  uint64_t items;  // work items: groups of GROUP slots (LPB <= GROUP) or blocks
 };
 
 struct Leaf {
@@ -95,253 +99,280 @@ __device__ __forceinline__ uint32_t read_le32_bytes(const uint8_t* p) {
   return v;
 }
 
-// One leaf of 1..4096 bytes at any alignment, by one lane.
-__device__ uint64_t hash_leaf_lane(const uint8_t* p, uint32_t len) {
-  const bool a16 = (reinterpret_cast<uintptr_t>(p) & 15) == 0;
-  uint32_t pos = 0;
-  uint64_t h;
-  if (len >= 32) {
-    uint64_t v1 = kP1 + kP2, v2 = kP2, v3 = 0, v4 = 0 - kP1;
-    const uint32_t stripes = len >> 5;
-    if (a16) {
-#pragma unroll 4
-      for (uint32_t i = 0; i < stripes; ++i) {
-        const uint4 x = load_stream16(p + 32 * i);
-        const uint4 y = load_stream16(p + 32 * i + 16);
-        v1 = xxh_round(v1, lo64(x));
-        v2 = xxh_round(v2, hi64(x));
-        v3 = xxh_round(v3, lo64(y));
-        v4 = xxh_round(v4, hi64(y));
-      }
-    } else {
-      for (uint32_t i = 0; i < stripes; ++i) {
-        const uint8_t* q = p + 32 * i;
-        v1 = xxh_round(v1, read_le64_bytes(q));
-        v2 = xxh_round(v2, read_le64_bytes(q + 8));
-        v3 = xxh_round(v3, read_le64_bytes(q + 16));
-        v4 = xxh_round(v4, read_le64_bytes(q + 24));
-      }
-    }
-    pos = stripes << 5;
-    h = xxh_converge(v1, v2, v3, v4);
-  } else {
-    h = kP5;
-  }
+// XXH64 after the stripe loop: fold (or the short-input start), length, tail, avalanche.
+// `p` is 16-byte aligned when `aligned`; the tail starts at a multiple of 32 from p.
+__device__ __forceinline__ uint64_t finish_leaf(uint64_t v1, uint64_t v2, uint64_t v3, uint64_t v4, const uint8_t* p,
+                                                uint32_t len, bool aligned) {
+  const uint32_t stripes = len >> 5;
+  uint64_t h = stripes ? xxh_converge(v1, v2, v3, v4) : kP5;
   h += len;
+  uint32_t pos = stripes << 5;
   for (; pos + 8 <= len; pos += 8)
-    h = xxh_tail8(h, a16 ? *reinterpret_cast<const uint64_t*>(p + pos) : read_le64_bytes(p + pos));
+    h = xxh_tail8(h, aligned ? *reinterpret_cast<const uint64_t*>(p + pos) : read_le64_bytes(p + pos));
   if (pos + 4 <= len) {
-    h = xxh_tail4(h, a16 ? *reinterpret_cast<const uint32_t*>(p + pos) : read_le32_bytes(p + pos));
+    h = xxh_tail4(h, aligned ? *reinterpret_cast<const uint32_t*>(p + pos) : read_le32_bytes(p + pos));
     pos += 4;
   }
   for (; pos < len; ++pos) h = xxh_tail1(h, p[pos]);
   return xxh_avalanche(h);
 }
 
-// 64 full, contiguous, 16-byte aligned leaves starting at `base`; lane l hashes leaf l.
-__device__ uint64_t hash_wave_streamed(const uint8_t* base, uint8_t* tile, int lane) {
-  // loader role: 16 lanes per 256-byte run, 4 leaves per load instruction
-  const int wm = lane / kRunLanes, wc = lane % kRunLanes;
-  const uint8_t* lp = base + wm * 4096 + wc * 16;
-  const int wslot = (wm * kRunLanes + (wc ^ (wm * 4))) * 16;
-  // reader role: leaf `lane` lives in load slot lane / 4, position lane % 4
-  const int rk = lane / kLeavesPerLoad, rm = lane % kLeavesPerLoad;
-  const uint8_t* rp = tile + rk * kSlotStride + rm * kRun;
-  const int rsw = rm * 4;
-
+// One leaf of 1..4096 bytes at any alignment, by one lane.
+__device__ uint64_t hash_leaf_lane(const uint8_t* p, uint32_t len) {
+  const bool a16 = (reinterpret_cast<uintptr_t>(p) & 15) == 0;
   uint64_t v1 = kP1 + kP2, v2 = kP2, v3 = 0, v4 = 0 - kP1;
+  const uint32_t stripes = len >> 5;
+  if (a16) {
+#pragma unroll 4
+    for (uint32_t i = 0; i < stripes; ++i) {
+      const uint4 x = load_stream16(p + 32 * i);
+      const uint4 y = load_stream16(p + 32 * i + 16);
+      v1 = xxh_round(v1, lo64(x));
+      v2 = xxh_round(v2, hi64(x));
+      v3 = xxh_round(v3, lo64(y));
+      v4 = xxh_round(v4, hi64(y));
+    }
+  } else {
+    for (uint32_t i = 0; i < stripes; ++i) {
+      const uint8_t* q = p + 32 * i;
+      v1 = xxh_round(v1, read_le64_bytes(q));
+      v2 = xxh_round(v2, read_le64_bytes(q + 8));
+      v3 = xxh_round(v3, read_le64_bytes(q + 16));
+      v4 = xxh_round(v4, read_le64_bytes(q + 24));
+    }
+  }
+  return finish_leaf(v1, v2, v3, v4, p, len, a16);
+}
+
+// Lane roles shared by the streamed paths.
+struct Roles {
+  int lm, lc;            // loader: leaf within the load instruction (0/1), 16-byte chunk (0..31)
+  int rl, rp;            // reader: leaf of the wave (0..31), half of each stripe (0/1)
+  const uint8_t* rbase;  // reader's half-stripe 0 in the tile (before the swizzle)
+  int rf;                // reader's swizzle key
+};
+
+__device__ __forceinline__ Roles roles(const uint8_t* tile, int lane) {
+  Roles r;
+  r.lm = lane / kRunLanes;
+  r.lc = lane % kRunLanes;
+  r.rl = lane >> 1;
+  r.rp = lane & 1;
+  r.rbase = tile + r.rl * kRun + r.rp * 16;
+  r.rf = r.rl & 7;
+  return r;
+}
+
+// Tile position of the chunk loaded by this lane for load instruction k:
+// leaf l = 2k + lm, stripe lc / 2 swizzled by (l mod 8), half lc % 2.
+__device__ __forceinline__ int tile_slot(const Roles& r, int k) {
+  const int l = 2 * k + r.lm;
+  return l * kRun + (((r.lc >> 1) ^ (l & 7)) * 32) + (r.lc & 1) * 16;
+}
+
+// 32 full, contiguous, 16-byte aligned leaves from `base`; lane pair l hashes leaf l.
+// Returns the leaf digest in the even lane.
+__device__ uint64_t hash_wave_contiguous(const uint8_t* base, uint8_t* tile, int lane) {
+  const Roles r = roles(tile, lane);
+  const uint8_t* lp = base + r.lm * 4096 + r.lc * 16;
+  uint64_t va = r.rp ? 0 : kP1 + kP2, vb = r.rp ? 0 - kP1 : kP2;
   uint4 R[kLoads];
 #pragma unroll
-  for (int k = 0; k < kLoads; ++k) R[k] = load_stream16(lp + k * kLeavesPerLoad * 4096);
+  for (int k = 0; k < kLoads; ++k) R[k] = load_stream16(lp + k * 2 * 4096);
   for (int s = 0; s < kStages; ++s) {
 #pragma unroll
-    for (int k = 0; k < kLoads; ++k) *reinterpret_cast<uint4*>(tile + k * kSlotStride + wslot) = R[k];
+    for (int k = 0; k < kLoads; ++k) *reinterpret_cast<uint4*>(tile + tile_slot(r, k)) = R[k];
     wave_lds_sync();
     if (s + 1 < kStages) {
 #pragma unroll
-      for (int k = 0; k < kLoads; ++k) R[k] = load_stream16(lp + k * kLeavesPerLoad * 4096 + (s + 1) * kRun);
+      for (int k = 0; k < kLoads; ++k) R[k] = load_stream16(lp + k * 2 * 4096 + (s + 1) * kRun);
     }
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       uint4 D[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) D[j] = *reinterpret_cast<const uint4*>(rp + (((half * 8 + j) ^ rsw) * 16));
+      for (int j = 0; j < 8; ++j) D[j] = *reinterpret_cast<const uint4*>(r.rbase + (((half * 8 + j) ^ r.rf) * 32));
 #pragma unroll
-      for (int j = 0; j < 8; j += 2) {
-        v1 = xxh_round(v1, lo64(D[j]));
-        v2 = xxh_round(v2, hi64(D[j]));
-        v3 = xxh_round(v3, lo64(D[j + 1]));
-        v4 = xxh_round(v4, hi64(D[j + 1]));
+      for (int j = 0; j < 8; ++j) {
+        va = xxh_round(va, lo64(D[j]));
+        vb = xxh_round(vb, hi64(D[j]));
       }
     }
     wave_lds_sync();
   }
-  return xxh_avalanche(xxh_converge(v1, v2, v3, v4) + 4096);
+  const uint64_t pa = shfl_xor64(va, 1), pb = shfl_xor64(vb, 1);
+  return r.rp ? 0 : xxh_avalanche(xxh_converge(va, vb, pa, pb) + 4096);
 }
 
-// Any 64 leaves whose present ones start 16-byte aligned (lengths 0..4096, anywhere in
-// memory): the full 32-byte stripes stream through the LDS tile as above, with each loader
-// lane holding the addresses of the 16 leaves it loads for; the wave runs as many stages as
-// its longest leaf needs. Each lane then finishes its own tail (< 32 bytes) directly.
-__device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, int lane) {
-  const int wm = lane / kRunLanes, wc = lane % kRunLanes;
-  const int wslot = (wm * kRunLanes + (wc ^ (wm * 4))) * 16;
-  const int rk = lane / kLeavesPerLoad, rm = lane % kLeavesPerLoad;
-  const uint8_t* rp = tile + rk * kSlotStride + rm * kRun;
-  const int rsw = rm * 4;
+// Any 32 leaves whose present ones start 16-byte aligned (lengths 0..4096, anywhere in
+// memory). Full stripes stream through the tile as above; the loader lanes find each
+// leaf's address and full-stripe chunk count in a small per-wave LDS table (kept out of
+// registers, which the streamed stage already fills); the wave runs as many stages as
+// its longest leaf needs; the even lane then finishes its leaf's tail directly.
+__device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
+  const Roles r = roles(tile, lane);
   const uint32_t stripes = lf.len >> 5;
-  const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
-
-  const uint8_t* la[kLoads];  // this loader lane's 16-byte chunk of leaf 4k + wm, stage 0
-  uint32_t lim[kLoads];       // that leaf's number of 16-byte chunks in full stripes
+  if ((lane & 1) == 0) {
+    table[lane] = reinterpret_cast<uint64_t>(lf.addr);  // entry of leaf lane / 2: {address, chunks}
+    table[lane + 1] = 2ull * stripes;
+  }
   uint32_t longest = stripes;
 #pragma unroll
-  for (int k = 0; k < kLoads; ++k) {
-    const int src = k * kLeavesPerLoad + wm;
-    la[k] = reinterpret_cast<const uint8_t*>(shfl64(addr, src)) + wc * 16;
-    lim[k] = 2 * (uint32_t)__shfl((int)stripes, src, 64);
-  }
-#pragma unroll
   for (int o = 32; o >= 1; o >>= 1) longest = max(longest, (uint32_t)__shfl_xor((int)longest, o, 64));
-  const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 7) / 8);
+  const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 15) / 16);
+  wave_lds_sync();
 
-  uint64_t v1 = kP1 + kP2, v2 = kP2, v3 = 0, v4 = 0 - kP1;
+  uint64_t va = r.rp ? 0 : kP1 + kP2, vb = r.rp ? 0 - kP1 : kP2;
   uint4 R[kLoads];
 #pragma unroll
-  for (int k = 0; k < kLoads; ++k) R[k] = (uint32_t)wc < lim[k] ? load_stream16(la[k]) : make_uint4(0, 0, 0, 0);
+  for (int k = 0; k < kLoads; ++k) {
+    const uint64_t* e = table + 2 * (2 * k + r.lm);
+    R[k] = (uint64_t)r.lc < e[1] ? load_stream16(reinterpret_cast<const uint8_t*>(e[0]) + r.lc * 16)
+                                 : make_uint4(0, 0, 0, 0);
+  }
   for (uint32_t s = 0; s < stages; ++s) {
 #pragma unroll
-    for (int k = 0; k < kLoads; ++k) *reinterpret_cast<uint4*>(tile + k * kSlotStride + wslot) = R[k];
+    for (int k = 0; k < kLoads; ++k) *reinterpret_cast<uint4*>(tile + tile_slot(r, k)) = R[k];
     wave_lds_sync();
     if (s + 1 < stages) {
-      const uint32_t chunk = (s + 1) * kRunLanes + wc;
+      const uint64_t chunk = (uint64_t)(s + 1) * kRunLanes + r.lc;
 #pragma unroll
-      for (int k = 0; k < kLoads; ++k)
-        R[k] = chunk < lim[k] ? load_stream16(la[k] + (s + 1) * kRun) : make_uint4(0, 0, 0, 0);
+      for (int k = 0; k < kLoads; ++k) {
+        const uint64_t* e = table + 2 * (2 * k + r.lm);
+        R[k] = chunk < e[1] ? load_stream16(reinterpret_cast<const uint8_t*>(e[0]) + chunk * 16)
+                            : make_uint4(0, 0, 0, 0);
+      }
     }
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       uint4 D[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) D[j] = *reinterpret_cast<const uint4*>(rp + (((half * 8 + j) ^ rsw) * 16));
+      for (int j = 0; j < 8; ++j) D[j] = *reinterpret_cast<const uint4*>(r.rbase + (((half * 8 + j) ^ r.rf) * 32));
 #pragma unroll
-      for (int j = 0; j < 8; j += 2) {
-        if (s * 8 + half * 4 + j / 2 < stripes) {
-          v1 = xxh_round(v1, lo64(D[j]));
-          v2 = xxh_round(v2, hi64(D[j]));
-          v3 = xxh_round(v3, lo64(D[j + 1]));
-          v4 = xxh_round(v4, hi64(D[j + 1]));
+      for (int j = 0; j < 8; ++j) {
+        if (s * 16 + half * 8 + j < stripes) {
+          va = xxh_round(va, lo64(D[j]));
+          vb = xxh_round(vb, hi64(D[j]));
         }
       }
     }
     wave_lds_sync();
   }
-  if (lf.len == 0) return 0;
-  uint64_t h = stripes ? xxh_converge(v1, v2, v3, v4) : kP5;
-  h += lf.len;
-  uint32_t pos = stripes << 5;
-  for (; pos + 8 <= lf.len; pos += 8) h = xxh_tail8(h, *reinterpret_cast<const uint64_t*>(lf.addr + pos));
-  if (pos + 4 <= lf.len) {
-    h = xxh_tail4(h, *reinterpret_cast<const uint32_t*>(lf.addr + pos));
-    pos += 4;
-  }
-  for (; pos < lf.len; ++pos) h = xxh_tail1(h, lf.addr[pos]);
-  return xxh_avalanche(h);
+  const uint64_t pa = shfl_xor64(va, 1), pb = shfl_xor64(vb, 1);
+  if (r.rp || lf.len == 0) return 0;
+  return finish_leaf(va, vb, pa, pb, lf.addr, lf.len, true);
 }
 
-__device__ __forceinline__ uint64_t hash_slot(const Leaf& lf, uint8_t* tile, int lane) {
+// Digest of this lane pair's leaf, in the even lane.
+__device__ __forceinline__ uint64_t hash_slot(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
   const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
   const uint64_t a0 = shfl64(addr, 0);
-  const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)lane * 4096 && (a0 & 15) == 0;
-  if (__all(contiguous)) return hash_wave_streamed(reinterpret_cast<const uint8_t*>(uniform64(a0)), tile, lane);
+  const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)(lane >> 1) * 4096 && (a0 & 15) == 0;
+  if (__all(contiguous)) return hash_wave_contiguous(reinterpret_cast<const uint8_t*>(uniform64(a0)), tile, lane);
   if (!__any(lf.len != 0)) return 0;
-  if (__all(lf.len == 0 || (addr & 15) == 0)) return hash_wave_gathered(lf, tile, lane);
-  return lf.len ? hash_leaf_lane(lf.addr, lf.len) : 0;
+  if (__all(lf.len == 0 || (addr & 15) == 0)) return hash_wave_gathered(lf, tile, table, lane);
+  return ((lane & 1) == 0 && lf.len) ? hash_leaf_lane(lf.addr, lf.len) : 0;
 }
 
-__global__ __launch_bounds__(kWG) void fp_kernel(FpArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[4 * kWaveLds];
-  __shared__ uint64_t roots[64];
+// Bottom-up tree over `count` roots in LDS (double-buffered), by one wave.
+__device__ uint64_t tree_reduce_lds(uint64_t* a, uint64_t* b, uint32_t count, int lane) {
+  while (count > 1) {
+    const uint32_t pairs = count / 2;
+    for (uint32_t i = lane; i < pairs; i += 64) b[i] = tree_node(a[2 * i], a[2 * i + 1]);
+    if ((count & 1) && lane == 0) b[pairs] = a[count - 1];
+    wave_lds_sync();
+    uint64_t* t = a;
+    a = b;
+    b = t;
+    count = pairs + (count & 1);
+  }
+  return a[0];
+}
+
+template <int WGT>
+__global__ __launch_bounds__(WGT) void fp_kernel(FpArgs a) {
+  constexpr int W = WGT / 64;
+  constexpr uint32_t GROUP = W * kLeavesPerWave;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[W * kWaveLds];
+  __shared__ uint64_t roots[2][kMaxRoots];
+  __shared__ uint64_t tables[W][2 * kLeavesPerWave];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   uint8_t* tile = lds + wave * kWaveLds;
+  uint64_t* table = tables[wave];
   const uint32_t L2 = a.lpb_log2;
-  const uint64_t lpb = 1ull << L2;
+  const uint32_t lpb = 1u << L2;
+  const bool even = (lane & 1) == 0;
 
   // Persistent workgroups: a grid of a few workgroups per CU walks the work items.
   for (uint64_t item = blockIdx.x; item < a.items; item += gridDim.x) {
-  __syncthreads();  // the previous item's roots have been consumed
-  if (L2 <= 8) {
-    // 256 consecutive slots: 256 / LPB whole blocks.
-    const uint64_t wave_slot0 = uniform64(item * kWG + (uint64_t)wave * 64);
-    const uint64_t slot = wave_slot0 + lane;
-    const uint64_t g = slot >> L2;
-    const uint32_t k = (uint32_t)(slot & (lpb - 1));
-    const uint64_t g_first = wave_slot0 >> L2;
-    const uint64_t s0 = g_first < a.n_blocks ? uniform64(find_segment(a.blk_first, a.n_seg, g_first)) : 0;
-    const Leaf lf = locate(a, g, k, s0);
-    const uint64_t d = hash_slot(lf, tile, lane);
-    if (a.leaf_out && g < a.n_blocks) a.leaf_out[slot] = lf.len ? d : 0;
-    const uint32_t G = L2 <= 6 ? (uint32_t)lpb : 64u;
-    const uint32_t p = k & (G - 1);
-    uint32_t n = lf.blk_leaves;
-    if (L2 > 6) {
-      const uint32_t before = k & ~63u;
-      n = n > before ? min(n - before, 64u) : 0u;
-    }
-    const uint64_t v = tree_reduce_lanes(d, p, n, G);
-    if (L2 <= 6) {
-      if (p == 0 && g < a.n_blocks) a.block_out[g] = v;
+    __syncthreads();  // the previous item's roots have been consumed
+    if (lpb <= GROUP) {
+      // GROUP consecutive slots: GROUP / LPB whole blocks.
+      const uint64_t wave_slot0 = uniform64(item * GROUP + (uint64_t)wave * kLeavesPerWave);
+      const uint64_t slot = wave_slot0 + (lane >> 1);
+      const uint64_t g = slot >> L2;
+      const uint32_t k = (uint32_t)(slot & (lpb - 1));
+      const uint64_t g_first = wave_slot0 >> L2;
+      const uint64_t s0 = g_first < a.n_blocks ? uniform64(find_segment(a.blk_first, a.n_seg, g_first)) : 0;
+      const Leaf lf = locate(a, g, k, s0);
+      const uint64_t d = hash_slot(lf, tile, table, lane);
+      if (a.leaf_out && even && g < a.n_blocks) a.leaf_out[slot] = lf.len ? d : 0;
+      const uint32_t G = lpb <= kLeavesPerWave ? lpb : (uint32_t)kLeavesPerWave;
+      const uint32_t p = k & (G - 1);
+      uint32_t n = lf.blk_leaves;
+      if (lpb > kLeavesPerWave) {
+        const uint32_t before = k & ~(uint32_t)(kLeavesPerWave - 1);
+        n = n > before ? min(n - before, (uint32_t)kLeavesPerWave) : 0u;
+      }
+      const uint64_t v = tree_reduce_lanes(d, p, n, G, 2);
+      if (lpb <= kLeavesPerWave) {
+        if (even && p == 0 && g < a.n_blocks) a.block_out[g] = v;
+      } else {
+        if (lane == 0) roots[0][wave] = v;
+        __syncthreads();
+        if (wave == 0) {
+          // W wave roots = GROUP / LPB blocks of G2 = LPB / 32 roots each
+          const uint32_t G2 = lpb / kLeavesPerWave;
+          const uint64_t g2 = ((item * GROUP) >> L2) + (uint64_t)(lane / G2);
+          uint32_t n2 = 0;
+          uint64_t v2 = 0;
+          if (lane < W && g2 < a.n_blocks) {
+            const Leaf head = locate(a, g2, 0, find_segment(a.blk_first, a.n_seg, g2));
+            n2 = (head.blk_leaves + kLeavesPerWave - 1) / kLeavesPerWave;
+            v2 = roots[0][lane];
+          }
+          v2 = tree_reduce_lanes(v2, lane & (G2 - 1), n2, G2);
+          if (lane < W && (lane & (G2 - 1)) == 0 && g2 < a.n_blocks) a.block_out[g2] = v2;
+        }
+      }
     } else {
-      if (lane == 0) roots[wave] = v;
+      // One block of LPB > GROUP leaves, GROUP slots at a time.
+      const uint64_t g = item;
+      const uint64_t s0 = uniform64(find_segment(a.blk_first, a.n_seg, g));
+      const uint32_t nleaf = locate(a, g, 0, s0).blk_leaves;
+      const uint32_t groups = a.leaf_out ? lpb / GROUP : (nleaf + GROUP - 1) / GROUP;
+      for (uint32_t grp = 0; grp < groups; ++grp) {
+        const uint32_t k = grp * GROUP + (uint32_t)wave * kLeavesPerWave + (lane >> 1);
+        const Leaf lf = locate(a, g, k, s0);
+        const uint64_t d = hash_slot(lf, tile, table, lane);
+        if (a.leaf_out && even) a.leaf_out[((uint64_t)g << L2) + k] = lf.len ? d : 0;
+        const uint32_t before = k & ~(uint32_t)(kLeavesPerWave - 1);
+        const uint32_t n = nleaf > before ? min(nleaf - before, (uint32_t)kLeavesPerWave) : 0u;
+        const uint64_t v = tree_reduce_lanes(d, (uint32_t)(lane >> 1), n, kLeavesPerWave, 2);
+        if (lane == 0) roots[0][grp * W + wave] = v;
+      }
       __syncthreads();
       if (wave == 0) {
-        // 4 group roots = 256 / LPB blocks of G2 = LPB / 64 roots each
-        const uint32_t G2 = (uint32_t)(lpb >> 6);
-        const uint64_t g2 = ((item * kWG) >> L2) + (uint64_t)(lane / G2);
-        uint32_t n2 = 0;
-        uint64_t v2 = 0;
-        if (lane < 4 && g2 < a.n_blocks) {
-          const Leaf head = locate(a, g2, 0, find_segment(a.blk_first, a.n_seg, g2));
-          n2 = (head.blk_leaves + 63) / 64;
-          v2 = roots[lane];
-        }
-        v2 = tree_reduce_lanes(v2, lane & (G2 - 1), n2, G2);
-        if (lane < 4 && (lane & (G2 - 1)) == 0 && g2 < a.n_blocks) a.block_out[g2] = v2;
+        const uint32_t n2 = (nleaf + kLeavesPerWave - 1) / kLeavesPerWave;  // <= kMaxRoots
+        const uint64_t r = tree_reduce_lds(roots[0], roots[1], n2, lane);
+        if (lane == 0) a.block_out[g] = r;
       }
     }
-  } else {
-    // One block of LPB > 256 leaves, 256 slots at a time.
-    const uint64_t g = item;
-    const uint64_t s0 = uniform64(find_segment(a.blk_first, a.n_seg, g));
-    const uint32_t nleaf = locate(a, g, 0, s0).blk_leaves;
-    const uint32_t groups = a.leaf_out ? (uint32_t)(lpb >> 8) : (nleaf + 255) / 256;
-    for (uint32_t grp = 0; grp < groups; ++grp) {
-      const uint32_t k = grp * kWG + threadIdx.x;
-      const Leaf lf = locate(a, g, k, s0);
-      const uint64_t d = hash_slot(lf, tile, lane);
-      if (a.leaf_out) a.leaf_out[(g << L2) + k] = lf.len ? d : 0;
-      const uint32_t before = k & ~63u;
-      const uint32_t n = nleaf > before ? min(nleaf - before, 64u) : 0u;
-      const uint64_t v = tree_reduce_lanes(d, (uint32_t)lane, n, 64);
-      if (lane == 0) roots[grp * 4 + wave] = v;
-    }
-    __syncthreads();
-    if (wave == 0) {
-      const uint32_t G2 = (uint32_t)(lpb >> 6);  // 8 .. 64 group roots
-      const uint32_t n2 = (nleaf + 63) / 64;
-      const uint64_t v2 = (uint32_t)lane < n2 ? roots[lane] : 0;
-      const uint64_t r = tree_reduce_lanes(v2, lane & (G2 - 1), (uint32_t)lane < G2 ? n2 : 0, G2);
-      if (lane == 0) a.block_out[g] = r;
-    }
-  }
   }
 }
 
 }  // namespace
-}  // namespace gleam
-
-namespace gleam {
 
 gleam_status validate_batch(const gleam_batch* b, const char* who) {
   if (!b) {
@@ -367,14 +398,18 @@ gleam_status launch_fp(const gleam_batch* b, uint64_t* d_block_digest, uint64_t*
   if (b->n_blocks == 0) return GLEAM_OK;
   const int lpb_log2 = log2_exact(b->block_bytes) - 12;
   const uint64_t lpb = 1ull << lpb_log2;
-  const uint64_t items = lpb_log2 <= 8 ? (b->n_blocks * lpb + kWG - 1) / kWG : b->n_blocks;
+  // 512 threads (256 slots) from 1 MiB blocks up, so such a block is one work item;
+  // 256 threads (128 slots) below, which keeps small batches spread over more CUs.
+  const bool big = lpb >= 256;
+  const uint64_t group = big ? 256 : 128;
+  const uint64_t items = lpb <= group ? (b->n_blocks * lpb + group - 1) / group : b->n_blocks;
   int cus = 0;
   gleam_status st = device_cu_count(&cus);
   if (st != GLEAM_OK) return st;
-  // Items of <= 1 MiB: four workgroups per CU (two resident at a time, by LDS) walk
-  // them, which trims the launch tail (measured best on MI355X). Larger blocks
-  // already amortise per-item setup and balance better with one workgroup per item.
-  const uint64_t cap = lpb_log2 <= 8 ? 4ull * (uint64_t)cus : items;
+  // 1 MiB blocks: a persistent grid of 8 workgroups per CU walks the items, which trims
+  // the launch tail. Smaller blocks (cheaper items) and larger blocks (longer items)
+  // balance better with one workgroup per item. Both measured on MI355X.
+  const uint64_t cap = lpb == 256 ? 8ull * (uint64_t)cus : items;
   const uint64_t grid = items < cap ? items : cap;
   if (grid > 0x7fffffffull) {
     set_error("fingerprint: batch needs more than 2^31 workgroups");
@@ -382,7 +417,10 @@ gleam_status launch_fp(const gleam_batch* b, uint64_t* d_block_digest, uint64_t*
   }
   FpArgs a{b->seg_addr, b->seg_len, b->blk_first, b->n_seg, b->n_blocks, d_block_digest, d_leaf_digest,
            (uint32_t)lpb_log2, items};
-  hipLaunchKernelGGL(fp_kernel, dim3((uint32_t)grid), dim3(kWG), 0, stream, a);
+  if (big)
+    hipLaunchKernelGGL(fp_kernel<512>, dim3((uint32_t)grid), dim3(512), 0, stream, a);
+  else
+    hipLaunchKernelGGL(fp_kernel<256>, dim3((uint32_t)grid), dim3(256), 0, stream, a);
   return launch_status("fp_kernel");
 }
 

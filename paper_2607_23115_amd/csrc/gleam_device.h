@@ -104,14 +104,16 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Bottom-up pairwise tree over aligned groups of G lanes (G a power of two <= 64).
-// Lane position p in [0, G) holds element p of level 0; n elements are present
-// (positions >= n absent). At the level with stride s, element e = p / s pairs
-// with e + 1 when e is even and e + 1 < ceil(n / s); an odd last element moves up
-// unchanged. Lane p == 0 ends with the group's root. Every lane must call this.
-__device__ __forceinline__ uint64_t tree_reduce_lanes(uint64_t v, uint32_t p, uint32_t n, uint32_t G) {
+// Bottom-up pairwise tree over aligned groups of G positions (G a power of two), one
+// position per `stride` lanes (stride * G <= 64). Position p in [0, G) holds element p
+// of level 0; n elements are present (positions >= n absent). At the level with step
+// s, element e = p / s pairs with e + 1 when e is even and e + 1 < ceil(n / s); an odd
+// last element moves up unchanged. Position 0 ends with the group's root. Every lane
+// must call this.
+__device__ __forceinline__ uint64_t tree_reduce_lanes(uint64_t v, uint32_t p, uint32_t n, uint32_t G,
+                                                      uint32_t stride = 1) {
   for (uint32_t s = 1; s < G; s <<= 1) {
-    const uint64_t o = shfl_xor64(v, (int)s);
+    const uint64_t o = shfl_xor64(v, (int)(s * stride));
     const uint32_t count = (n + s - 1) / s;
     if ((p & (2 * s - 1)) == 0 && p / s + 1 < count) v = tree_node(v, o);
   }
