@@ -74,7 +74,7 @@ def pmc_traffic(algo_bytes: int):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip()
     try:
-        if kv.get("fp_chunks.hip sha256[:16]") != source_digest():
+        if kv.get("fp_chunks.hip sha256 prefix") != source_digest():
             return None
         fetch = float(kv["fp FETCH_SIZE KiB per dispatch"]) * 1024 * float(kv["copy fetch scale"])
         write = float(kv["fp WRITE_SIZE KiB per dispatch"]) * 1024 * float(kv["copy write scale"])
