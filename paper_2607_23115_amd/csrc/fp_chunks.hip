@@ -7,10 +7,15 @@
 // Work decomposition. Leaf slot = g * LPB + k (block g, leaf k, LPB = leaves per
 // block). Two lanes own one slot: the even lane keeps XXH64 accumulators 1 and 2, the
 // odd lane 3 and 4, so each lane runs two independent chains of 128 rounds and a
-// wave covers 32 leaves. A workgroup of W waves owns GROUP = 32 W consecutive slots
-// (LPB <= GROUP), or one whole block walked GROUP slots at a time (LPB > GROUP);
-// W = 4 for blocks up to 512 KiB and 8 for larger blocks, so a 1 MiB block is one
-// work item.
+// wave covers 32 leaves. A workgroup of 4 waves owns GROUP = 128 consecutive slots
+// (LPB <= GROUP), or one whole block walked GROUP slots at a time (LPB > GROUP).
+//
+// Occupancy. HBM read rate on MI355X rises as fewer waves stream at once: one 4-wave
+// workgroup per CU reads faster than two or more (measured with plain read kernels and
+// with this one). For blocks of 1 MiB and up the workgroup's LDS is padded past half
+// of the CU's 160 KiB, so each CU holds exactly one, and a grid of 4 per CU walks the
+// blocks. Smaller blocks keep one workgroup per item at normal occupancy: their
+// gathered and per-lane paths need the extra waves to hide latency.
 //
 // Memory path (the kernel is HBM-bound; XXH64 itself runs far above HBM rate).
 // A wave whose 32 leaves are full, contiguous and 16-byte aligned streams them with
@@ -289,11 +294,14 @@ __device__ uint64_t tree_reduce_lds(uint64_t* a, uint64_t* b, uint32_t count, in
   return a[0];
 }
 
-template <int WGT>
-__global__ __launch_bounds__(WGT) void fp_kernel(FpArgs a) {
-  constexpr int W = WGT / 64;
+constexpr int kThreads = 256;
+constexpr int kSoloPad = 24 << 10;  // takes the workgroup's LDS past 80 KiB: one per CU
+
+template <bool kSolo>
+__global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
+  constexpr int W = kThreads / 64;
   constexpr uint32_t GROUP = W * kLeavesPerWave;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[W * kWaveLds];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[W * kWaveLds + (kSolo ? kSoloPad : 0)];
   __shared__ uint64_t roots[2][kMaxRoots];
   __shared__ uint64_t tables[W][2 * kLeavesPerWave];
   const int lane = threadIdx.x & 63;
@@ -398,29 +406,28 @@ gleam_status launch_fp(const gleam_batch* b, uint64_t* d_block_digest, uint64_t*
   if (b->n_blocks == 0) return GLEAM_OK;
   const int lpb_log2 = log2_exact(b->block_bytes) - 12;
   const uint64_t lpb = 1ull << lpb_log2;
-  // 512 threads (256 slots) from 1 MiB blocks up, so such a block is one work item;
-  // 256 threads (128 slots) below, which keeps small batches spread over more CUs.
-  const bool big = lpb >= 256;
-  const uint64_t group = big ? 256 : 128;
+  constexpr uint64_t group = (kThreads / 64) * kLeavesPerWave;
   const uint64_t items = lpb <= group ? (b->n_blocks * lpb + group - 1) / group : b->n_blocks;
-  int cus = 0;
-  gleam_status st = device_cu_count(&cus);
-  if (st != GLEAM_OK) return st;
-  // 1 MiB blocks: a persistent grid of 8 workgroups per CU walks the items, which trims
-  // the launch tail. Smaller blocks (cheaper items) and larger blocks (longer items)
-  // balance better with one workgroup per item. Both measured on MI355X.
-  const uint64_t cap = lpb == 256 ? 8ull * (uint64_t)cus : items;
-  const uint64_t grid = items < cap ? items : cap;
+  // 1 MiB blocks and up: one workgroup resident per CU, a grid of 4 per CU walking the
+  // blocks. Smaller blocks: one workgroup per item (both measured best on MI355X).
+  const bool solo = lpb >= 256;
+  uint64_t grid = items;
+  if (solo) {
+    int cus = 0;
+    gleam_status st = device_cu_count(&cus);
+    if (st != GLEAM_OK) return st;
+    grid = items < 4ull * (uint64_t)cus ? items : 4ull * (uint64_t)cus;
+  }
   if (grid > 0x7fffffffull) {
     set_error("fingerprint: batch needs more than 2^31 workgroups");
     return GLEAM_E_UNSUPPORTED;
   }
   FpArgs a{b->seg_addr, b->seg_len, b->blk_first, b->n_seg, b->n_blocks, d_block_digest, d_leaf_digest,
            (uint32_t)lpb_log2, items};
-  if (big)
-    hipLaunchKernelGGL(fp_kernel<512>, dim3((uint32_t)grid), dim3(512), 0, stream, a);
+  if (solo)
+    hipLaunchKernelGGL(fp_kernel<true>, dim3((uint32_t)grid), dim3(kThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(fp_kernel<256>, dim3((uint32_t)grid), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(fp_kernel<false>, dim3((uint32_t)grid), dim3(kThreads), 0, stream, a);
   return launch_status("fp_kernel");
 }
 
