@@ -2,12 +2,15 @@
 // on a miss the full chunk is transmitted), as an ascending index list, its length
 // and its byte total.
 //
-// Order-preserving stream compaction in three passes over tiles of 2048 statuses:
-// count per tile, one-workgroup exclusive scan of the tile counts,
-// then each tile writes its MISS indices at its offset using a workgroup scan of
-// per-thread counts. Byte total = count * block_bytes minus, for every payload
-// whose short last block is a MISS, the part of that block that does not exist
-// (each tile handles the payloads whose last block it holds).
+// Order-preserving stream compaction. Up to kSmallItems statuses (and payloads), one
+// 1024-thread workgroup does it all in one launch: rounds of 16 statuses per thread,
+// a workgroup scan per round, and a workgroup sum for the short-block bytes. Larger
+// inputs take three passes over tiles of 2048 statuses: count per tile, one-workgroup
+// exclusive scan of the tile counts, then each tile writes its MISS indices at its
+// offset using a workgroup scan of per-thread counts.
+// Byte total = count * block_bytes minus, for every payload whose short last block is
+// a MISS, the part of that block that does not exist (in the tiled path each tile
+// handles the payloads whose last block it holds).
 // All sums are integer, so the results do not depend on thread timing.
 
 #include "gleam_device.h"
@@ -19,6 +22,8 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kPerThread = (int)(kTileItems / kThreads);  // 8 statuses per thread
 constexpr int kScanThreads = 1024;
+constexpr int kSmallPerThread = 16;
+constexpr uint64_t kSmallItems = 1u << 16;  // single-workgroup path up to this many statuses
 
 __device__ __forceinline__ uint32_t count_misses(const uint8_t* status, uint64_t n, uint64_t first) {
   uint32_t c = 0;
@@ -146,6 +151,65 @@ __global__ __launch_bounds__(kThreads) void compact_scatter_kernel(const uint8_t
     atomicAdd(reinterpret_cast<unsigned long long*>(sb.miss_bytes), (unsigned long long)(0 - deficit));
 }
 
+// Inputs of up to kSmallItems statuses and payloads: count, scan, scatter and byte total
+// in one workgroup (launch count is what such sizes pay for, not bytes). `sb` is used
+// only when n > 0; *miss_bytes (nullable) gets the byte total.
+__global__ __launch_bounds__(kScanThreads) void compact_small_kernel(const uint8_t* status, uint64_t n,
+                                                                     uint64_t* miss_idx, uint64_t* miss_count,
+                                                                     uint64_t* miss_bytes, uint64_t block_bytes,
+                                                                     ShortBlocks sb) {
+  __shared__ uint32_t wave_sums[kScanThreads / 64];
+  __shared__ uint64_t deficits[kScanThreads / 64];
+  const bool vec = (reinterpret_cast<uintptr_t>(status) & 15) == 0;
+  uint64_t carry = 0;
+  for (uint64_t base = 0; base < n; base += (uint64_t)kScanThreads * kSmallPerThread) {
+    const uint64_t first = base + (uint64_t)threadIdx.x * kSmallPerThread;
+    uint32_t bits = 0;
+    if (vec && first + kSmallPerThread <= n) {
+      const uint4 v = *reinterpret_cast<const uint4*>(status + first);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < kSmallPerThread; ++e)
+        bits |= ((w[e >> 2] >> (8 * (e & 3))) & 0xFFu) == GLEAM_MISS ? (1u << e) : 0u;
+    } else {
+#pragma unroll
+      for (int e = 0; e < kSmallPerThread; ++e) {
+        const uint64_t g = first + e;
+        bits |= (g < n && status[g] == GLEAM_MISS) ? (1u << e) : 0u;
+      }
+    }
+    uint32_t total;
+    const uint32_t excl = block_exclusive_scan<kScanThreads / 64>((uint32_t)__builtin_popcount(bits), wave_sums,
+                                                                   &total);
+    uint64_t out = carry + excl;
+    for (uint32_t m = bits; m; m &= m - 1) miss_idx[out++] = first + (uint64_t)__builtin_ctz(m);
+    carry += total;
+  }
+  const bool short_blocks = miss_bytes && n > 0;
+  if (short_blocks) {
+    uint64_t deficit = 0;
+    for (uint64_t s = threadIdx.x; s < sb.n_seg; s += kScanThreads) {
+      const uint64_t b0 = sb.blk_first[s], b1 = sb.blk_first[s + 1];
+      if (b1 <= b0 || b1 - 1 >= n || status[b1 - 1] != GLEAM_MISS) continue;
+      const uint64_t last_len = sb.seg_len[s] - (b1 - b0 - 1) * block_bytes;
+      if (last_len < block_bytes) deficit += block_bytes - last_len;
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) deficit += shfl_xor64(deficit, o);
+    if ((threadIdx.x & 63) == 0) deficits[threadIdx.x >> 6] = deficit;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    *miss_count = carry;
+    if (miss_bytes) {
+      uint64_t d = 0;
+      if (short_blocks)
+        for (int w = 0; w < kScanThreads / 64; ++w) d += deficits[w];
+      *miss_bytes = carry * block_bytes - d;
+    }
+  }
+}
+
 }  // namespace
 }  // namespace gleam
 
@@ -179,18 +243,22 @@ extern "C" gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, 
   }
   if (L.tiles > 0x7fffffffull) return GLEAM_E_UNSUPPORTED;
   hipStream_t s = (hipStream_t)stream;
+  if (n <= kSmallItems && (!d_miss_bytes || b->n_seg <= kSmallItems)) {
+    ShortBlocks sb{nullptr, nullptr, 0, 0, nullptr};
+    if (d_miss_bytes) sb = ShortBlocks{b->seg_len, b->blk_first, b->n_seg, b->block_bytes, d_miss_bytes};
+    hipLaunchKernelGGL(compact_small_kernel, dim3(1), dim3(kScanThreads), 0, s, d_status, n,
+                       d_miss_idx, d_miss_count, d_miss_bytes, (uint64_t)(d_miss_bytes ? b->block_bytes : 0), sb);
+    return launch_status("compact_small_kernel");
+  }
   uint64_t* counts = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(d_ws) + L.tiles_off);
   uint64_t* offsets = counts + L.tiles;
   const uint64_t block_bytes = d_miss_bytes ? b->block_bytes : 0;
   gleam_status st;
-  if (n > 0) {
-    hipLaunchKernelGGL(compact_count_kernel, dim3((uint32_t)L.tiles), dim3(kThreads), 0, s, d_status, n, counts);
-    if ((st = launch_status("compact_count_kernel")) != GLEAM_OK) return st;
-  }
+  hipLaunchKernelGGL(compact_count_kernel, dim3((uint32_t)L.tiles), dim3(kThreads), 0, s, d_status, n, counts);
+  if ((st = launch_status("compact_count_kernel")) != GLEAM_OK) return st;
   hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, counts, L.tiles, offsets, d_miss_count,
                      d_miss_bytes, block_bytes);
   if ((st = launch_status("compact_scan_kernel")) != GLEAM_OK) return st;
-  if (n == 0) return GLEAM_OK;
   ShortBlocks sb{nullptr, nullptr, 0, 0, nullptr};
   if (d_miss_bytes) sb = ShortBlocks{b->seg_len, b->blk_first, b->n_seg, block_bytes, d_miss_bytes};
   hipLaunchKernelGGL(compact_scatter_kernel, dim3((uint32_t)L.tiles), dim3(kThreads), 0, s, d_status, n, offsets,

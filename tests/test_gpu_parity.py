@@ -199,7 +199,33 @@ def test_capacity_is_enforced():
     assert st.cpu().numpy().tolist() == [1] * 8 + [0]
 
 
-@pytest.mark.parametrize("n", [1, 63, 2047, 2048, 2049, 3 * 2048 + 17, 100_003, 2_500_001])
+def short_block_batch(rng, n, block=4096):
+    """A batch of n blocks whose payloads end in short blocks."""
+    lens = []
+    left = n
+    while left:
+        k = int(min(left, rng.integers(1, 6)))
+        lens.append((k - 1) * block + int(rng.integers(1, block + 1)))
+        left -= k
+    batch = g.Batch(np.full(len(lens), 0, np.uint64), lens, block)
+    assert batch.n_blocks == n
+    return batch, lens
+
+
+def check_compaction(status, d_status, batch, lens, block=4096):
+    counters = torch.full((2,), -1, dtype=torch.int64, device="cuda")
+    miss_idx, counters = g.miss_compact(d_status, batch, counters=counters)
+    torch.cuda.synchronize()
+    c = u64(counters)
+    _, blen = oracle.geometry(lens, block)
+    eidx, ecnt, ebytes = oracle.compact(status, blen)
+    assert int(c[0]) == ecnt and int(c[1]) == ebytes
+    assert np.array_equal(u64(miss_idx)[:ecnt], eidx)
+
+
+# one workgroup up to 65,536 statuses (16,384 per round), tiles of 2,048 above
+@pytest.mark.parametrize("n", [1, 63, 2047, 2048, 2049, 3 * 2048 + 17, 16_383, 16_384, 16_385, 65_536, 65_537,
+                               100_003, 2_500_001])
 def test_compaction_tiles(n):
     rng = np.random.default_rng(600 + n)
     status = rng.choice(np.array([0, 1, 2], np.uint8), n, p=[0.3, 0.5, 0.2])
@@ -214,14 +240,34 @@ def test_compaction_tiles(n):
     batch = g.Batch(np.full(len(lens), 0, np.uint64), lens, block)
     assert batch.n_blocks == n
     say("compaction n", n)
-    d_status = to_device(status)
-    miss_idx, counters = g.miss_compact(d_status, batch)
-    torch.cuda.synchronize()
-    c = u64(counters)
-    _, blen = oracle.geometry(lens, block)
-    eidx, ecnt, ebytes = oracle.compact(status, blen)
-    assert int(c[0]) == ecnt and int(c[1]) == ebytes
-    assert np.array_equal(u64(miss_idx)[:ecnt], eidx)
+    check_compaction(status, to_device(status), batch, lens)
+
+
+@pytest.mark.parametrize("offset", [1, 3, 8])
+def test_compaction_status_at_odd_address(offset):
+    rng = np.random.default_rng(650 + offset)
+    n = 40_000
+    status = rng.choice(np.array([0, 1, 2], np.uint8), n, p=[0.4, 0.4, 0.2])
+    batch, lens = short_block_batch(rng, n)
+    say("compaction status offset", offset)
+    buf = torch.zeros(n + 16, dtype=torch.uint8, device="cuda")
+    d_status = buf[offset:offset + n]
+    d_status.copy_(torch.from_numpy(status).to("cuda"))
+    check_compaction(status, d_status, batch, lens)
+
+
+def test_compaction_more_payloads_than_small_path():
+    # few blocks but over 65,536 payloads (zero-length ones between): the tiled path
+    rng = np.random.default_rng(660)
+    n = 30_000
+    status = rng.choice(np.array([0, 1, 2], np.uint8), n, p=[0.5, 0.3, 0.2])
+    lens = []
+    for _ in range(n):  # one short block each, then two empty payloads
+        lens += [int(rng.integers(1, 4097)), 0, 0]
+    batch = g.Batch(np.full(len(lens), 0, np.uint64), lens, 4096)
+    assert batch.n_blocks == n and batch.n_seg > 65_536
+    say("compaction payloads", batch.n_seg)
+    check_compaction(status, to_device(status), batch, lens)
 
 
 def test_empty_inputs():
