@@ -409,6 +409,30 @@ WORKLOADS = {"decoder7b": build_decoder7b, "random16": build_random16, "small_co
              "resnet50": build_resnet50, "large_bf16": build_large_bf16}
 
 
+def payload_tensor(keep):
+    """The device tensor holding the timed payload bytes (what a builder keeps alive)."""
+    return keep[-1] if isinstance(keep, (tuple, list)) else keep
+
+
+def time_fresh_insert(g, torch, batch, digests, reps):
+    """Median ms of inserting a batch's digests into an empty table (a first pass)."""
+    n = batch.n_blocks
+    vals = torch.arange(n, dtype=torch.int64, device="cuda")
+    ws = g.workspace(n)
+    n_new = torch.empty(1, dtype=torch.int64, device="cuda")
+    tables = [g.Cache(1 << 10) for _ in range(reps)]
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    torch.cuda.synchronize()
+    for t, (a, b) in zip(tables, evs):
+        a.record()
+        t.insert(digests[:n], vals, ws=ws, n_new=n_new)
+        b.record()
+    torch.cuda.synchronize()
+    if int(n_new.item()) != n:
+        raise SystemExit(f"first-pass insert added {int(n_new.item())} keys, expected {n}")
+    return round(float(np.median([a.elapsed_time(b) for a, b in evs])), 4)
+
+
 def run_cpu_baseline(payloads, block, threads, budget_bytes):
     """The oracle as it stands, over the leading payloads up to budget_bytes."""
     import oracle
@@ -425,9 +449,24 @@ def run_cpu_baseline(payloads, block, threads, budget_bytes):
         oracle.run(sample, block, oracle.Table(), threads=threads)
         times.append(time.perf_counter() - t0)
     dt = float(np.median(times))
+    # one thread, on a sample a thread-count times smaller
+    one, one_total = [], 0
+    for p in sample:
+        if one and one_total + p.size > max(total // threads, 1):
+            break
+        one.append(p)
+        one_total += p.size
+    times1 = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        oracle.run(one, block, oracle.Table(), threads=1)
+        times1.append(time.perf_counter() - t0)
+    dt1 = float(np.median(times1))
     return {"value": round(total / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"{len(sample)} of {len(payloads)} payloads ({total} bytes), median of 3 runs "
-                      f"{dt:.3f} s, {cpu_model()}"}
+                      f"{dt:.3f} s, {cpu_model()}",
+            "one_thread": {"value": round(one_total / dt1 / 1e9, 3), "unit": "GB/s",
+                           "sample": f"{len(one)} payloads ({one_total} bytes), median of 3 runs {dt1:.3f} s"}}
 
 
 def copy_calibration(torch, nbytes=4 << 30, reps=3):
@@ -444,7 +483,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="decoder7b", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-gb", type=float, default=20.0)
@@ -452,6 +491,11 @@ def main():
     ap.add_argument("--path", default="detect", choices=["detect", "identify", "md5prefix", "lifecycle", "transfer"],
                     help="detect: fingerprint+lookup+compact (default); identify: free-time weight "
                          "identification; md5prefix: the paper's MD5-of-first-1024-bits identifier")
+    ap.add_argument("--no-flush", action="store_true",
+                    help="skip the cold leg (K more steps, each after writing 1 GiB to evict L2 and MALL)")
+    ap.add_argument("--graph", action="store_true",
+                    help="detect path: capture one step in a HIP graph and time K replays (cuts launch "
+                         "overhead on small batches); the fp launch time then comes from an eager leg")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -516,15 +560,79 @@ def main():
 
     K = args.steps
     ev_fp = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    ev_step = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    graph = None
+    if args.graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side), torch.cuda.graph(graph, stream=side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        for _ in range(args.warmup):
+            graph.replay()
     torch.cuda.synchronize()
     start.record()
+    ev_step[0].record()
     for k in range(K):
-        step(*ev_fp[k])
+        if graph is not None:
+            graph.replay()
+        else:
+            step(*ev_fp[k])
+        ev_step[k + 1].record()
     end.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
+    warm_ms = [ev_step[k].elapsed_time(ev_step[k + 1]) for k in range(K)]
+    if graph is not None:
+        c = g.as_u64(counters)
+        if int(c[0]) != expect_miss:
+            raise SystemExit(f"graph replay broke the planted truth: {int(c[0])} misses")
+        for a, b in ev_fp:  # eager fp launches for the kernel's own time
+            a.record()
+            g.fp_chunks(batch, out=digests)
+            b.record()
+        torch.cuda.synchronize()
     fp_ms = [a.elapsed_time(b) for a, b in ev_fp]
+
+    cold = None
+    if not args.no_flush:
+        # each repetition after writing 1 GiB, so no payload byte is left in L2 or MALL
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        ev_cold = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+        for k, (a, b) in enumerate(ev_cold):
+            flush.fill_(k & 0xFF)
+            a.record()
+            if graph is not None:
+                graph.replay()
+            else:
+                step()
+            b.record()
+        torch.cuda.synchronize()
+        cold_ms = [a.elapsed_time(b) for a, b in ev_cold]
+        del flush
+        cold = {"ms_median": round(float(np.median(cold_ms)), 4), "ms_min": round(min(cold_ms), 4),
+                "ms_max": round(max(cold_ms), 4),
+                "gbs_median": round(payload_bytes / (float(np.median(cold_ms)) * 1e-3) / 1e9, 2)}
+
+    # measured read ceiling: the fingerprint kernel's load pattern with no hashing
+    src = payload_tensor(keep)
+    nread = (src.numel() * src.element_size()) & ~15
+    sink = torch.zeros(1, dtype=torch.int64, device=dev)
+    ev_read = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    g.read_stream(src, nread, sink)
+    for a, b in ev_read:
+        a.record()
+        g.read_stream(src, nread, sink)
+        b.record()
+    torch.cuda.synchronize()
+    read_ms = float(np.mean([a.elapsed_time(b) for a, b in ev_read]))
+    read_gbs = nread / (read_ms * 1e-3) / 1e9
+
+    insert_ms = None
+    if args.workload == "random16":
+        insert_ms = time_fresh_insert(g, torch, batch, digests, K)
     fp_avg_ms = float(np.mean(fp_ms))
     ms_per_step = total_ms / K
     value = payload_bytes / (ms_per_step * 1e-3) / 1e9
@@ -533,7 +641,8 @@ def main():
     achieved = algo_bytes / (fp_avg_ms * 1e-3) / 1e9
     traffic = pmc_traffic(algo_bytes) if args.workload == "decoder7b" else None
     log(f"{desc}: {n} blocks, {miss_count} misses ({miss_bytes} bytes), fp {fp_avg_ms:.3f} ms "
-        f"(min {min(fp_ms):.3f}, max {max(fp_ms):.3f}), step {ms_per_step:.3f} ms")
+        f"(min {min(fp_ms):.3f}, max {max(fp_ms):.3f}), step {ms_per_step:.3f} ms, cold {cold}, "
+        f"read ceiling {read_gbs:.0f} GB/s")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -555,10 +664,15 @@ def main():
         "data": "synthetic",
         "config": {"workload": desc, "payload_bytes": payload_bytes, "payloads": batch.n_seg, "blocks": n,
                    "block_bytes": batch.block_bytes, "leaf_bytes": 4096, "misses": miss_count,
-                   "miss_bytes": miss_bytes, "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2)},
+                   "miss_bytes": miss_bytes, "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+                   "launch": "hip_graph" if graph is not None else "eager",
+                   "step_ms": {"median": round(float(np.median(warm_ms)), 4), "min": round(min(warm_ms), 4),
+                               "max": round(max(warm_ms), 4)},
+                   "cold": cold, "insert_ms": insert_ms},
         "roofline": {"bound": "hbm", "kernel": "fp_kernel", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "algorithmic_bytes": algo_bytes, "avg_launch_ms": round(fp_avg_ms, 4)},
+                     "algorithmic_bytes": algo_bytes, "avg_launch_ms": round(fp_avg_ms, 4),
+                     "measured_read_gbs": round(read_gbs, 1), "frac_of_measured": round(achieved / read_gbs, 4)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

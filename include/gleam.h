@@ -212,7 +212,8 @@ gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam
  * calls must not overlap, on any stream, with other calls on the same table.
  *
  * gleam_cache_maint_bytes: device workspace bytes for evict, erase and export of this
- * table (0 for NULL or a table above 2^31 slots).
+ * table (0 for NULL, a table above 2^31 slots, or when the radix sort's storage query
+ * fails; evict, erase and export then return GLEAM_E_HIP).
  *
  * gleam_cache_touch: for every key present, stamp = max(stamp, epoch), the epoch being
  * d_epochs[i] (device u64[n]) or, when d_epochs is NULL, the scalar `epoch`.
@@ -351,6 +352,16 @@ gleam_status gleam_pack_misses(const gleam_batch* b, const gleam_send_record* d_
 gleam_status gleam_restore_blocks(const gleam_batch* dst, const gleam_send_record* d_records,
                                   const uint8_t* d_packed, uint64_t packed_bytes, const uint64_t* d_held,
                                   void* stream);
+
+/*
+ * Calibration (a measurement aid, not a step of the path): read `bytes` bytes at d_src
+ * (device, 16-byte aligned, bytes a multiple of 16) once, with the fastest plain read
+ * pattern measured on MI355X, and XOR into *d_sink (device u64, caller-initialised) the
+ * XOR of every 8-byte little-endian word read. Its duration gives the measured HBM read
+ * ceiling against which the fingerprint kernel's roofline fraction is also reported.
+ * Errors: GLEAM_E_INVALID (null pointers, misaligned source or length), GLEAM_E_HIP.
+ */
+gleam_status gleam_read_stream(const void* d_src, uint64_t bytes, uint64_t* d_sink, void* stream);
 
 /* Static text for a status code. */
 const char* gleam_status_string(gleam_status s);

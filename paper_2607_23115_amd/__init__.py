@@ -33,7 +33,7 @@ EXPORTS = (
     "gleam_miss_compact", "gleam_status_string", "gleam_last_error", "gleam_identify_weights",
     "gleam_md5_prefix", "gleam_cache_maint_bytes", "gleam_cache_touch", "gleam_cache_evict", "gleam_cache_erase",
     "gleam_cache_export", "gleam_cache_set_key_bound", "gleam_send_plan", "gleam_pack_misses",
-    "gleam_restore_blocks",
+    "gleam_restore_blocks", "gleam_read_stream",
 )
 
 
@@ -77,6 +77,7 @@ def _load() -> ctypes.CDLL:
         "gleam_send_plan": ([ctypes.POINTER(_Batch), vp, vp, vp, vp, vp, vp, sz, vp], st),
         "gleam_pack_misses": ([ctypes.POINTER(_Batch), vp, vp, u64, vp], st),
         "gleam_restore_blocks": ([ctypes.POINTER(_Batch), vp, vp, u64, vp, vp], st),
+        "gleam_read_stream": ([vp, u64, vp, vp], st),
         "gleam_status_string": ([st], ctypes.c_char_p),
         "gleam_last_error": ([], ctypes.c_char_p),
     }
@@ -374,6 +375,17 @@ def restore_blocks(dst: Batch, records: torch.Tensor, packed: torch.Tensor, held
                    stream=None) -> None:
     _check(lib.gleam_restore_blocks(ctypes.byref(dst.c_struct()), _ptr(records), _ptr(packed), packed.numel(),
                                     _ptr(held), _stream(stream)))
+
+
+def read_stream(src: torch.Tensor, nbytes: int | None = None, sink: torch.Tensor | None = None,
+                stream=None) -> torch.Tensor:
+    """Calibration read of the first nbytes of a device tensor with the fingerprint
+    kernel's load pattern; XORs the fold of its 8-byte words into sink (int64[1])."""
+    nbytes = src.numel() * src.element_size() if nbytes is None else int(nbytes)
+    if sink is None:
+        sink = torch.zeros(1, dtype=torch.int64, device=src.device)
+    _check(lib.gleam_read_stream(_ptr(src), nbytes, _ptr(sink), _stream(stream)))
+    return sink
 
 
 def records_to_numpy(records: torch.Tensor) -> np.ndarray:

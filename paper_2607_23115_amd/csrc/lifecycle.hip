@@ -36,6 +36,7 @@ struct Entries {  // gathered entries; m = capacity + 1, the last one is the key
 struct MaintLayout {
   uint64_t m;
   size_t counters, key, val, stamp, live, flag, k_a, k_b, i_a, i_b, sort_tmp, sort_bytes, total;
+  bool ok;  // the sort's temporary-storage queries succeeded
 };
 
 MaintLayout maint_layout(uint64_t capacity) {
@@ -58,10 +59,11 @@ MaintLayout maint_layout(uint64_t capacity) {
   L.i_a = take(8 * L.m);
   L.i_b = take(8 * L.m);
   size_t full = 0, one_bit = 0;
-  rocprim::radix_sort_pairs(nullptr, full, (const uint64_t*)nullptr, (uint64_t*)nullptr, (const uint64_t*)nullptr,
-                            (uint64_t*)nullptr, (size_t)L.m, 0, 64);
-  rocprim::radix_sort_pairs(nullptr, one_bit, (const uint64_t*)nullptr, (uint64_t*)nullptr,
-                            (const uint64_t*)nullptr, (uint64_t*)nullptr, (size_t)L.m, 0, 1);
+  const hipError_t e_full = rocprim::radix_sort_pairs(nullptr, full, (const uint64_t*)nullptr, (uint64_t*)nullptr,
+                                                      (const uint64_t*)nullptr, (uint64_t*)nullptr, (size_t)L.m, 0, 64);
+  const hipError_t e_bit = rocprim::radix_sort_pairs(nullptr, one_bit, (const uint64_t*)nullptr, (uint64_t*)nullptr,
+                                                     (const uint64_t*)nullptr, (uint64_t*)nullptr, (size_t)L.m, 0, 1);
+  L.ok = e_full == hipSuccess && e_bit == hipSuccess;
   L.sort_bytes = full > one_bit ? full : one_bit;
   L.sort_tmp = take(L.sort_bytes);
   L.total = off;
@@ -265,6 +267,10 @@ gleam_status check_maint(const gleam_cache* c, void* ws, size_t ws_bytes, const 
     return GLEAM_E_UNSUPPORTED;
   }
   *L = maint_layout(c->capacity);
+  if (!L->ok) {
+    set_error("%s: radix sort storage query failed", who);
+    return GLEAM_E_HIP;
+  }
   if (!ws || !aligned256(ws)) {
     set_error("%s: workspace must be non-null and 256-byte aligned", who);
     return GLEAM_E_INVALID;
@@ -303,7 +309,8 @@ gleam_status sort_pass(void* ws, const MaintLayout& L, const uint64_t* kin, uint
 
 extern "C" size_t gleam_cache_maint_bytes(const gleam_cache* c) {
   if (!c || c->capacity > (1ull << 31)) return 0;
-  return gleam::maint_layout(c->capacity).total;
+  const gleam::MaintLayout L = gleam::maint_layout(c->capacity);
+  return L.ok ? L.total : 0;
 }
 
 extern "C" gleam_status gleam_cache_touch(gleam_cache* c, const uint64_t* d_keys, uint64_t n,
