@@ -75,7 +75,7 @@ WsLayout ws_layout(uint64_t n) {
   L.scratch_cap = cap;
   L.scratch_off = kHeaderBytes;
   L.tiles = (n + kTileItems - 1) / kTileItems;
-  L.tiles_off = L.scratch_off + (size_t)cap * 16;
+  L.tiles_off = L.scratch_off + (size_t)cap * 8;
   L.total = L.tiles_off + (size_t)(L.tiles + 1) * 16;
   L.total = (L.total + 255) & ~(size_t)255;
   return L;

@@ -10,7 +10,10 @@
 //
 // Determinism: results never depend on thread timing. Duplicates inside one call
 // are resolved through a workspace scratch table that keeps, per key, the lowest
-// index (atomicMin); only that index inserts (insert) or is the MISS (lookup).
+// index; only that index inserts (insert) or is the MISS (lookup). A scratch slot
+// holds just an index: its key is keys[index], the same for every index the slot
+// ever holds. So a key's first index takes a slot with one compare-and-swap, and
+// only later duplicates need an atomicMin.
 
 #include <new>
 
@@ -24,10 +27,12 @@ constexpr int kThreads = 256;
 
 struct ScratchRef {
   uint64_t* hdr;    // [0] min index of key kEmpty, [1] new-key counter
-  uint64_t* slots;  // cap x {key, min index}
+  uint64_t* slots;  // cap x lowest index so far of one key (kFree: unused)
   uint64_t mask;
   int shift;
 };
+
+constexpr uint64_t kFree = ~0ull;
 
 __device__ __forceinline__ unsigned long long* ull(uint64_t* p) { return reinterpret_cast<unsigned long long*>(p); }
 
@@ -36,31 +41,33 @@ __global__ void fill_kernel(uint64_t* p, uint64_t n, uint64_t value) {
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = value;
 }
 
-// Scratch: record index i for key k, keeping the minimum index per key.
-__device__ void scratch_mark(const ScratchRef& sc, uint64_t k, uint64_t i) {
+// Scratch: record index i of key k = keys[i], keeping the lowest index per key.
+__device__ void scratch_mark(const ScratchRef& sc, const uint64_t* keys, uint64_t k, uint64_t i) {
   if (k == kEmpty) {
     atomicMin(ull(&sc.hdr[0]), (unsigned long long)i);
     return;
   }
   uint64_t pos = slot_hash(k, sc.shift);
   for (uint64_t probe = 0; probe <= sc.mask; ++probe) {
-    uint64_t* slot = sc.slots + 2 * pos;
-    const uint64_t prev = atomicCAS(ull(slot), (unsigned long long)kEmpty, (unsigned long long)k);
-    if (prev == kEmpty || prev == k) {
-      atomicMin(ull(slot + 1), (unsigned long long)i);
+    uint64_t* slot = sc.slots + pos;
+    const uint64_t prev = atomicCAS(ull(slot), (unsigned long long)kFree, (unsigned long long)i);
+    if (prev == kFree) return;
+    if (keys[prev] == k) {  // the slot of k; its value only decreases
+      if (i < prev) atomicMin(ull(slot), (unsigned long long)i);
       return;
     }
     pos = (pos + 1) & sc.mask;
   }
 }
 
-// Scratch: the minimum index recorded for key k (k was marked earlier).
-__device__ uint64_t scratch_min(const ScratchRef& sc, uint64_t k) {
+// Scratch: the lowest index recorded for key k = keys[g] (g was marked earlier).
+__device__ uint64_t scratch_min(const ScratchRef& sc, const uint64_t* keys, uint64_t k, uint64_t g) {
   if (k == kEmpty) return sc.hdr[0];
   uint64_t pos = slot_hash(k, sc.shift);
   for (uint64_t probe = 0; probe <= sc.mask; ++probe) {
-    const uint64_t* slot = sc.slots + 2 * pos;
-    if (slot[0] == k) return slot[1];
+    const uint64_t v = sc.slots[pos];
+    if (v == kFree) break;
+    if (v == g || keys[v] == k) return v;  // v == g: g's own key, so the slot of k
     pos = (pos + 1) & sc.mask;
   }
   return ~0ull;
@@ -68,7 +75,7 @@ __device__ uint64_t scratch_min(const ScratchRef& sc, uint64_t k) {
 
 __global__ void insert_mark_kernel(ScratchRef sc, const uint64_t* keys, uint64_t n) {
   const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) scratch_mark(sc, keys[i], i);
+  if (i < n) scratch_mark(sc, keys, keys[i], i);
 }
 
 __global__ void insert_commit_kernel(TableRef t, ScratchRef sc, const uint64_t* keys, const uint64_t* vals,
@@ -76,7 +83,7 @@ __global__ void insert_commit_kernel(TableRef t, ScratchRef sc, const uint64_t* 
   const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const uint64_t k = keys[i];
-  if (scratch_min(sc, k) != i) return;  // a lower index carries this key
+  if (scratch_min(sc, keys, k, i) != i) return;  // a lower index carries this key
   if (k == kEmpty) {
     if (atomicCAS(ull(&t.hdr[0]), 0ull, 1ull) == 0ull) {
       t.hdr[1] = vals[i];
@@ -129,7 +136,7 @@ __global__ void lookup_probe_kernel(TableRef t, ScratchRef sc, const uint64_t* k
     if (ref) ref[g] = val;
   } else {
     status[g] = 0xFF;
-    scratch_mark(sc, k, g);
+    scratch_mark(sc, keys, k, g);
   }
 }
 
@@ -138,7 +145,7 @@ __global__ void lookup_resolve_kernel(ScratchRef sc, const uint64_t* keys, uint6
                                       uint64_t* ref) {
   const uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (g >= n || status[g] != 0xFF) return;
-  const uint64_t g0 = scratch_min(sc, keys[g]);
+  const uint64_t g0 = scratch_min(sc, keys, keys[g], g);
   status[g] = g0 == g ? GLEAM_MISS : GLEAM_HIT_BATCH;
   if (ref) ref[g] = g0;
 }
@@ -152,8 +159,8 @@ ScratchRef scratch_ref(void* ws, const WsLayout& L) {
   return s;
 }
 
-// One launch resets the scratch table: slot keys to kEmpty and min-indices to all-ones,
-// header word 0 (min index of key kEmpty) to all-ones, words 1..3 and *also_zero to 0.
+// One launch resets the scratch table: every slot to kFree, header word 0 (min index of
+// key kEmpty) to all-ones, words 1..3 and *also_zero to 0.
 __global__ void scratch_clear_kernel(uint64_t* hdr, uint64_t* slots, uint64_t words, uint64_t* also_zero) {
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
   const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -165,7 +172,7 @@ __global__ void scratch_clear_kernel(uint64_t* hdr, uint64_t* slots, uint64_t wo
 gleam_status clear_scratch(void* ws, const WsLayout& L, hipStream_t stream, uint64_t* also_zero = nullptr) {
   uint64_t* hdr = reinterpret_cast<uint64_t*>(ws);
   uint64_t* slots = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + L.scratch_off);
-  const uint64_t words = 2 * L.scratch_cap;
+  const uint64_t words = L.scratch_cap;
   const uint64_t want = (words + kThreads - 1) / kThreads;
   const uint32_t grid = (uint32_t)(want < 2048 ? want : 2048);
   hipLaunchKernelGGL(scratch_clear_kernel, dim3(grid), dim3(kThreads), 0, stream, hdr, slots, words, also_zero);

@@ -184,6 +184,46 @@ def test_insert_lowest_index_wins_and_existing_kept():
         assert np.array_equal(u64(ref), eref)
 
 
+GOLDEN = 0x9E3779B97F4A7C15  # the multiplier of the library's slot hash (Fibonacci hashing)
+
+
+def colliding_keys(rng, count, top_bits):
+    """`count` distinct keys whose Fibonacci hash has the same top `top_bits` bits, so all
+    of them start probing at one slot of a 2**top_bits-slot table."""
+    inv = pow(GOLDEN, -1, 2**64)
+    home = int(rng.integers(0, 2**top_bits))
+    low = rng.choice(2**(64 - top_bits) - 1, count, replace=False) + 1
+    return np.array([((home << (64 - top_bits) | int(v)) * inv) % 2**64 for v in low], np.uint64)
+
+
+@pytest.mark.parametrize("n_keys,repeats", [(8, 5), (24, 3), (40, 1)])
+def test_scratch_collisions_with_duplicates(n_keys, repeats):
+    # every key of the batch starts at one slot of the scratch table (a power of two
+    # >= max(64, 2n) slots), duplicates interleaved at random: the lowest index must win
+    rng = np.random.default_rng(800 + n_keys)
+    n = n_keys * repeats
+    cap = 64
+    while cap < 2 * n:
+        cap *= 2
+    distinct = colliding_keys(rng, n_keys, cap.bit_length() - 1)
+    keys = np.repeat(distinct, repeats)
+    keys = keys[rng.permutation(keys.size)]
+    say("scratch collisions", n_keys, repeats)
+    table, ot = g.Cache(1 << 10), oracle.Table()
+    status, ref = table.lookup(keys_to_device(keys))
+    torch.cuda.synchronize()
+    est, eref = oracle.lookup(keys, ot)
+    assert np.array_equal(status.cpu().numpy(), est)
+    assert np.array_equal(u64(ref), eref)
+    vals = np.arange(keys.size, dtype=np.uint64) + 1000
+    n_new = table.insert(keys_to_device(keys), keys_to_device(vals))
+    assert int(n_new.item()) == ot.insert(keys, vals) == n_keys
+    st2, ref2 = table.lookup(keys_to_device(keys))
+    torch.cuda.synchronize()
+    est2, eref2 = oracle.lookup(keys, ot)
+    assert np.array_equal(st2.cpu().numpy(), est2) and np.array_equal(u64(ref2), eref2)
+
+
 def test_capacity_is_enforced():
     table = g.Cache(16, max_load=0.5)  # at most 8 keys
     k = keys_to_device(np.arange(9, dtype=np.uint64))
