@@ -9,8 +9,7 @@
 // exclusive scan of the tile counts, then each tile writes its MISS indices at its
 // offset using a workgroup scan of per-thread counts.
 // Byte total = count * block_bytes minus, for every payload whose short last block is
-// a MISS, the part of that block that does not exist (in the tiled path each tile
-// handles the payloads whose last block it holds).
+// a MISS, the part of that block that does not exist.
 // All sums are integer, so the results do not depend on thread timing.
 
 #include "gleam_device.h"
@@ -93,17 +92,6 @@ __global__ __launch_bounds__(kScanThreads) void compact_scan_kernel(const uint64
   }
 }
 
-// Number of payloads s with blk_first[s + 1] <= x (blk_first is non-decreasing).
-__device__ __forceinline__ uint64_t segments_ending_by(const uint64_t* blk_first, uint64_t n_seg, uint64_t x) {
-  uint64_t lo = 0, hi = n_seg;
-  while (lo < hi) {
-    const uint64_t mid = (lo + hi) >> 1;
-    if (blk_first[mid + 1] <= x) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
 struct ShortBlocks {  // payload geometry for the byte total; seg_len == nullptr: not wanted
   const uint64_t* seg_len;
   const uint64_t* blk_first;
@@ -112,8 +100,8 @@ struct ShortBlocks {  // payload geometry for the byte total; seg_len == nullptr
   uint64_t* miss_bytes;
 };
 
-// Writes the tile's MISS indices at its offset; also subtracts, for every payload whose
-// last block lies in this tile, is short and is a MISS, the bytes that block lacks.
+// Writes the tile's MISS indices at its offset; also subtracts, for every payload of its
+// grid-stride share whose last block is short and a MISS, the bytes that block lacks.
 __global__ __launch_bounds__(kThreads) void compact_scatter_kernel(const uint8_t* status, uint64_t n,
                                                                    const uint64_t* tile_offsets,
                                                                    uint64_t* miss_idx, ShortBlocks sb) {
@@ -129,13 +117,11 @@ __global__ __launch_bounds__(kThreads) void compact_scatter_kernel(const uint8_t
     if (g < n && status[g] == GLEAM_MISS) miss_idx[out++] = g;
   }
   if (!sb.seg_len) return;
-  // payloads whose last block g = blk_first[s + 1] - 1 falls in [lo, hi)
-  const uint64_t lo = (uint64_t)blockIdx.x * kTileItems;
-  const uint64_t hi = min(lo + kTileItems, n);
-  const uint64_t s_begin = segments_ending_by(sb.blk_first, sb.n_seg, lo);
-  const uint64_t s_end = segments_ending_by(sb.blk_first, sb.n_seg, hi);
+  // the grid strides over all payloads (a per-tile range would need a binary search of
+  // blk_first: a chain of dependent reads)
   uint64_t deficit = 0;
-  for (uint64_t s = s_begin + threadIdx.x; s < s_end; s += kThreads) {
+  const uint64_t stride = (uint64_t)gridDim.x * kThreads;
+  for (uint64_t s = (uint64_t)blockIdx.x * kThreads + threadIdx.x; s < sb.n_seg; s += stride) {
     const uint64_t b0 = sb.blk_first[s], b1 = sb.blk_first[s + 1];
     if (b1 <= b0 || b1 - 1 >= n || status[b1 - 1] != GLEAM_MISS) continue;
     const uint64_t last_len = sb.seg_len[s] - (b1 - b0 - 1) * sb.block_bytes;

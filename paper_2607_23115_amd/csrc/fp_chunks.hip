@@ -71,11 +71,10 @@ __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-// Leaf k of block g. `s` is a segment with blk_first[s] <= g (a lower start for the walk).
-__device__ __forceinline__ Leaf locate(const FpArgs& a, uint64_t g, uint32_t k, uint64_t s) {
+// Leaf k of block g, which lies in segment s.
+__device__ __forceinline__ Leaf locate_at(const FpArgs& a, uint64_t g, uint32_t k, uint64_t s) {
   Leaf lf{nullptr, 0, 0};
   if (g >= a.n_blocks) return lf;
-  while (s + 1 < a.n_seg && a.blk_first[s + 1] <= g) ++s;
   const uint32_t shift = 12 + a.lpb_log2;
   const uint64_t j = g - a.blk_first[s];
   const uint64_t start = j << shift;
@@ -89,6 +88,23 @@ __device__ __forceinline__ Leaf locate(const FpArgs& a, uint64_t g, uint32_t k, 
     lf.len = (uint32_t)min(len_s - off, (uint64_t)4096);
   }
   return lf;
+}
+
+// Leaf k of block g. `s` is a segment with blk_first[s] <= g (a lower start for the walk).
+__device__ __forceinline__ Leaf locate(const FpArgs& a, uint64_t g, uint32_t k, uint64_t s) {
+  if (g >= a.n_blocks) return Leaf{nullptr, 0, 0};
+  while (s + 1 < a.n_seg && a.blk_first[s + 1] <= g) ++s;
+  return locate_at(a, g, k, s);
+}
+
+// Leaf k of block g for every lane of a wave whose blocks start at block g_first (the same
+// in every lane): the wave finds g_first's segment, then each lane its own (a wave of
+// small payloads spans many segments). Every lane must call this.
+__device__ __forceinline__ Leaf locate_wave(const FpArgs& a, uint64_t g_first, uint64_t g, uint32_t k, int lane) {
+  if (g_first >= a.n_blocks) return Leaf{nullptr, 0, 0};
+  const uint64_t s0 = uniform64(wave_find_segment(a.blk_first, a.n_seg, g_first, lane));
+  const uint64_t s = lane_segment(a.blk_first, a.n_seg, s0, g < a.n_blocks ? g : a.n_blocks - 1, lane);
+  return locate_at(a, g, k, s);
 }
 
 __device__ __forceinline__ uint64_t read_le64_bytes(const uint8_t* p) {
@@ -321,9 +337,7 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
       const uint64_t slot = wave_slot0 + (lane >> 1);
       const uint64_t g = slot >> L2;
       const uint32_t k = (uint32_t)(slot & (lpb - 1));
-      const uint64_t g_first = wave_slot0 >> L2;
-      const uint64_t s0 = g_first < a.n_blocks ? uniform64(find_segment(a.blk_first, a.n_seg, g_first)) : 0;
-      const Leaf lf = locate(a, g, k, s0);
+      const Leaf lf = locate_wave(a, wave_slot0 >> L2, g, k, lane);
       const uint64_t d = hash_slot(lf, tile, table, lane);
       if (a.leaf_out && even && g < a.n_blocks) a.leaf_out[slot] = lf.len ? d : 0;
       const uint32_t G = lpb <= kLeavesPerWave ? lpb : (uint32_t)kLeavesPerWave;
@@ -345,8 +359,8 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
           const uint64_t g2 = ((item * GROUP) >> L2) + (uint64_t)(lane / G2);
           uint32_t n2 = 0;
           uint64_t v2 = 0;
+          const Leaf head = locate_wave(a, (item * GROUP) >> L2, g2, 0, lane);
           if (lane < W && g2 < a.n_blocks) {
-            const Leaf head = locate(a, g2, 0, find_segment(a.blk_first, a.n_seg, g2));
             n2 = (head.blk_leaves + kLeavesPerWave - 1) / kLeavesPerWave;
             v2 = roots[0][lane];
           }

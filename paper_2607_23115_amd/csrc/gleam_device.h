@@ -131,6 +131,51 @@ __device__ __forceinline__ uint64_t find_segment(const uint64_t* blk_first, uint
   return lo;
 }
 
+// find_segment for a g that is the same in every lane, by the whole wave: each round
+// reads 64 evenly spaced pivots at once and keeps the interval the ballot points to, so
+// n_seg payloads cost about log64(n_seg) dependent reads instead of log2(n_seg). Every
+// lane must call this with the same arguments; blk_first[0] <= g < blk_first[n_seg].
+__device__ __forceinline__ uint64_t wave_find_segment(const uint64_t* blk_first, uint64_t n_seg, uint64_t g,
+                                                      int lane) {
+  uint64_t lo = 0, hi = n_seg;  // the answer lies in [lo, hi) and blk_first[lo] <= g
+  while (hi - lo > 64) {
+    const uint64_t step = (hi - lo + 63) / 64;
+    const uint64_t idx = lo + (uint64_t)lane * step;
+    const bool le = idx < hi && blk_first[idx] <= g;
+    // pivots 0..c-1 are <= g; c >= 1 for a well-formed blk_first (the max keeps every
+    // read inside [0, n_seg) even for a malformed one)
+    const uint32_t c = max((uint32_t)__popcll(__ballot(le)), 1u);
+    lo += (uint64_t)(c - 1) * step;
+    hi = min(lo + step, hi);
+  }
+  const uint64_t idx = lo + (uint64_t)lane;
+  const bool le = idx < hi && blk_first[idx] <= g;
+  return lo + (uint64_t)max((uint32_t)__popcll(__ballot(le)), 1u) - 1;
+}
+
+// Per-lane find_segment for blocks at or after the start of segment s0 (same in every
+// lane): one read of the 64 segment starts after s0, a binary search over them through
+// lane shuffles, and a forward walk only for a block beyond that window. Every lane must
+// call this; g need only be meaningful in lanes whose result is used (g < n_blocks).
+__device__ __forceinline__ uint64_t lane_segment(const uint64_t* blk_first, uint64_t n_seg, uint64_t s0,
+                                                 uint64_t g, int lane) {
+  const uint64_t e = s0 + 1 + (uint64_t)lane;
+  const uint64_t w = e < n_seg ? blk_first[e] : ~0ull;  // start of the lane-th segment after s0
+  const uint64_t last = shfl64(w, 63);
+  uint32_t c = 0;  // number of window starts <= g
+#pragma unroll
+  for (uint32_t step = 32; step >= 1; step >>= 1) {
+    const uint64_t v = shfl64(w, (int)(c + step - 1));
+    if (v <= g) c += step;
+  }
+  uint64_t s = s0 + c;
+  if (last <= g) {  // beyond the window
+    s = s0 + 64;
+    while (s + 1 < n_seg && blk_first[s + 1] <= g) ++s;
+  }
+  return s;
+}
+
 // Table hashing: Fibonacci multiplicative hash, top bits.
 __device__ __forceinline__ uint64_t slot_hash(uint64_t key, int shift) {
   return (key * 0x9E3779B97F4A7C15ull) >> shift;

@@ -94,6 +94,23 @@ def test_mixed_alignment_in_one_wave(block):
     assert np.array_equal(gpu["leaves"], ref["leaves"])
 
 
+@pytest.mark.parametrize("block", [4096, 65536])
+def test_many_empty_payloads_between_small_ones(block):
+    # runs of up to 150 zero-length payloads: a wave's blocks then lie more than 64
+    # payloads past its first block's payload, and the batch has over 64^2 payloads
+    rng = np.random.default_rng(900 + block)
+    payloads = []
+    for _ in range(120):
+        payloads += [np.zeros(0, np.uint8)] * int(rng.integers(0, 151))
+        payloads.append(np.frombuffer(rng.bytes(int(rng.integers(1, 3 * block))), np.uint8))
+    arena, offs, lens = W.pack(payloads)
+    batch = g.Batch.from_arena(to_device(arena), offs, lens, block)
+    assert batch.n_seg > 64 * 64
+    say("many empty payloads", block, batch.n_seg, batch.n_blocks)
+    gpu = run_path(batch, g.Cache(1 << 10))
+    assert_same(gpu, oracle_path(payloads, block, oracle.Table()), "empty runs")
+
+
 def test_random16_three_passes():
     block = W.RANDOM16_BLOCK
     p = W.random16_payload()
