@@ -213,20 +213,28 @@ def colliding_keys(rng, count, top_bits):
     return np.array([((home << (64 - top_bits) | int(v)) * inv) % 2**64 for v in low], np.uint64)
 
 
-@pytest.mark.parametrize("n_keys,repeats", [(8, 5), (24, 3), (40, 1)])
-def test_scratch_collisions_with_duplicates(n_keys, repeats):
-    # every key of the batch starts at one slot of the scratch table (a power of two
-    # >= max(64, 2n) slots), duplicates interleaved at random: the lowest index must win
-    rng = np.random.default_rng(800 + n_keys)
-    n = n_keys * repeats
-    cap = 64
-    while cap < 2 * n:
-        cap *= 2
-    distinct = colliding_keys(rng, n_keys, cap.bit_length() - 1)
-    keys = np.repeat(distinct, repeats)
+# Lookups of up to 4,096 keys dedup in one workgroup's LDS table of 8,192 slots; larger
+# ones in a workspace table of a power of two >= 2n slots.
+@pytest.mark.parametrize("n_keys,repeats,filler", [(8, 5, 0), (24, 3, 0), (40, 1, 0), (40, 4, 3_900),
+                                                   (30, 3, 20_000)])
+def test_dedup_collisions_with_duplicates(n_keys, repeats, filler):
+    # the colliding keys all start probing at one slot of the dedup table the lookup uses,
+    # duplicates interleaved at random (and random filler keys): the lowest index must win
+    rng = np.random.default_rng(800 + n_keys + filler)
+    n = n_keys * repeats + filler
+    if n <= 4_096:
+        bits = 13
+    else:
+        cap = 64
+        while cap < 2 * n:
+            cap *= 2
+        bits = cap.bit_length() - 1
+    distinct = colliding_keys(rng, n_keys, bits)
+    keys = np.concatenate([np.repeat(distinct, repeats),
+                           rng.integers(0, 2**64, filler, dtype=np.uint64, endpoint=False)])
     keys = keys[rng.permutation(keys.size)]
-    say("scratch collisions", n_keys, repeats)
-    table, ot = g.Cache(1 << 10), oracle.Table()
+    say("dedup collisions", n_keys, repeats, filler)
+    table, ot = g.Cache(1 << 16), oracle.Table()
     status, ref = table.lookup(keys_to_device(keys))
     torch.cuda.synchronize()
     est, eref = oracle.lookup(keys, ot)
@@ -234,11 +242,32 @@ def test_scratch_collisions_with_duplicates(n_keys, repeats):
     assert np.array_equal(u64(ref), eref)
     vals = np.arange(keys.size, dtype=np.uint64) + 1000
     n_new = table.insert(keys_to_device(keys), keys_to_device(vals))
-    assert int(n_new.item()) == ot.insert(keys, vals) == n_keys
+    assert int(n_new.item()) == ot.insert(keys, vals) == np.unique(keys).size
     st2, ref2 = table.lookup(keys_to_device(keys))
     torch.cuda.synchronize()
     est2, eref2 = oracle.lookup(keys, ot)
     assert np.array_equal(st2.cpu().numpy(), est2) and np.array_equal(u64(ref2), eref2)
+
+
+@pytest.mark.parametrize("n", [4_095, 4_096, 4_097])
+def test_lookup_at_single_workgroup_limit(n):
+    rng = np.random.default_rng(850 + n)
+    pool = np.concatenate([rng.integers(0, 2**64, n // 3, dtype=np.uint64, endpoint=False),
+                           np.array([0, 2**64 - 1], np.uint64)])
+    keys = pool[rng.integers(0, pool.size, n)]
+    cached = np.concatenate([pool[rng.choice(pool.size, pool.size // 2, replace=False)],
+                             np.array([2**64 - 1], np.uint64)])
+    cvals = rng.integers(0, 2**64, cached.size, dtype=np.uint64, endpoint=False)
+    say("lookup limit", n)
+    table, ot = g.Cache(1 << 15), oracle.Table()
+    table.insert(keys_to_device(cached), keys_to_device(cvals))
+    ot.insert(cached, cvals)
+    status, ref = table.lookup(keys_to_device(keys))
+    torch.cuda.synchronize()
+    est, eref = oracle.lookup(keys, ot)
+    assert np.array_equal(status.cpu().numpy(), est)
+    assert np.array_equal(u64(ref), eref)
+    assert {0, 1, 2} <= set(est.tolist())
 
 
 def test_capacity_is_enforced():
