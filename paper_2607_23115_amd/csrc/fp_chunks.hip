@@ -394,6 +394,156 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
   }
 }
 
+// ---- Small batches: four lanes per leaf ---------------------------------------------
+// A batch too small to fill the GPU (at most kQuadMaxSlots leaf slots, where the kernel
+// above would launch at most two workgroups per CU) is latency-bound: a wave's time is
+// its chain of load round trips. Here four lanes own one leaf (lane 4l + a keeps XXH64
+// accumulator a + 1 of the wave's leaf l), so a wave covers 16 leaves in 4 stages of
+// 1 KiB per leaf instead of 32 leaves in 8 stages, and the batch gets twice the waves.
+// Loads keep the pattern above (two 512-byte runs of two leaves per instruction); the
+// stage tile holds 1 KiB per leaf with 32-byte stripes XOR-swizzled by the leaf index,
+// and each lane reads the 8-byte word of its accumulator from every stripe. Blocks of
+// up to 16 leaves (64 KiB) only, so a wave holds whole blocks.
+
+constexpr int kQuadLeaves = 16;                  // leaves per wave
+constexpr int kQuadStage = 1024;                 // bytes of each leaf per stage
+constexpr int kQuadStages = 4096 / kQuadStage;   // 4 stages per leaf
+constexpr int kQuadLoads = 16;                   // load instructions per stage
+constexpr int kQuadWaveLds = kQuadLeaves * kQuadStage;
+constexpr uint64_t kQuadGroup = (kThreads / 64) * kQuadLeaves;  // slots per workgroup
+constexpr uint64_t kQuadMaxSlots = 1u << 16;
+
+// Load instruction k (0..15) of a stage: lanes 0-31 (lm = 0) and 32-63 (lm = 1) read
+// leaf 2 (k mod 8) + lm, run k / 8 (the first or second 512 bytes of the stage's 1 KiB),
+// 16-byte chunk lc = lane mod 32 of the run.
+__device__ __forceinline__ int quad_leaf(int lm, int k) { return 2 * (k & 7) + lm; }
+__device__ __forceinline__ int quad_chunk(int lc, int k) { return (k >> 3) * 32 + lc; }  // in the stage
+// Tile position of that chunk: stripe j = chunk / 2 of leaf l at slot j ^ l, half chunk mod 2.
+__device__ __forceinline__ int quad_tile_slot(int lm, int lc, int k) {
+  const int l = quad_leaf(lm, k), c = quad_chunk(lc, k);
+  return l * kQuadStage + (((c >> 1) ^ l) * 32) + (c & 1) * 16;
+}
+
+__device__ __forceinline__ uint64_t quad_acc_init(int a) {
+  return a == 0 ? kP1 + kP2 : a == 1 ? kP2 : a == 2 ? 0ull : 0ull - kP1;
+}
+
+// XXH64 rounds of accumulator `a` over the tile's `count` stripes of leaf l (count <= 32).
+__device__ __forceinline__ uint64_t quad_rounds(uint64_t v, const uint8_t* tile, int l, int a, int count) {
+  const uint8_t* rb = tile + l * kQuadStage + a * 8;
+#pragma unroll
+  for (int j0 = 0; j0 < 32; j0 += 8) {
+    uint64_t w[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w[j] = *reinterpret_cast<const uint64_t*>(rb + (((j0 + j) ^ l) * 32));
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (j0 + j < count) v = xxh_round(v, w[j]);
+  }
+  return v;
+}
+
+// 16 full, contiguous, 16-byte aligned leaves from `base`; digest in lane 4l of leaf l.
+__device__ uint64_t hash_quad_contiguous(const uint8_t* base, uint8_t* tile, int lane) {
+  const int lm = lane / 32, lc = lane % 32, rl = lane >> 2, ra = lane & 3;
+  uint64_t v = quad_acc_init(ra);
+  uint4 R[kQuadLoads];
+#pragma unroll
+  for (int k = 0; k < kQuadLoads; ++k) R[k] = load_stream16(base + quad_leaf(lm, k) * 4096 + quad_chunk(lc, k) * 16);
+  for (int s = 0; s < kQuadStages; ++s) {
+#pragma unroll
+    for (int k = 0; k < kQuadLoads; ++k) *reinterpret_cast<uint4*>(tile + quad_tile_slot(lm, lc, k)) = R[k];
+    wave_lds_sync();
+    if (s + 1 < kQuadStages) {
+#pragma unroll
+      for (int k = 0; k < kQuadLoads; ++k)
+        R[k] = load_stream16(base + quad_leaf(lm, k) * 4096 + (s + 1) * kQuadStage + quad_chunk(lc, k) * 16);
+    }
+    v = quad_rounds(v, tile, rl, ra, 32);
+    wave_lds_sync();
+  }
+  const int q = lane & ~3;
+  const uint64_t v1 = shfl64(v, q), v2 = shfl64(v, q + 1), v3 = shfl64(v, q + 2), v4 = shfl64(v, q + 3);
+  return ra ? 0 : xxh_avalanche(xxh_converge(v1, v2, v3, v4) + 4096);
+}
+
+// Any 16 leaves whose present ones start 16-byte aligned: full stripes through the tile
+// (leaf addresses and full-stripe chunk counts in a per-wave LDS table), as many stages
+// as the longest leaf needs; lane 4l finishes leaf l's tail.
+__device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
+  const int lm = lane / 32, lc = lane % 32, rl = lane >> 2, ra = lane & 3;
+  const uint32_t stripes = lf.len >> 5;
+  if (ra == 0) {
+    table[2 * rl] = reinterpret_cast<uint64_t>(lf.addr);
+    table[2 * rl + 1] = 2ull * stripes;
+  }
+  uint32_t longest = stripes;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) longest = max(longest, (uint32_t)__shfl_xor((int)longest, o, 64));
+  const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 31) / 32);
+  wave_lds_sync();
+  uint64_t v = quad_acc_init(ra);
+  uint4 R[kQuadLoads];
+#pragma unroll
+  for (int k = 0; k < kQuadLoads; ++k) {
+    const uint64_t* e = table + 2 * quad_leaf(lm, k);
+    const uint64_t c = (uint64_t)quad_chunk(lc, k);
+    R[k] = c < e[1] ? load_stream16(reinterpret_cast<const uint8_t*>(e[0]) + c * 16) : make_uint4(0, 0, 0, 0);
+  }
+  for (uint32_t s = 0; s < stages; ++s) {
+#pragma unroll
+    for (int k = 0; k < kQuadLoads; ++k) *reinterpret_cast<uint4*>(tile + quad_tile_slot(lm, lc, k)) = R[k];
+    wave_lds_sync();
+    if (s + 1 < stages) {
+#pragma unroll
+      for (int k = 0; k < kQuadLoads; ++k) {
+        const uint64_t* e = table + 2 * quad_leaf(lm, k);
+        const uint64_t c = (uint64_t)(s + 1) * 64 + quad_chunk(lc, k);
+        R[k] = c < e[1] ? load_stream16(reinterpret_cast<const uint8_t*>(e[0]) + c * 16) : make_uint4(0, 0, 0, 0);
+      }
+    }
+    const int left = (int)stripes - (int)(s * 32);
+    v = quad_rounds(v, tile, rl, ra, left < 0 ? 0 : (left > 32 ? 32 : left));
+    wave_lds_sync();
+  }
+  const int q = lane & ~3;
+  const uint64_t v1 = shfl64(v, q), v2 = shfl64(v, q + 1), v3 = shfl64(v, q + 2), v4 = shfl64(v, q + 3);
+  if (ra || lf.len == 0) return 0;
+  return finish_leaf(v1, v2, v3, v4, lf.addr, lf.len, true);
+}
+
+// Digest of this lane quad's leaf, in lane 4l.
+__device__ __forceinline__ uint64_t hash_slot_quad(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
+  const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
+  const uint64_t a0 = shfl64(addr, 0);
+  const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)(lane >> 2) * 4096 && (a0 & 15) == 0;
+  if (__all(contiguous)) return hash_quad_contiguous(reinterpret_cast<const uint8_t*>(uniform64(a0)), tile, lane);
+  if (!__any(lf.len != 0)) return 0;
+  if (__all(lf.len == 0 || (addr & 15) == 0)) return hash_quad_gathered(lf, tile, table, lane);
+  return ((lane & 3) == 0 && lf.len) ? hash_leaf_lane(lf.addr, lf.len) : 0;
+}
+
+// One workgroup per kQuadGroup slots; LPB <= kQuadLeaves, so every wave holds whole blocks.
+__global__ __launch_bounds__(kThreads) void fp_quad_kernel(FpArgs a) {
+  constexpr int W = kThreads / 64;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[W * kQuadWaveLds];
+  __shared__ uint64_t tables[W][2 * kQuadLeaves];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const uint32_t L2 = a.lpb_log2;
+  const uint32_t lpb = 1u << L2;
+  const uint64_t wave_slot0 = uniform64((uint64_t)blockIdx.x * kQuadGroup + (uint64_t)wave * kQuadLeaves);
+  const uint64_t slot = wave_slot0 + (lane >> 2);
+  const uint64_t g = slot >> L2;
+  const uint32_t k = (uint32_t)(slot & (lpb - 1));
+  const Leaf lf = locate_wave(a, wave_slot0 >> L2, g, k, lane);
+  const uint64_t d = hash_slot_quad(lf, lds + wave * kQuadWaveLds, tables[wave], lane);
+  const bool head = (lane & 3) == 0;
+  if (a.leaf_out && head && g < a.n_blocks) a.leaf_out[slot] = lf.len ? d : 0;
+  const uint64_t v = tree_reduce_lanes(d, k, lf.blk_leaves, lpb, 4);
+  if (head && k == 0 && g < a.n_blocks) a.block_out[g] = v;
+}
+
 }  // namespace
 
 gleam_status validate_batch(const gleam_batch* b, const char* who) {
@@ -420,6 +570,13 @@ gleam_status launch_fp(const gleam_batch* b, uint64_t* d_block_digest, uint64_t*
   if (b->n_blocks == 0) return GLEAM_OK;
   const int lpb_log2 = log2_exact(b->block_bytes) - 12;
   const uint64_t lpb = 1ull << lpb_log2;
+  if (lpb <= (uint64_t)kQuadLeaves && b->n_blocks * lpb <= kQuadMaxSlots) {
+    const uint64_t grid = (b->n_blocks * lpb + kQuadGroup - 1) / kQuadGroup;
+    FpArgs a{b->seg_addr, b->seg_len, b->blk_first, b->n_seg, b->n_blocks, d_block_digest, d_leaf_digest,
+             (uint32_t)lpb_log2, grid};
+    hipLaunchKernelGGL(fp_quad_kernel, dim3((uint32_t)grid), dim3(kThreads), 0, stream, a);
+    return launch_status("fp_quad_kernel");
+  }
   constexpr uint64_t group = (kThreads / 64) * kLeavesPerWave;
   const uint64_t items = lpb <= group ? (b->n_blocks * lpb + group - 1) / group : b->n_blocks;
   // 1 MiB blocks and up: one workgroup resident per CU, a grid of 4 per CU walking the

@@ -21,7 +21,10 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kPerThread = (int)(kTileItems / kThreads);  // 8 blocks per thread
 constexpr int kScanThreads = 1024;
-constexpr uint32_t kMaxCopyGrid = 4096;
+// Copy grid: one workgroup per 64 KiB item up to 2^24 items (1 TiB), a grid-stride loop
+// beyond. Measured on a 4 GiB copy (read + write traffic): one workgroup per item 5.48 TB/s;
+// a persistent grid of 1-16 workgroups per CU 4.9-5.3 TB/s; hipMemcpyAsync 4.68 TB/s.
+constexpr uint32_t kMaxCopyGrid = 1u << 24;
 constexpr uint64_t kChunk = 64 << 10;  // copy work item: up to 64 KiB of one block
 
 __device__ __forceinline__ uint64_t round16(uint64_t n) { return (n + 15) & ~15ull; }

@@ -111,6 +111,39 @@ def test_many_empty_payloads_between_small_ones(block):
     assert_same(gpu, oracle_path(payloads, block, oracle.Table()), "empty runs")
 
 
+def mixed_layout_payloads(rng, block, min_slots):
+    """Payloads of every layout the kernels distinguish (full and contiguous, short,
+    empty, odd-aligned starts) until the batch has at least `min_slots` leaf slots."""
+    payloads, offsets, slots, pos = [], [], 0, 0
+    while slots < min_slots:
+        kind = int(rng.integers(0, 4))
+        n = [int(rng.integers(8, 20)) * block, int(rng.integers(1, block)), 0, int(rng.integers(1, 3 * block))][kind]
+        pos = (pos + 255) // 256 * 256 + (int(rng.integers(1, 16)) if kind == 3 else 0)
+        payloads.append(np.frombuffer(rng.bytes(n), np.uint8))
+        offsets.append(pos)
+        pos += n
+        slots += -(-n // block) * (block // 4096)
+    arena = np.zeros(pos + 16, np.uint8)
+    for o, p in zip(offsets, payloads):
+        arena[o:o + p.size] = p
+    return payloads, arena, np.array(offsets, np.uint64), np.array([p.size for p in payloads], np.uint64)
+
+
+# Batches of blocks up to 64 KiB and at most 65,536 leaf slots use the four-lanes-per-leaf
+# kernel; larger ones the two-lanes-per-leaf kernel. Same layouts on both sides.
+@pytest.mark.parametrize("block", [4096, 65536])
+@pytest.mark.parametrize("min_slots", [60_000, 70_000])
+def test_both_small_block_kernels_on_mixed_layouts(block, min_slots):
+    rng = np.random.default_rng(950 + block + min_slots)
+    payloads, arena, offs, lens = mixed_layout_payloads(rng, block, min_slots)
+    batch = g.Batch.from_arena(to_device(arena), offs, lens, block)
+    slots = batch.n_blocks * (block // 4096)
+    assert (slots <= 65_536) == (min_slots == 60_000)
+    say("mixed layouts", block, slots)
+    gpu = run_path(batch, g.Cache(1 << 15), with_leaves=True)
+    assert_same(gpu, oracle_path(payloads, block, oracle.Table()), "mixed layouts")
+
+
 def test_random16_three_passes():
     block = W.RANDOM16_BLOCK
     p = W.random16_payload()
