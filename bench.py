@@ -203,12 +203,16 @@ def identify_path(args, g, torch, threads, batch, payloads, keep):
         raise SystemExit(f"identification truth violated: {weights} weight allocations of {n_regions}")
     K = args.steps
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     start.record()
-    for _ in range(K):
+    evs[0].record()
+    for k in range(K):
         g.identify_weights(batch, recorded, rf, ws=ws)
+        evs[k + 1].record()
     end.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / K
+    per_call = [evs[k].elapsed_time(evs[k + 1]) for k in range(K)]
     payload_bytes = int(batch.host_len.sum())
     cpu = None
     if not args.no_cpu_baseline:
@@ -228,7 +232,10 @@ def identify_path(args, g, torch, threads, batch, payloads, keep):
                                   "3 layers updated in place after the write; 1 MiB blocks",
                       "payload_bytes": payload_bytes, "blocks": batch.n_blocks, "allocations": n_regions,
                       "weight_allocations": weights,
-                      "pct_of_hbm_peak": round(100 * payload_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 2)},
+                      "pct_of_hbm_peak": round(100 * payload_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+                      "call_ms": {"median": round(float(np.median(per_call)), 4), "min": round(min(per_call), 4),
+                                  "max": round(max(per_call), 4)},
+                      "gbs_at_median": round(payload_bytes / (float(np.median(per_call)) * 1e-3) / 1e9, 2)},
            "cpu_baseline": cpu}
     print(json.dumps(out), flush=True)
 
