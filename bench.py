@@ -1,6 +1,6 @@
 """Benchmark: payload GB/s of weight-cache hit detection (fingerprint + table lookup +
 miss compaction) on one MI355X, with the HBM roofline of the fingerprint kernel and
-the reference oracle timed on the host's cores.
+the CPU oracle timed on the host's cores.
 
 Workload (default): the weights of a 7B decoder (32 layers, d_model 4096, FFN 11008,
 vocab 32000; 291 fp16 tensors, 13,476,831,232 bytes) as one batch of host-to-device
@@ -506,7 +506,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (see DESIGN.md, sharding)",
+        print("bench.py measures one GPU only: the library has no multi-GPU path; run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 

@@ -62,7 +62,7 @@ enum {
   GLEAM_E_CAPACITY = -2,    /* an insert could push the table past its maximum load */
   GLEAM_E_WORKSPACE = -3,   /* workspace smaller than gleam_workspace_bytes(n) */
   GLEAM_E_HIP = -4,         /* a HIP call or kernel launch failed */
-  GLEAM_E_UNSUPPORTED = -5  /* valid, but beyond what this build handles */
+  GLEAM_E_UNSUPPORTED = -5  /* valid, but beyond what this library handles */
 };
 
 /* Per-block status byte written by gleam_cache_lookup. */

@@ -175,6 +175,26 @@ def test_random16_three_passes():
     assert gpu3["miss_idx"].tolist() == chosen.tolist()
 
 
+@pytest.mark.parametrize("block", [65536, 1 << 20])
+def test_single_payload_above_4gib(block):
+    # byte offsets past 2^32 and leaf indices past 2^20 in one payload (4.5 GiB plus a
+    # short last block, 16 bytes into its buffer): the streamed path's offset arithmetic
+    rng = np.random.default_rng(990)
+    n = (9 << 29) + 12345
+    host = np.empty(n + 16, np.uint8)
+    step = 1 << 26  # fill in 64 MiB pieces, each with its own bytes
+    for o in range(0, host.size, step):
+        k = min(step, host.size - o)
+        host[o:o + k] = np.frombuffer(rng.bytes(k), np.uint8)
+    payload = host[16:16 + n]
+    say("payload above 4 GiB", block)
+    batch = g.Batch.from_arena(to_device(host), [16], [n], block)
+    d = g.fp_chunks(batch)
+    torch.cuda.synchronize()
+    want, _ = oracle.batch_digests([payload], block, threads=host_threads())
+    assert np.array_equal(u64(d), want)
+
+
 def test_repeated_runs_identical():
     block = 65536
     rng = np.random.default_rng(300)

@@ -2,7 +2,7 @@
 
 This module only produces payload bytes, selections and random digests. It holds
 none of the method's arithmetic (no hashing, no lookup, no compaction), so both
-the GPU library's callers and the reference oracle's tests can use it.
+the GPU library's callers and the CPU oracle's tests can use it.
 
 Every random draw comes from numpy's PCG64 seeded by
 SeedSequence([workload, purpose, index]); purposes: 0 payload bytes, 1 selection,
