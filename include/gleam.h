@@ -24,6 +24,7 @@
  *                          1024 bits), as an ablation
  *   gleam_send_plan / gleam_pack_misses / gleam_restore_blocks -- the transfer
  *                          around the decision: what travels, packed, and rebuilt
+ *   gleam_read_stream   -- calibration only: the measured HBM read ceiling
  *
  * Conventions for every entry point:
  *   - C ABI; no exception crosses it; functions are thread-compatible (distinct
@@ -40,6 +41,12 @@
  *     error a negative status is returned and nothing has been enqueued. A HIP
  *     launch failure returns GLEAM_E_HIP; gleam_last_error() then holds the HIP
  *     message (thread-local).
+ *   - HIP graph capture: every call except gleam_cache_evict, _erase and _export
+ *     enqueues kernel launches only (clears are fill kernels, not memsets), so a
+ *     caller may capture it in a graph and replay it. gleam_cache_insert's host-side
+ *     key bound grows once, when the call is captured, not on each replay. Evict,
+ *     erase and export sort with rocPRIM, which also enqueues memsets; keep them out
+ *     of captured graphs.
  *   - Device descriptor contents (seg_addr, seg_len, blk_first) are not read on
  *     the host. The caller guarantees they describe the batch; kernels never read
  *     payload bytes outside [seg_addr[s], seg_addr[s] + seg_len[s]) whatever they

@@ -1,7 +1,8 @@
-"""The detect path (fingerprint -> lookup -> compaction) captured once in a HIP graph and
-replayed: every replay equals an eager run, with eager work and synchronisations between
-replays, and a replay after the payload bytes change in place sees the new bytes. Every
-step is a plain kernel launch (clears are fill kernels, nothing allocates or syncs), so
+"""Calls captured once in a HIP graph and replayed: the detect path (fingerprint ->
+lookup -> compaction), and identify, MD5 prefix, touch, send plan, pack and restore. Every
+replay equals an eager run, with eager work and synchronisations between replays, and a
+replay after the payload bytes change in place sees the new bytes. Every call is plain
+kernel launches (clears are fill kernels, nothing allocates device memory or syncs), so
 the calls are capture-safe."""
 
 import numpy as np
@@ -100,3 +101,84 @@ def test_graph_replays_match_eager(which):
     want = oracle.run([arena2[int(o):int(o) + int(n)] for o, n in zip(offs, lens)], block, ot)
     assert np.array_equal(replayed[0], want["digests"]) and np.array_equal(replayed[1], want["status"])
     assert int(replayed[4][0]) == want["miss_count"] and int(replayed[4][1]) == want["miss_bytes"]
+
+
+def test_graph_replays_the_other_capturable_calls():
+    """identify, MD5 prefix, touch, send plan, pack and restore in one captured graph:
+    every replay (with eager work and a scribble over the outputs before it) reproduces the
+    eager outputs, and the receiver's rebuild equals the payloads."""
+    block = 65536
+    rng = np.random.default_rng(1300)
+    pool = [rng.bytes(block) for _ in range(6)]
+    payloads = []
+    for _ in range(24):
+        parts = [pool[int(i)] for i in rng.integers(0, 6, int(rng.integers(0, 4)))]
+        payloads.append(np.frombuffer(b"".join(parts) + rng.bytes(int(rng.integers(0, block))), np.uint8))
+    payloads.append(np.zeros(0, np.uint8))
+    held = pool[:3]  # blocks the receiver already holds; table values = their addresses
+    d_pool = torch.from_numpy(np.frombuffer(b"".join(held), np.uint8).copy()).to("cuda")
+    keys = np.concatenate([oracle.payload_digests(np.frombuffer(b, np.uint8), block)[0] for b in held])
+    addrs = np.array([d_pool.data_ptr() + i * block for i in range(len(held))], np.uint64)
+    table = g.Cache(1 << 12)
+    table.insert(torch.from_numpy(keys.view(np.int64)).to("cuda"), torch.from_numpy(addrs.view(np.int64)).to("cuda"))
+    arena, offs, lens = W.pack(payloads)
+    d_arena = torch.from_numpy(arena).to("cuda")
+    src = g.Batch.from_arena(d_arena, offs, lens, block)
+    d = g.fp_chunks(src)
+    status, ref = table.lookup(d)
+    recorded = d.clone()
+    region_first = torch.tensor([0, 8, 16, len(payloads)], dtype=torch.int64, device="cuda")
+    _, tot0 = g.send_plan(src, d, status, ref)
+    torch.cuda.synchronize()
+    packed = torch.zeros(max(int(u64(tot0)[3]), 1), dtype=torch.uint8, device="cuda")
+    dst_arena, doffs, dlens = W.pack([np.zeros(p.size, np.uint8) for p in payloads], skew=5)
+    d_dst = torch.from_numpy(dst_arena).to("cuda")
+    dst = g.Batch.from_arena(d_dst, doffs, dlens, block)
+    touch_keys = torch.from_numpy(keys.view(np.int64)).to("cuda")
+    n_touched = torch.empty(1, dtype=torch.int64, device="cuda")
+    ws = g.workspace(src.n_blocks + src.n_seg)
+
+    def calls():
+        out = {}
+        out["match"], out["first_diff"], out["weight"] = g.identify_weights(src, recorded, region_first, ws=ws)
+        out["md5"], out["md5_key"], out["eligible"] = g.md5_prefix(src)
+        out["records"], out["totals"] = g.send_plan(src, d, status, ref, ws=ws)
+        g.pack_misses(src, out["records"], packed)
+        g.restore_blocks(dst, out["records"], packed, held=ref)
+        out["touched"] = table.touch(touch_keys, epoch=7)
+        return out
+
+    def snapshot(out):
+        torch.cuda.synchronize()
+        res = {k: v.cpu().numpy().copy() for k, v in out.items()}
+        res["packed"] = packed.cpu().numpy().copy()
+        res["dst"] = d_dst.cpu().numpy().copy()
+        return res
+
+    say("graph other calls eager")
+    eager = snapshot(calls())
+    rebuilt = eager["dst"]
+    for p, o in zip(payloads, doffs.tolist()):
+        assert np.array_equal(rebuilt[o:o + p.size], p)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side), torch.cuda.graph(graph, stream=side):
+        captured = calls()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for i in range(3):
+        say("graph other calls replay", i)
+        for t in captured.values():
+            t.fill_(0x5A if t.dtype == torch.uint8 else -3)
+        # pack leaves the padding between packed blocks unwritten and restore the gaps
+        # between destination payloads: clear both to their eager-run state (zeros), so
+        # every byte a replay fails to write still differs
+        packed.zero_()
+        d_dst.zero_()
+        graph.replay()
+        got = snapshot(captured)
+        for k in eager:
+            assert np.array_equal(got[k], eager[k]), f"replay {i}: {k}"
+        g.fp_chunks(src, out=d)  # eager work between replays
+        torch.cuda.synchronize()
