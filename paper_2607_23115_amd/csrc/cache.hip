@@ -392,6 +392,10 @@ extern "C" gleam_status gleam_cache_insert(gleam_cache* c, const uint64_t* d_key
     set_error("gleam_cache_insert: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
     return GLEAM_E_WORKSPACE;
   }
+  if (n > 0x7fffffffull * kThreads) {
+    set_error("gleam_cache_insert: more than 2^31 workgroups of keys");
+    return GLEAM_E_UNSUPPORTED;
+  }
   if (n > c->max_keys || c->key_bound > c->max_keys - n) {
     set_error("gleam_cache_insert: %llu more keys could exceed the maximum load (%llu keys, bound %llu)",
               (unsigned long long)n, (unsigned long long)c->max_keys, (unsigned long long)c->key_bound);
@@ -436,7 +440,10 @@ extern "C" gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t*
     set_error("gleam_cache_lookup: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
     return GLEAM_E_WORKSPACE;
   }
-  if (n > 0xFFFFFFFFull * kThreads) return GLEAM_E_UNSUPPORTED;
+  if (n > 0x7fffffffull * kThreads) {
+    set_error("gleam_cache_lookup: more than 2^31 workgroups of keys");
+    return GLEAM_E_UNSUPPORTED;
+  }
   hipStream_t s = (hipStream_t)stream;
   if (n <= kSmallKeys) {
     hipLaunchKernelGGL(lookup_small_kernel, dim3(1), dim3(kSmallThreads), 0, s, table_ref(c), d_keys, n, d_status,

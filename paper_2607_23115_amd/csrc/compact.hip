@@ -227,7 +227,10 @@ extern "C" gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, 
     set_error("gleam_miss_compact: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
     return GLEAM_E_WORKSPACE;
   }
-  if (L.tiles > 0x7fffffffull) return GLEAM_E_UNSUPPORTED;
+  if (L.tiles > 0x7fffffffull) {
+    set_error("gleam_miss_compact: more than 2^31 tiles");
+    return GLEAM_E_UNSUPPORTED;
+  }
   hipStream_t s = (hipStream_t)stream;
   if (n <= kSmallItems && (!d_miss_bytes || b->n_seg <= kSmallItems)) {
     ShortBlocks sb{nullptr, nullptr, 0, 0, nullptr};

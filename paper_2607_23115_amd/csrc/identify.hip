@@ -66,7 +66,11 @@ extern "C" gleam_status gleam_identify_weights(const gleam_batch* b, const uint6
     set_error("gleam_identify_weights: null recorded digests, region list or output");
     return GLEAM_E_INVALID;
   }
-  if (b->n_seg > (UINT64_MAX >> 8) || n_regions > (UINT64_MAX >> 8)) return GLEAM_E_UNSUPPORTED;
+  if (b->n_seg > 0x7fffffffull * kThreads || n_regions > 0x7fffffffull * kThreads ||
+      b->n_blocks > 0x7fffffffull * kThreads) {
+    set_error("gleam_identify_weights: more than 2^31 workgroups of blocks, payloads or regions");
+    return GLEAM_E_UNSUPPORTED;
+  }
   const WsLayout L = ws_layout(b->n_blocks + b->n_seg);
   if (!d_ws || !aligned256(d_ws)) {
     set_error("gleam_identify_weights: workspace must be non-null and 256-byte aligned");

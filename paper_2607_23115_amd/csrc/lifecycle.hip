@@ -326,7 +326,10 @@ extern "C" gleam_status gleam_cache_touch(gleam_cache* c, const uint64_t* d_keys
     set_error("gleam_cache_touch: null keys");
     return GLEAM_E_INVALID;
   }
-  if (n > 0x7fffffffull * kThreads) return GLEAM_E_UNSUPPORTED;
+  if (n > 0x7fffffffull * kThreads) {
+    set_error("gleam_cache_touch: more than 2^31 workgroups of keys");
+    return GLEAM_E_UNSUPPORTED;
+  }
   hipStream_t s = (hipStream_t)stream;
   gleam_status st = GLEAM_OK;
   if (d_n_touched) st = fill_u64(d_n_touched, 1, 0, s);
@@ -384,7 +387,10 @@ extern "C" gleam_status gleam_cache_erase(gleam_cache* c, const uint64_t* d_keys
     set_error("gleam_cache_erase: null keys or counts");
     return GLEAM_E_INVALID;
   }
-  if (n > 0x7fffffffull * kThreads) return GLEAM_E_UNSUPPORTED;
+  if (n > 0x7fffffffull * kThreads) {
+    set_error("gleam_cache_erase: more than 2^31 workgroups of keys");
+    return GLEAM_E_UNSUPPORTED;
+  }
   hipStream_t s = (hipStream_t)stream;
   uint8_t* b = static_cast<uint8_t*>(d_ws);
   const Entries e = entries_at(d_ws, L);

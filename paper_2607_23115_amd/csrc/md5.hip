@@ -126,7 +126,10 @@ extern "C" gleam_status gleam_md5_prefix(const gleam_batch* b, uint32_t prefix_b
     return GLEAM_E_INVALID;
   }
   const uint64_t grid = (b->n_seg + kThreads - 1) / kThreads;
-  if (grid > 0x7fffffffull) return GLEAM_E_UNSUPPORTED;
+  if (grid > 0x7fffffffull) {
+    set_error("gleam_md5_prefix: more than 2^31 workgroups of payloads");
+    return GLEAM_E_UNSUPPORTED;
+  }
   hipLaunchKernelGGL(md5_prefix_kernel, dim3((uint32_t)grid), dim3(kThreads), 0, (hipStream_t)stream, b->seg_addr,
                      b->seg_len, b->n_seg, prefix_bytes, min_len, d_digest, d_key, d_eligible);
   return launch_status("md5_prefix_kernel");

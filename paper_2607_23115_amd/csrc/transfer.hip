@@ -276,7 +276,10 @@ extern "C" gleam_status gleam_send_plan(const gleam_batch* b, const uint64_t* d_
     set_error("gleam_send_plan: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
     return GLEAM_E_WORKSPACE;
   }
-  if (L.tiles > 0x7fffffffull) return GLEAM_E_UNSUPPORTED;
+  if (L.tiles > 0x7fffffffull) {
+    set_error("gleam_send_plan: more than 2^31 tiles");
+    return GLEAM_E_UNSUPPORTED;
+  }
   hipStream_t s = (hipStream_t)stream;
   uint64_t* tiles = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(d_ws) + L.scratch_off);
   uint64_t* offs = tiles + 2 * L.tiles;
