@@ -48,9 +48,9 @@
  *     erase and export sort with rocPRIM, which also enqueues memsets; keep them out
  *     of captured graphs.
  *   - Device descriptor contents (seg_addr, seg_len, blk_first) are not read on
- *     the host. The caller guarantees they describe the batch; kernels never read
- *     payload bytes outside [seg_addr[s], seg_addr[s] + seg_len[s]) whatever they
- *     hold.
+ *     the host. The caller guarantees they describe the batch; whatever they hold,
+ *     kernels read payload memory only in the aligned 8-byte words that contain
+ *     bytes of [seg_addr[s], seg_addr[s] + seg_len[s]) (so never another page).
  */
 #ifndef GLEAM_H
 #define GLEAM_H
