@@ -95,12 +95,16 @@ def xxh64(data, seed: int = 0) -> int:
 
 
 def node(left: int, right: int) -> int:
-    """Tree node: XXH64(LE64(left) || LE64(right), seed 0)."""
+    """Tree node: XXH64(LE64(left) || LE64(right), seed 0). The paper hashes a chunk's
+    bytes as its identifier (Sec. 4.1.2); folding leaf digests pairwise is this path's
+    reading for blocks larger than one leaf."""
     return int(_load().oracle_node(left, right))
 
 
 def tree(digests) -> int:
-    """Bottom-up pairwise tree over >= 1 leaf digests; an odd last element moves up unchanged."""
+    """Block identifier from its leaf digests (Sec. 4.1.2 identifier, leaf-tree reading):
+    bottom-up pairwise tree over >= 1 leaf digests; an odd last element moves up
+    unchanged; a single leaf's digest is the block's."""
     work = np.array(digests, dtype=np.uint64)
     if work.size == 0:
         raise ValueError("a block has at least one leaf")
@@ -113,7 +117,9 @@ def num_blocks(length: int, block_bytes: int) -> int:
 
 def payload_digests(payload, block_bytes: int, leaf_bytes: int = LEAF_BYTES,
                     with_leaves: bool = False, first_block: int = 0, count: int | None = None):
-    """Block digests (and optionally padded leaf digests) of one payload.
+    """Block digests (and optionally padded leaf digests) of one payload: Sec. 4.1.1's
+    payload (the bytes of one host-to-device copy) cut into blocks from its start, each
+    identified by the hash of its bytes (Sec. 4.1.2).
 
     Returns (block_digests u64[count], leaf_digests u64[count, block/leaf] or None).
     """
@@ -134,7 +140,9 @@ def payload_digests(payload, block_bytes: int, leaf_bytes: int = LEAF_BYTES,
 
 def geometry(seg_lens, block_bytes: int):
     """Per-batch geometry: blk_first[S+1] (exclusive prefix of blocks per payload)
-    and blk_len[n_blocks] (bytes of each block; only a payload's last block is short)."""
+    and blk_len[n_blocks] (bytes of each block; only a payload's last block is short).
+    Blocks restart at every payload start, since the decision is per host-to-device
+    copy (Sec. 4.1.1, 4.1.2); a zero-length payload has no blocks."""
     lens = np.asarray(seg_lens, dtype=np.uint64).reshape(-1)
     nblk = [num_blocks(n, block_bytes) for n in lens.tolist()]
     blk_first = np.zeros(len(nblk) + 1, dtype=np.uint64)
@@ -207,8 +215,10 @@ class Table:
         self.keys, self.vals, self.stamps = k[order], v[order], t[order]
 
     def insert(self, keys, vals) -> int:
-        """Insert in batch order: a key already present keeps its value; among equal
-        keys of this batch the lowest index wins. Returns the number of new keys."""
+        """Sec. 4.1.2 and 4.1.3: identified chunks join the server's identifier set.
+        Insert in batch order: a key already present keeps its value; among equal keys
+        of this batch the lowest index wins (the paper is silent on both; these are the
+        readings taken). Returns the number of new keys."""
         keys = np.asarray(keys, dtype=np.uint64).reshape(-1)
         vals = np.asarray(vals, dtype=np.uint64).reshape(-1)
         if keys.size != vals.size:
@@ -241,8 +251,8 @@ class Table:
 
     # -- lifecycle (Sec. 4.1.3: LRU eviction keeps the cache bounded) --------------- #
     def touch(self, keys, epochs) -> int:
-        """Stamp present keys with max(stamp, epoch). Returns how many keys (with
-        repetition) were present."""
+        """Sec. 4.1.3 (LRU over the shared pool): record a use. Stamp present keys with
+        max(stamp, epoch). Returns how many keys (with repetition) were present."""
         keys = np.asarray(keys, dtype=np.uint64).reshape(-1)
         epochs = np.broadcast_to(np.asarray(epochs, dtype=np.uint64), keys.shape)
         present = self.contains(keys)
@@ -251,8 +261,9 @@ class Table:
         return int(present.sum())
 
     def evict(self, keep: int) -> np.ndarray:
-        """Keep the `keep` most recently used entries: entries are ordered by (stamp, key)
-        ascending and the first len - keep are removed. Returns them in that order."""
+        """Sec. 4.1.3 LRU eviction: keep the `keep` most recently used entries. Entries are
+        ordered by (stamp, key) ascending (ties in last use: smaller key first, a reading)
+        and the first len - keep are removed. Returns them in that order."""
         n_evict = max(0, len(self) - int(keep))
         order = np.lexsort((self.keys, self.stamps))   # primary: stamp, secondary: key
         gone = order[:n_evict]
@@ -263,7 +274,8 @@ class Table:
         return evicted
 
     def erase(self, keys) -> int:
-        """Remove the given keys that are present. Returns how many entries went."""
+        """Sec. 4.1.3: chunks leave the shared pool. Remove the given keys that are
+        present. Returns how many entries went."""
         keys = np.unique(np.asarray(keys, dtype=np.uint64).reshape(-1))
         gone = self.contains(keys)
         mask = ~np.isin(self.keys, keys[gone])
@@ -277,7 +289,10 @@ class Table:
 
 
 def lookup(digests, table: Table):
-    """status u8[n] and ref u64[n] for a batch of block digests.
+    """status u8[n] and ref u64[n] for a batch of block digests (Sec. 4.1.2: a held
+    identifier means only the identifier and size travel; any other chunk sends its
+    bytes; the paper is silent on a chunk repeated inside one batch, and the reading
+    taken is that only its earliest copy travels).
 
     HIT_CACHE (1): digest in the table; ref = its value.
     HIT_BATCH (2): otherwise, an earlier block g0 < g has the same digest; ref = the
@@ -306,7 +321,8 @@ def lookup(digests, table: Table):
 
 
 def compact(status, blk_len=None):
-    """Ascending MISS block indices, their count, and (given blk_len) their total bytes."""
+    """The bytes that must still travel (Sec. 4.1.2: on a miss the full chunk is sent):
+    ascending MISS block indices, their count, and (given blk_len) their total bytes."""
     st = np.asarray(status, dtype=np.uint8).reshape(-1)
     idx = np.flatnonzero(st == MISS).astype(np.uint64)
     nbytes = None
@@ -316,7 +332,7 @@ def compact(status, blk_len=None):
 
 
 def run(payloads, block_bytes: int, table: Table, threads: int = 1):
-    """The whole path: digests -> lookup -> compaction for one batch."""
+    """The whole decision of Sec. 4.1.2 for one batch: digests -> lookup -> compaction."""
     digests, _ = batch_digests(payloads, block_bytes, threads=threads)
     _, blk_len = geometry([_as_u8(p).size for p in payloads], block_bytes)
     status, ref = lookup(digests, table)
