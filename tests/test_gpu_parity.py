@@ -269,7 +269,7 @@ def colliding_keys(rng, count, top_bits):
 # Lookups of up to 4,096 keys dedup in one workgroup's LDS table of 8,192 slots; larger
 # ones in a workspace table of a power of two >= 2n slots.
 @pytest.mark.parametrize("n_keys,repeats,filler", [(8, 5, 0), (24, 3, 0), (40, 1, 0), (40, 4, 3_900),
-                                                   (30, 3, 20_000)])
+                                                   (40, 4, 10_000), (30, 3, 20_000)])
 def test_dedup_collisions_with_duplicates(n_keys, repeats, filler):
     # the colliding keys all start probing at one slot of the dedup table the lookup uses,
     # duplicates interleaved at random (and random filler keys): the lowest index must win
@@ -302,7 +302,7 @@ def test_dedup_collisions_with_duplicates(n_keys, repeats, filler):
     assert np.array_equal(st2.cpu().numpy(), est2) and np.array_equal(u64(ref2), eref2)
 
 
-@pytest.mark.parametrize("n", [4_095, 4_096, 4_097])
+@pytest.mark.parametrize("n", [4_095, 4_096, 4_097, 16_384, 16_385])
 def test_lookup_at_single_workgroup_limit(n):
     rng = np.random.default_rng(850 + n)
     pool = np.concatenate([rng.integers(0, 2**64, n // 3, dtype=np.uint64, endpoint=False),
