@@ -416,6 +416,52 @@ WORKLOADS = {"decoder7b": build_decoder7b, "random16": build_random16, "small_co
              "resnet50": build_resnet50, "large_bf16": build_large_bf16}
 
 
+def per_buffer_leg(g, torch, batch, table, count, keep):
+    """The first `count` payloads, each as its own fingerprint -> lookup -> compaction
+    (descriptors, outputs and workspaces prepared before timing), against the same
+    payloads as one batched pass."""
+    src = payload_tensor(keep)
+    base = src.data_ptr()
+    addr = batch.d_addr.cpu().numpy().view(np.uint64)[:count]
+    lens = batch.host_len[:count]
+    singles = []
+    for a, n in zip(addr.tolist(), lens.tolist()):
+        b = g.Batch.from_arena(src, [a - base], [n], batch.block_bytes)
+        m = max(b.n_blocks, 1)
+        singles.append((b, torch.empty(m, dtype=torch.int64, device="cuda"),
+                        torch.empty(m, dtype=torch.uint8, device="cuda"), torch.empty(m, dtype=torch.int64, device="cuda"),
+                        torch.empty(m, dtype=torch.int64, device="cuda"), torch.zeros(2, dtype=torch.int64, device="cuda"),
+                        g.workspace(m)))
+    joint = g.Batch.from_arena(src, (addr - np.uint64(base)).astype(np.uint64), lens, batch.block_bytes)
+    nj = joint.n_blocks
+    jo = (torch.empty(nj, dtype=torch.int64, device="cuda"), torch.empty(nj, dtype=torch.uint8, device="cuda"),
+          torch.empty(nj, dtype=torch.int64, device="cuda"), torch.empty(nj, dtype=torch.int64, device="cuda"),
+          torch.zeros(2, dtype=torch.int64, device="cuda"), g.workspace(nj))
+
+    def one(b, d, st, ref, idx, cnt, ws):
+        g.fp_chunks(b, out=d)
+        table.lookup(d[:b.n_blocks], status=st, ref=ref, ws=ws)
+        g.miss_compact(st[:b.n_blocks], b, miss_idx=idx, counters=cnt, ws=ws)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        e.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(e)
+
+    ms_each = timed(lambda: [one(*x) for x in singles])
+    ms_joint = timed(lambda: one(joint, *jo))
+    nbytes = int(lens.sum())
+    return {"buffers": count, "bytes": nbytes, "separate_ms": round(ms_each, 4),
+            "separate_us_per_buffer": round(ms_each * 1e3 / count, 2),
+            "separate_gbs": round(nbytes / (ms_each * 1e-3) / 1e9, 2), "batched_ms": round(ms_joint, 4),
+            "batched_gbs": round(nbytes / (ms_joint * 1e-3) / 1e9, 2)}
+
+
 def pipelined_leg(g, torch, batch, table, K, warmup, expect_miss, n, ws):
     """K detect steps with each step's lookup + compaction on a second stream, overlapping
     the next step's fingerprint. Digests are double-buffered; a fingerprint waits for the
@@ -550,6 +596,9 @@ def main():
                          "identification; md5prefix: the paper's MD5-of-first-1024-bits identifier")
     ap.add_argument("--no-flush", action="store_true",
                     help="skip the cold leg (K more steps, each after writing 1 GiB to evict L2 and MALL)")
+    ap.add_argument("--per-buffer", type=int, default=0, metavar="N",
+                    help="detect path: also time the first N payloads as N separate calls (one payload "
+                         "each), to show what batching saves in launches")
     ap.add_argument("--pipeline", action="store_true",
                     help="detect path: overlap each batch's lookup and compaction (second stream) with the "
                          "next batch's fingerprint (double-buffered digests); every step still does all its work")
@@ -656,6 +705,11 @@ def main():
         torch.cuda.synchronize()
     fp_ms = [a.elapsed_time(b) for a, b in ev_fp]
 
+    per_buffer = None
+    if args.per_buffer > 0:
+        per_buffer = per_buffer_leg(g, torch, batch, table, args.per_buffer, keep)
+        log(f"per-buffer calls: {per_buffer}")
+
     pipe = None
     if args.pipeline:
         pipe = pipelined_leg(g, torch, batch, table, K, args.warmup, expect_miss, n, ws)
@@ -733,7 +787,7 @@ def main():
                    "launch": "hip_graph" if graph is not None else "eager",
                    "step_ms": {"median": round(float(np.median(warm_ms)), 4), "min": round(min(warm_ms), 4),
                                "max": round(max(warm_ms), 4)},
-                   "cold": cold, "insert_ms": insert_ms, "pipelined": pipe},
+                   "cold": cold, "insert_ms": insert_ms, "pipelined": pipe, "per_buffer": per_buffer},
         "roofline": {"bound": "hbm", "kernel": "fp_kernel", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes": algo_bytes, "avg_launch_ms": round(fp_avg_ms, 4),
