@@ -58,7 +58,7 @@ def test_digests_every_block_size(block):
 
 
 @pytest.mark.parametrize("skew", [1, 3, 8, 12])
-@pytest.mark.parametrize("block", [4096, 65536, 1 << 20])
+@pytest.mark.parametrize("block", [4096, 65536, 256 << 10, 1 << 20, 2 << 20, 16 << 20])
 def test_unaligned_payload_starts(skew, block):
     rng = np.random.default_rng(200 + skew + block.bit_length())
     payloads = make_payloads(rng, block)
@@ -71,7 +71,7 @@ def test_unaligned_payload_starts(skew, block):
     assert np.array_equal(gpu["leaves"], ref["leaves"])
 
 
-@pytest.mark.parametrize("block", [4096, 65536])
+@pytest.mark.parametrize("block", [4096, 65536, 1 << 20])
 def test_mixed_alignment_in_one_wave(block):
     """Aligned and unaligned payloads side by side, so waves mix both kinds."""
     rng = np.random.default_rng(250 + block.bit_length())
@@ -131,7 +131,7 @@ def mixed_layout_payloads(rng, block, min_slots):
 
 # Batches of blocks up to 64 KiB and at most 65,536 leaf slots use the four-lanes-per-leaf
 # kernel; larger ones the two-lanes-per-leaf kernel. Same layouts on both sides.
-@pytest.mark.parametrize("block", [4096, 65536])
+@pytest.mark.parametrize("block", [4096, 8192, 32768, 65536])
 @pytest.mark.parametrize("min_slots", [60_000, 70_000])
 def test_both_small_block_kernels_on_mixed_layouts(block, min_slots):
     rng = np.random.default_rng(950 + block + min_slots)
