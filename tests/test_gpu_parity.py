@@ -427,3 +427,26 @@ def test_empty_inputs():
     batch = g.Batch.from_arena(to_device(arena), offs, lens, 4096)
     gpu = run_path(batch, table)
     assert_same(gpu, oracle_path(payloads, 4096, oracle.Table()), "zero-length")
+
+
+@pytest.mark.parametrize("n", [1_000, 10_000, 100_000])  # one-workgroup and grid lookups; both compactions
+def test_optional_outputs_absent(n):
+    """Lookup without the ref output and compaction without a batch (no byte total) give
+    the same statuses and miss lists as with them."""
+    rng = np.random.default_rng(1500 + n)
+    pool = rng.integers(0, 2**64, n // 2, dtype=np.uint64, endpoint=False)
+    keys = pool[rng.integers(0, pool.size, n)]
+    table, ot = g.Cache(1 << 17), oracle.Table()
+    cached = pool[: pool.size // 3]
+    table.insert(keys_to_device(cached), keys_to_device(cached))
+    ot.insert(cached, cached)
+    say("optional outputs", n)
+    st_noref, ref_none = table.lookup(keys_to_device(keys), want_ref=False)
+    assert ref_none is None
+    miss_idx, counters = g.miss_compact(st_noref)  # no batch: count only
+    torch.cuda.synchronize()
+    est, _ = oracle.lookup(keys, ot)
+    eidx, ecnt, _ = oracle.compact(est)
+    assert np.array_equal(st_noref.cpu().numpy(), est)
+    assert int(u64(counters)[0]) == ecnt
+    assert np.array_equal(u64(miss_idx)[:ecnt], eidx)
