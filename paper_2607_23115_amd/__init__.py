@@ -160,7 +160,11 @@ class Batch:
 
     @classmethod
     def from_tensors(cls, tensors, block_bytes: int) -> "Batch":
-        """One payload per device tensor (its whole storage extent as bytes)."""
+        """One payload per contiguous device tensor: its bytes, from data_ptr() for
+        numel() * element_size() bytes (a non-contiguous view is refused)."""
+        for t in tensors:
+            if not t.is_contiguous():
+                raise ValueError("Batch.from_tensors needs contiguous tensors (call .contiguous() first)")
         addr = [t.data_ptr() for t in tensors]
         lens = [t.numel() * t.element_size() for t in tensors]
         dev = tensors[0].device if tensors else "cuda"

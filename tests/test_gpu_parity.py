@@ -450,3 +450,26 @@ def test_optional_outputs_absent(n):
     assert np.array_equal(st_noref.cpu().numpy(), est)
     assert int(u64(counters)[0]) == ecnt
     assert np.array_equal(u64(miss_idx)[:ecnt], eidx)
+
+
+def test_batch_from_tensors():
+    """Payloads given as torch tensors (several dtypes, contiguous slices at odd byte
+    offsets): the digests are those of each tensor's bytes."""
+    torch.manual_seed(1600)
+    base = torch.randint(-128, 127, (300_000,), dtype=torch.int8, device="cuda")
+    tensors = [torch.randn(257, 129, device="cuda").to(torch.float16),
+               torch.randn(70_000, device="cuda").to(torch.bfloat16),
+               torch.randn(33, 1000, device="cuda"),
+               base[3:200_003],          # contiguous, 3 bytes into its storage
+               base[100_001:100_001],    # empty
+               torch.arange(5, dtype=torch.int64, device="cuda")]
+    say("batch from tensors")
+    batch = g.Batch.from_tensors(tensors, 65536)
+    d = g.fp_chunks(batch)
+    torch.cuda.synchronize()
+    payloads = [t.cpu().contiguous().view(torch.uint8).numpy() if t.numel() else np.zeros(0, np.uint8)
+                for t in tensors]
+    want, _ = oracle.batch_digests(payloads, 65536)
+    assert np.array_equal(u64(d), want)
+    with pytest.raises(ValueError):
+        g.Batch.from_tensors([torch.zeros(8, 8, device="cuda").t()], 65536)
