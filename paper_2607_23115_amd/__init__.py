@@ -101,6 +101,28 @@ def _ptr(t: torch.Tensor | None):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _dev(t: torch.Tensor | None, name: str, dtypes, min_numel: int = 0, optional: bool = False):
+    """Check a tensor handed to the library: on a GPU, contiguous, of the expected dtype
+    and at least min_numel elements (the kernels read and write plain memory)."""
+    if t is None:
+        if optional:
+            return None
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a tensor on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise ValueError(f"{name} must be {' or '.join(str(d) for d in dtypes)}, not {t.dtype}")
+    if t.numel() < min_numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, {min_numel} needed")
+    return t
+
+
+_U64 = (torch.int64,)
+_U8 = (torch.uint8,)
+
+
 def _stream(stream) -> ctypes.c_void_p:
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -186,6 +208,8 @@ def fp_chunks(batch: Batch, out: torch.Tensor | None = None, leaf_out: torch.Ten
         out = torch.empty(max(batch.n_blocks, 1), dtype=torch.int64, device=dev)
     if with_leaves and leaf_out is None:
         leaf_out = torch.empty(max(batch.n_blocks * batch.leaves_per_block, 1), dtype=torch.int64, device=dev)
+    _dev(out, "out", _U64, batch.n_blocks)
+    _dev(leaf_out, "leaf_out", _U64, batch.n_blocks * batch.leaves_per_block, optional=True)
     _check(lib.gleam_fp_chunks(ctypes.byref(batch.c_struct()), _ptr(out), _ptr(leaf_out), _stream(stream)))
     if with_leaves:
         return out[:batch.n_blocks], leaf_out[:batch.n_blocks * batch.leaves_per_block]
@@ -224,6 +248,10 @@ class Cache:
             ws = workspace(n, keys.device)
         if n_new is None:
             n_new = torch.empty(1, dtype=torch.int64, device=keys.device)
+        _dev(keys, "keys", _U64)
+        _dev(vals, "vals", _U64)
+        _dev(n_new, "n_new", _U64, 1)
+        _dev(ws, "ws", _U8)
         _check(lib.gleam_cache_insert(self.handle, _ptr(keys), _ptr(vals), n, _ptr(n_new), _ptr(ws), ws.numel(),
                                       _stream(stream)))
         return n_new
@@ -237,6 +265,10 @@ class Cache:
             ref = torch.empty(max(n, 1), dtype=torch.int64, device=keys.device)
         if ws is None:
             ws = workspace(n, keys.device)
+        _dev(keys, "keys", _U64)
+        _dev(status, "status", _U8, n)
+        _dev(ref, "ref", _U64, n, optional=True)
+        _dev(ws, "ws", _U8)
         _check(lib.gleam_cache_lookup(self.handle, _ptr(keys), n, _ptr(status), _ptr(ref), _ptr(ws), ws.numel(),
                                       _stream(stream)))
         return status[:n], (ref[:n] if ref is not None else None)
@@ -251,6 +283,8 @@ class Cache:
     def touch(self, keys: torch.Tensor, epochs: torch.Tensor | None = None, epoch: int = 0, stream=None):
         """Stamp present keys with max(stamp, epoch); returns the device count of present keys."""
         n_touched = torch.empty(1, dtype=torch.int64, device=keys.device)
+        _dev(keys, "keys", _U64)
+        _dev(epochs, "epochs", _U64, keys.numel(), optional=True)
         _check(lib.gleam_cache_touch(self.handle, _ptr(keys), keys.numel(), _ptr(epochs), epoch, _ptr(n_touched),
                                      _stream(stream)))
         return n_touched
@@ -260,6 +294,7 @@ class Cache:
         ws = self.maint_workspace() if ws is None else ws
         evicted = torch.empty(self.capacity + 1, dtype=torch.int64, device=ws.device)
         counts = torch.empty(2, dtype=torch.int64, device=ws.device)
+        _dev(ws, "ws", _U8)
         _check(lib.gleam_cache_evict(self.handle, keep, _ptr(evicted), _ptr(counts), _ptr(ws), ws.numel(),
                                      _stream(stream)))
         return evicted, counts
@@ -267,6 +302,8 @@ class Cache:
     def erase(self, keys: torch.Tensor, ws: torch.Tensor | None = None, stream=None):
         ws = self.maint_workspace() if ws is None else ws
         counts = torch.empty(2, dtype=torch.int64, device=ws.device)
+        _dev(keys, "keys", _U64)
+        _dev(ws, "ws", _U8)
         _check(lib.gleam_cache_erase(self.handle, _ptr(keys), keys.numel(), _ptr(counts), _ptr(ws), ws.numel(),
                                      _stream(stream)))
         return counts
@@ -279,6 +316,7 @@ class Cache:
         vals = torch.empty_like(keys)
         stamps = torch.empty_like(keys)
         count = torch.empty(1, dtype=torch.int64, device=dev)
+        _dev(ws, "ws", _U8)
         _check(lib.gleam_cache_export(self.handle, _ptr(keys), _ptr(vals), _ptr(stamps), _ptr(count), _ptr(ws),
                                       ws.numel(), _stream(stream)))
         return keys, vals, stamps, count
@@ -313,6 +351,10 @@ def miss_compact(status: torch.Tensor, batch: Batch | None = None, miss_idx: tor
     if ws is None:
         ws = workspace(n, dev)
     cb = ctypes.byref(batch.c_struct()) if batch is not None else None
+    _dev(status, "status", _U8)
+    _dev(miss_idx, "miss_idx", _U64, n)
+    _dev(counters, "counters", _U64, 2 if batch is not None else 1)
+    _dev(ws, "ws", _U8)
     bytes_ptr = ctypes.c_void_p(counters.data_ptr() + 8) if batch is not None else None
     _check(lib.gleam_miss_compact(_ptr(status), n, cb, _ptr(miss_idx), _ptr(counters), bytes_ptr, _ptr(ws),
                                   ws.numel(), _stream(stream)))
@@ -332,6 +374,9 @@ def identify_weights(batch: Batch, recorded: torch.Tensor, region_first, ws: tor
     region_weight = torch.empty(max(n_regions, 1), dtype=torch.uint8, device=dev)
     if ws is None:
         ws = workspace(batch.n_blocks + batch.n_seg, dev)
+    _dev(recorded, "recorded", _U64, batch.n_blocks)
+    _dev(rf, "region_first", _U64, 1)
+    _dev(ws, "ws", _U8)
     _check(lib.gleam_identify_weights(ctypes.byref(batch.c_struct()), _ptr(recorded), _ptr(rf), n_regions,
                                       _ptr(block_match), _ptr(first_diff), _ptr(region_weight), _ptr(ws),
                                       ws.numel(), _stream(stream)))
@@ -364,12 +409,18 @@ def send_plan(batch: Batch, digests: torch.Tensor, status: torch.Tensor, ref: to
     totals = torch.empty(4, dtype=torch.int64, device=dev)
     if ws is None:
         ws = workspace(batch.n_blocks, dev)
+    _dev(digests, "digests", _U64, batch.n_blocks)
+    _dev(status, "status", _U8, batch.n_blocks)
+    _dev(ref, "ref", _U64, batch.n_blocks)
+    _dev(ws, "ws", _U8)
     _check(lib.gleam_send_plan(ctypes.byref(batch.c_struct()), _ptr(digests), _ptr(status), _ptr(ref),
                                _ptr(records), _ptr(totals), _ptr(ws), ws.numel(), _stream(stream)))
     return records[:batch.n_blocks * RECORD_BYTES], totals
 
 
 def pack_misses(batch: Batch, records: torch.Tensor, out: torch.Tensor, stream=None) -> torch.Tensor:
+    _dev(records, "records", _U8, batch.n_blocks * RECORD_BYTES)
+    _dev(out, "out", _U8)
     _check(lib.gleam_pack_misses(ctypes.byref(batch.c_struct()), _ptr(records), _ptr(out), out.numel(),
                                  _stream(stream)))
     return out
@@ -377,6 +428,9 @@ def pack_misses(batch: Batch, records: torch.Tensor, out: torch.Tensor, stream=N
 
 def restore_blocks(dst: Batch, records: torch.Tensor, packed: torch.Tensor, held: torch.Tensor | None = None,
                    stream=None) -> None:
+    _dev(records, "records", _U8, dst.n_blocks * RECORD_BYTES)
+    _dev(packed, "packed", _U8)
+    _dev(held, "held", _U64, dst.n_blocks, optional=True)
     _check(lib.gleam_restore_blocks(ctypes.byref(dst.c_struct()), _ptr(records), _ptr(packed), packed.numel(),
                                     _ptr(held), _stream(stream)))
 
@@ -388,6 +442,10 @@ def read_stream(src: torch.Tensor, nbytes: int | None = None, sink: torch.Tensor
     nbytes = src.numel() * src.element_size() if nbytes is None else int(nbytes)
     if sink is None:
         sink = torch.zeros(1, dtype=torch.int64, device=src.device)
+    _dev(src, "src", None)
+    if nbytes > src.numel() * src.element_size():
+        raise ValueError("nbytes exceeds the source tensor")
+    _dev(sink, "sink", _U64, 1)
     _check(lib.gleam_read_stream(_ptr(src), nbytes, _ptr(sink), _stream(stream)))
     return sink
 

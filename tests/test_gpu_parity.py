@@ -473,3 +473,19 @@ def test_batch_from_tensors():
     assert np.array_equal(u64(d), want)
     with pytest.raises(ValueError):
         g.Batch.from_tensors([torch.zeros(8, 8, device="cuda").t()], 65536)
+
+
+def test_binding_refuses_tensors_the_kernels_would_misread():
+    batch = g.Batch.from_arena(torch.zeros(1 << 16, dtype=torch.uint8, device="cuda"), [0], [1 << 16], 4096)
+    table = g.Cache(1 << 10)
+    keys = torch.zeros(16, dtype=torch.int64, device="cuda")
+    with pytest.raises(ValueError):  # wrong dtype
+        g.fp_chunks(batch, out=torch.zeros(16, dtype=torch.int32, device="cuda"))
+    with pytest.raises(ValueError):  # too short
+        g.fp_chunks(batch, out=torch.zeros(8, dtype=torch.int64, device="cuda"))
+    with pytest.raises(ValueError):  # not contiguous
+        table.lookup(torch.zeros(16, 2, dtype=torch.int64, device="cuda")[:, 0])
+    with pytest.raises(ValueError):  # host memory
+        table.insert(keys.cpu(), keys)
+    with pytest.raises(ValueError):  # status must be u8
+        g.miss_compact(torch.zeros(16, dtype=torch.int64, device="cuda"))
