@@ -24,7 +24,8 @@ The oracle computes, per fixed-size block of each payload:
                    equal keys of one insert batch the lowest index's value wins
 
 The fingerprint is C (gleam_oracle.c) because the oracle must digest tens of GB;
-everything after it is numpy.
+everything after it is numpy. remap.py holds the address-remap interval map of the
+weight-sharing layer (Sec. 4.3, Sec. 6).
 """
 
 from __future__ import annotations
