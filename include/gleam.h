@@ -24,6 +24,8 @@
  *                          1024 bits), as an ablation
  *   gleam_send_plan / gleam_pack_misses / gleam_restore_blocks -- the transfer
  *                          around the decision: what travels, packed, and rebuilt
+ *   gleam_remap_*       -- the address-remap map of the weight-sharing layer: ranges
+ *                          of client device addresses onto shareable positions (4.3)
  *   gleam_read_stream   -- calibration only: the measured HBM read ceiling
  *
  * Conventions for every entry point:
@@ -41,12 +43,12 @@
  *     error a negative status is returned and nothing has been enqueued. A HIP
  *     launch failure returns GLEAM_E_HIP; gleam_last_error() then holds the HIP
  *     message (thread-local).
- *   - HIP graph capture: every call except gleam_cache_evict, _erase and _export
- *     enqueues kernel launches only (clears are fill kernels, not memsets), so a
- *     caller may capture it in a graph and replay it. gleam_cache_insert's host-side
- *     key bound grows once, when the call is captured, not on each replay. Evict,
- *     erase and export sort with rocPRIM, which also enqueues memsets; keep them out
- *     of captured graphs.
+ *   - HIP graph capture: every call except gleam_cache_evict, _erase, _export and
+ *     gleam_remap_update enqueues kernel launches only (clears are fill kernels, not
+ *     memsets), so a caller may capture it in a graph and replay it.
+ *     gleam_cache_insert's host-side key bound grows once, when the call is captured,
+ *     not on each replay. The four exceptions sort or scan with rocPRIM, which also
+ *     enqueues memsets; keep them out of captured graphs.
  *   - Device descriptor contents (seg_addr, seg_len, blk_first) are not read on
  *     the host. The caller guarantees they describe the batch; whatever they hold,
  *     kernels read payload memory only in the aligned 8-byte words that contain
@@ -360,6 +362,83 @@ gleam_status gleam_pack_misses(const gleam_batch* b, const gleam_send_record* d_
 gleam_status gleam_restore_blocks(const gleam_batch* dst, const gleam_send_record* d_records,
                                   const uint8_t* d_packed, uint64_t packed_bytes, const uint64_t* d_held,
                                   void* stream);
+
+/*
+ * Address-remap map (Sec. 4.3, weight sharing: two chunks written into one client
+ * allocation may find their shareable copies in two different server allocations, so
+ * a virtual memory layer maps client device addresses onto the actual shareable
+ * positions; Sec. 6: each task gets a 1 TB virtual address space and the mappings are
+ * kept in a red-black tree). Device pointers carried by remoted calls are translated
+ * through it.
+ *
+ * The map holds disjoint, non-empty intervals [start, start + length) of the 64-bit
+ * address space, each with a target: address p inside one translates to
+ * target + (p - start), any other address to GLEAM_UNMAPPED. One map may serve many
+ * tasks when each task's addresses live in a range of its own (e.g. task t at
+ * [t << 40, (t + 1) << 40), the paper's 1 TB per task). Storage is caller-owned device
+ * memory that must outlive the handle: a 256-byte header (u64 interval count, fence
+ * stride, fence length), u64 start[capacity] sorted ascending, {end (exclusive),
+ * target}[capacity] pairs in the same order, and a 4096-entry fence (every stride-th
+ * start) that translation searches in LDS first. Calls on one map must not overlap, on
+ * any stream, with an update of it.
+ *
+ * gleam_remap_bytes: storage bytes for `capacity` intervals (1 <= capacity <= 2^31):
+ * 256 + 24 * capacity + 32768; 0 for an invalid capacity.
+ *
+ * gleam_remap_create: a handle over d_storage (device, 256-byte aligned, >=
+ * gleam_remap_bytes(capacity) bytes) and the clear of its header (an empty map).
+ * *out (host) receives the handle, freed by gleam_remap_destroy (storage untouched;
+ * NULL allowed). Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
+ *
+ * gleam_remap_update: one batch of changes, removals first, then additions:
+ *   d_del_start, d_del_len   device u64[n_del]: every interval sharing an address with
+ *                            a range [start, start + len) (clipped at 2^64; len 0 is an
+ *                            empty range) is removed whole
+ *   d_add_start, d_add_len, d_add_target   device u64[n_add]: intervals to add
+ *   d_add_status  nullable device u8[n_add]: GLEAM_REMAP_ADDED; GLEAM_REMAP_INVALID
+ *                 (length 0, or start + length or target + length above 2^64 - 1);
+ *                 GLEAM_REMAP_OVERLAP (shares an address with a surviving interval or
+ *                 with another valid addition of this call: both of two clashing
+ *                 additions are refused, whatever their order); GLEAM_REMAP_FULL
+ *   d_counts      device u64[4]: {intervals after, added, removed, additions refused}
+ *   d_ws          device workspace, 256-byte aligned,
+ *                 >= gleam_remap_update_bytes(m, n_add, n_del)
+ * If the survivors and the accepted additions exceed the capacity, the map is left
+ * exactly as it was (the removals included) and those additions get GLEAM_REMAP_FULL.
+ * The work is O(capacity + n_add) whatever the count: size the capacity to the map.
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED (n_add or n_del
+ * above 2^31), GLEAM_E_HIP. gleam_remap_update_bytes returns 0 for a NULL map, counts
+ * above 2^31 or a failed rocPRIM storage query.
+ *
+ * gleam_remap_translate: d_out[i] (device u64[n]) = the translation of d_addr[i]
+ * (device u64[n]). The map is only read. Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
+ *
+ * gleam_remap_export: the intervals in start order into device u64[capacity] arrays
+ * d_start, d_len, d_target; *d_count (device u64[1]) = their number. Adding the
+ * exported intervals to an empty map rebuilds it. Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
+ */
+typedef struct gleam_remap gleam_remap;
+enum {
+  GLEAM_REMAP_ADDED = 0,
+  GLEAM_REMAP_INVALID = 1,
+  GLEAM_REMAP_OVERLAP = 2,
+  GLEAM_REMAP_FULL = 3
+};
+#define GLEAM_UNMAPPED UINT64_MAX
+
+size_t gleam_remap_bytes(uint64_t capacity);
+gleam_status gleam_remap_create(void* d_storage, size_t bytes, uint64_t capacity, gleam_remap** out,
+                                void* stream);
+gleam_status gleam_remap_destroy(gleam_remap* m);
+size_t gleam_remap_update_bytes(const gleam_remap* m, uint64_t n_add, uint64_t n_del);
+gleam_status gleam_remap_update(gleam_remap* m, const uint64_t* d_del_start, const uint64_t* d_del_len,
+                                uint64_t n_del, const uint64_t* d_add_start, const uint64_t* d_add_len,
+                                const uint64_t* d_add_target, uint64_t n_add, uint8_t* d_add_status,
+                                uint64_t* d_counts, void* d_ws, size_t ws_bytes, void* stream);
+gleam_status gleam_remap_translate(const gleam_remap* m, const uint64_t* d_addr, uint64_t n, uint64_t* d_out,
+                                   void* stream);
+gleam_status gleam_remap_export(const gleam_remap* m, uint64_t* d_start, uint64_t* d_len, uint64_t* d_target,
+                                uint64_t* d_count, void* stream);
 
 /*
  * Calibration (a measurement aid, not a step of the path): read `bytes` bytes at d_src

@@ -82,9 +82,12 @@ class RemapMap:
         keep = np.ones(len(self), bool)
         if rs.size and len(self):
             nz = rl > 0
-            r_first = rs[nz]
-            # last address of [d, d + dlen), clipped at 2^64 - 1 (in Python ints: no wrap)
-            r_last = np.array([min(int(d) + int(n) - 1, _TOP) for d, n in zip(r_first, rl[nz])], np.uint64)
+            r_first, r_len = rs[nz], rl[nz]
+            # last address of [d, d + dlen), clipped at 2^64 - 1: d + (dlen - 1) passes the
+            # top exactly when dlen - 1 > (2^64 - 1) - d
+            top = np.uint64(_TOP)
+            over = (r_len - np.uint64(1)) > top - r_first
+            r_last = np.where(over, top, r_first + (r_len - np.uint64(1)))  # (the unused sum may wrap)
             if r_first.size:
                 last = self.start + (self.length - np.uint64(1))
                 keep = overlap_counts(self.start, last, r_first, r_last) == 0
@@ -92,11 +95,10 @@ class RemapMap:
         s_start, s_len, s_target = self.start[keep], self.length[keep], self.target[keep]
 
         # 2. invalid additions
+        # (s + n > 2^64 - 1 is s > (2^64 - 1) - n, which cannot wrap in u64)
+        top = np.uint64(_TOP)
         status = np.full(n_add, ADDED, np.uint8)
-        for i in range(n_add):
-            s, n, t = int(a_s[i]), int(a_l[i]), int(a_t[i])
-            if n == 0 or s + n > _TOP or t + n > _TOP:
-                status[i] = INVALID
+        status[(a_l == 0) | (a_s > top - a_l) | (a_t > top - a_l)] = INVALID
         valid = status == ADDED
 
         # 3. overlaps with survivors and with the other valid additions

@@ -25,6 +25,8 @@ LIB_PATH = os.path.join(_PKG, "libgleam.so")
 
 OK, E_INVALID, E_CAPACITY, E_WORKSPACE, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 MISS, HIT_CACHE, HIT_BATCH = 0, 1, 2
+REMAP_ADDED, REMAP_INVALID, REMAP_OVERLAP, REMAP_FULL = 0, 1, 2, 3
+UNMAPPED = (1 << 64) - 1
 LEAF_BYTES = 4096
 
 EXPORTS = (
@@ -33,7 +35,8 @@ EXPORTS = (
     "gleam_miss_compact", "gleam_status_string", "gleam_last_error", "gleam_identify_weights",
     "gleam_md5_prefix", "gleam_cache_maint_bytes", "gleam_cache_touch", "gleam_cache_evict", "gleam_cache_erase",
     "gleam_cache_export", "gleam_cache_set_key_bound", "gleam_send_plan", "gleam_pack_misses",
-    "gleam_restore_blocks", "gleam_read_stream",
+    "gleam_restore_blocks", "gleam_read_stream", "gleam_remap_bytes", "gleam_remap_create", "gleam_remap_destroy",
+    "gleam_remap_update_bytes", "gleam_remap_update", "gleam_remap_translate", "gleam_remap_export",
 )
 
 
@@ -78,6 +81,13 @@ def _load() -> ctypes.CDLL:
         "gleam_pack_misses": ([ctypes.POINTER(_Batch), vp, vp, u64, vp], st),
         "gleam_restore_blocks": ([ctypes.POINTER(_Batch), vp, vp, u64, vp, vp], st),
         "gleam_read_stream": ([vp, u64, vp, vp], st),
+        "gleam_remap_bytes": ([u64], sz),
+        "gleam_remap_create": ([vp, sz, u64, ctypes.POINTER(vp), vp], st),
+        "gleam_remap_destroy": ([vp], st),
+        "gleam_remap_update_bytes": ([vp, u64, u64], sz),
+        "gleam_remap_update": ([vp, vp, vp, u64, vp, vp, vp, u64, vp, vp, vp, sz, vp], st),
+        "gleam_remap_translate": ([vp, vp, u64, vp, vp], st),
+        "gleam_remap_export": ([vp, vp, vp, vp, vp, vp], st),
         "gleam_status_string": ([st], ctypes.c_char_p),
         "gleam_last_error": ([], ctypes.c_char_p),
     }
@@ -327,6 +337,99 @@ class Cache:
     def close(self) -> None:
         if self._h is not None:
             lib.gleam_cache_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Remap:
+    """The address-remap map of the weight-sharing layer over a torch-allocated storage
+    tensor: disjoint intervals of client device addresses, each mapped onto a target."""
+
+    def __init__(self, capacity: int, device="cuda", stream=None):
+        nbytes = int(lib.gleam_remap_bytes(capacity))
+        if nbytes == 0:
+            raise GleamError(E_INVALID, f"invalid capacity {capacity}")
+        self.capacity = capacity
+        self.storage = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        h = ctypes.c_void_p()
+        _check(lib.gleam_remap_create(_ptr(self.storage), nbytes, capacity, ctypes.byref(h), _stream(stream)))
+        self._h = h
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        if self._h is None:
+            raise GleamError(E_INVALID, "map handle already destroyed")
+        return self._h
+
+    def update_workspace(self, n_add: int, n_del: int) -> torch.Tensor:
+        n = int(lib.gleam_remap_update_bytes(self.handle, n_add, n_del))
+        if n == 0:
+            raise GleamError(E_UNSUPPORTED, "no update workspace for these sizes")
+        return torch.empty(n, dtype=torch.uint8, device=self.storage.device)
+
+    def update(self, del_start: torch.Tensor | None = None, del_len: torch.Tensor | None = None,
+               add_start: torch.Tensor | None = None, add_len: torch.Tensor | None = None,
+               add_target: torch.Tensor | None = None, status: torch.Tensor | None = None,
+               counts: torch.Tensor | None = None, ws: torch.Tensor | None = None, want_status: bool = True,
+               stream=None):
+        """Removals, then additions: (status u8[n_add] or None, counts int64[4] =
+        {intervals after, added, removed, refused}) on the device."""
+        dev = self.storage.device
+        n_del = 0 if del_start is None else del_start.numel()
+        n_add = 0 if add_start is None else add_start.numel()
+        if n_del and (del_len is None or del_len.numel() != n_del):
+            raise ValueError("del_start and del_len differ in length")
+        if n_add and (add_len is None or add_target is None or add_len.numel() != n_add
+                      or add_target.numel() != n_add):
+            raise ValueError("add_start, add_len and add_target differ in length")
+        if status is None and want_status:
+            status = torch.empty(max(n_add, 1), dtype=torch.uint8, device=dev)
+        if counts is None:
+            counts = torch.empty(4, dtype=torch.int64, device=dev)
+        if ws is None:
+            ws = self.update_workspace(n_add, n_del)
+        for t, name in ((del_start, "del_start"), (del_len, "del_len")):
+            _dev(t, name, _U64, n_del, optional=n_del == 0)
+        for t, name in ((add_start, "add_start"), (add_len, "add_len"), (add_target, "add_target")):
+            _dev(t, name, _U64, n_add, optional=n_add == 0)
+        _dev(status, "status", _U8, n_add, optional=True)
+        _dev(counts, "counts", _U64, 4)
+        _dev(ws, "ws", _U8)
+        live = (lambda t, n: _ptr(t) if n else None)
+        _check(lib.gleam_remap_update(self.handle, live(del_start, n_del), live(del_len, n_del), n_del,
+                                      live(add_start, n_add), live(add_len, n_add), live(add_target, n_add),
+                                      n_add, _ptr(status), _ptr(counts), _ptr(ws), ws.numel(), _stream(stream)))
+        return (status[:n_add] if status is not None else None), counts
+
+    def translate(self, addr: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """target + (p - start) for each address inside an interval, else UNMAPPED (-1)."""
+        n = addr.numel()
+        if out is None:
+            out = torch.empty(max(n, 1), dtype=torch.int64, device=addr.device)
+        _dev(addr, "addr", _U64)
+        _dev(out, "out", _U64, n)
+        _check(lib.gleam_remap_translate(self.handle, _ptr(addr), n, _ptr(out), _stream(stream)))
+        return out[:n]
+
+    def export(self, stream=None):
+        """(start, length, target, count): the first count intervals, in start order."""
+        dev = self.storage.device
+        start = torch.empty(self.capacity, dtype=torch.int64, device=dev)
+        length = torch.empty_like(start)
+        target = torch.empty_like(start)
+        count = torch.empty(1, dtype=torch.int64, device=dev)
+        _check(lib.gleam_remap_export(self.handle, _ptr(start), _ptr(length), _ptr(target), _ptr(count),
+                                      _stream(stream)))
+        return start, length, target, count
+
+    def close(self) -> None:
+        if self._h is not None:
+            lib.gleam_remap_destroy(self._h)
             self._h = None
 
     def __del__(self):

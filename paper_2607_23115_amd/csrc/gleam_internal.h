@@ -18,6 +18,13 @@ struct gleam_cache {
   uint64_t key_bound;  // upper bound on keys present
 };
 
+// Host view of an address-remap map: storage = [256-byte header][capacity x start]
+// [capacity x {end, target}][fence], sorted by start (layout in remap.hip).
+struct gleam_remap {
+  uint8_t* storage;
+  uint64_t capacity;
+};
+
 namespace gleam {
 
 constexpr size_t kHeaderBytes = 256;

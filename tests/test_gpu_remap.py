@@ -1,0 +1,245 @@
+"""GPU parity of the address-remap map (Sec. 4.3 weight sharing; Sec. 6 virtual memory
+map): after every update the statuses, counts and exported intervals equal the
+oracle's bit for bit, and so does the translation of every probed address."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_23115_amd as g
+import workloads
+from gpu_util import keys_to_device, say, u64
+from oracle import remap as oremap
+
+pytestmark = pytest.mark.gpu
+
+TOP = (1 << 64) - 1
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a visible GPU")
+    torch.cuda.init()
+
+
+def dev(a) -> torch.Tensor:
+    return keys_to_device(np.asarray(a, dtype=np.uint64).reshape(-1))
+
+
+def update_both(m, om, rem=((), ()), add=((), (), ())):
+    rs, rl = (np.asarray(x, np.uint64) for x in rem)
+    a_s, a_l, a_t = (np.asarray(x, np.uint64) for x in add)
+    st, counts = m.update(dev(rs) if rs.size else None, dev(rl) if rs.size else None,
+                          dev(a_s) if a_s.size else None, dev(a_l) if a_s.size else None,
+                          dev(a_t) if a_s.size else None)
+    torch.cuda.synchronize()
+    est, ecounts = om.update(rs, rl, a_s, a_l, a_t)
+    return st.cpu().numpy(), tuple(int(c) for c in u64(counts)), est, tuple(ecounts)
+
+
+def assert_map(m, om, what):
+    s, n, t, c = m.export()
+    torch.cuda.synchronize()
+    k = int(c.item())
+    es, en, et = om.export()
+    assert k == es.size, f"{what}: count"
+    assert np.array_equal(u64(s)[:k], es), f"{what}: starts"
+    assert np.array_equal(u64(n)[:k], en), f"{what}: lengths"
+    assert np.array_equal(u64(t)[:k], et), f"{what}: targets"
+
+
+def probes(om, rng, n_random, space):
+    """Random addresses plus every interval's first, last, one-past-last and one-before."""
+    s, n, _ = om.export()
+    edge = np.concatenate([s, s + n - np.uint64(1), s + n, s - np.uint64(1)]) if s.size else np.zeros(0, np.uint64)
+    rnd = rng.integers(0, space, n_random, dtype=np.uint64)
+    return np.concatenate([edge, rnd, np.array([0, TOP, TOP - 1], np.uint64)])
+
+
+def assert_translate(m, om, addrs, what):
+    got = u64(m.translate(dev(addrs)))
+    torch.cuda.synchronize()
+    assert np.array_equal(got, om.translate(addrs)), f"{what}: translation"
+
+
+@pytest.mark.parametrize("cap,space", [(1, 64), (16, 128), (200, 2000), (5000, 40000)])
+def test_random_update_sequence(cap, space):
+    rng = np.random.default_rng(cap)
+    m, om = g.Remap(cap), oremap.RemapMap(cap)
+    for step in range(40):
+        n_del = int(rng.integers(0, 1 + max(2, cap // 20)))
+        n_add = int(rng.integers(0, 1 + max(4, cap // 4)))
+        maxlen = max(4, space // max(cap, 1))
+        rem = (rng.integers(0, space, n_del, dtype=np.uint64), rng.integers(0, 2 * maxlen, n_del, dtype=np.uint64))
+        add = (rng.integers(0, space, n_add, dtype=np.uint64), rng.integers(0, maxlen, n_add, dtype=np.uint64),
+               rng.integers(0, 1 << 62, n_add, dtype=np.uint64))
+        say("remap sequence cap", cap, "step", step, "n_del", n_del, "n_add", n_add)
+        st, counts, est, ecounts = update_both(m, om, rem, add)
+        assert np.array_equal(st, est), f"step {step}: statuses"
+        assert counts == ecounts, f"step {step}: counts"
+        assert_map(m, om, f"step {step}")
+        assert_translate(m, om, probes(om, rng, 500, space + 16), f"step {step}")
+
+
+def test_edges_of_the_address_space():
+    say("remap edges")
+    m, om = g.Remap(8), oremap.RemapMap(8)
+    add = ([0, TOP - 5, TOP - 3, 100, 200, 300, TOP, 50], [1, 5, 4, 0, 8, 8, 1, TOP],
+           [TOP - 1, 7, 9, 1, TOP - 8, TOP - 7, 0, 0])
+    st, counts, est, ecounts = update_both(m, om, add=add)
+    assert np.array_equal(st, est) and counts == ecounts
+    assert st.tolist() == [0, 0, 1, 1, 0, 1, 1, 1]
+    assert_translate(m, om, np.array([0, 1, TOP - 5, TOP - 1, TOP, 207, 199, 208], np.uint64), "edges")
+    # removal clipped at 2^64; empty removal; removal of everything
+    for rem in (([TOP - 2], [TOP]), ([203], [0]), ([0], [TOP])):
+        st, counts, est, ecounts = update_both(m, om, rem=rem)
+        assert counts == ecounts, rem
+        assert_map(m, om, f"removal {rem}")
+
+
+def test_no_op_update_and_empty_map():
+    say("remap no-op")
+    m, om = g.Remap(4), oremap.RemapMap(4)
+    st, counts, est, ecounts = update_both(m, om)
+    assert counts == ecounts == (0, 0, 0, 0)
+    assert_translate(m, om, np.array([0, 5, TOP], np.uint64), "empty")
+    update_both(m, om, add=([10], [5], [1000]))
+    st, counts, est, ecounts = update_both(m, om, rem=([100], [5]))
+    assert counts == ecounts == (1, 0, 0, 0)
+
+
+def test_full_leaves_the_map_unchanged():
+    say("remap full")
+    m, om = g.Remap(3), oremap.RemapMap(3)
+    update_both(m, om, add=([0, 10], [5, 5], [100, 200]))
+    st, counts, est, ecounts = update_both(m, om, rem=([0], [1]), add=([20, 30, 40, 40], [1, 1, 1, 0], [1, 2, 3, 4]))
+    assert st.tolist() == est.tolist() == [3, 3, 3, 1]
+    assert counts == ecounts == (2, 0, 0, 4)
+    assert_map(m, om, "after FULL")
+
+
+def test_paper_two_chunks_in_one_allocation():
+    """Sec. 4.3: two chunks of one client allocation map into two server allocations."""
+    say("remap paper case")
+    va = (3 << 40) + 0x4000
+    pos1, pos2 = 0x7F00_0000_0000, 0x7F80_0000_1000
+    m, om = g.Remap(16), oremap.RemapMap(16)
+    st, counts, est, ecounts = update_both(m, om, add=([va, va + 0x3000], [0x3000, 0x500], [pos1, pos2]))
+    assert st.tolist() == [0, 0]
+    probe = np.array([va, va + 0x2FFF, va + 0x3000, va + 0x3004, va + 0x34FF, va + 0x3500, va - 1], np.uint64)
+    got = u64(m.translate(dev(probe)))
+    assert got.tolist() == [pos1, pos1 + 0x2FFF, pos2, pos2 + 4, pos2 + 0x4FF, TOP, TOP]
+
+
+def test_many_tasks_workload():
+    """256 tasks (the 7B decoder, ResNet-50 and the 2,000-tensor set) mapped at once, 2^20
+    pointers translated, then tasks freed and new ones loaded in one update."""
+    tasks = workloads.RemapTasks(256)
+    start, length, target = tasks.intervals()
+    cap = 1 << 18
+    m, om = g.Remap(cap), oremap.RemapMap(cap)
+    say("remap tasks: load", start.size, "intervals")
+    st, counts, est, ecounts = update_both(m, om, add=(start, length, target))
+    assert counts == ecounts and counts[1] == start.size
+    assert_map(m, om, "tasks loaded")
+    ptr = tasks.pointers(1 << 20)
+    say("remap tasks: translate", ptr.size)
+    assert_translate(m, om, ptr, "tasks")
+    # free 16 tasks (their whole 1 TB spaces) and load the intervals of 16 others shifted
+    # into the freed spaces
+    gone = np.arange(0, 256, 16)
+    rem = (gone.astype(np.uint64) << np.uint64(40), np.full(gone.size, 1 << 40, np.uint64))
+    s2, l2, t2 = tasks.intervals(gone + 1)
+    s2 = s2 - np.uint64(1 << 40)
+    say("remap tasks: replace", gone.size, "tasks")
+    st, counts, est, ecounts = update_both(m, om, rem=rem, add=(s2, l2, t2))
+    assert np.array_equal(st, est) and counts == ecounts
+    assert counts[1] == s2.size and counts[2] > 0
+    assert_map(m, om, "tasks replaced")
+    assert_translate(m, om, ptr, "tasks replaced")
+
+
+@pytest.mark.parametrize("count", [4095, 4096, 4097, 8192, 8193, 12_289])
+def test_fence_strides(count):
+    """Translation searches a fence of every S-th start (S = ceil(count / 4096)) first:
+    probe every interval edge at counts around the stride changes, then shrink the map."""
+    rng = np.random.default_rng(count)
+    start = np.sort(rng.choice(1 << 30, count, replace=False).astype(np.uint64)) * np.uint64(4)
+    length = rng.integers(1, 5, count, dtype=np.uint64)
+    target = rng.integers(0, 1 << 62, count, dtype=np.uint64)
+    m, om = g.Remap(count), oremap.RemapMap(count)
+    say("remap fence: count", count)
+    st, counts, est, ecounts = update_both(m, om, add=(start, length, target))
+    assert counts == ecounts and counts[0] == count
+    assert_translate(m, om, probes(om, rng, 10_000, 1 << 33), f"fence {count}")
+    keep = start[::1000]
+    st, counts, est, ecounts = update_both(m, om, rem=([0], [1 << 33]), add=(keep, length[::1000], target[::1000]))
+    assert counts == ecounts and counts[0] == keep.size
+    assert_translate(m, om, probes(om, rng, 10_000, 1 << 33), f"fence {count} shrunk")
+
+
+def test_beyond_one_grid_pass():
+    """More candidates than one pass of the capped grid (8192 x 256 lanes)."""
+    n = 3_000_000
+    rng = np.random.default_rng(77)
+    start = np.sort(rng.choice(1 << 40, n, replace=False).astype(np.uint64)) * np.uint64(8)
+    length = rng.integers(1, 9, n, dtype=np.uint64)
+    target = rng.integers(0, 1 << 60, n, dtype=np.uint64)
+    perm = rng.permutation(n)
+    m, om = g.Remap(1 << 22), oremap.RemapMap(1 << 22)
+    say("remap grid-stride: add", n)
+    st, counts, est, ecounts = update_both(m, om, add=(start[perm], length[perm], target[perm]))
+    assert np.array_equal(st, est) and counts == ecounts
+    say("remap grid-stride: remove 1/3 and add overlapping")
+    rem = (start[::3], np.ones(start[::3].size, np.uint64))
+    add = (start[1::5] + np.uint64(4), np.full(start[1::5].size, 2, np.uint64),
+           np.zeros(start[1::5].size, np.uint64))
+    st, counts, est, ecounts = update_both(m, om, rem=rem, add=add)
+    assert np.array_equal(st, est) and counts == ecounts
+    assert_map(m, om, "grid-stride")
+    probe = np.concatenate([start[:: 7], start[::11] + np.uint64(5), rng.integers(0, 1 << 43, 10**5,
+                                                                                  dtype=np.uint64)])
+    assert_translate(m, om, probe, "grid-stride")
+
+
+def test_translate_replays_in_a_graph():
+    """Translation enqueues one kernel launch and reads the map's own count, so a captured
+    graph sees later updates on every replay."""
+    say("remap graph")
+    m, om = g.Remap(64), oremap.RemapMap(64)
+    update_both(m, om, add=([0, 100], [50, 50], [1000, 5000]))
+    addrs = dev(np.arange(0, 200, 3, dtype=np.uint64))
+    out = torch.empty(addrs.numel(), dtype=torch.int64, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        m.translate(addrs, out=out, stream=s)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=s):
+            m.translate(addrs, out=out, stream=s)
+    torch.cuda.synchronize()
+    host = np.arange(0, 200, 3, dtype=np.uint64)
+    for k in range(3):
+        out.fill_(0)
+        update_both(m, om, add=([200 + 10 * k], [5], [7]))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(u64(out), om.translate(host)), f"replay {k}"
+
+
+def test_binding_refusals():
+    say("remap refusals")
+    m = g.Remap(4)
+    with pytest.raises(ValueError):
+        m.update(add_start=dev([1, 2]), add_len=dev([1]), add_target=dev([1, 2]))
+    with pytest.raises(ValueError):
+        m.translate(torch.zeros(4, dtype=torch.int32, device="cuda"))
+    with pytest.raises(g.GleamError) as e:
+        m.update(add_start=dev([1]), add_len=dev([1]), add_target=dev([1]),
+                 ws=torch.empty(256, dtype=torch.uint8, device="cuda"))
+    assert e.value.status == g.E_WORKSPACE
+    m.close()
+    with pytest.raises(g.GleamError):
+        m.translate(dev([1]))

@@ -311,3 +311,70 @@ class LargeSet:
     def cached_blocks(self, n_blocks: int, frac: float = 0.6) -> np.ndarray:
         k = int(math.floor(frac * n_blocks))
         return np.sort(rng(self.workload, PURPOSE_SELECT, 0).choice(n_blocks, k, replace=False))
+
+
+# --------------------------------------------------------------------------- #
+# Address-remap intervals of many tasks (workload 6)
+# --------------------------------------------------------------------------- #
+TASK_SPACE_BITS = 40          # one 1 TB virtual address space per task
+ALLOC_ROUND = 512             # the caching allocator's rounding of tensor sizes
+POOL_BASE = 0x7000_0000_0000  # where the server's shareable pool regions start
+
+
+def model_type_sizes() -> list[np.ndarray]:
+    """Tensor byte sizes of the three model types a task can be: the 7B decoder and
+    ResNet-50 in fp16, and the 2,000-tensor bf16 set."""
+    dec = Decoder()
+    res = [2 * math.prod(s) for _, s in resnet50_shapes()]
+    return [np.array(dec.nbytes, np.uint64), np.array(res, np.uint64), LargeSet().sizes.copy()]
+
+
+def _packed(sizes: np.ndarray, base: int) -> np.ndarray:
+    rounded = (sizes + np.uint64(ALLOC_ROUND - 1)) // np.uint64(ALLOC_ROUND) * np.uint64(ALLOC_ROUND)
+    return np.uint64(base) + np.concatenate([[0], np.cumsum(rounded)[:-1]]).astype(np.uint64)
+
+
+class RemapTasks:
+    """`n_tasks` tasks, each of a model type drawn uniformly, that loaded their tensors
+    back to back (sizes rounded up to 512 bytes) from a random 2 MiB-aligned base in the
+    lower half of their own 1 TB space [t << 40, (t + 1) << 40). Every tensor maps onto the
+    shareable copy of the same tensor of its type: one pool region per type at
+    POOL_BASE + type << 40, packed the same way. Homogeneous tasks therefore share
+    targets; intervals of different tasks never meet."""
+
+    def __init__(self, n_tasks: int = 256, workload: int = 6, types=None):
+        self.workload = workload
+        self.type_sizes = model_type_sizes() if types is None else [np.asarray(t, np.uint64) for t in types]
+        sel = rng(workload, PURPOSE_SELECT, 0)
+        self.task_type = sel.integers(0, len(self.type_sizes), n_tasks)
+        self.task_base = sel.integers(0, 1 << (TASK_SPACE_BITS - 1 - 21), n_tasks).astype(np.uint64) << np.uint64(21)
+        self.pool = [_packed(s, POOL_BASE + (k << TASK_SPACE_BITS)) for k, s in enumerate(self.type_sizes)]
+        self.n_tasks = n_tasks
+
+    def task(self, t: int):
+        """(start, length, target) of task t's tensors."""
+        k = int(self.task_type[t])
+        sizes = self.type_sizes[k]
+        base = (t << TASK_SPACE_BITS) + int(self.task_base[t])
+        return _packed(sizes, base), sizes.copy(), self.pool[k].copy()
+
+    def intervals(self, tasks=None):
+        tasks = range(self.n_tasks) if tasks is None else tasks
+        parts = [self.task(int(t)) for t in tasks]
+        if not parts:
+            z = np.zeros(0, np.uint64)
+            return z, z, z
+        return tuple(np.concatenate([p[i] for p in parts]) for i in range(3))
+
+    def pointers(self, n: int, hit_frac: float = 0.9, index: int = 0) -> np.ndarray:
+        """n pointers: a fraction `hit_frac` at uniform offsets inside uniformly chosen
+        tensors, the rest uniform over a random task's whole 1 TB space."""
+        start, length, _ = self.intervals()
+        g = rng(self.workload, PURPOSE_SELECT, 1 + index)
+        inside = g.random(n) < hit_frac
+        pick = g.integers(0, start.size, n)
+        off = (g.random(n) * length[pick].astype(np.float64)).astype(np.uint64)
+        off = np.minimum(off, length[pick] - np.uint64(1))
+        task = g.integers(0, self.n_tasks, n).astype(np.uint64)
+        anywhere = (task << np.uint64(TASK_SPACE_BITS)) + g.integers(0, 1 << TASK_SPACE_BITS, n).astype(np.uint64)
+        return np.where(inside, start[pick] + off, anywhere).astype(np.uint64)
