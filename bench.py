@@ -360,9 +360,16 @@ def remap_path(args, g, torch):
     s2, l2, t2 = tasks.intervals(gone + 1)
     s2 = s2 - np.uint64(1 << 40)
     ds, dl, dt, drs, drl, ds2, dl2, dt2 = (d(a) for a in (start, length, target, rem_s, rem_l, s2, l2, t2))
+    # one task swapped: free the space of the first task of the 2,000-tensor type and load
+    # its tensors again, in one call
+    t_swap = int(np.flatnonzero(tasks.task_type == 2)[0])
+    w_s, w_l, w_t = tasks.intervals([t_swap])
+    dws, dwl, dwt = d(w_s), d(w_l), d(w_t)
+    dwr, dwrl = d(np.array([t_swap << 40], np.uint64)), d(np.array([1 << 40], np.uint64))
     m = g.Remap(cap)
     load_ws = m.update_workspace(start.size, 0)
     rep_ws = m.update_workspace(s2.size, gone.size)
+    swap_ws = m.update_workspace(w_s.size, 1)
     status = torch.empty(start.size, dtype=torch.uint8, device="cuda")
     counts = torch.empty(4, dtype=torch.int64, device="cuda")
     n_ptr = 1 << 22
@@ -384,6 +391,10 @@ def remap_path(args, g, torch):
         m.update(del_start=drs, del_len=drl, add_start=ds2, add_len=dl2, add_target=dt2, status=status,
                  counts=counts, ws=rep_ws)
 
+    def swap():
+        m.update(del_start=dwr, del_len=dwrl, add_start=dws, add_len=dwl, add_target=dwt, status=status,
+                 counts=counts, ws=swap_ws)
+
     def timed(fn, before=None):
         ms = []
         for step in range(args.warmup + args.steps):
@@ -401,6 +412,8 @@ def remap_path(args, g, torch):
 
     log("remap: load", start.size, "intervals")
     load_ms = timed(load, before=clear)
+    swap_ms = timed(swap, before=lambda: (clear(), load()))
+    swap_counts = g.as_u64(counts).copy()
     replace_ms = timed(replace, before=lambda: (clear(), load()))
     rep_counts = g.as_u64(counts).copy()
     # translation against the replaced map
@@ -415,6 +428,8 @@ def remap_path(args, g, torch):
     cpu_s = time.perf_counter() - t0
     if tuple(int(c) for c in rep_counts) != tuple(ecounts) or not np.array_equal(got, want):
         raise SystemExit(f"remap results differ from the oracle: counts {rep_counts} vs {ecounts}")
+    if tuple(int(c) for c in swap_counts) != (start.size, w_s.size, w_s.size, 0):
+        raise SystemExit(f"task swap counts wrong: {swap_counts}")
     med = tr_ms[0]
     algo = 16 * n_ptr + 24 * int(ecounts[0])  # pointer in, translation out, the map read once
     cpu = None
@@ -431,6 +446,8 @@ def remap_path(args, g, torch):
                    "intervals": int(ecounts[0]), "capacity": cap, "pointers": n_ptr,
                    "translate_ms": [round(x, 4) for x in tr_ms],
                    "load_ms": [round(x, 3) for x in load_ms], "load_intervals": int(start.size),
+                   "swap_ms": [round(x, 3) for x in swap_ms],
+                   "swap": f"free task {t_swap} and load its {w_s.size} tensors again in one call",
                    "replace_ms": [round(x, 3) for x in replace_ms],
                    "replace": f"free {gone.size} tasks, load {s2.size} intervals"},
         "roofline": {"bound": "hbm", "achieved": round(algo / (med * 1e-3) / 1e9, 1), "peak": 8000.0,

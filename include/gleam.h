@@ -405,7 +405,8 @@ gleam_status gleam_restore_blocks(const gleam_batch* dst, const gleam_send_recor
  *                 >= gleam_remap_update_bytes(m, n_add, n_del)
  * If the survivors and the accepted additions exceed the capacity, the map is left
  * exactly as it was (the removals included) and those additions get GLEAM_REMAP_FULL.
- * The work is O(capacity + n_add) whatever the count: size the capacity to the map.
+ * Every update passes over the whole capacity (survivors are marked and compacted)
+ * whatever the count, plus a sort of the additions: size the capacity to the map.
  * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED (n_add or n_del
  * above 2^31), GLEAM_E_HIP. gleam_remap_update_bytes returns 0 for a NULL map, counts
  * above 2^31 or a failed rocPRIM storage query.

@@ -7,25 +7,31 @@
 // storage: [256-byte header: u64 count, fence stride, fence length][start x cap]
 // [{end, target} x cap][fence: 4096 x u64], end exclusive. A sorted array answers the
 // same ordered queries as the tree; on the GPU a batch of pointers is translated by
-// one search per lane, and a batch of changes rebuilds the array in a few passes
-// instead of rebalancing node by node.
+// one search per lane, and a batch of changes is merged in a few passes instead of
+// rebalancing node by node.
 //
-// Translation is bound by dependent, lane-divergent loads (each level of a binary
-// search is a different cache line for every lane), not by bytes. So every update also
+// Translation is bound by lane-divergent loads (each level of a binary search is a
+// different cache line for nearly every lane), not by bytes. So every update also
 // writes a fence, every S-th start with S = ceil(count / 4096); a translating workgroup
 // keeps the fence in LDS and searches it first, leaving log2(S) levels for global
 // memory (6 instead of 18 at 208k intervals), and end and target sit side by side so
-// the final step is one 16-byte load. The update:
+// the final step is one 16-byte load.
 //
+// An update never re-sorts the intervals it keeps (they are already in order):
 //   1. removal ranges are sorted by start, with a running maximum of their last
 //      addresses, so one binary search tells whether an interval meets any of them;
-//   2. survivors and valid additions are sorted together by start (rocPRIM radix sort;
-//      everything else takes the key kNone and sorts last);
-//   3. a running maximum of interval ends: an addition meets an earlier-starting entry
-//      iff that maximum, just before it, passes its start, and a later-starting one iff
-//      the next start falls before its end;
-//   4. an exclusive scan of the kept entries gives their new positions; the scatter
-//      writes them only if they fit the capacity, so a refused call changes nothing.
+//      the survivors are compacted, in order, into the workspace (one scan);
+//   2. only the valid additions are sorted (rocPRIM radix sort; invalid ones take the
+//      key kNone and sort last);
+//   3. an addition meets an earlier-starting addition iff the running maximum of ends
+//      just before it passes its start, a later-starting one iff the next start comes
+//      before its end, and a survivor iff the last survivor starting at or before its
+//      last address ends after its start (survivors are disjoint, so their ends are
+//      sorted too); additions that meet nothing are kept (a scan numbers them);
+//   4. the two sorted runs are merged by rank: a survivor lands at its own index plus
+//      the kept additions that start before it, a kept addition at its own number plus
+//      the survivors that start before it. Nothing is written unless everything fits
+//      the capacity, so a refused call changes nothing.
 
 #include <new>
 
@@ -41,7 +47,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kTranslateThreads = 1024;
 constexpr uint32_t kMaxGrid = 8192;
-constexpr uint64_t kNone = ~0ull;  // sort key of an entry that takes no part; no valid start equals it
+constexpr uint64_t kNone = ~0ull;  // sort key of an addition that takes no part; no valid start equals it
 constexpr uint64_t kMaxCount = 1ull << 31;
 
 constexpr uint32_t kFence = 4096;  // fence entries (32 KiB of LDS)
@@ -61,47 +67,49 @@ MapRef map_ref(const gleam_remap* m) {
   return MapRef{hdr, start, et, reinterpret_cast<uint64_t*>(et + m->capacity), m->capacity};
 }
 
+// Workspace of one update (cap = capacity, A = additions, R = removal ranges).
 struct UpdLayout {
-  uint64_t m;  // capacity + n_add candidates
-  uint64_t r;  // removal ranges
-  size_t counters, ckey_a, ckey_b, cval_a, cval_b, cend, cmax, ctgt, acc, pos;
-  size_t dkey_a, dkey_b, dval_a, dval_b, dmax, tmp, tmp_bytes, total;
+  size_t keep, kpos, s_start, s_et;         // cap: survivor flag, its scan, compacted survivors
+  size_t ka, kb, va, vb, aend, amax, acc, apos;  // A: sort keys/values, ends, running max, kept flag, scan
+  size_t rka, rkb, rva, rvb, rmax;          // R: removal ranges sorted by start, running max of last
+  size_t tmp, tmp_bytes, total;
   bool ok;  // rocPRIM's storage queries succeeded
 };
 
 UpdLayout upd_layout(uint64_t cap, uint64_t n_add, uint64_t n_del) {
   UpdLayout L;
-  L.m = cap + n_add;
-  L.r = n_del;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
     off = (off + bytes + 255) & ~(size_t)255;
     return o;
   };
-  L.counters = take(256);
-  L.ckey_a = take(8 * L.m);
-  L.ckey_b = take(8 * L.m);
-  L.cval_a = take(8 * L.m);
-  L.cval_b = take(8 * L.m);
-  L.cend = take(8 * L.m);
-  L.cmax = take(8 * L.m);
-  L.ctgt = take(8 * L.m);
-  L.acc = take(8 * L.m);
-  L.pos = take(8 * L.m);
-  L.dkey_a = take(8 * L.r);
-  L.dkey_b = take(8 * L.r);
-  L.dval_a = take(8 * L.r);
-  L.dval_b = take(8 * L.r);
-  L.dmax = take(8 * L.r);
-  const uint64_t big = L.m > L.r ? L.m : L.r;
+  L.keep = take(8 * cap);
+  L.kpos = take(8 * cap);
+  L.s_start = take(8 * cap);
+  L.s_et = take(16 * cap);
+  L.ka = take(8 * n_add);
+  L.kb = take(8 * n_add);
+  L.va = take(8 * n_add);
+  L.vb = take(8 * n_add);
+  L.aend = take(8 * n_add);
+  L.amax = take(8 * n_add);
+  L.acc = take(8 * n_add);
+  L.apos = take(8 * n_add);
+  L.rka = take(8 * n_del);
+  L.rkb = take(8 * n_del);
+  L.rva = take(8 * n_del);
+  L.rvb = take(8 * n_del);
+  L.rmax = take(8 * n_del);
+  const uint64_t ar = n_add > n_del ? n_add : n_del;
+  const uint64_t ca = cap > n_add ? cap : n_add;
   size_t sort_b = 0, max_b = 0, sum_b = 0;
   const hipError_t e1 = rocprim::radix_sort_pairs(nullptr, sort_b, (const uint64_t*)nullptr, (uint64_t*)nullptr,
-                                                  (const uint64_t*)nullptr, (uint64_t*)nullptr, (size_t)big, 0, 64);
+                                                  (const uint64_t*)nullptr, (uint64_t*)nullptr, (size_t)ar, 0, 64);
   const hipError_t e2 = rocprim::inclusive_scan(nullptr, max_b, (const uint64_t*)nullptr, (uint64_t*)nullptr,
-                                                (size_t)big, rocprim::maximum<uint64_t>());
+                                                (size_t)ar, rocprim::maximum<uint64_t>());
   const hipError_t e3 = rocprim::exclusive_scan(nullptr, sum_b, (const uint64_t*)nullptr, (uint64_t*)nullptr,
-                                                (uint64_t)0, (size_t)L.m, rocprim::plus<uint64_t>());
+                                                (uint64_t)0, (size_t)ca, rocprim::plus<uint64_t>());
   L.ok = e1 == hipSuccess && e2 == hipSuccess && e3 == hipSuccess;
   L.tmp_bytes = sort_b;
   if (max_b > L.tmp_bytes) L.tmp_bytes = max_b;
@@ -116,20 +124,23 @@ uint32_t grid_for(uint64_t n) {
   return (uint32_t)(g == 0 ? 1 : (g < kMaxGrid ? g : kMaxGrid));
 }
 
-__device__ __forceinline__ unsigned long long* ull(uint64_t* p) { return reinterpret_cast<unsigned long long*>(p); }
-
-__device__ __forceinline__ void wave_add(uint64_t* counter, uint64_t x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += shfl_xor64(x, o);
-  if ((threadIdx.x & 63) == 0 && x) atomicAdd(ull(counter), (unsigned long long)x);
-}
-
-// Number of entries of the ascending keys[0, n) that are <= x.
+// Number of entries of the ascending keys[0, n) that are <= x (upper bound).
 __device__ __forceinline__ uint64_t count_le(const uint64_t* keys, uint64_t n, uint64_t x) {
   uint64_t lo = 0, hi = n;
   while (lo < hi) {
     const uint64_t mid = lo + ((hi - lo) >> 1);
     if (keys[mid] <= x) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Number of entries of the ascending keys[0, n) that are < x (lower bound).
+__device__ __forceinline__ uint64_t count_lt(const uint64_t* keys, uint64_t n, uint64_t x) {
+  uint64_t lo = 0, hi = n;
+  while (lo < hi) {
+    const uint64_t mid = lo + ((hi - lo) >> 1);
+    if (keys[mid] < x) lo = mid + 1;
     else hi = mid;
   }
   return lo;
@@ -147,123 +158,302 @@ __global__ void removal_prep_kernel(const uint64_t* d_start, const uint64_t* d_l
   }
 }
 
-// Candidates: slot p < cap is interval p (if it exists and survives the removals),
-// p >= cap is addition p - cap (if valid). Key = start or kNone, value = p.
-__global__ void candidates_kernel(MapRef map, const uint64_t* rkey, const uint64_t* rmax, uint64_t r,
-                                  const uint64_t* a_start, const uint64_t* a_len, const uint64_t* a_target,
-                                  uint64_t m, uint8_t* status, uint64_t* ckey, uint64_t* cval, uint64_t* counters) {
+// keep[p] = 1 for an interval that meets no removal range.
+__global__ void survive_kernel(MapRef map, const uint64_t* rkey, const uint64_t* rmax, uint64_t r, uint64_t* keep) {
   const uint64_t count = map.hdr[0];
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  // every lane of a wave runs the same number of iterations, so wave_add sees them all
-  const uint64_t base0 = (uint64_t)blockIdx.x * blockDim.x;
-  for (uint64_t base = base0; base < m; base += stride) {
-    const uint64_t p = base + threadIdx.x;
-    uint64_t removed = 0;
-    if (p < m) {
-      uint64_t key = kNone;
-      if (p < map.cap) {
-        if (p < count) {
-          const uint64_t s = map.start[p], last = map.et[p].x - 1;
-          // the removals starting at or before `last`: does the furthest of them reach s?
-          const uint64_t q = r ? count_le(rkey, r, last) : 0;
-          if (q && rmax[q - 1] >= s) removed = 1;
-          else key = s;
+  for (uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; p < map.cap; p += stride) {
+    uint64_t k = 0;
+    if (p < count) {
+      const uint64_t s = map.start[p], last = map.et[p].x - 1;
+      // the removals starting at or before `last`: does the furthest of them reach s?
+      const uint64_t q = r ? count_le(rkey, r, last) : 0;
+      k = (q && rmax[q - 1] >= s) ? 0 : 1;
+    }
+    keep[p] = k;
+  }
+}
+
+__global__ void compact_kernel(MapRef map, const uint64_t* keep, const uint64_t* kpos, uint64_t* s_start,
+                               ulonglong2* s_et) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; p < map.cap; p += stride) {
+    if (!keep[p]) continue;
+    s_start[kpos[p]] = map.start[p];
+    s_et[kpos[p]] = map.et[p];
+  }
+}
+
+// Sort key of addition j: its start if valid, else kNone (status INVALID).
+__global__ void addition_prep_kernel(const uint64_t* a_start, const uint64_t* a_len, const uint64_t* a_target,
+                                     uint64_t n_add, uint8_t* status, uint64_t* key, uint64_t* val) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n_add; j += stride) {
+    const uint64_t s = a_start[j], n = a_len[j], t = a_target[j];
+    const bool valid = n != 0 && n <= kNone - s && n <= kNone - t;
+    if (!valid && status) status[j] = GLEAM_REMAP_INVALID;
+    key[j] = valid ? s : kNone;
+    val[j] = j;
+  }
+}
+
+// End of each sorted addition; an invalid one ends at 0 (it sorts last, after every
+// valid one, so the running maximum of ends only ever sees real ends before it).
+__global__ void addition_end_kernel(const uint64_t* key, const uint64_t* val, const uint64_t* a_len, uint64_t n_add,
+                                    uint64_t* aend) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n_add; k += stride)
+    aend[k] = key[k] == kNone ? 0 : key[k] + a_len[val[k]];
+}
+
+// Keep a valid addition that meets no other valid addition and no survivor.
+__global__ void addition_classify_kernel(const uint64_t* key, const uint64_t* val, const uint64_t* aend,
+                                         const uint64_t* amax, uint64_t n_add, const uint64_t* s_start,
+                                         const ulonglong2* s_et, const uint64_t* keep, const uint64_t* kpos,
+                                         uint64_t cap, uint8_t* status, uint64_t* acc) {
+  const uint64_t n_surv = kpos[cap - 1] + keep[cap - 1];
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n_add; k += stride) {
+    const uint64_t s = key[k];
+    uint64_t a = 0;
+    if (s != kNone) {
+      const uint64_t e = aend[k];
+      bool clash = (k > 0 && amax[k - 1] > s) || (k + 1 < n_add && key[k + 1] < e);
+      if (!clash) {
+        const uint64_t q = count_le(s_start, n_surv, e - 1);
+        clash = q && s_et[q - 1].x > s;
+      }
+      a = clash ? 0 : 1;
+      if (status) status[val[k]] = clash ? GLEAM_REMAP_OVERLAP : GLEAM_REMAP_ADDED;
+    }
+    acc[k] = a;
+  }
+}
+
+// Batches of at most kSmall removals or additions (a task's allocations, its tensors) are
+// handled by one 1024-lane workgroup in LDS instead of the several launches of the
+// rocPRIM sort and scans: a bitonic sort of (key, index) pairs and Hillis-Steele scans
+// over at most 2048 entries.
+constexpr int kSmallThreads = 1024;
+constexpr uint32_t kSmall = 2 * kSmallThreads;
+
+__device__ __forceinline__ uint32_t pow2_at_least(uint32_t n) {  // n <= kSmall
+  uint32_t p = 1;
+  while (p < n) p <<= 1;
+  return p;
+}
+
+// Sort the pairs (key[i], idx[i]), i < n, ascending by key and then by idx. The indices
+// are distinct, so this is a total order and the result is what a stable sort by key
+// gives. n is a power of two <= kSmall; every lane of the workgroup calls it.
+__device__ void bitonic_sort(uint64_t* key, uint32_t* idx, uint32_t n) {
+  for (uint32_t k = 2; k <= n; k <<= 1) {
+    for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+      const uint32_t t = threadIdx.x;  // pair t of n / 2 <= kSmallThreads
+      if (t < n / 2) {
+        const uint32_t i = ((t & ~(j - 1)) << 1) | (t & (j - 1));  // bit j of i is clear
+        const uint32_t l = i | j;
+        const uint64_t ki = key[i], kl = key[l];
+        const uint32_t ii = idx[i], il = idx[l];
+        const bool greater = ki > kl || (ki == kl && ii > il);
+        if (greater == ((i & k) == 0)) {  // out of order for this run's direction
+          key[i] = kl;
+          key[l] = ki;
+          idx[i] = il;
+          idx[l] = ii;
         }
-      } else {
-        const uint64_t j = p - map.cap;
-        const uint64_t s = a_start[j], n = a_len[j], t = a_target[j];
-        if (n != 0 && n <= kNone - s && n <= kNone - t) key = s;
-        else if (status) status[j] = GLEAM_REMAP_INVALID;
       }
-      ckey[p] = key;
-      cval[p] = p;
+      __syncthreads();
     }
-    wave_add(&counters[0], removed);
   }
 }
 
-// End and target of each sorted candidate; a non-candidate ends at 0, so the running
-// maximum of ends is the furthest end of the real entries before it.
-__global__ void gather_kernel(MapRef map, const uint64_t* a_len, const uint64_t* a_target, const uint64_t* ckey,
-                              const uint64_t* cval, uint64_t m, uint64_t* cend, uint64_t* ctgt) {
-  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  for (uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; p < m; p += stride) {
-    const uint64_t key = ckey[p];
-    uint64_t e = 0, t = 0;
-    if (key != kNone) {
-      const uint64_t v = cval[p];
-      if (v < map.cap) {
-        const ulonglong2 et = map.et[v];
-        e = et.x;
-        t = et.y;
-      } else {
-        e = key + a_len[v - map.cap];
-        t = a_target[v - map.cap];
-      }
-    }
-    cend[p] = e;
-    ctgt[p] = t;
+// In-place inclusive scan of buf[0, n) (n <= kSmall) with `op`; every lane of the
+// workgroup calls it; lane t owns entries t and t + kSmallThreads.
+template <class Op>
+__device__ void block_scan(uint64_t* buf, uint32_t n, Op op) {
+  const uint32_t i0 = threadIdx.x, i1 = threadIdx.x + kSmallThreads;
+  for (uint32_t off = 1; off < n; off <<= 1) {
+    uint64_t v0 = 0, v1 = 0;
+    if (i0 < n) v0 = i0 >= off ? op(buf[i0 - off], buf[i0]) : buf[i0];
+    if (i1 < n) v1 = i1 >= off ? op(buf[i1 - off], buf[i1]) : buf[i1];
+    __syncthreads();
+    if (i0 < n) buf[i0] = v0;
+    if (i1 < n) buf[i1] = v1;
+    __syncthreads();
   }
 }
 
-// Keep every survivor; keep an addition unless it meets an entry that starts before it
-// (the running maximum of earlier ends passes its start) or at/after it (the next
-// start comes before its end).
-__global__ void classify_kernel(const uint64_t* ckey, const uint64_t* cval, const uint64_t* cend,
-                                const uint64_t* cmax, uint64_t cap, uint64_t m, uint8_t* status, uint64_t* acc) {
-  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  for (uint64_t p = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; p < m; p += stride) {
-    const uint64_t key = ckey[p];
-    uint64_t keep = 0;
-    if (key != kNone) {
-      const uint64_t v = cval[p];
-      if (v < cap) {
-        keep = 1;
-      } else {
-        const bool clash = (p > 0 && cmax[p - 1] > key) || (p + 1 < m && ckey[p + 1] < cend[p]);
-        keep = clash ? 0 : 1;
-        if (status) status[v - cap] = clash ? GLEAM_REMAP_OVERLAP : GLEAM_REMAP_ADDED;
-      }
+struct MaxOp {
+  __device__ uint64_t operator()(uint64_t a, uint64_t b) const { return a > b ? a : b; }
+};
+struct AddOp {
+  __device__ uint64_t operator()(uint64_t a, uint64_t b) const { return a + b; }
+};
+
+// Removal ranges sorted by start, with the running maximum of their last addresses
+// (what the radix sort and the scan produce for larger batches).
+__global__ void __launch_bounds__(kSmallThreads)
+removals_small_kernel(const uint64_t* d_start, const uint64_t* d_len, uint32_t r, uint64_t* rkey, uint64_t* rmax) {
+  __shared__ uint64_t key[kSmall], last[kSmall], buf[kSmall];
+  __shared__ uint32_t idx[kSmall];
+  const uint32_t n = pow2_at_least(r);
+  for (uint32_t i = threadIdx.x; i < n; i += kSmallThreads) {
+    uint64_t k = kNone, l = 0;  // padding sorts after every range
+    if (i < r) {
+      const uint64_t s = d_start[i], len = d_len[i];
+      k = len ? s : kNone;
+      l = len ? (len - 1 > kNone - s ? kNone : s + len - 1) : 0;
     }
-    acc[p] = keep;
+    key[i] = k;
+    last[i] = l;
+    idx[i] = i;
+  }
+  __syncthreads();
+  bitonic_sort(key, idx, n);
+  for (uint32_t i = threadIdx.x; i < r; i += kSmallThreads) {
+    rkey[i] = key[i];
+    buf[i] = last[idx[i]];
+  }
+  __syncthreads();
+  block_scan(buf, r, MaxOp());
+  for (uint32_t i = threadIdx.x; i < r; i += kSmallThreads) rmax[i] = buf[i];
+}
+
+// Additions sorted, checked against each other and the survivors, and numbered: the
+// same outputs (kb, vb, aend, acc, apos) and statuses as the batched path.
+__global__ void __launch_bounds__(kSmallThreads)
+additions_small_kernel(const uint64_t* a_start, const uint64_t* a_len, const uint64_t* a_target, uint32_t n_add,
+                       uint8_t* status, const uint64_t* s_start, const ulonglong2* s_et, const uint64_t* keep,
+                       const uint64_t* kpos, uint64_t cap, uint64_t* kb, uint64_t* vb, uint64_t* aend,
+                       uint64_t* acc, uint64_t* apos) {
+  __shared__ uint64_t key[kSmall], buf[kSmall];
+  __shared__ uint32_t idx[kSmall];
+  const uint64_t n_surv = kpos[cap - 1] + keep[cap - 1];
+  const uint32_t n = pow2_at_least(n_add);
+  for (uint32_t j = threadIdx.x; j < n; j += kSmallThreads) {
+    uint64_t k = kNone;  // invalid additions and padding sort last (padding after them)
+    if (j < n_add) {
+      const uint64_t s = a_start[j], len = a_len[j], t = a_target[j];
+      const bool valid = len != 0 && len <= kNone - s && len <= kNone - t;
+      if (!valid && status) status[j] = GLEAM_REMAP_INVALID;
+      if (valid) k = s;
+    }
+    key[j] = k;
+    idx[j] = j;
+  }
+  __syncthreads();
+  bitonic_sort(key, idx, n);
+  uint64_t e[2] = {0, 0};
+  for (uint32_t h = 0; h < 2; ++h) {
+    const uint32_t k = threadIdx.x + h * kSmallThreads;
+    if (k >= n_add) continue;
+    e[h] = key[k] == kNone ? 0 : key[k] + a_len[idx[k]];
+    kb[k] = key[k];
+    vb[k] = idx[k];
+    aend[k] = e[h];
+    buf[k] = e[h];
+  }
+  __syncthreads();
+  block_scan(buf, n_add, MaxOp());  // buf[k] = running maximum of ends through k
+  uint64_t a[2] = {0, 0};
+  for (uint32_t h = 0; h < 2; ++h) {
+    const uint32_t k = threadIdx.x + h * kSmallThreads;
+    if (k >= n_add || key[k] == kNone) continue;
+    const uint64_t s = key[k];
+    bool clash = (k > 0 && buf[k - 1] > s) || (k + 1 < n_add && key[k + 1] < e[h]);
+    if (!clash) {
+      const uint64_t q = count_le(s_start, n_surv, e[h] - 1);
+      clash = q && s_et[q - 1].x > s;
+    }
+    a[h] = clash ? 0 : 1;
+    if (status) status[idx[k]] = clash ? GLEAM_REMAP_OVERLAP : GLEAM_REMAP_ADDED;
+  }
+  __syncthreads();  // every lane has read buf
+  for (uint32_t h = 0; h < 2; ++h) {
+    const uint32_t k = threadIdx.x + h * kSmallThreads;
+    if (k < n_add) {
+      acc[k] = a[h];
+      buf[k] = a[h];
+    }
+  }
+  __syncthreads();
+  block_scan(buf, n_add, AddOp());  // inclusive count of kept additions
+  for (uint32_t h = 0; h < 2; ++h) {
+    const uint32_t k = threadIdx.x + h * kSmallThreads;
+    if (k < n_add) apos[k] = buf[k] - a[h];
   }
 }
 
-// Write the kept entries at their scanned positions, and every S-th start into the
-// fence, if they all fit; otherwise leave the map as it was and mark the additions that
-// would have entered FULL.
-__global__ void scatter_kernel(MapRef map, const uint64_t* ckey, const uint64_t* cval, const uint64_t* cend,
-                               const uint64_t* ctgt, const uint64_t* acc, const uint64_t* pos, uint64_t m,
-                               uint64_t n_add, uint8_t* status, const uint64_t* counters, uint64_t* counts) {
-  const uint64_t total = pos[m - 1] + acc[m - 1];
-  const bool fits = total <= map.cap;
-  const uint64_t S = total > kFence ? (total + kFence - 1) / kFence : 1;
+struct Totals {
+  uint64_t n_surv, n_acc, total, S;
+  bool fits;
+};
+
+__device__ __forceinline__ Totals totals(const uint64_t* keep, const uint64_t* kpos, uint64_t cap,
+                                         const uint64_t* acc, const uint64_t* apos, uint64_t n_add) {
+  Totals t;
+  t.n_surv = kpos[cap - 1] + keep[cap - 1];
+  t.n_acc = n_add ? apos[n_add - 1] + acc[n_add - 1] : 0;
+  t.total = t.n_surv + t.n_acc;
+  t.fits = t.total <= cap;
+  t.S = t.total > kFence ? (t.total + kFence - 1) / kFence : 1;
+  return t;
+}
+
+__device__ __forceinline__ void place(const MapRef& map, uint64_t q, uint64_t s, ulonglong2 et, uint64_t S) {
+  map.start[q] = s;
+  map.et[q] = et;
+  if (q % S == 0) map.fence[q / S] = s;
+}
+
+// Survivor i lands at i + (kept additions that start before it).
+__global__ void place_survivors_kernel(MapRef map, const uint64_t* s_start, const ulonglong2* s_et,
+                                       const uint64_t* keep, const uint64_t* kpos, const uint64_t* key,
+                                       const uint64_t* acc, const uint64_t* apos, uint64_t n_add) {
+  const Totals t = totals(keep, kpos, map.cap, acc, apos, n_add);
+  if (!t.fits) return;
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  const uint64_t first = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (first == 0) {
-    // kept = the survivors (before - removed) and the accepted additions
-    const uint64_t before = map.hdr[0];
-    const uint64_t added = fits ? total - (before - counters[0]) : 0;
-    counts[0] = fits ? total : before;
-    counts[1] = added;
-    counts[2] = fits ? counters[0] : 0;
-    counts[3] = n_add - added;
-    if (fits) {
-      map.hdr[0] = total;
-      map.hdr[1] = S;
-      map.hdr[2] = (total + S - 1) / S;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < t.n_surv; i += stride) {
+    const uint64_t s = s_start[i];
+    const uint64_t k = count_lt(key, n_add, s);  // additions (any status) starting before s
+    const uint64_t before = k < n_add ? apos[k] : t.n_acc;
+    place(map, i + before, s, s_et[i], t.S);
+  }
+}
+
+// Kept addition k lands at its number among kept additions + (survivors that start
+// before it); when the result would not fit, it is FULL instead.
+__global__ void place_additions_kernel(MapRef map, const uint64_t* s_start, const uint64_t* keep,
+                                       const uint64_t* kpos, const uint64_t* key, const uint64_t* val,
+                                       const uint64_t* aend, const uint64_t* acc, const uint64_t* apos,
+                                       uint64_t n_add, const uint64_t* a_target, uint8_t* status) {
+  const Totals t = totals(keep, kpos, map.cap, acc, apos, n_add);
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n_add; k += stride) {
+    if (!acc[k]) continue;
+    if (t.fits) {
+      const uint64_t s = key[k];
+      place(map, apos[k] + count_lt(s_start, t.n_surv, s), s, make_ulonglong2(aend[k], a_target[val[k]]), t.S);
+    } else if (status) {
+      status[val[k]] = GLEAM_REMAP_FULL;
     }
   }
-  for (uint64_t p = first; p < m; p += stride) {
-    if (!acc[p]) continue;
-    if (fits) {
-      const uint64_t q = pos[p];
-      map.start[q] = ckey[p];
-      map.et[q] = make_ulonglong2(cend[p], ctgt[p]);
-      if (q % S == 0) map.fence[q / S] = ckey[p];
-    } else if (status && cval[p] >= map.cap) {
-      status[cval[p] - map.cap] = GLEAM_REMAP_FULL;
-    }
+}
+
+// Header and counts, after both placements.
+__global__ void finish_kernel(MapRef map, const uint64_t* keep, const uint64_t* kpos, const uint64_t* acc,
+                              const uint64_t* apos, uint64_t n_add, uint64_t* counts) {
+  const Totals t = totals(keep, kpos, map.cap, acc, apos, n_add);
+  const uint64_t before = map.hdr[0];
+  counts[0] = t.fits ? t.total : before;
+  counts[1] = t.fits ? t.n_acc : 0;
+  counts[2] = t.fits ? before - t.n_surv : 0;
+  counts[3] = n_add - (t.fits ? t.n_acc : 0);
+  if (t.fits) {
+    map.hdr[0] = t.total;
+    map.hdr[1] = t.S;
+    map.hdr[2] = (t.total + t.S - 1) / t.S;
   }
 }
 
@@ -423,59 +613,97 @@ extern "C" gleam_status gleam_remap_update(gleam_remap* m, const uint64_t* d_del
   hipStream_t s = (hipStream_t)stream;
   uint8_t* b = static_cast<uint8_t*>(d_ws);
   auto at = [&](size_t off) { return reinterpret_cast<uint64_t*>(b + off); };
-  uint64_t* counters = at(L.counters);
   void* tmp = b + L.tmp;
-  size_t tmp_bytes = L.tmp_bytes;
+  size_t tmp_bytes;
   const MapRef map = map_ref(m);
-  gleam_status st = fill_u64(counters, 4, 0, s);
-  if (st != GLEAM_OK) return st;
+  const uint64_t cap = m->capacity;
+  gleam_status st;
 
+  // 1. removals, survivors
   const uint64_t* rkey = nullptr;
   const uint64_t* rmax = nullptr;
-  if (n_del > 0) {
+  if (n_del > 0 && n_del <= kSmall) {
+    hipLaunchKernelGGL(removals_small_kernel, dim3(1), dim3(kSmallThreads), 0, s, d_del_start, d_del_len,
+                       (uint32_t)n_del, at(L.rkb), at(L.rmax));
+    if ((st = launch_status("removals_small_kernel")) != GLEAM_OK) return st;
+    rkey = at(L.rkb);
+    rmax = at(L.rmax);
+  } else if (n_del > 0) {
     hipLaunchKernelGGL(removal_prep_kernel, dim3(grid_for(n_del)), dim3(kThreads), 0, s, d_del_start, d_del_len,
-                       n_del, at(L.dkey_a), at(L.dval_a));
+                       n_del, at(L.rka), at(L.rva));
     if ((st = launch_status("removal_prep_kernel")) != GLEAM_OK) return st;
-    st = hip_call(rocprim::radix_sort_pairs(tmp, tmp_bytes, at(L.dkey_a), at(L.dkey_b), at(L.dval_a), at(L.dval_b),
+    tmp_bytes = L.tmp_bytes;
+    st = hip_call(rocprim::radix_sort_pairs(tmp, tmp_bytes, at(L.rka), at(L.rkb), at(L.rva), at(L.rvb),
                                             (size_t)n_del, 0, 64, s),
                   "radix sort (removals)");
     if (st != GLEAM_OK) return st;
     tmp_bytes = L.tmp_bytes;
-    st = hip_call(rocprim::inclusive_scan(tmp, tmp_bytes, at(L.dval_b), at(L.dmax), (size_t)n_del,
+    st = hip_call(rocprim::inclusive_scan(tmp, tmp_bytes, at(L.rvb), at(L.rmax), (size_t)n_del,
                                           rocprim::maximum<uint64_t>(), s),
                   "running maximum (removals)");
     if (st != GLEAM_OK) return st;
-    rkey = at(L.dkey_b);
-    rmax = at(L.dmax);
+    rkey = at(L.rkb);
+    rmax = at(L.rmax);
   }
-  const dim3 grid(grid_for(L.m)), block(kThreads);
-  hipLaunchKernelGGL(candidates_kernel, grid, block, 0, s, map, rkey, rmax, n_del, d_add_start, d_add_len,
-                     d_add_target, L.m, d_add_status, at(L.ckey_a), at(L.cval_a), counters);
-  if ((st = launch_status("candidates_kernel")) != GLEAM_OK) return st;
+  const dim3 block(kThreads), gcap(grid_for(cap)), gadd(grid_for(n_add));
+  hipLaunchKernelGGL(survive_kernel, gcap, block, 0, s, map, rkey, rmax, n_del, at(L.keep));
+  if ((st = launch_status("survive_kernel")) != GLEAM_OK) return st;
   tmp_bytes = L.tmp_bytes;
-  st = hip_call(rocprim::radix_sort_pairs(tmp, tmp_bytes, at(L.ckey_a), at(L.ckey_b), at(L.cval_a), at(L.cval_b),
-                                          (size_t)L.m, 0, 64, s),
-                "radix sort (candidates)");
-  if (st != GLEAM_OK) return st;
-  hipLaunchKernelGGL(gather_kernel, grid, block, 0, s, map, d_add_len, d_add_target, at(L.ckey_b), at(L.cval_b),
-                     L.m, at(L.cend), at(L.ctgt));
-  if ((st = launch_status("gather_kernel")) != GLEAM_OK) return st;
-  tmp_bytes = L.tmp_bytes;
-  st = hip_call(rocprim::inclusive_scan(tmp, tmp_bytes, at(L.cend), at(L.cmax), (size_t)L.m,
-                                        rocprim::maximum<uint64_t>(), s),
-                "running maximum (ends)");
-  if (st != GLEAM_OK) return st;
-  hipLaunchKernelGGL(classify_kernel, grid, block, 0, s, at(L.ckey_b), at(L.cval_b), at(L.cend), at(L.cmax),
-                     m->capacity, L.m, d_add_status, at(L.acc));
-  if ((st = launch_status("classify_kernel")) != GLEAM_OK) return st;
-  tmp_bytes = L.tmp_bytes;
-  st = hip_call(rocprim::exclusive_scan(tmp, tmp_bytes, at(L.acc), at(L.pos), (uint64_t)0, (size_t)L.m,
+  st = hip_call(rocprim::exclusive_scan(tmp, tmp_bytes, at(L.keep), at(L.kpos), (uint64_t)0, (size_t)cap,
                                         rocprim::plus<uint64_t>(), s),
-                "scan (positions)");
+                "scan (survivors)");
   if (st != GLEAM_OK) return st;
-  hipLaunchKernelGGL(scatter_kernel, grid, block, 0, s, map, at(L.ckey_b), at(L.cval_b), at(L.cend), at(L.ctgt),
-                     at(L.acc), at(L.pos), L.m, n_add, d_add_status, counters, d_counts);
-  return launch_status("scatter_kernel");
+  hipLaunchKernelGGL(compact_kernel, gcap, block, 0, s, map, at(L.keep), at(L.kpos), at(L.s_start),
+                     reinterpret_cast<ulonglong2*>(at(L.s_et)));
+  if ((st = launch_status("compact_kernel")) != GLEAM_OK) return st;
+
+  // 2-3. additions: sorted, checked against each other and the survivors, numbered
+  if (n_add > 0 && n_add <= kSmall) {
+    hipLaunchKernelGGL(additions_small_kernel, dim3(1), dim3(kSmallThreads), 0, s, d_add_start, d_add_len,
+                       d_add_target, (uint32_t)n_add, d_add_status, at(L.s_start),
+                       reinterpret_cast<const ulonglong2*>(at(L.s_et)), at(L.keep), at(L.kpos), cap, at(L.kb),
+                       at(L.vb), at(L.aend), at(L.acc), at(L.apos));
+    if ((st = launch_status("additions_small_kernel")) != GLEAM_OK) return st;
+  } else if (n_add > 0) {
+    hipLaunchKernelGGL(addition_prep_kernel, gadd, block, 0, s, d_add_start, d_add_len, d_add_target, n_add,
+                       d_add_status, at(L.ka), at(L.va));
+    if ((st = launch_status("addition_prep_kernel")) != GLEAM_OK) return st;
+    tmp_bytes = L.tmp_bytes;
+    st = hip_call(rocprim::radix_sort_pairs(tmp, tmp_bytes, at(L.ka), at(L.kb), at(L.va), at(L.vb), (size_t)n_add,
+                                            0, 64, s),
+                  "radix sort (additions)");
+    if (st != GLEAM_OK) return st;
+    hipLaunchKernelGGL(addition_end_kernel, gadd, block, 0, s, at(L.kb), at(L.vb), d_add_len, n_add, at(L.aend));
+    if ((st = launch_status("addition_end_kernel")) != GLEAM_OK) return st;
+    tmp_bytes = L.tmp_bytes;
+    st = hip_call(rocprim::inclusive_scan(tmp, tmp_bytes, at(L.aend), at(L.amax), (size_t)n_add,
+                                          rocprim::maximum<uint64_t>(), s),
+                  "running maximum (additions)");
+    if (st != GLEAM_OK) return st;
+    hipLaunchKernelGGL(addition_classify_kernel, gadd, block, 0, s, at(L.kb), at(L.vb), at(L.aend), at(L.amax),
+                       n_add, at(L.s_start), reinterpret_cast<const ulonglong2*>(at(L.s_et)), at(L.keep),
+                       at(L.kpos), cap, d_add_status, at(L.acc));
+    if ((st = launch_status("addition_classify_kernel")) != GLEAM_OK) return st;
+    tmp_bytes = L.tmp_bytes;
+    st = hip_call(rocprim::exclusive_scan(tmp, tmp_bytes, at(L.acc), at(L.apos), (uint64_t)0, (size_t)n_add,
+                                          rocprim::plus<uint64_t>(), s),
+                  "scan (additions)");
+    if (st != GLEAM_OK) return st;
+  }
+
+  // 4. merge by rank into the storage (only if everything fits), then the header
+  hipLaunchKernelGGL(place_survivors_kernel, gcap, block, 0, s, map, at(L.s_start),
+                     reinterpret_cast<const ulonglong2*>(at(L.s_et)), at(L.keep), at(L.kpos), at(L.kb), at(L.acc),
+                     at(L.apos), n_add);
+  if ((st = launch_status("place_survivors_kernel")) != GLEAM_OK) return st;
+  if (n_add > 0) {
+    hipLaunchKernelGGL(place_additions_kernel, gadd, block, 0, s, map, at(L.s_start), at(L.keep), at(L.kpos),
+                       at(L.kb), at(L.vb), at(L.aend), at(L.acc), at(L.apos), n_add, d_add_target, d_add_status);
+    if ((st = launch_status("place_additions_kernel")) != GLEAM_OK) return st;
+  }
+  hipLaunchKernelGGL(finish_kernel, dim3(1), dim3(1), 0, s, map, at(L.keep), at(L.kpos), at(L.acc), at(L.apos),
+                     n_add, d_counts);
+  return launch_status("finish_kernel");
 }
 
 extern "C" gleam_status gleam_remap_translate(const gleam_remap* m, const uint64_t* d_addr, uint64_t n,

@@ -179,6 +179,30 @@ def test_fence_strides(count):
     assert_translate(m, om, probes(om, rng, 10_000, 1 << 33), f"fence {count} shrunk")
 
 
+@pytest.mark.parametrize("n_add,n_del", [(1, 1), (2047, 2048), (2048, 2049), (2049, 5), (3000, 2047)])
+def test_one_workgroup_and_batched_updates(n_add, n_del):
+    """Batches of up to 2048 removals or additions run in one workgroup, larger ones
+    through the radix sort and scans: both sides of the switch, with clashes, invalid
+    additions and empty removal ranges mixed in."""
+    rng = np.random.default_rng(n_add * 7 + n_del)
+    space = 1 << 20
+    m, om = g.Remap(1 << 14), oremap.RemapMap(1 << 14)
+    base = (rng.choice(space // 64, 4000, replace=False).astype(np.uint64) * np.uint64(64),
+            rng.integers(1, 64, 4000, dtype=np.uint64), rng.integers(0, 1 << 62, 4000, dtype=np.uint64))
+    update_both(m, om, add=base)
+    for step in range(3):
+        rem = (rng.integers(0, space, n_del, dtype=np.uint64), rng.integers(0, 200, n_del, dtype=np.uint64))
+        a_len = rng.integers(0, 300, n_add, dtype=np.uint64)
+        add = (rng.integers(0, space, n_add, dtype=np.uint64), a_len, rng.integers(0, 1 << 62, n_add,
+                                                                                   dtype=np.uint64))
+        say("remap switch-over n_add", n_add, "n_del", n_del, "step", step)
+        st, counts, est, ecounts = update_both(m, om, rem, add)
+        assert np.array_equal(st, est), f"step {step}: statuses"
+        assert counts == ecounts, f"step {step}: counts"
+        assert_map(m, om, f"step {step}")
+        assert_translate(m, om, probes(om, rng, 2000, space), f"step {step}")
+
+
 def test_beyond_one_grid_pass():
     """More candidates than one pass of the capped grid (8192 x 256 lanes)."""
     n = 3_000_000
