@@ -1,6 +1,7 @@
-"""The C ABI used from plain C (tests/c_abi/detect.c: hipMalloc'd buffers, a HIP stream,
-no torch): fingerprint -> insert -> lookup -> compaction on four payloads, its printed
-outputs compared with the oracle on the same bytes."""
+"""The C ABI used from plain C (hipMalloc'd buffers, a HIP stream, no torch):
+tests/c_abi/detect.c runs fingerprint -> insert -> lookup -> compaction on four payloads,
+tests/c_abi/remap.c the address-remap calls; their printed outputs are compared with the
+oracle on the same inputs."""
 
 import os
 import subprocess
@@ -57,3 +58,40 @@ def test_plain_c_caller_matches_oracle():
     assert np.array_equal(misses, want["miss_idx"])
     # payload 0's blocks and payload 2's first block are held; payload 3 repeats payload 1
     assert (status == 1).sum() == first.size + 1 and (status == 2).sum() == 1
+
+
+REMAP_BINARY = os.path.join(os.path.dirname(os.path.abspath(__file__)), "c_abi", "remap")
+
+
+def test_plain_c_remap_matches_oracle():
+    """tests/c_abi/remap.c: the weight-sharing case of two chunks of one client allocation
+    mapped into two server allocations, a later overlapping addition refused, probes
+    translated before and after the allocation is freed; everything printed equals the
+    oracle."""
+    from oracle import remap as oremap
+    if not os.path.exists(REMAP_BINARY):
+        pytest.fail(f"{REMAP_BINARY} is not built; run __graft_entry__.build()")
+    print("[gpu-case] c abi remap", flush=True)
+    res = subprocess.run([REMAP_BINARY], capture_output=True, text=True, timeout=120)
+    assert res.returncode == 0, res.stderr
+    by_tag = {}
+    for ln in res.stdout.splitlines():
+        f = ln.split()
+        by_tag.setdefault(f[0], []).append(f[1:])
+    va = (3 << 40) + 0x4000
+    m = oremap.RemapMap(64)
+    st, counts = m.update(add_start=[va, va + 0x3000, 4 << 40], add_len=[0x3000, 0x500, 16],
+                          add_target=[0x7F0000000000, 0x7F8000001000, 1 << 20])
+    st_c, counts_c = m.update(add_start=[va + 0x100], add_len=[8], add_target=[5])
+    probe = [va, va + 0x2FFF, va + 0x3000, va + 0x3004, va + 0x3500, va - 1, (4 << 40) + 15, (4 << 40) + 16,
+             (1 << 64) - 1]
+    before = m.translate(probe)
+    _, counts_f = m.update(rem_start=[va], rem_len=[0x4000])
+    after = m.translate(probe)
+    assert tuple(int(x) for x in by_tag["add"][0]) == counts == (3, 3, 0, 0)
+    assert [int(x[1]) for x in by_tag["status"]] == st.tolist()
+    assert tuple(int(x) for x in by_tag["clash"][0]) == (*counts_c, oremap.OVERLAP) and st_c[0] == oremap.OVERLAP
+    assert [int(x[1], 16) for x in by_tag["before"]] == before.tolist()
+    assert before[3] == 0x7F8000001000 + 4
+    assert tuple(int(x) for x in by_tag["free"][0]) == counts_f == (1, 0, 2, 0)
+    assert [int(x[1], 16) for x in by_tag["after"]] == after.tolist()
