@@ -214,6 +214,43 @@ def test_repeated_runs_identical():
     assert (first["status"] == g.HIT_BATCH).sum() > 100
 
 
+@pytest.mark.parametrize("block", [4096, 65536, 1 << 20])
+def test_digests_do_not_depend_on_batch_position(block):
+    """A payload's block digests are a function of its bytes alone: the same payloads
+    hashed alone (the small-batch kernel), in shuffled order, behind 70,000 tiny payloads
+    (past that kernel's 65,536-slot limit, so the two-lane kernel and another wave packing)
+    and at shifted start offsets (the unaligned load path) all agree, and with the
+    oracle."""
+    rng = np.random.default_rng(7 + block.bit_length())
+    payloads = make_payloads(rng, block, extra=[5 * block + 77])
+    ref, _ = oracle.batch_digests(payloads, block, threads=host_threads())
+    def per_payload(digests, lens, idx):
+        f, _ = oracle.geometry(lens, block)
+        return [digests[int(f[i]):int(f[i + 1])] for i in idx]
+
+    want = per_payload(ref, [p.size for p in payloads], range(len(payloads)))
+    tiny = [np.frombuffer(rng.bytes(int(n)), np.uint8) for n in rng.integers(1, 300, 70_000)]
+    order = rng.permutation(len(payloads))
+    layouts = {
+        "shuffled": ([payloads[i] for i in order], list(order), 0, 0),
+        "behind 70,000 tiny payloads": (tiny + [payloads[i] for i in order], list(order), len(tiny), 0),
+        "offset 5": (payloads, list(range(len(payloads))), 0, 5),
+    }
+    for name, (batch_payloads, idx, skip, skew) in layouts.items():
+        arena, offs, lens = W.pack(batch_payloads, align=256, skew=skew)
+        say("position independence", block, name)
+        batch = g.Batch.from_arena(to_device(arena), offs, lens, block)
+        d = u64(g.fp_chunks(batch))
+        got = per_payload(d, lens, range(skip, skip + len(idx)))
+        for k, i in enumerate(idx):
+            assert np.array_equal(got[k], want[i]), f"{name}: payload {i}"
+    for i in (0, len(payloads) // 2, len(payloads) - 1):
+        arena, offs, lens = W.pack([payloads[i]], align=256)
+        say("position independence", block, "alone", i)
+        batch = g.Batch.from_arena(to_device(arena), offs, lens, block)
+        assert np.array_equal(u64(g.fp_chunks(batch)), want[i]), f"alone: payload {i}"
+
+
 def test_lookup_special_keys_and_duplicates():
     rng = np.random.default_rng(400)
     pool = np.concatenate([rng.integers(0, 2**64, 500, dtype=np.uint64, endpoint=False),
