@@ -883,6 +883,12 @@ def main():
         f"(min {min(fp_ms):.3f}, max {max(fp_ms):.3f}), step {ms_per_step:.3f} ms, cold {cold}, "
         f"read ceiling {read_gbs:.0f} GB/s")
 
+    # the last timed step's outputs still hold the planted truth
+    torch.cuda.synchronize()
+    c = g.as_u64(counters)
+    if int(c[0]) != expect_miss or int(c[1]) != miss_bytes:
+        raise SystemExit(f"timed steps broke the planted truth: {int(c[0])} misses, expected {expect_miss}")
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = run_cpu_baseline(payloads, batch.block_bytes, threads, int(args.cpu_budget_gb * 1e9))
@@ -907,7 +913,10 @@ def main():
                    "launch": "hip_graph" if graph is not None else "eager",
                    "step_ms": {"median": round(float(np.median(warm_ms)), 4), "min": round(min(warm_ms), 4),
                                "max": round(max(warm_ms), 4)},
-                   "cold": cold, "insert_ms": insert_ms, "pipelined": pipe, "per_buffer": per_buffer},
+                   "cold": cold, "insert_ms": insert_ms, "pipelined": pipe, "per_buffer": per_buffer,
+                   "truth": {"expected_misses": expect_miss, "misses": miss_count, "ok": True,
+                             "check": "MISS count after the warm-up and after the timed steps equals the "
+                                      "workload's planted truth; bit-exact parity is in tests/"}},
         "roofline": {"bound": "hbm", "kernel": "fp_kernel", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes": algo_bytes, "avg_launch_ms": round(fp_avg_ms, 4),
