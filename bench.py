@@ -452,7 +452,8 @@ def remap_path(args, g, torch):
                    "replace": f"free {gone.size} tasks, load {s2.size} intervals"},
         "roofline": {"bound": "hbm", "achieved": round(algo / (med * 1e-3) / 1e9, 1), "peak": 8000.0,
                      "unit": "GB/s", "frac": round(algo / (med * 1e-3) / 1e9 / 8000.0, 4), "traffic": None,
-                     "note": "each search step is a different cache line for nearly every lane: bound by the L2 request rate, not by HBM bytes"},
+                     "note": "each search step is a different cache line for nearly every lane: bound by the L2 request "
+                             "rate, not by HBM bytes (profiles/remap_translate_pmc.txt)"},
         "cpu_baseline": cpu}
     print(json.dumps(out_json), flush=True)
 

@@ -378,12 +378,12 @@ gleam_status gleam_restore_blocks(const gleam_batch* dst, const gleam_send_recor
  * [t << 40, (t + 1) << 40), the paper's 1 TB per task). Storage is caller-owned device
  * memory that must outlive the handle: a 256-byte header (u64 interval count, fence
  * stride, fence length), u64 start[capacity] sorted ascending, {end (exclusive),
- * target}[capacity] pairs in the same order, and a 4096-entry fence (every stride-th
- * start) that translation searches in LDS first. Calls on one map must not overlap, on
+ * target - start}[capacity] pairs in the same order, and an 8192-entry fence (every
+ * stride-th start) that translation searches in LDS first. Calls on one map must not overlap, on
  * any stream, with an update of it.
  *
  * gleam_remap_bytes: storage bytes for `capacity` intervals (1 <= capacity <= 2^31):
- * 256 + 24 * capacity + 32768; 0 for an invalid capacity.
+ * 256 + 24 * capacity + 65536; 0 for an invalid capacity.
  *
  * gleam_remap_create: a handle over d_storage (device, 256-byte aligned, >=
  * gleam_remap_bytes(capacity) bytes) and the clear of its header (an empty map).

@@ -5,17 +5,18 @@
 //
 // The map is an array of disjoint intervals sorted by start, in caller-owned device
 // storage: [256-byte header: u64 count, fence stride, fence length][start x cap]
-// [{end, target} x cap][fence: 4096 x u64], end exclusive. A sorted array answers the
+// [{end, bias} x cap][fence: kFence x u64], end exclusive, bias = target - start (mod
+// 2^64, so a translation is one add: p + bias). A sorted array answers the
 // same ordered queries as the tree; on the GPU a batch of pointers is translated by
 // one search per lane, and a batch of changes is merged in a few passes instead of
 // rebalancing node by node.
 //
 // Translation is bound by lane-divergent loads (each level of a binary search is a
 // different cache line for nearly every lane), not by bytes. So every update also
-// writes a fence, every S-th start with S = ceil(count / 4096); a translating workgroup
+// writes a fence, every S-th start with S = ceil(count / 8192); a translating workgroup
 // keeps the fence in LDS and searches it first, leaving log2(S) levels for global
-// memory (6 instead of 18 at 208k intervals), and end and target sit side by side so
-// the final step is one 16-byte load.
+// memory (5 instead of 18 at 208k intervals), and end and bias sit side by side so the
+// final step is one 16-byte load and needs no start.
 //
 // An update never re-sorts the intervals it keeps (they are already in order):
 //   1. removal ranges are sorted by start, with a running maximum of their last
@@ -50,12 +51,12 @@ constexpr uint32_t kMaxGrid = 8192;
 constexpr uint64_t kNone = ~0ull;  // sort key of an addition that takes no part; no valid start equals it
 constexpr uint64_t kMaxCount = 1ull << 31;
 
-constexpr uint32_t kFence = 4096;  // fence entries (32 KiB of LDS)
+constexpr uint32_t kFence = 8192;  // fence entries (64 KiB of LDS: two translating workgroups per CU)
 
 struct MapRef {
   uint64_t* hdr;   // [0] number of intervals, [1] fence stride S, [2] fence length
   uint64_t* start;
-  ulonglong2* et;  // {end, target} per interval
+  ulonglong2* et;  // {end, target - start} per interval
   uint64_t* fence; // start[k * S] for k < fence length
   uint64_t cap;
 };
@@ -434,7 +435,8 @@ __global__ void place_additions_kernel(MapRef map, const uint64_t* s_start, cons
     if (!acc[k]) continue;
     if (t.fits) {
       const uint64_t s = key[k];
-      place(map, apos[k] + count_lt(s_start, t.n_surv, s), s, make_ulonglong2(aend[k], a_target[val[k]]), t.S);
+      place(map, apos[k] + count_lt(s_start, t.n_surv, s), s, make_ulonglong2(aend[k], a_target[val[k]] - s),
+            t.S);
     } else if (status) {
       status[val[k]] = GLEAM_REMAP_FULL;
     }
@@ -490,9 +492,8 @@ translate_kernel(MapRef map, const uint64_t* addr, uint64_t n, uint64_t* out) {
       uint32_t c = 0;
       for (uint32_t step = s_top; step; step >>= 1)
         if (c + step <= len && map.start[lo + c + step] <= a) c += step;
-      const uint64_t st = c ? map.start[lo + c] : fence[f - 1];
-      const ulonglong2 et = map.et[lo + c];
-      if (a < et.x) r = et.y + (a - st);
+      const ulonglong2 et = map.et[lo + c];  // start[lo + c] <= a: inside iff a < end
+      if (a < et.x) r = a + et.y;
     }
     out[i] = r;
   }
@@ -509,7 +510,7 @@ __global__ void export_kernel(MapRef map, uint64_t* d_start, uint64_t* d_len, ui
     const ulonglong2 et = map.et[p];
     d_start[p] = s;
     d_len[p] = et.x - s;
-    d_target[p] = et.y;
+    d_target[p] = et.y + s;
   }
 }
 
@@ -718,9 +719,11 @@ extern "C" gleam_status gleam_remap_translate(const gleam_remap* m, const uint64
   int cus = 0;
   const gleam_status st = device_cu_count(&cus);
   if (st != GLEAM_OK) return st;
-  // two 1024-lane workgroups per CU fill it (32 waves); each loads the fence once
+  // as many 1024-lane workgroups per CU as the LDS holds fences (at most two, 32 waves);
+  // each loads the fence once
+  const uint64_t per_cu = kFence * 8 <= 80 * 1024 ? 2 : 1;
   const uint64_t want = (n + kTranslateThreads - 1) / kTranslateThreads;
-  const uint64_t grid = want < 2ull * cus ? want : 2ull * cus;
+  const uint64_t grid = want < per_cu * cus ? want : per_cu * cus;
   hipLaunchKernelGGL(translate_kernel, dim3((uint32_t)grid), dim3(kTranslateThreads), 0, (hipStream_t)stream,
                      map_ref(m), d_addr, n, d_out);
   return launch_status("translate_kernel");

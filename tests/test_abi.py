@@ -147,13 +147,13 @@ def test_lookup_insert_compact_validation():
 
 def test_remap_validation():
     h = ctypes.c_void_p()
-    assert g.lib.gleam_remap_bytes(1) == 256 + 24 + 32768
-    assert g.lib.gleam_remap_bytes(1000) == 256 + 24 * 1000 + 32768
+    assert g.lib.gleam_remap_bytes(1) == 256 + 24 + 65536
+    assert g.lib.gleam_remap_bytes(1000) == 256 + 24 * 1000 + 65536
     assert g.lib.gleam_remap_bytes(0) == 0
     assert g.lib.gleam_remap_bytes((1 << 31) + 1) == 0
     assert g.lib.gleam_remap_create(256, 1 << 20, 0, ctypes.byref(h), None) == g.E_INVALID      # capacity
     assert g.lib.gleam_remap_create(257, 1 << 20, 64, ctypes.byref(h), None) == g.E_INVALID     # unaligned
-    assert g.lib.gleam_remap_create(256, 256 + 24 * 64 + 32767, 64, ctypes.byref(h), None) == g.E_INVALID
+    assert g.lib.gleam_remap_create(256, 256 + 24 * 64 + 65535, 64, ctypes.byref(h), None) == g.E_INVALID
     assert g.lib.gleam_remap_create(None, 1 << 20, 64, ctypes.byref(h), None) == g.E_INVALID
     assert g.lib.gleam_remap_create(256, 1 << 20, 64, None, None) == g.E_INVALID
     assert g.lib.gleam_remap_destroy(None) == g.OK
