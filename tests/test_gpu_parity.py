@@ -251,6 +251,27 @@ def test_digests_do_not_depend_on_batch_position(block):
         assert np.array_equal(u64(g.fp_chunks(batch)), want[i]), f"alone: payload {i}"
 
 
+@pytest.mark.parametrize("skew", [0, 3, 16])
+def test_4k_blocks_past_the_small_batch_limit(skew):
+    """4 KiB blocks past the small-batch kernel's 65,536 slots, every tail length: 80,000
+    payloads of lengths 0 (between the others), 1, 31..33, 511..513, 1000, 2048,
+    4095..4097, 8192, 9000 and 12289, at aligned and unaligned starts, leaf digests on;
+    every digest equals the oracle's."""
+    rng = np.random.default_rng(4242 + skew)
+    n = 80_000
+    lens = rng.choice(np.array([0, 1, 31, 32, 33, 511, 512, 513, 1000, 2048, 4095, 4096, 4097, 8192, 9000, 12289]),
+                      n, p=[0.05] + [0.95 / 15] * 15).astype(np.int64)
+    payloads = [np.frombuffer(rng.bytes(int(m)), np.uint8) for m in lens]
+    arena, offs, blens = W.pack(payloads, align=256, skew=skew)
+    say("4 KiB blocks past the small-batch limit, skew", skew, "payloads", n)
+    batch = g.Batch.from_arena(to_device(arena), offs, blens, 4096)
+    assert batch.n_blocks > 65536
+    d, lv = g.fp_chunks(batch, with_leaves=True)
+    want, wleaves = oracle.batch_digests(payloads, 4096, with_leaves=True, threads=host_threads())
+    assert np.array_equal(u64(d), want)
+    assert np.array_equal(u64(lv), wleaves.reshape(-1))
+
+
 def test_lookup_special_keys_and_duplicates():
     rng = np.random.default_rng(400)
     pool = np.concatenate([rng.integers(0, 2**64, 500, dtype=np.uint64, endpoint=False),
