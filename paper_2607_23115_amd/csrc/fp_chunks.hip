@@ -107,58 +107,42 @@ __device__ __forceinline__ Leaf locate_wave(const FpArgs& a, uint64_t g_first, u
   return locate_at(a, g, k, s);
 }
 
-__device__ __forceinline__ uint64_t read_le64_bytes(const uint8_t* p) {
-  uint64_t v = 0;
-#pragma unroll
-  for (int i = 7; i >= 0; --i) v = (v << 8) | p[i];
-  return v;
-}
-__device__ __forceinline__ uint32_t read_le32_bytes(const uint8_t* p) {
-  uint32_t v = 0;
-#pragma unroll
-  for (int i = 3; i >= 0; --i) v = (v << 8) | p[i];
-  return v;
-}
-
 // XXH64 after the stripe loop: fold (or the short-input start), length, tail, avalanche.
-// `p` is 16-byte aligned when `aligned`; the tail starts at a multiple of 32 from p.
-// Aligned, the tail's < 32 bytes lie in at most four aligned 8-byte words, which are
-// loaded together (one round trip instead of up to seven dependent ones) and stepped
-// through in registers: whole words, then a 4-byte step, then single bytes.
+// The tail (the < 32 bytes after the last full stripe, at any address) lies in at most
+// five aligned 8-byte words, each holding tail bytes. They are loaded together (one
+// round trip, no byte loads), the tail's own 8-byte words are shifted out of adjacent
+// pairs, and the XXH64 tail steps run in registers: whole words, then a 4-byte step,
+// then single bytes.
 __device__ __forceinline__ uint64_t finish_leaf(uint64_t v1, uint64_t v2, uint64_t v3, uint64_t v4, const uint8_t* p,
-                                                uint32_t len, bool aligned) {
+                                                uint32_t len) {
   const uint32_t stripes = len >> 5;
   uint64_t h = stripes ? xxh_converge(v1, v2, v3, v4) : kP5;
   h += len;
-  uint32_t pos = stripes << 5;
-  if (aligned) {
-    const uint32_t tail = len - pos;         // 0..31
-    const uint32_t words = (tail + 7) >> 3;  // aligned words holding tail bytes
-    const uint64_t* w = reinterpret_cast<const uint64_t*>(p + pos);
-    uint64_t t[4];
+  const uint32_t tail = len - (stripes << 5);  // 0..31
+  const uint64_t at = reinterpret_cast<uint64_t>(p) + (stripes << 5);
+  const uint32_t lead = (uint32_t)(at & 7);    // tail bytes start this far into a word
+  const uint32_t words = tail ? (lead + tail + 7) >> 3 : 0;
+  const uint64_t* w = reinterpret_cast<const uint64_t*>(at - lead);
+  uint64_t W[5];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) t[i] = (uint32_t)i < words ? w[i] : 0;
-    const uint32_t whole = tail >> 3;
+  for (int i = 0; i < 5; ++i) W[i] = (uint32_t)i < words ? w[i] : 0;
+  const uint32_t sh = lead * 8;
+  uint64_t t[4];
 #pragma unroll
-    for (int i = 0; i < 3; ++i)
-      if ((uint32_t)i < whole) h = xxh_tail8(h, t[i]);
-    uint64_t rest = whole == 0 ? t[0] : whole == 1 ? t[1] : whole == 2 ? t[2] : t[3];
-    if (tail & 4) {
-      h = xxh_tail4(h, (uint32_t)rest);
-      rest >>= 32;
-    }
-    for (uint32_t i = 0; i < (tail & 3); ++i) {
-      h = xxh_tail1(h, (uint8_t)rest);
-      rest >>= 8;
-    }
-    return xxh_avalanche(h);
+  for (int j = 0; j < 4; ++j) t[j] = sh ? (W[j] >> sh) | (W[j + 1] << (64 - sh)) : W[j];
+  const uint32_t whole = tail >> 3;
+#pragma unroll
+  for (int j = 0; j < 3; ++j)
+    if ((uint32_t)j < whole) h = xxh_tail8(h, t[j]);
+  uint64_t rest = whole == 0 ? t[0] : whole == 1 ? t[1] : whole == 2 ? t[2] : t[3];
+  if (tail & 4) {
+    h = xxh_tail4(h, (uint32_t)rest);
+    rest >>= 32;
   }
-  for (; pos + 8 <= len; pos += 8) h = xxh_tail8(h, read_le64_bytes(p + pos));
-  if (pos + 4 <= len) {
-    h = xxh_tail4(h, read_le32_bytes(p + pos));
-    pos += 4;
+  for (uint32_t i = 0; i < (tail & 3); ++i) {
+    h = xxh_tail1(h, (uint8_t)rest);
+    rest >>= 8;
   }
-  for (; pos < len; ++pos) h = xxh_tail1(h, p[pos]);
   return xxh_avalanche(h);
 }
 
@@ -199,7 +183,7 @@ __device__ uint64_t hash_leaf_group(const uint8_t* p, uint32_t len, int lane) {
 #pragma unroll
   for (int k = 0; k < 4; ++k) v[k] = shfl64(acc[k % kAcc], g0 + k / kAcc);
   if (r != 0 || len == 0) return 0;
-  return finish_leaf(v[0], v[1], v[2], v[3], p, len, (a & 15) == 0);
+  return finish_leaf(v[0], v[1], v[2], v[3], p, len);
 }
 
 // Lane roles shared by the streamed paths.
@@ -318,7 +302,7 @@ __device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
   }
   const uint64_t pa = shfl_xor64(va, 1), pb = shfl_xor64(vb, 1);
   if (r.rp || lf.len == 0) return 0;
-  return finish_leaf(va, vb, pa, pb, lf.addr, lf.len, true);
+  return finish_leaf(va, vb, pa, pb, lf.addr, lf.len);
 }
 
 // Bytes [d, d + 16) of the 32 bytes c0 || c1 (d in 0..15), as a 16-byte value.
@@ -406,7 +390,7 @@ __device__ uint64_t hash_wave_shifted(const Leaf& lf, uint8_t* tile, uint64_t* t
   }
   const uint64_t pa = shfl_xor64(va, 1), pb = shfl_xor64(vb, 1);
   if (r.rp || lf.len == 0) return 0;
-  return finish_leaf(va, vb, pa, pb, lf.addr, lf.len, d == 0);
+  return finish_leaf(va, vb, pa, pb, lf.addr, lf.len);
 }
 
 // Digest of this lane pair's leaf, in the even lane.
@@ -635,7 +619,7 @@ __device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
   const int q = lane & ~3;
   const uint64_t v1 = shfl64(v, q), v2 = shfl64(v, q + 1), v3 = shfl64(v, q + 2), v4 = shfl64(v, q + 3);
   if (ra || lf.len == 0) return 0;
-  return finish_leaf(v1, v2, v3, v4, lf.addr, lf.len, true);
+  return finish_leaf(v1, v2, v3, v4, lf.addr, lf.len);
 }
 
 // Digest of this lane quad's leaf, in lane 4l.
