@@ -167,7 +167,8 @@ gleam_status gleam_cache_destroy(gleam_cache* c);
  * carried keys already present). UINT64_MAX for a NULL handle. */
 uint64_t gleam_cache_key_bound(const gleam_cache* c);
 
-/* Device workspace bytes needed by lookup, insert and compaction of n items. */
+/* Device workspace bytes needed by lookup, insert and compaction of n items; 0 for n
+ * above 2^40, which those calls refuse with GLEAM_E_UNSUPPORTED. */
 size_t gleam_workspace_bytes(uint64_t n);
 
 /*
@@ -180,7 +181,8 @@ size_t gleam_workspace_bytes(uint64_t n);
  *   d_ws, ws_bytes  device workspace, 256-byte aligned, >= gleam_workspace_bytes(n)
  * Capacity is enforced on the host without a device sync: if key_bound + n could
  * exceed the maximum load, GLEAM_E_CAPACITY is returned and nothing is inserted.
- * Errors: GLEAM_E_INVALID, GLEAM_E_CAPACITY, GLEAM_E_WORKSPACE, GLEAM_E_HIP.
+ * Errors: GLEAM_E_INVALID, GLEAM_E_CAPACITY, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED (n
+ * above 2^31 workgroups of 256 keys, or 2^40), GLEAM_E_HIP.
  */
 gleam_status gleam_cache_insert(gleam_cache* c, const uint64_t* d_keys, const uint64_t* d_vals, uint64_t n,
                                 uint64_t* d_n_new, void* d_ws, size_t ws_bytes, void* stream);
@@ -192,7 +194,8 @@ gleam_status gleam_cache_insert(gleam_cache* c, const uint64_t* d_keys, const ui
  *   d_ref     nullable device u64[n] output (see the status enum)
  *   d_ws      device workspace, 256-byte aligned, >= gleam_workspace_bytes(n)
  * The table is only read.
- * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_HIP. n == 0 is a no-op.
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED (n above 2^31
+ * workgroups of 256 keys, or 2^40), GLEAM_E_HIP. n == 0 is a no-op.
  */
 gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t* d_keys, uint64_t n, uint8_t* d_status,
                                 uint64_t* d_ref, void* d_ws, size_t ws_bytes, void* stream);
@@ -208,8 +211,8 @@ gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t* d_keys, ui
  *   d_miss_count  device u64[1] output
  *   d_miss_bytes  nullable device u64[1] output: total bytes of those blocks
  *   d_ws          device workspace, 256-byte aligned, >= gleam_workspace_bytes(n)
- * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_HIP. With n == 0 the
- * counters are still set to 0.
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED (n above 2^40),
+ * GLEAM_E_HIP. With n == 0 the counters are still set to 0.
  */
 gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam_batch* b, uint64_t* d_miss_idx,
                                 uint64_t* d_miss_count, uint64_t* d_miss_bytes, void* d_ws, size_t ws_bytes,

@@ -69,7 +69,11 @@ gleam_status device_cu_count(int* cus) {
 }
 
 WsLayout ws_layout(uint64_t n) {
-  WsLayout L;
+  WsLayout L{};
+  if (n > kMaxWsItems) {  // no workspace is that large; the calls refuse such an n
+    L.total = SIZE_MAX;
+    return L;
+  }
   uint64_t cap = 64;
   while (cap < 2 * n) cap <<= 1;
   L.scratch_cap = cap;
@@ -79,6 +83,22 @@ WsLayout ws_layout(uint64_t n) {
   L.total = L.tiles_off + (size_t)(L.tiles + 1) * 16;
   L.total = (L.total + 255) & ~(size_t)255;
   return L;
+}
+
+gleam_status check_workspace(const WsLayout& L, const void* ws, size_t ws_bytes, const char* who) {
+  if (L.total == SIZE_MAX) {
+    set_error("%s: more than 2^40 items", who);
+    return GLEAM_E_UNSUPPORTED;
+  }
+  if (!ws || !aligned256(ws)) {
+    set_error("%s: workspace must be non-null and 256-byte aligned", who);
+    return GLEAM_E_INVALID;
+  }
+  if (ws_bytes < L.total) {
+    set_error("%s: workspace of %zu bytes, %zu needed", who, ws_bytes, L.total);
+    return GLEAM_E_WORKSPACE;
+  }
+  return GLEAM_OK;
 }
 
 }  // namespace gleam
@@ -98,7 +118,7 @@ extern "C" const char* gleam_status_string(gleam_status s) {
 extern "C" const char* gleam_last_error(void) { return gleam::g_last_error; }
 
 extern "C" size_t gleam_workspace_bytes(uint64_t n) {
-  if (n > (1ull << 40)) return 0;
+  if (n > gleam::kMaxWsItems) return 0;
   return gleam::ws_layout(n).total;
 }
 

@@ -384,14 +384,8 @@ extern "C" gleam_status gleam_cache_insert(gleam_cache* c, const uint64_t* d_key
     return GLEAM_E_INVALID;
   }
   const WsLayout L = ws_layout(n);
-  if (!d_ws || !aligned256(d_ws)) {
-    set_error("gleam_cache_insert: workspace must be non-null and 256-byte aligned");
-    return GLEAM_E_INVALID;
-  }
-  if (ws_bytes < L.total) {
-    set_error("gleam_cache_insert: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
-    return GLEAM_E_WORKSPACE;
-  }
+  gleam_status st = check_workspace(L, d_ws, ws_bytes, "gleam_cache_insert");
+  if (st != GLEAM_OK) return st;
   if (n > 0x7fffffffull * kThreads) {
     set_error("gleam_cache_insert: more than 2^31 workgroups of keys");
     return GLEAM_E_UNSUPPORTED;
@@ -402,7 +396,7 @@ extern "C" gleam_status gleam_cache_insert(gleam_cache* c, const uint64_t* d_key
     return GLEAM_E_CAPACITY;
   }
   hipStream_t s = (hipStream_t)stream;
-  gleam_status st = clear_scratch(d_ws, L, s, d_n_new);
+  st = clear_scratch(d_ws, L, s, d_n_new);
   uint64_t* counter = d_n_new ? d_n_new : reinterpret_cast<uint64_t*>(d_ws) + 1;
   if (st != GLEAM_OK) return st;
   if (n == 0) return GLEAM_OK;
@@ -432,14 +426,8 @@ extern "C" gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t*
     return GLEAM_E_INVALID;
   }
   const WsLayout L = ws_layout(n);
-  if (!d_ws || !aligned256(d_ws)) {
-    set_error("gleam_cache_lookup: workspace must be non-null and 256-byte aligned");
-    return GLEAM_E_INVALID;
-  }
-  if (ws_bytes < L.total) {
-    set_error("gleam_cache_lookup: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
-    return GLEAM_E_WORKSPACE;
-  }
+  gleam_status st = check_workspace(L, d_ws, ws_bytes, "gleam_cache_lookup");
+  if (st != GLEAM_OK) return st;
   if (n > 0x7fffffffull * kThreads) {
     set_error("gleam_cache_lookup: more than 2^31 workgroups of keys");
     return GLEAM_E_UNSUPPORTED;
@@ -450,7 +438,7 @@ extern "C" gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t*
                        d_ref);
     return launch_status("lookup_small_kernel");
   }
-  gleam_status st = clear_scratch(d_ws, L, s);
+  st = clear_scratch(d_ws, L, s);
   if (st != GLEAM_OK) return st;
   const ScratchRef sc = scratch_ref(d_ws, L);
   const TableRef t = table_ref(c);

@@ -219,14 +219,8 @@ extern "C" gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, 
     }
   }
   const WsLayout L = ws_layout(n);
-  if (!d_ws || !aligned256(d_ws)) {
-    set_error("gleam_miss_compact: workspace must be non-null and 256-byte aligned");
-    return GLEAM_E_INVALID;
-  }
-  if (ws_bytes < L.total) {
-    set_error("gleam_miss_compact: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
-    return GLEAM_E_WORKSPACE;
-  }
+  gleam_status st = check_workspace(L, d_ws, ws_bytes, "gleam_miss_compact");
+  if (st != GLEAM_OK) return st;
   if (L.tiles > 0x7fffffffull) {
     set_error("gleam_miss_compact: more than 2^31 tiles");
     return GLEAM_E_UNSUPPORTED;
@@ -242,7 +236,6 @@ extern "C" gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, 
   uint64_t* counts = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(d_ws) + L.tiles_off);
   uint64_t* offsets = counts + L.tiles;
   const uint64_t block_bytes = d_miss_bytes ? b->block_bytes : 0;
-  gleam_status st;
   hipLaunchKernelGGL(compact_count_kernel, dim3((uint32_t)L.tiles), dim3(kThreads), 0, s, d_status, n, counts);
   if ((st = launch_status("compact_count_kernel")) != GLEAM_OK) return st;
   hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, counts, L.tiles, offsets, d_miss_count,

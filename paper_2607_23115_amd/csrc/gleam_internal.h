@@ -62,7 +62,12 @@ struct WsLayout {
   size_t tiles_off;
   size_t total;
 };
+constexpr uint64_t kMaxWsItems = 1ull << 40;  // larger n: total = SIZE_MAX, refused
 WsLayout ws_layout(uint64_t n);
+// The workspace checks every call makes, in one order: an n beyond any layout
+// (GLEAM_E_UNSUPPORTED), a null or unaligned pointer (GLEAM_E_INVALID), too few bytes
+// (GLEAM_E_WORKSPACE). Sets the error text with `who`.
+gleam_status check_workspace(const WsLayout& L, const void* ws, size_t ws_bytes, const char* who);
 
 void set_error(const char* fmt, ...);
 void clear_error();

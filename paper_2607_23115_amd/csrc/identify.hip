@@ -72,14 +72,8 @@ extern "C" gleam_status gleam_identify_weights(const gleam_batch* b, const uint6
     return GLEAM_E_UNSUPPORTED;
   }
   const WsLayout L = ws_layout(b->n_blocks + b->n_seg);
-  if (!d_ws || !aligned256(d_ws)) {
-    set_error("gleam_identify_weights: workspace must be non-null and 256-byte aligned");
-    return GLEAM_E_INVALID;
-  }
-  if (ws_bytes < L.total) {
-    set_error("gleam_identify_weights: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
-    return GLEAM_E_WORKSPACE;
-  }
+  st = check_workspace(L, d_ws, ws_bytes, "gleam_identify_weights");
+  if (st != GLEAM_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   uint64_t* current = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(d_ws) + L.scratch_off);
   uint64_t* first_diff = d_seg_first_diff ? d_seg_first_diff : current + b->n_blocks;

@@ -268,14 +268,8 @@ extern "C" gleam_status gleam_send_plan(const gleam_batch* b, const uint64_t* d_
     return GLEAM_E_INVALID;
   }
   const WsLayout L = ws_layout(b->n_blocks);
-  if (!d_ws || !aligned256(d_ws)) {
-    set_error("gleam_send_plan: workspace must be non-null and 256-byte aligned");
-    return GLEAM_E_INVALID;
-  }
-  if (ws_bytes < L.total) {
-    set_error("gleam_send_plan: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
-    return GLEAM_E_WORKSPACE;
-  }
+  st = check_workspace(L, d_ws, ws_bytes, "gleam_send_plan");
+  if (st != GLEAM_OK) return st;
   if (L.tiles > 0x7fffffffull) {
     set_error("gleam_send_plan: more than 2^31 tiles");
     return GLEAM_E_UNSUPPORTED;

@@ -163,3 +163,12 @@ def test_remap_validation():
     assert g.lib.gleam_remap_translate(None, 256, 1, 256, None) == g.E_INVALID
     assert g.lib.gleam_remap_export(None, 256, 256, 256, 256, None) == g.E_INVALID
     assert b"gleam_remap_export" in g.lib.gleam_last_error()
+
+
+def test_counts_beyond_any_workspace_are_refused():
+    """n above 2^40 items has no workspace layout (its size would overflow): the call
+    returns GLEAM_E_UNSUPPORTED at once, before anything is enqueued."""
+    for n in (2**40 + 1, 2**62 + 1, 2**64 - 1):
+        assert g.lib.gleam_miss_compact(256, n, None, 256, 256, None, 256, 1 << 20, None) == g.E_UNSUPPORTED
+        assert b"2^40" in g.lib.gleam_last_error()
+        assert g.lib.gleam_workspace_bytes(n) == 0
