@@ -345,8 +345,9 @@ gleam_status gleam_send_plan(const gleam_batch* b, const uint64_t* d_digest, con
 
 /*
  * Copy every MISS block's bytes to its planned offset in d_out (device, out_bytes long,
- * at least the plan's packed total; a block that would not fit is skipped). Padding
- * bytes between blocks are not written.
+ * at least the plan's packed total). A record whose block is not inside its payload of
+ * `b`, or whose bytes would not fit d_out, is skipped. Padding bytes between blocks are
+ * not written.
  * Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
  */
 gleam_status gleam_pack_misses(const gleam_batch* b, const gleam_send_record* d_records, uint8_t* d_out,
@@ -359,7 +360,9 @@ gleam_status gleam_pack_misses(const gleam_batch* b, const gleam_send_record* d_
  * receiver's own copy at device address d_held[g] (device u64[n_blocks], e.g. the
  * lookup's ref output when table values are addresses of held blocks; nullable: then
  * HIT_CACHE blocks are left untouched); HIT_BATCH blocks from the packed bytes of the
- * block they repeat. Records that point outside the buffers are skipped.
+ * block they repeat. A record whose block is not inside its payload of `dst`, whose
+ * packed bytes lie outside d_packed, or whose kind is unknown is skipped; d_held
+ * addresses are the caller's and are read as given.
  * Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
  */
 gleam_status gleam_restore_blocks(const gleam_batch* dst, const gleam_send_record* d_records,

@@ -214,34 +214,49 @@ __device__ __forceinline__ void wg_copy(uint8_t* dst, const uint8_t* src, uint64
   }
 }
 
-// Work items: (block, 64 KiB chunk of it); `per_block` chunks per block.
-__global__ __launch_bounds__(kThreads) void pack_kernel(const uint64_t* seg_addr, const gleam_send_record* rec,
-                                                        uint64_t n, uint64_t per_block, uint8_t* out,
-                                                        uint64_t out_bytes) {
+// [at, at + len) lies inside [0, size), without overflow.
+__device__ __forceinline__ bool inside(uint64_t at, uint64_t len, uint64_t size) {
+  return at <= size && len <= size - at;
+}
+
+// The record's block lies inside its payload of the batch.
+__device__ __forceinline__ bool block_in_batch(const gleam_send_record& r, const uint64_t* seg_len, uint64_t n_seg) {
+  return r.payload < n_seg && inside(r.offset, r.length, seg_len[r.payload]);
+}
+
+// Work items: (block, 64 KiB chunk of it); `per_block` chunks per block. Records whose
+// block is not inside its payload, or whose bytes are not inside the packed buffer, are
+// skipped.
+__global__ __launch_bounds__(kThreads) void pack_kernel(const uint64_t* seg_addr, const uint64_t* seg_len,
+                                                        uint64_t n_seg, const gleam_send_record* rec, uint64_t n,
+                                                        uint64_t per_block, uint8_t* out, uint64_t out_bytes) {
   for (uint64_t item = blockIdx.x; item < n * per_block; item += gridDim.x) {
     const uint64_t g = item / per_block, c0 = (item % per_block) * kChunk;
     const gleam_send_record r = rec[g];
-    if (r.kind != GLEAM_MISS || c0 >= r.length || r.ident + r.length > out_bytes) continue;
+    if (r.kind != GLEAM_MISS || c0 >= r.length || !inside(r.ident, r.length, out_bytes) ||
+        !block_in_batch(r, seg_len, n_seg))
+      continue;
     const uint64_t len = min((uint64_t)r.length - c0, kChunk);
     wg_copy(out + r.ident + c0, reinterpret_cast<const uint8_t*>(seg_addr[r.payload]) + r.offset + c0, len);
   }
 }
 
-__global__ __launch_bounds__(kThreads) void restore_kernel(const uint64_t* dst_addr, const gleam_send_record* rec,
-                                                           uint64_t n, uint64_t per_block, const uint8_t* packed,
+__global__ __launch_bounds__(kThreads) void restore_kernel(const uint64_t* dst_addr, const uint64_t* dst_len,
+                                                           uint64_t n_seg, const gleam_send_record* rec, uint64_t n,
+                                                           uint64_t per_block, const uint8_t* packed,
                                                            uint64_t packed_bytes, const uint64_t* held) {
   for (uint64_t item = blockIdx.x; item < n * per_block; item += gridDim.x) {
     const uint64_t g = item / per_block, c0 = (item % per_block) * kChunk;
     const gleam_send_record r = rec[g];
-    if (c0 >= r.length) continue;
+    if (c0 >= r.length || !block_in_batch(r, dst_len, n_seg)) continue;
     const uint8_t* src = nullptr;
     if (r.kind == GLEAM_MISS) {
-      if (r.ident + r.length <= packed_bytes) src = packed + r.ident;
+      if (inside(r.ident, r.length, packed_bytes)) src = packed + r.ident;
     } else if (r.kind == GLEAM_HIT_CACHE) {
       src = held ? reinterpret_cast<const uint8_t*>(held[g]) : nullptr;
-    } else if (r.ident < n) {
+    } else if (r.kind == GLEAM_HIT_BATCH && r.ident < n) {
       const gleam_send_record first = rec[r.ident];
-      if (first.kind == GLEAM_MISS && first.length == r.length && first.ident + r.length <= packed_bytes)
+      if (first.kind == GLEAM_MISS && first.length == r.length && inside(first.ident, r.length, packed_bytes))
         src = packed + first.ident;
     }
     if (!src) continue;
@@ -303,7 +318,7 @@ extern "C" gleam_status gleam_pack_misses(const gleam_batch* b, const gleam_send
   }
   const uint64_t per = chunks_per_block(b->block_bytes);
   hipLaunchKernelGGL(pack_kernel, dim3(copy_grid(b->n_blocks * per)), dim3(kThreads), 0, (hipStream_t)stream,
-                     b->seg_addr, d_records, b->n_blocks, per, d_out, out_bytes);
+                     b->seg_addr, b->seg_len, b->n_seg, d_records, b->n_blocks, per, d_out, out_bytes);
   return launch_status("pack_kernel");
 }
 
@@ -321,6 +336,7 @@ extern "C" gleam_status gleam_restore_blocks(const gleam_batch* dst, const gleam
   }
   const uint64_t per = chunks_per_block(dst->block_bytes);
   hipLaunchKernelGGL(restore_kernel, dim3(copy_grid(dst->n_blocks * per)), dim3(kThreads), 0, (hipStream_t)stream,
-                     dst->seg_addr, d_records, dst->n_blocks, per, d_packed, packed_bytes, d_held);
+                     dst->seg_addr, dst->seg_len, dst->n_seg, d_records, dst->n_blocks, per, d_packed, packed_bytes,
+                     d_held);
   return launch_status("restore_kernel");
 }

@@ -117,3 +117,59 @@ def test_transfer_decoder7b_full():
     res = oracle.run(payloads, block, ot, threads=threads)
     erec, etot = oracle.send_plan(lens, block, res["digests"], res["status"], res["ref"])
     assert np.array_equal(g.records_to_numpy(records), erec) and np.array_equal(tot, etot)
+
+
+def test_malformed_records_are_skipped():
+    """Records that the kernels' own checks reject are skipped: a payload index past the
+    batch, a block running past its payload's end, packed bytes past the buffer (also
+    with an offset that would wrap 2^64), and an unknown kind. Every other block is
+    packed and restored as planned."""
+    rng = np.random.default_rng(77)
+    block = 4096
+    payloads = [np.frombuffer(rng.bytes(n), np.uint8) for n in (3 * block, 2 * block + 100, block, 5000)]
+    payloads.append(payloads[0].copy())  # repeats payload 0: HIT_BATCH blocks
+    arena, offs, lens = W.pack(payloads)
+    src = g.Batch.from_arena(to_device(arena), offs, lens, block)
+    d = g.fp_chunks(src)
+    status, ref = g.Cache(1 << 10).lookup(d)
+    records, totals = g.send_plan(src, d, status, ref)
+    torch.cuda.synchronize()
+    rec = g.records_to_numpy(records).copy()
+    n_packed = int(u64(totals)[3])
+    miss = np.flatnonzero(rec["kind"] == g.MISS)
+    batch_rep = np.flatnonzero(rec["kind"] == g.HIT_BATCH)
+    assert miss.size >= 5 and batch_rep.size >= 2
+    bad = {}
+    r = rec.copy()
+    r["payload"][miss[0]] = len(payloads) + 3            # no such payload
+    r["offset"][miss[1]] = int(lens[r["payload"][miss[1]]]) - 10  # runs past the payload's end
+    r["ident"][miss[2]] = n_packed - 8                    # packed bytes past the buffer
+    r["ident"][miss[3]] = (1 << 64) - 8                   # ... with a wrapping offset
+    r["kind"][batch_rep[0]] = 7                           # unknown kind
+    for k, i in enumerate((miss[0], miss[1], miss[2], miss[3], batch_rep[0])):
+        bad[int(i)] = k
+    d_rec = torch.from_numpy(r.view(np.uint8).copy()).to("cuda")
+    say("malformed records: pack")
+    packed = torch.zeros(max(n_packed, 1), dtype=torch.uint8, device="cuda")
+    g.pack_misses(src, d_rec, packed)
+    dst_arena, doffs, dlens = W.pack([np.zeros(p.size, np.uint8) for p in payloads])
+    d_dst = to_device(dst_arena)
+    dst = g.Batch.from_arena(d_dst, doffs, dlens, block)
+    say("malformed records: restore")
+    g.restore_blocks(dst, d_rec, packed, held=None)
+    torch.cuda.synchronize()
+    got_packed = packed.cpu().numpy()
+    out = d_dst.cpu().numpy()
+    for i in range(rec.size):
+        p, o, n, kind = int(rec["payload"][i]), int(rec["offset"][i]), int(rec["length"][i]), int(rec["kind"][i])
+        got = out[int(doffs[p]) + o:int(doffs[p]) + o + n]
+        if i in bad:
+            assert not got.any(), f"record {i} should have been skipped"
+        elif kind == g.MISS:
+            ident = int(rec["ident"][i])
+            assert np.array_equal(got_packed[ident:ident + n], payloads[p][o:o + n]), f"packed block {i}"
+            assert np.array_equal(got, payloads[p][o:o + n]), f"restored block {i}"
+        elif kind == g.HIT_BATCH and int(rec["ident"][i]) not in bad:
+            assert np.array_equal(got, payloads[p][o:o + n]), f"repeated block {i}"
+        # a HIT_BATCH block repeating a skipped MISS gets that block's unwritten packed
+        # bytes or nothing; either way it stays inside its own payload
