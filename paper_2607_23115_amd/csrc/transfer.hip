@@ -247,13 +247,16 @@ __global__ __launch_bounds__(kThreads) void restore_kernel(const uint64_t* dst_a
                                                            uint64_t packed_bytes, const uint64_t* held) {
   for (uint64_t item = blockIdx.x; item < n * per_block; item += gridDim.x) {
     const uint64_t g = item / per_block, c0 = (item % per_block) * kChunk;
+    // the held address does not depend on the record: read both at once, so the range
+    // check of the record is the only dependent read before the copy
+    const uint64_t held_addr = held ? held[g] : 0;
     const gleam_send_record r = rec[g];
     if (c0 >= r.length || !block_in_batch(r, dst_len, n_seg)) continue;
     const uint8_t* src = nullptr;
     if (r.kind == GLEAM_MISS) {
       if (inside(r.ident, r.length, packed_bytes)) src = packed + r.ident;
     } else if (r.kind == GLEAM_HIT_CACHE) {
-      src = held ? reinterpret_cast<const uint8_t*>(held[g]) : nullptr;
+      src = reinterpret_cast<const uint8_t*>(held_addr);
     } else if (r.kind == GLEAM_HIT_BATCH && r.ident < n) {
       const gleam_send_record first = rec[r.ident];
       if (first.kind == GLEAM_MISS && first.length == r.length && inside(first.ident, r.length, packed_bytes))
