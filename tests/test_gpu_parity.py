@@ -272,6 +272,43 @@ def test_4k_blocks_past_the_small_batch_limit(skew):
     assert np.array_equal(u64(lv), wleaves.reshape(-1))
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_randomized_batches(seed):
+    """Seeded random batch geometries: block size 4 KiB..16 MiB, 1..4000 payloads whose
+    lengths mix empty, tiny, leaf- and block-edge and multi-block sizes, repeated
+    payloads, an optional skew of every start, a table holding a random part of the
+    digests; every output (digests, leaf digests, status, ref, miss list, count, bytes)
+    equals the oracle's."""
+    rng = np.random.default_rng(90_000 + seed)
+    block = 4096 << int(rng.integers(0, 13))
+    n = int(rng.choice([1, 7, 64, 300, 1500, 4000]))
+    budget = 48 << 20
+    edges = np.array([0, 1, 31, 32, 33, 4095, 4096, 4097, block - 1, block, block + 1, 2 * block + 17])
+    kind = rng.integers(0, 3, n)
+    lens = np.where(kind == 0, rng.choice(edges, n),
+                    np.where(kind == 1, rng.integers(0, 8192, n), rng.integers(0, 3 * block + 1, n)))
+    lens = np.minimum(lens, budget // n)
+    payloads = [np.frombuffer(rng.bytes(int(m)), np.uint8) for m in lens]
+    for i in rng.integers(0, n, n // 10):  # some payloads repeat an earlier one
+        j = int(rng.integers(0, n))
+        payloads[int(i)] = payloads[j].copy()
+    skew = int(rng.choice([0, 0, 0, 4, 8, 13]))
+    arena, offs, blens = W.pack(payloads, align=256, skew=skew)
+    say("randomized batch", seed, "block", block, "payloads", n, "bytes", int(blens.sum()), "skew", skew)
+    batch = g.Batch.from_arena(to_device(arena), offs, blens, block)
+    dig, _ = oracle.batch_digests(payloads, block, threads=host_threads())
+    held = np.unique(dig[rng.random(dig.size) < 0.3]) if dig.size else np.zeros(0, np.uint64)
+    table, otable = g.Cache(1 << 16), oracle.Table()
+    if held.size:
+        vals = rng.integers(0, 2**63, held.size, dtype=np.uint64)
+        table.insert(keys_to_device(held), keys_to_device(vals))
+        otable.insert(held, vals)
+    gpu = run_path(batch, table, with_leaves=True)
+    ref = oracle_path(payloads, block, otable)
+    assert_same(gpu, ref, f"seed {seed}")
+    assert np.array_equal(gpu["leaves"], ref["leaves"])
+
+
 def test_lookup_special_keys_and_duplicates():
     rng = np.random.default_rng(400)
     pool = np.concatenate([rng.integers(0, 2**64, 500, dtype=np.uint64, endpoint=False),
