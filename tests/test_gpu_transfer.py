@@ -173,3 +173,61 @@ def test_malformed_records_are_skipped():
             assert np.array_equal(got, payloads[p][o:o + n]), f"repeated block {i}"
         # a HIT_BATCH block repeating a skipped MISS gets that block's unwritten packed
         # bytes or nothing; either way it stays inside its own payload
+
+
+@pytest.mark.parametrize("block", [4096, 1 << 20])
+def test_connect_protocol_with_separate_tables(block):
+    """The paper's flow (Sec. 4.1.2) with a client and a server table:
+    1. at connect the server sends its identifier set (export of its table, whose values
+       are the device addresses of the blocks it holds);
+    2. the client builds its own table from those identifiers, fingerprints its
+       payloads, looks them up, plans and packs;
+    3. the server resolves each HIT_CACHE digest it receives through its own table
+       (digest -> address of its copy) and rebuilds every payload."""
+    rng = np.random.default_rng(5150 + block.bit_length())
+    pool = [rng.bytes(block) for _ in range(8)]
+    payloads = []
+    for _ in range(20):
+        parts = [pool[int(i)] for i in rng.integers(0, 8, int(rng.integers(0, 4)))]
+        payloads.append(np.frombuffer(b"".join(parts) + rng.bytes(int(rng.integers(0, block))), np.uint8))
+    # server: holds pool[:5]; table value = device address of the held copy
+    held = to_device(np.frombuffer(b"".join(pool[:5]), np.uint8).copy())
+    skeys = np.concatenate([oracle.payload_digests(np.frombuffer(b, np.uint8), block)[0] for b in pool[:5]])
+    saddr = np.array([held.data_ptr() + i * block for i in range(5)], np.uint64)
+    server = g.Cache(1 << 10)
+    server.insert(keys_to_device(skeys), keys_to_device(saddr))
+    say("connect protocol: export", block)
+    keys, _, _, count = server.export()
+    torch.cuda.synchronize()
+    shipped = keys[:int(count.item())].clone()  # the identifier set sent at connect
+    # client: its own table holds only the identifiers
+    client = g.Cache(1 << 10)
+    client.insert(shipped, torch.zeros_like(shipped))
+    arena, offs, lens = W.pack(payloads)
+    src = g.Batch.from_arena(to_device(arena), offs, lens, block)
+    d = g.fp_chunks(src)
+    status, ref = client.lookup(d)
+    records, totals = g.send_plan(src, d, status, ref)
+    torch.cuda.synchronize()
+    tot = u64(totals)
+    assert tot[1] > 0 and tot[0] > 0
+    packed = torch.zeros(max(int(tot[3]), 1), dtype=torch.uint8, device="cuda")
+    g.pack_misses(src, records, packed)
+    # server: digest -> held address for the HIT_CACHE records
+    rec = g.records_to_numpy(records)
+    idents = keys_to_device(rec["ident"].astype(np.uint64))
+    sstatus, saddr_of = server.lookup(idents)
+    torch.cuda.synchronize()
+    hc = rec["kind"] == g.HIT_CACHE
+    assert np.all(sstatus.cpu().numpy()[hc] == g.HIT_CACHE)  # the server holds every block the client skipped
+    dst_arena, doffs, dlens = W.pack([np.zeros(p.size, np.uint8) for p in payloads], skew=3)
+    d_dst = to_device(dst_arena)
+    dst = g.Batch.from_arena(d_dst, doffs, dlens, block)
+    say("connect protocol: restore", block)
+    g.restore_blocks(dst, records, packed, held=saddr_of)
+    torch.cuda.synchronize()
+    out = d_dst.cpu().numpy()
+    for p, o in zip(payloads, doffs.tolist()):
+        assert np.array_equal(out[o:o + p.size], p)
+    # bytes that crossed the network: the packed MISS blocks, not the held ones
+    assert int(tot[3]) < int(lens.sum())
