@@ -349,6 +349,49 @@ def test_insert_lowest_index_wins_and_existing_kept():
         assert np.array_equal(u64(ref), eref)
 
 
+@pytest.mark.parametrize("seed", range(16))
+def test_randomized_table_rounds(seed):
+    """Seeded random table rounds: capacity 16..2^16 slots filled towards max_load 0.9 in
+    several inserts (duplicates inside a call, keys already present, keys 0 and 2^64-1,
+    keys clustered on a few home slots so probe runs are long and wrap past the table's
+    end), each followed by a lookup of present, absent and repeated keys with batch sizes
+    on both sides of the single-workgroup limit (4096); new-key counts, statuses and refs
+    equal the oracle's after every round."""
+    rng = np.random.default_rng(7700 + seed)
+    cap = 1 << int(rng.integers(4, 17))
+    table, ot = g.Cache(cap, max_load=0.9), oracle.Table()
+    limit = int(0.9 * cap)
+    bits = cap.bit_length() - 1
+    for rnd in range(6):
+        room = limit - table.key_bound()  # the host bound counts every key of a call
+        if room <= 0:
+            break
+        n = int(rng.integers(1, min(room, 3000) + 1))
+        pool = np.concatenate([rng.integers(0, 2**64 - 1, n, dtype=np.uint64, endpoint=True),
+                               colliding_keys(rng, max(1, n // 4), bits)])
+        keys = rng.choice(pool, n)
+        keys[rng.random(n) < 0.02] = 0
+        keys[rng.random(n) < 0.02] = 2**64 - 1
+        if len(ot):
+            old_keys, _, _ = ot.export()
+            pick = rng.random(n) < 0.2
+            keys[pick] = rng.choice(old_keys, int(pick.sum()))
+        vals = rng.integers(0, 2**64 - 1, n, dtype=np.uint64, endpoint=True)
+        say("table round seed", seed, "cap", cap, "round", rnd, "n", n)
+        n_new = table.insert(keys_to_device(keys), keys_to_device(vals))
+        assert int(n_new.item()) == ot.insert(keys, vals)
+        stored, _, _ = ot.export()
+        m = int(rng.choice([17, 4095, 4096, 4097, 9000]))
+        probe = np.concatenate([rng.choice(stored, m // 2), rng.integers(0, 2**64 - 1, m - m // 2,
+                                                                         dtype=np.uint64, endpoint=True)])
+        probe = probe[rng.permutation(probe.size)]
+        st, ref = table.lookup(keys_to_device(probe))
+        torch.cuda.synchronize()
+        est, eref = oracle.lookup(probe, ot)
+        assert np.array_equal(st.cpu().numpy(), est), f"round {rnd}: status"
+        assert np.array_equal(u64(ref), eref), f"round {rnd}: ref"
+
+
 GOLDEN = 0x9E3779B97F4A7C15  # the multiplier of the library's slot hash (Fibonacci hashing)
 
 
