@@ -167,6 +167,8 @@ class Batch:
     """A batch of payloads in device memory: addresses, lengths and block geometry."""
 
     def __init__(self, seg_addr, seg_len, block_bytes: int, device="cuda", keepalive=None):
+        if torch.device(device).type != "cuda":
+            raise ValueError("a Batch's descriptors live in GPU memory: device must be a CUDA device")
         addr = np.ascontiguousarray(seg_addr, dtype=np.uint64).reshape(-1)
         lens = np.ascontiguousarray(seg_len, dtype=np.uint64).reshape(-1)
         if addr.size != lens.size:
@@ -185,21 +187,31 @@ class Batch:
 
     @classmethod
     def from_arena(cls, arena: torch.Tensor, offsets, lengths, block_bytes: int) -> "Batch":
-        """Payloads at byte offsets of one device u8 tensor."""
-        base = arena.data_ptr()
-        offs = np.asarray(offsets, dtype=np.uint64)
-        return cls(offs + np.uint64(base), lengths, block_bytes, arena.device, keepalive=arena)
+        """Payloads at byte offsets of one contiguous GPU tensor; every payload must lie
+        inside it (the kernels read exactly those bytes)."""
+        if not isinstance(arena, torch.Tensor) or arena.device.type != "cuda" or not arena.is_contiguous():
+            raise ValueError("Batch.from_arena needs a contiguous tensor on the GPU")
+        offs = np.ascontiguousarray(offsets, dtype=np.uint64).reshape(-1)
+        lens = np.ascontiguousarray(lengths, dtype=np.uint64).reshape(-1)
+        if offs.size != lens.size:
+            raise ValueError("offsets and lengths differ in length")
+        size = arena.numel() * arena.element_size()
+        if offs.size and (int(offs.max()) > size or np.any(lens > np.uint64(size) - offs)):
+            raise ValueError("a payload reaches past the end of the arena")
+        return cls(offs + np.uint64(arena.data_ptr()), lens, block_bytes, arena.device, keepalive=arena)
 
     @classmethod
     def from_tensors(cls, tensors, block_bytes: int) -> "Batch":
         """One payload per contiguous device tensor: its bytes, from data_ptr() for
         numel() * element_size() bytes (a non-contiguous view is refused)."""
+        dev = tensors[0].device if tensors else torch.device("cuda")
         for t in tensors:
+            if t.device.type != "cuda" or t.device != dev:
+                raise ValueError("Batch.from_tensors needs tensors on one GPU")
             if not t.is_contiguous():
                 raise ValueError("Batch.from_tensors needs contiguous tensors (call .contiguous() first)")
         addr = [t.data_ptr() for t in tensors]
         lens = [t.numel() * t.element_size() for t in tensors]
-        dev = tensors[0].device if tensors else "cuda"
         return cls(addr, lens, block_bytes, dev, keepalive=list(tensors))
 
     @property

@@ -172,3 +172,15 @@ def test_counts_beyond_any_workspace_are_refused():
         assert g.lib.gleam_miss_compact(256, n, None, 256, 256, None, 256, 1 << 20, None) == g.E_UNSUPPORTED
         assert b"2^40" in g.lib.gleam_last_error()
         assert g.lib.gleam_workspace_bytes(n) == 0
+
+
+def test_binding_refuses_batches_the_kernels_would_misread():
+    """A Batch's descriptors and payloads must be GPU memory, and an arena's payloads must
+    lie inside it; the binding refuses the rest before any GPU work (runs without a GPU)."""
+    import torch
+    with pytest.raises(ValueError):
+        g.Batch.from_tensors([torch.zeros(16)], 4096)        # host tensor
+    with pytest.raises(ValueError):
+        g.Batch.from_arena(torch.zeros(64, dtype=torch.uint8), [0], [16], 4096)
+    with pytest.raises(ValueError):
+        g.Batch([0], [16], 4096, device="cpu")

@@ -627,3 +627,11 @@ def test_binding_refuses_tensors_the_kernels_would_misread():
         table.insert(keys.cpu(), keys)
     with pytest.raises(ValueError):  # status must be u8
         g.miss_compact(torch.zeros(16, dtype=torch.int64, device="cuda"))
+    arena = torch.zeros(4096, dtype=torch.uint8, device="cuda")
+    with pytest.raises(ValueError):  # a payload past the arena's end
+        g.Batch.from_arena(arena, [4000], [200], 4096)
+    with pytest.raises(ValueError):  # an offset past the end
+        g.Batch.from_arena(arena, [5000], [0], 4096)
+    with pytest.raises(ValueError):  # not contiguous
+        g.Batch.from_arena(torch.zeros(64, 2, dtype=torch.uint8, device="cuda")[:, 0], [0], [8], 4096)
+    assert g.Batch.from_arena(arena, [4000], [96], 4096).n_blocks == 1  # ends exactly at the end
