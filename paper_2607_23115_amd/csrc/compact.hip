@@ -5,9 +5,12 @@
 // Order-preserving stream compaction. Up to kSmallItems statuses (and payloads), one
 // 1024-thread workgroup does it all in one launch: rounds of 16 statuses per thread,
 // a workgroup scan per round, and a workgroup sum for the short-block bytes. Larger
-// inputs take three passes over tiles of 2048 statuses: count per tile, one-workgroup
-// exclusive scan of the tile counts, then each tile writes its MISS indices at its
-// offset using a workgroup scan of per-thread counts.
+// inputs are cut into tiles of 2048 statuses. Up to kPrefixTiles tiles take two passes:
+// a tally (count per tile, and the short-block bytes summed per workgroup over a grid
+// wide enough for one payload per thread), then each tile sums the counts before it and
+// writes its MISS indices at that offset using a workgroup scan of per-thread counts.
+// More tiles take three passes: count per tile, one-workgroup exclusive scan of the
+// tile counts, then the same per-tile writes.
 // Byte total = count * block_bytes minus, for every payload whose short last block is
 // a MISS, the part of that block that does not exist.
 // All sums are integer, so the results do not depend on thread timing.
@@ -137,6 +140,84 @@ __global__ __launch_bounds__(kThreads) void compact_scatter_kernel(const uint8_t
     atomicAdd(reinterpret_cast<unsigned long long*>(sb.miss_bytes), (unsigned long long)(0 - deficit));
 }
 
+// ---- Two launches for up to kPrefixTiles tiles -------------------------------------
+// Pass 1 (tally): workgroups below `tiles` count their tile's MISS statuses; every
+// workgroup also sums, over its grid-stride share of payloads, the bytes that a short
+// last block which is a MISS lacks, into deficits[blockIdx.x] (the grid is made wide
+// enough that most threads take one payload). Pass 2 (place): each tile sums the counts
+// of the tiles before it for its offset and writes its MISS indices; the last tile
+// writes the count and the byte total.
+constexpr uint64_t kPrefixTiles = 1024;
+constexpr uint64_t kMaxDeficitGroups = 1024;
+
+__device__ __forceinline__ uint64_t block_sum64(uint64_t x, uint64_t* wave_parts) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += shfl_xor64(x, o);
+  if ((threadIdx.x & 63) == 0) wave_parts[threadIdx.x >> 6] = x;
+  __syncthreads();
+  uint64_t s = 0;
+#pragma unroll
+  for (int w = 0; w < kThreads / 64; ++w) s += wave_parts[w];
+  __syncthreads();
+  return s;
+}
+
+__global__ __launch_bounds__(kThreads) void compact_tally_kernel(const uint8_t* status, uint64_t n, uint64_t tiles,
+                                                                 uint64_t* tile_counts, uint64_t* deficits,
+                                                                 ShortBlocks sb) {
+  __shared__ uint32_t wave_sums[kThreads / 64];
+  __shared__ uint64_t wave_parts[kThreads / 64];
+  if (blockIdx.x < tiles) {
+    const uint64_t first = (uint64_t)blockIdx.x * kTileItems + (uint64_t)threadIdx.x * kPerThread;
+    uint32_t total;
+    block_exclusive_scan<kThreads / 64>(count_misses(status, n, first), wave_sums, &total);
+    if (threadIdx.x == 0) tile_counts[blockIdx.x] = total;
+  }
+  if (!sb.seg_len) return;
+  uint64_t deficit = 0;
+  const uint64_t stride = (uint64_t)gridDim.x * kThreads;
+  for (uint64_t s = (uint64_t)blockIdx.x * kThreads + threadIdx.x; s < sb.n_seg; s += stride) {
+    const uint64_t b0 = sb.blk_first[s], b1 = sb.blk_first[s + 1], len = sb.seg_len[s];
+    if (b1 <= b0 || b1 - 1 >= n || status[b1 - 1] != GLEAM_MISS) continue;
+    const uint64_t last_len = len - (b1 - b0 - 1) * sb.block_bytes;
+    if (last_len < sb.block_bytes) deficit += sb.block_bytes - last_len;
+  }
+  deficit = block_sum64(deficit, wave_parts);
+  if (threadIdx.x == 0) deficits[blockIdx.x] = deficit;
+}
+
+__global__ __launch_bounds__(kThreads) void compact_place_kernel(const uint8_t* status, uint64_t n, uint64_t tiles,
+                                                                 const uint64_t* tile_counts, const uint64_t* deficits,
+                                                                 uint64_t n_def, uint64_t* miss_idx,
+                                                                 uint64_t* miss_count, uint64_t* miss_bytes,
+                                                                 uint64_t block_bytes) {
+  __shared__ uint32_t wave_sums[kThreads / 64];
+  __shared__ uint64_t wave_parts[kThreads / 64];
+  uint64_t before = 0;
+  for (uint64_t t = threadIdx.x; t < blockIdx.x; t += kThreads) before += tile_counts[t];
+  before = block_sum64(before, wave_parts);
+  const uint64_t first = (uint64_t)blockIdx.x * kTileItems + (uint64_t)threadIdx.x * kPerThread;
+  const uint32_t c = count_misses(status, n, first);
+  uint32_t total;
+  const uint32_t excl = block_exclusive_scan<kThreads / 64>(c, wave_sums, &total);
+  uint64_t out = before + excl;
+#pragma unroll
+  for (int e = 0; e < kPerThread; ++e) {
+    const uint64_t g = first + e;
+    if (g < n && status[g] == GLEAM_MISS) miss_idx[out++] = g;
+  }
+  if (blockIdx.x + 1 != tiles) return;
+  uint64_t d = 0;
+  if (miss_bytes)
+    for (uint64_t w = threadIdx.x; w < n_def; w += kThreads) d += deficits[w];
+  d = block_sum64(d, wave_parts);
+  if (threadIdx.x == 0) {
+    const uint64_t count = before + total;
+    *miss_count = count;
+    if (miss_bytes) *miss_bytes = count * block_bytes - d;
+  }
+}
+
 // Inputs of up to kSmallItems statuses and payloads: count, scan, scatter and byte total
 // in one workgroup (launch count is what such sizes pay for, not bytes). `sb` is used
 // only when n > 0; *miss_bytes (nullable) gets the byte total.
@@ -236,6 +317,28 @@ extern "C" gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, 
   uint64_t* counts = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(d_ws) + L.tiles_off);
   uint64_t* offsets = counts + L.tiles;
   const uint64_t block_bytes = d_miss_bytes ? b->block_bytes : 0;
+  if (L.tiles <= kPrefixTiles) {
+    // deficit partials go to the scratch table's words, which compaction does not use
+    uint64_t n_def = 0;
+    if (d_miss_bytes) {
+      n_def = (b->n_seg + kThreads - 1) / kThreads;
+      if (n_def > kMaxDeficitGroups) n_def = kMaxDeficitGroups;
+      if (n_def > L.scratch_cap) n_def = L.scratch_cap;
+    }
+    uint64_t* deficits = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(d_ws) + L.scratch_off);
+    ShortBlocks sb{nullptr, nullptr, 0, 0, nullptr};
+    if (d_miss_bytes) sb = ShortBlocks{b->seg_len, b->blk_first, b->n_seg, block_bytes, d_miss_bytes};
+    const uint64_t grid = L.tiles > n_def ? L.tiles : n_def;
+    hipLaunchKernelGGL(compact_tally_kernel, dim3((uint32_t)grid), dim3(kThreads), 0, s, d_status, n, L.tiles,
+                       counts, deficits, sb);
+    if ((st = launch_status("compact_tally_kernel")) != GLEAM_OK) return st;
+    // every tally workgroup writes a partial (grid <= max(kPrefixTiles, kMaxDeficitGroups),
+    // and tiles <= n <= scratch_cap / 2, so the partials fit in the scratch words)
+    hipLaunchKernelGGL(compact_place_kernel, dim3((uint32_t)L.tiles), dim3(kThreads), 0, s, d_status, n, L.tiles,
+                       counts, deficits, d_miss_bytes ? grid : 0, d_miss_idx, d_miss_count, d_miss_bytes,
+                       block_bytes);
+    return launch_status("compact_place_kernel");
+  }
   hipLaunchKernelGGL(compact_count_kernel, dim3((uint32_t)L.tiles), dim3(kThreads), 0, s, d_status, n, counts);
   if ((st = launch_status("compact_count_kernel")) != GLEAM_OK) return st;
   hipLaunchKernelGGL(compact_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, counts, L.tiles, offsets, d_miss_count,

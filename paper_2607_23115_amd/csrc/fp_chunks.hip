@@ -109,23 +109,33 @@ __device__ __forceinline__ Leaf locate_wave(const FpArgs& a, uint64_t g_first, u
 
 // XXH64 after the stripe loop: fold (or the short-input start), length, tail, avalanche.
 // The tail (the < 32 bytes after the last full stripe, at any address) lies in at most
-// five aligned 8-byte words, each holding tail bytes. They are loaded together (one
-// round trip, no byte loads), the tail's own 8-byte words are shifted out of adjacent
-// pairs, and the XXH64 tail steps run in registers: whole words, then a 4-byte step,
-// then single bytes.
-__device__ __forceinline__ uint64_t finish_leaf(uint64_t v1, uint64_t v2, uint64_t v3, uint64_t v4, const uint8_t* p,
-                                                uint32_t len) {
+// five aligned 8-byte words, each holding tail bytes. load_tail reads them together (one
+// round trip, no byte loads; the streamed paths issue it before their stage loop, so it
+// overlaps the first stage's loads); finish_leaf_words shifts the tail's own 8-byte
+// words out of adjacent pairs and runs the XXH64 tail steps in registers: whole words,
+// then a 4-byte step, then single bytes.
+
+// The aligned 8-byte words holding the tail of a leaf of `len` bytes at p; W[i] = 0 past
+// them (len 0: no read).
+__device__ __forceinline__ void load_tail(const uint8_t* p, uint32_t len, uint64_t W[5]) {
+  const uint32_t stripes = len >> 5;
+  const uint32_t tail = len - (stripes << 5);
+  const uint64_t at = reinterpret_cast<uint64_t>(p) + (stripes << 5);
+  const uint32_t lead = (uint32_t)(at & 7);
+  const uint32_t words = tail ? (lead + tail + 7) >> 3 : 0;
+  const uint64_t* w = reinterpret_cast<const uint64_t*>(at - lead);
+#pragma unroll
+  for (int i = 0; i < 5; ++i) W[i] = (uint32_t)i < words ? w[i] : 0;
+}
+
+__device__ __forceinline__ uint64_t finish_leaf_words(uint64_t v1, uint64_t v2, uint64_t v3, uint64_t v4,
+                                                      const uint8_t* p, uint32_t len, const uint64_t W[5]) {
   const uint32_t stripes = len >> 5;
   uint64_t h = stripes ? xxh_converge(v1, v2, v3, v4) : kP5;
   h += len;
   const uint32_t tail = len - (stripes << 5);  // 0..31
   const uint64_t at = reinterpret_cast<uint64_t>(p) + (stripes << 5);
   const uint32_t lead = (uint32_t)(at & 7);    // tail bytes start this far into a word
-  const uint32_t words = tail ? (lead + tail + 7) >> 3 : 0;
-  const uint64_t* w = reinterpret_cast<const uint64_t*>(at - lead);
-  uint64_t W[5];
-#pragma unroll
-  for (int i = 0; i < 5; ++i) W[i] = (uint32_t)i < words ? w[i] : 0;
   const uint32_t sh = lead * 8;
   uint64_t t[4];
 #pragma unroll
@@ -144,6 +154,13 @@ __device__ __forceinline__ uint64_t finish_leaf(uint64_t v1, uint64_t v2, uint64
     rest >>= 8;
   }
   return xxh_avalanche(h);
+}
+
+__device__ __forceinline__ uint64_t finish_leaf(uint64_t v1, uint64_t v2, uint64_t v3, uint64_t v4, const uint8_t* p,
+                                                uint32_t len) {
+  uint64_t W[5];
+  load_tail(p, len, W);
+  return finish_leaf_words(v1, v2, v3, v4, p, len, W);
 }
 
 // One leaf of 0..4096 bytes at any alignment by the LPL lanes (2 or 4) that own it:
@@ -262,6 +279,8 @@ __device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) longest = max(longest, (uint32_t)__shfl_xor((int)longest, o, 64));
   const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 15) / 16);
+  uint64_t W[5];
+  load_tail(lf.addr, r.rp ? 0u : lf.len, W);
   wave_lds_sync();
 
   uint64_t va = r.rp ? 0 : kP1 + kP2, vb = r.rp ? 0 - kP1 : kP2;
@@ -302,7 +321,7 @@ __device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
   }
   const uint64_t pa = shfl_xor64(va, 1), pb = shfl_xor64(vb, 1);
   if (r.rp || lf.len == 0) return 0;
-  return finish_leaf(va, vb, pa, pb, lf.addr, lf.len);
+  return finish_leaf_words(va, vb, pa, pb, lf.addr, lf.len, W);
 }
 
 // Bytes [d, d + 16) of the 32 bytes c0 || c1 (d in 0..15), as a 16-byte value.
@@ -339,6 +358,8 @@ __device__ uint64_t hash_wave_shifted(const Leaf& lf, uint8_t* tile, uint64_t* t
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) longest = max(longest, (uint32_t)__shfl_xor((int)longest, o, 64));
   const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 15) / 16);
+  uint64_t W[5];
+  load_tail(lf.addr, r.rp ? 0u : lf.len, W);
   wave_lds_sync();
 
   uint64_t va = r.rp ? 0 : kP1 + kP2, vb = r.rp ? 0 - kP1 : kP2;
@@ -390,7 +411,7 @@ __device__ uint64_t hash_wave_shifted(const Leaf& lf, uint8_t* tile, uint64_t* t
   }
   const uint64_t pa = shfl_xor64(va, 1), pb = shfl_xor64(vb, 1);
   if (r.rp || lf.len == 0) return 0;
-  return finish_leaf(va, vb, pa, pb, lf.addr, lf.len);
+  return finish_leaf_words(va, vb, pa, pb, lf.addr, lf.len, W);
 }
 
 // Digest of this lane pair's leaf, in the even lane.
@@ -591,6 +612,8 @@ __device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) longest = max(longest, (uint32_t)__shfl_xor((int)longest, o, 64));
   const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 31) / 32);
+  uint64_t W[5];
+  load_tail(lf.addr, ra ? 0u : lf.len, W);
   wave_lds_sync();
   uint64_t v = quad_acc_init(ra);
   uint4 R[kQuadLoads];
@@ -619,7 +642,7 @@ __device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
   const int q = lane & ~3;
   const uint64_t v1 = shfl64(v, q), v2 = shfl64(v, q + 1), v3 = shfl64(v, q + 2), v4 = shfl64(v, q + 3);
   if (ra || lf.len == 0) return 0;
-  return finish_leaf(v1, v2, v3, v4, lf.addr, lf.len);
+  return finish_leaf_words(v1, v2, v3, v4, lf.addr, lf.len, W);
 }
 
 // Digest of this lane quad's leaf, in lane 4l.

@@ -500,9 +500,10 @@ def check_compaction(status, d_status, batch, lens, block=4096):
     assert np.array_equal(u64(miss_idx)[:ecnt], eidx)
 
 
-# one workgroup up to 65,536 statuses (16,384 per round), tiles of 2,048 above
+# one workgroup up to 65,536 statuses (16,384 per round), tiles of 2,048 above: two
+# launches up to 1,024 tiles (2,097,152 statuses), three beyond
 @pytest.mark.parametrize("n", [1, 63, 2047, 2048, 2049, 3 * 2048 + 17, 16_383, 16_384, 16_385, 65_536, 65_537,
-                               100_003, 2_500_001])
+                               100_003, 2_097_152, 2_097_153, 2_500_001])
 def test_compaction_tiles(n):
     rng = np.random.default_rng(600 + n)
     status = rng.choice(np.array([0, 1, 2], np.uint8), n, p=[0.3, 0.5, 0.2])
@@ -533,14 +534,18 @@ def test_compaction_status_at_odd_address(offset):
     check_compaction(status, d_status, batch, lens)
 
 
-def test_compaction_more_payloads_than_small_path():
-    # few blocks but over 65,536 payloads (zero-length ones between): the tiled path
-    rng = np.random.default_rng(660)
-    n = 30_000
+# few blocks but over 65,536 payloads (zero-length ones between): the tiled path. 30,000
+# blocks: one payload per byte-total thread; 100,000 (300,000 payloads): more payloads
+# than the 1,024 byte-total workgroups cover in one step; 10 blocks: those workgroups
+# capped by the workspace's 64 scratch words.
+@pytest.mark.parametrize("n", [30_000, 100_000, 10])
+def test_compaction_more_payloads_than_small_path(n):
+    rng = np.random.default_rng(660 + n)
     status = rng.choice(np.array([0, 1, 2], np.uint8), n, p=[0.5, 0.3, 0.2])
     lens = []
-    for _ in range(n):  # one short block each, then two empty payloads
-        lens += [int(rng.integers(1, 4097)), 0, 0]
+    empties = 2 if n > 1_000 else 7_000
+    for _ in range(n):  # one short block each, then empty payloads
+        lens += [int(rng.integers(1, 4097))] + [0] * empties
     batch = g.Batch(np.full(len(lens), 0, np.uint64), lens, 4096)
     assert batch.n_blocks == n and batch.n_seg > 65_536
     say("compaction payloads", batch.n_seg)
