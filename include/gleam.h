@@ -39,6 +39,9 @@
  *   - `stream` is a hipStream_t (NULL = the default stream). Work is enqueued
  *     asynchronously on it; outputs are valid once the stream has synchronised.
  *     The library never synchronises.
+ *   - A workspace (d_ws) is scratch for the one call it is passed to: its contents on
+ *     entry do not matter and are undefined on return. Calls that may run at the same
+ *     time (on different streams) need separate workspaces.
  *   - Arguments are validated on the host before anything is enqueued; on any
  *     error a negative status is returned and nothing has been enqueued. A HIP
  *     launch failure returns GLEAM_E_HIP; gleam_last_error() then holds the HIP
@@ -51,8 +54,9 @@
  *     enqueues memsets; keep them out of captured graphs.
  *   - Device descriptor contents (seg_addr, seg_len, blk_first) are not read on
  *     the host. The caller guarantees they describe the batch; whatever they hold,
- *     kernels read payload memory only in the aligned 8-byte words that contain
- *     bytes of [seg_addr[s], seg_addr[s] + seg_len[s]) (so never another page).
+ *     kernels read payload memory only in aligned 16-byte units that contain at
+ *     least one byte of [seg_addr[s], seg_addr[s] + seg_len[s]) (so never another
+ *     page).
  */
 #ifndef GLEAM_H
 #define GLEAM_H
