@@ -10,10 +10,19 @@ been built (python -m paper_2607_23115_amd.build).
     table = Cache(capacity=1 << 15)
     status, ref = table.lookup(digests)
     miss_idx, miss_count, miss_bytes = miss_compact(status, batch)
+
+Every call takes `stream` (a torch stream, a raw hipStream_t handle, or None for torch's
+current stream). Tensors a call creates itself (outputs not passed in, workspaces,
+zeroed counters) are allocated and filled on that stream, so they are ordered before the
+call's kernels and are not reused by torch's allocator while that stream still needs
+them. Tensors passed in are the caller's: order them yourself when they come from other
+streams. A Cache's or Remap's storage belongs to the stream current at construction;
+synchronise the other streams that used it before dropping the object.
 """
 
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
@@ -141,6 +150,34 @@ def _stream(stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(int(stream))
 
 
+def _torch_stream(stream, device) -> torch.cuda.Stream:
+    """The torch stream object of a call's stream (None: torch's current stream; a raw
+    hipStream_t handle is wrapped)."""
+    cur = torch.cuda.current_stream(device)
+    if stream is None or (isinstance(stream, torch.cuda.Stream) and stream == cur):
+        return cur
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    h = int(stream)
+    if h == cur.cuda_stream:
+        return cur
+    if h == 0:
+        return torch.cuda.default_stream(device)
+    return torch.cuda.ExternalStream(h, device=device)
+
+
+@contextlib.contextmanager
+def _on_stream(stream, device):
+    """Run a call's own allocations and fills on the stream its kernels run on, and yield
+    that stream's handle. Tensors a call creates (outputs, workspaces, zeroed counters)
+    then belong to that stream: a fill is ordered before the kernels that use the memory,
+    and the caching allocator does not hand the memory out again before the stream is
+    done with it, whichever stream is torch's current one."""
+    s = _torch_stream(stream, device)
+    with torch.cuda.stream(s):
+        yield _stream(s)
+
+
 def _u64_device(a: np.ndarray, device) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint64).view(np.int64)).to(device)
 
@@ -226,13 +263,14 @@ def fp_chunks(batch: Batch, out: torch.Tensor | None = None, leaf_out: torch.Ten
               with_leaves: bool = False, stream=None):
     """Block digests (u64 as int64 tensor); optionally padded leaf digests."""
     dev = batch.d_first.device
-    if out is None:
-        out = torch.empty(max(batch.n_blocks, 1), dtype=torch.int64, device=dev)
-    if with_leaves and leaf_out is None:
-        leaf_out = torch.empty(max(batch.n_blocks * batch.leaves_per_block, 1), dtype=torch.int64, device=dev)
-    _dev(out, "out", _U64, batch.n_blocks)
-    _dev(leaf_out, "leaf_out", _U64, batch.n_blocks * batch.leaves_per_block, optional=True)
-    _check(lib.gleam_fp_chunks(ctypes.byref(batch.c_struct()), _ptr(out), _ptr(leaf_out), _stream(stream)))
+    with _on_stream(stream, dev) as hs:
+        if out is None:
+            out = torch.empty(max(batch.n_blocks, 1), dtype=torch.int64, device=dev)
+        if with_leaves and leaf_out is None:
+            leaf_out = torch.empty(max(batch.n_blocks * batch.leaves_per_block, 1), dtype=torch.int64, device=dev)
+        _dev(out, "out", _U64, batch.n_blocks)
+        _dev(leaf_out, "leaf_out", _U64, batch.n_blocks * batch.leaves_per_block, optional=True)
+        _check(lib.gleam_fp_chunks(ctypes.byref(batch.c_struct()), _ptr(out), _ptr(leaf_out), hs))
     if with_leaves:
         return out[:batch.n_blocks], leaf_out[:batch.n_blocks * batch.leaves_per_block]
     return out[:batch.n_blocks]
@@ -266,33 +304,35 @@ class Cache:
         n = keys.numel()
         if vals.numel() != n:
             raise ValueError("keys and vals differ in length")
-        if ws is None:
-            ws = workspace(n, keys.device)
-        if n_new is None:
-            n_new = torch.empty(1, dtype=torch.int64, device=keys.device)
         _dev(keys, "keys", _U64)
-        _dev(vals, "vals", _U64)
-        _dev(n_new, "n_new", _U64, 1)
-        _dev(ws, "ws", _U8)
-        _check(lib.gleam_cache_insert(self.handle, _ptr(keys), _ptr(vals), n, _ptr(n_new), _ptr(ws), ws.numel(),
-                                      _stream(stream)))
+        with _on_stream(stream, keys.device) as hs:
+            if ws is None:
+                ws = workspace(n, keys.device)
+            if n_new is None:
+                n_new = torch.empty(1, dtype=torch.int64, device=keys.device)
+            _dev(vals, "vals", _U64)
+            _dev(n_new, "n_new", _U64, 1)
+            _dev(ws, "ws", _U8)
+            _check(lib.gleam_cache_insert(self.handle, _ptr(keys), _ptr(vals), n, _ptr(n_new), _ptr(ws),
+                                          ws.numel(), hs))
         return n_new
 
     def lookup(self, keys: torch.Tensor, status: torch.Tensor | None = None, ref: torch.Tensor | None = None,
                ws: torch.Tensor | None = None, want_ref: bool = True, stream=None):
         n = keys.numel()
-        if status is None:
-            status = torch.empty(max(n, 1), dtype=torch.uint8, device=keys.device)
-        if ref is None and want_ref:
-            ref = torch.empty(max(n, 1), dtype=torch.int64, device=keys.device)
-        if ws is None:
-            ws = workspace(n, keys.device)
         _dev(keys, "keys", _U64)
-        _dev(status, "status", _U8, n)
-        _dev(ref, "ref", _U64, n, optional=True)
-        _dev(ws, "ws", _U8)
-        _check(lib.gleam_cache_lookup(self.handle, _ptr(keys), n, _ptr(status), _ptr(ref), _ptr(ws), ws.numel(),
-                                      _stream(stream)))
+        with _on_stream(stream, keys.device) as hs:
+            if status is None:
+                status = torch.empty(max(n, 1), dtype=torch.uint8, device=keys.device)
+            if ref is None and want_ref:
+                ref = torch.empty(max(n, 1), dtype=torch.int64, device=keys.device)
+            if ws is None:
+                ws = workspace(n, keys.device)
+            _dev(status, "status", _U8, n)
+            _dev(ref, "ref", _U64, n, optional=True)
+            _dev(ws, "ws", _U8)
+            _check(lib.gleam_cache_lookup(self.handle, _ptr(keys), n, _ptr(status), _ptr(ref), _ptr(ws),
+                                          ws.numel(), hs))
         return status[:n], (ref[:n] if ref is not None else None)
 
     # -- lifecycle ------------------------------------------------------------------ #
@@ -304,43 +344,48 @@ class Cache:
 
     def touch(self, keys: torch.Tensor, epochs: torch.Tensor | None = None, epoch: int = 0, stream=None):
         """Stamp present keys with max(stamp, epoch); returns the device count of present keys."""
-        n_touched = torch.empty(1, dtype=torch.int64, device=keys.device)
         _dev(keys, "keys", _U64)
         _dev(epochs, "epochs", _U64, keys.numel(), optional=True)
-        _check(lib.gleam_cache_touch(self.handle, _ptr(keys), keys.numel(), _ptr(epochs), epoch, _ptr(n_touched),
-                                     _stream(stream)))
+        with _on_stream(stream, keys.device) as hs:
+            n_touched = torch.empty(1, dtype=torch.int64, device=keys.device)
+            _check(lib.gleam_cache_touch(self.handle, _ptr(keys), keys.numel(), _ptr(epochs), epoch,
+                                         _ptr(n_touched), hs))
         return n_touched
 
     def evict(self, keep: int, ws: torch.Tensor | None = None, stream=None):
         """Keep the `keep` most recently used entries: (evicted keys [capacity+1], counts[2])."""
-        ws = self.maint_workspace() if ws is None else ws
-        evicted = torch.empty(self.capacity + 1, dtype=torch.int64, device=ws.device)
-        counts = torch.empty(2, dtype=torch.int64, device=ws.device)
-        _dev(ws, "ws", _U8)
-        _check(lib.gleam_cache_evict(self.handle, keep, _ptr(evicted), _ptr(counts), _ptr(ws), ws.numel(),
-                                     _stream(stream)))
+        dev = self.storage.device
+        with _on_stream(stream, dev) as hs:
+            ws = self.maint_workspace() if ws is None else ws
+            evicted = torch.empty(self.capacity + 1, dtype=torch.int64, device=dev)
+            counts = torch.empty(2, dtype=torch.int64, device=dev)
+            _dev(ws, "ws", _U8)
+            _check(lib.gleam_cache_evict(self.handle, keep, _ptr(evicted), _ptr(counts), _ptr(ws), ws.numel(), hs))
         return evicted, counts
 
     def erase(self, keys: torch.Tensor, ws: torch.Tensor | None = None, stream=None):
-        ws = self.maint_workspace() if ws is None else ws
-        counts = torch.empty(2, dtype=torch.int64, device=ws.device)
         _dev(keys, "keys", _U64)
-        _dev(ws, "ws", _U8)
-        _check(lib.gleam_cache_erase(self.handle, _ptr(keys), keys.numel(), _ptr(counts), _ptr(ws), ws.numel(),
-                                     _stream(stream)))
+        dev = self.storage.device
+        with _on_stream(stream, dev) as hs:
+            ws = self.maint_workspace() if ws is None else ws
+            counts = torch.empty(2, dtype=torch.int64, device=dev)
+            _dev(ws, "ws", _U8)
+            _check(lib.gleam_cache_erase(self.handle, _ptr(keys), keys.numel(), _ptr(counts), _ptr(ws), ws.numel(),
+                                         hs))
         return counts
 
     def export(self, ws: torch.Tensor | None = None, stream=None):
         """(keys, vals, stamps, count) with the first count entries valid, sorted by key."""
-        ws = self.maint_workspace() if ws is None else ws
-        dev = ws.device
-        keys = torch.empty(self.capacity + 1, dtype=torch.int64, device=dev)
-        vals = torch.empty_like(keys)
-        stamps = torch.empty_like(keys)
-        count = torch.empty(1, dtype=torch.int64, device=dev)
-        _dev(ws, "ws", _U8)
-        _check(lib.gleam_cache_export(self.handle, _ptr(keys), _ptr(vals), _ptr(stamps), _ptr(count), _ptr(ws),
-                                      ws.numel(), _stream(stream)))
+        dev = self.storage.device
+        with _on_stream(stream, dev) as hs:
+            ws = self.maint_workspace() if ws is None else ws
+            keys = torch.empty(self.capacity + 1, dtype=torch.int64, device=dev)
+            vals = torch.empty_like(keys)
+            stamps = torch.empty_like(keys)
+            count = torch.empty(1, dtype=torch.int64, device=dev)
+            _dev(ws, "ws", _U8)
+            _check(lib.gleam_cache_export(self.handle, _ptr(keys), _ptr(vals), _ptr(stamps), _ptr(count),
+                                          _ptr(ws), ws.numel(), hs))
         return keys, vals, stamps, count
 
     def set_key_bound(self, n: int) -> None:
@@ -399,44 +444,46 @@ class Remap:
         if n_add and (add_len is None or add_target is None or add_len.numel() != n_add
                       or add_target.numel() != n_add):
             raise ValueError("add_start, add_len and add_target differ in length")
-        if status is None and want_status:
-            status = torch.empty(max(n_add, 1), dtype=torch.uint8, device=dev)
-        if counts is None:
-            counts = torch.empty(4, dtype=torch.int64, device=dev)
-        if ws is None:
-            ws = self.update_workspace(n_add, n_del)
         for t, name in ((del_start, "del_start"), (del_len, "del_len")):
             _dev(t, name, _U64, n_del, optional=n_del == 0)
         for t, name in ((add_start, "add_start"), (add_len, "add_len"), (add_target, "add_target")):
             _dev(t, name, _U64, n_add, optional=n_add == 0)
-        _dev(status, "status", _U8, n_add, optional=True)
-        _dev(counts, "counts", _U64, 4)
-        _dev(ws, "ws", _U8)
         live = (lambda t, n: _ptr(t) if n else None)
-        _check(lib.gleam_remap_update(self.handle, live(del_start, n_del), live(del_len, n_del), n_del,
-                                      live(add_start, n_add), live(add_len, n_add), live(add_target, n_add),
-                                      n_add, _ptr(status), _ptr(counts), _ptr(ws), ws.numel(), _stream(stream)))
+        with _on_stream(stream, dev) as hs:
+            if status is None and want_status:
+                status = torch.empty(max(n_add, 1), dtype=torch.uint8, device=dev)
+            if counts is None:
+                counts = torch.empty(4, dtype=torch.int64, device=dev)
+            if ws is None:
+                ws = self.update_workspace(n_add, n_del)
+            _dev(status, "status", _U8, n_add, optional=True)
+            _dev(counts, "counts", _U64, 4)
+            _dev(ws, "ws", _U8)
+            _check(lib.gleam_remap_update(self.handle, live(del_start, n_del), live(del_len, n_del), n_del,
+                                          live(add_start, n_add), live(add_len, n_add), live(add_target, n_add),
+                                          n_add, _ptr(status), _ptr(counts), _ptr(ws), ws.numel(), hs))
         return (status[:n_add] if status is not None else None), counts
 
     def translate(self, addr: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
         """target + (p - start) for each address inside an interval, else UNMAPPED (-1)."""
         n = addr.numel()
-        if out is None:
-            out = torch.empty(max(n, 1), dtype=torch.int64, device=addr.device)
         _dev(addr, "addr", _U64)
-        _dev(out, "out", _U64, n)
-        _check(lib.gleam_remap_translate(self.handle, _ptr(addr), n, _ptr(out), _stream(stream)))
+        with _on_stream(stream, addr.device) as hs:
+            if out is None:
+                out = torch.empty(max(n, 1), dtype=torch.int64, device=addr.device)
+            _dev(out, "out", _U64, n)
+            _check(lib.gleam_remap_translate(self.handle, _ptr(addr), n, _ptr(out), hs))
         return out[:n]
 
     def export(self, stream=None):
         """(start, length, target, count): the first count intervals, in start order."""
         dev = self.storage.device
-        start = torch.empty(self.capacity, dtype=torch.int64, device=dev)
-        length = torch.empty_like(start)
-        target = torch.empty_like(start)
-        count = torch.empty(1, dtype=torch.int64, device=dev)
-        _check(lib.gleam_remap_export(self.handle, _ptr(start), _ptr(length), _ptr(target), _ptr(count),
-                                      _stream(stream)))
+        with _on_stream(stream, dev) as hs:
+            start = torch.empty(self.capacity, dtype=torch.int64, device=dev)
+            length = torch.empty_like(start)
+            target = torch.empty_like(start)
+            count = torch.empty(1, dtype=torch.int64, device=dev)
+            _check(lib.gleam_remap_export(self.handle, _ptr(start), _ptr(length), _ptr(target), _ptr(count), hs))
         return start, length, target, count
 
     def close(self) -> None:
@@ -458,21 +505,22 @@ def miss_compact(status: torch.Tensor, batch: Batch | None = None, miss_idx: tor
     The first counters[0] entries of miss_idx are valid; counters[1] is filled when
     `batch` is given."""
     n = status.numel()
-    dev = status.device
-    if miss_idx is None:
-        miss_idx = torch.empty(max(n, 1), dtype=torch.int64, device=dev)
-    if counters is None:
-        counters = torch.zeros(2, dtype=torch.int64, device=dev)
-    if ws is None:
-        ws = workspace(n, dev)
-    cb = ctypes.byref(batch.c_struct()) if batch is not None else None
     _dev(status, "status", _U8)
-    _dev(miss_idx, "miss_idx", _U64, n)
-    _dev(counters, "counters", _U64, 2 if batch is not None else 1)
-    _dev(ws, "ws", _U8)
-    bytes_ptr = ctypes.c_void_p(counters.data_ptr() + 8) if batch is not None else None
-    _check(lib.gleam_miss_compact(_ptr(status), n, cb, _ptr(miss_idx), _ptr(counters), bytes_ptr, _ptr(ws),
-                                  ws.numel(), _stream(stream)))
+    dev = status.device
+    cb = ctypes.byref(batch.c_struct()) if batch is not None else None
+    with _on_stream(stream, dev) as hs:
+        if miss_idx is None:
+            miss_idx = torch.empty(max(n, 1), dtype=torch.int64, device=dev)
+        if counters is None:
+            counters = torch.zeros(2, dtype=torch.int64, device=dev)
+        if ws is None:
+            ws = workspace(n, dev)
+        _dev(miss_idx, "miss_idx", _U64, n)
+        _dev(counters, "counters", _U64, 2 if batch is not None else 1)
+        _dev(ws, "ws", _U8)
+        bytes_ptr = ctypes.c_void_p(counters.data_ptr() + 8) if batch is not None else None
+        _check(lib.gleam_miss_compact(_ptr(status), n, cb, _ptr(miss_idx), _ptr(counters), bytes_ptr, _ptr(ws),
+                                      ws.numel(), hs))
     return miss_idx, counters
 
 
@@ -482,19 +530,20 @@ def identify_weights(batch: Batch, recorded: torch.Tensor, region_first, ws: tor
     region_weight u8[n_regions]) on the device. `recorded` holds the block digests taken
     when the payloads were written; `region_first` the allocation boundaries over payloads."""
     dev = batch.d_first.device
-    rf = region_first if isinstance(region_first, torch.Tensor) else _u64_device(np.asarray(region_first), dev)
-    n_regions = rf.numel() - 1
-    block_match = torch.empty(max(batch.n_blocks, 1), dtype=torch.uint8, device=dev)
-    first_diff = torch.empty(max(batch.n_seg, 1), dtype=torch.int64, device=dev)
-    region_weight = torch.empty(max(n_regions, 1), dtype=torch.uint8, device=dev)
-    if ws is None:
-        ws = workspace(batch.n_blocks + batch.n_seg, dev)
     _dev(recorded, "recorded", _U64, batch.n_blocks)
-    _dev(rf, "region_first", _U64, 1)
-    _dev(ws, "ws", _U8)
-    _check(lib.gleam_identify_weights(ctypes.byref(batch.c_struct()), _ptr(recorded), _ptr(rf), n_regions,
-                                      _ptr(block_match), _ptr(first_diff), _ptr(region_weight), _ptr(ws),
-                                      ws.numel(), _stream(stream)))
+    with _on_stream(stream, dev) as hs:
+        rf = region_first if isinstance(region_first, torch.Tensor) else _u64_device(np.asarray(region_first), dev)
+        n_regions = rf.numel() - 1
+        block_match = torch.empty(max(batch.n_blocks, 1), dtype=torch.uint8, device=dev)
+        first_diff = torch.empty(max(batch.n_seg, 1), dtype=torch.int64, device=dev)
+        region_weight = torch.empty(max(n_regions, 1), dtype=torch.uint8, device=dev)
+        if ws is None:
+            ws = workspace(batch.n_blocks + batch.n_seg, dev)
+        _dev(rf, "region_first", _U64, 1)
+        _dev(ws, "ws", _U8)
+        _check(lib.gleam_identify_weights(ctypes.byref(batch.c_struct()), _ptr(recorded), _ptr(rf), n_regions,
+                                          _ptr(block_match), _ptr(first_diff), _ptr(region_weight), _ptr(ws),
+                                          ws.numel(), hs))
     return block_match[:batch.n_blocks], first_diff[:batch.n_seg], region_weight[:n_regions]
 
 
@@ -502,11 +551,12 @@ def md5_prefix(batch: Batch, prefix_bytes: int = 128, min_len: int = 1024, strea
     """The paper's identifier per payload: (digest int64[S, 2], key int64[S], eligible u8[S])."""
     dev = batch.d_first.device
     S = max(batch.n_seg, 1)
-    digest = torch.empty(2 * S, dtype=torch.int64, device=dev)
-    key = torch.empty(S, dtype=torch.int64, device=dev)
-    eligible = torch.empty(S, dtype=torch.uint8, device=dev)
-    _check(lib.gleam_md5_prefix(ctypes.byref(batch.c_struct()), prefix_bytes, min_len, _ptr(digest), _ptr(key),
-                                _ptr(eligible), _stream(stream)))
+    with _on_stream(stream, dev) as hs:
+        digest = torch.empty(2 * S, dtype=torch.int64, device=dev)
+        key = torch.empty(S, dtype=torch.int64, device=dev)
+        eligible = torch.empty(S, dtype=torch.uint8, device=dev)
+        _check(lib.gleam_md5_prefix(ctypes.byref(batch.c_struct()), prefix_bytes, min_len, _ptr(digest), _ptr(key),
+                                    _ptr(eligible), hs))
     n = batch.n_seg
     return digest[:2 * n].view(n, 2), key[:n], eligible[:n]
 
@@ -520,16 +570,17 @@ def send_plan(batch: Batch, digests: torch.Tensor, status: torch.Tensor, ref: to
               ws: torch.Tensor | None = None, stream=None):
     """(records as a u8 tensor of n_blocks x 40 bytes, totals int64[4]) on the device."""
     dev = batch.d_first.device
-    records = torch.empty(max(batch.n_blocks, 1) * RECORD_BYTES, dtype=torch.uint8, device=dev)
-    totals = torch.empty(4, dtype=torch.int64, device=dev)
-    if ws is None:
-        ws = workspace(batch.n_blocks, dev)
     _dev(digests, "digests", _U64, batch.n_blocks)
     _dev(status, "status", _U8, batch.n_blocks)
     _dev(ref, "ref", _U64, batch.n_blocks)
-    _dev(ws, "ws", _U8)
-    _check(lib.gleam_send_plan(ctypes.byref(batch.c_struct()), _ptr(digests), _ptr(status), _ptr(ref),
-                               _ptr(records), _ptr(totals), _ptr(ws), ws.numel(), _stream(stream)))
+    with _on_stream(stream, dev) as hs:
+        records = torch.empty(max(batch.n_blocks, 1) * RECORD_BYTES, dtype=torch.uint8, device=dev)
+        totals = torch.empty(4, dtype=torch.int64, device=dev)
+        if ws is None:
+            ws = workspace(batch.n_blocks, dev)
+        _dev(ws, "ws", _U8)
+        _check(lib.gleam_send_plan(ctypes.byref(batch.c_struct()), _ptr(digests), _ptr(status), _ptr(ref),
+                                   _ptr(records), _ptr(totals), _ptr(ws), ws.numel(), hs))
     return records[:batch.n_blocks * RECORD_BYTES], totals
 
 
@@ -555,13 +606,14 @@ def read_stream(src: torch.Tensor, nbytes: int | None = None, sink: torch.Tensor
     """Calibration read of the first nbytes of a device tensor with the fingerprint
     kernel's load pattern; XORs the fold of its 8-byte words into sink (int64[1])."""
     nbytes = src.numel() * src.element_size() if nbytes is None else int(nbytes)
-    if sink is None:
-        sink = torch.zeros(1, dtype=torch.int64, device=src.device)
     _dev(src, "src", None)
     if nbytes > src.numel() * src.element_size():
         raise ValueError("nbytes exceeds the source tensor")
-    _dev(sink, "sink", _U64, 1)
-    _check(lib.gleam_read_stream(_ptr(src), nbytes, _ptr(sink), _stream(stream)))
+    with _on_stream(stream, src.device) as hs:
+        if sink is None:
+            sink = torch.zeros(1, dtype=torch.int64, device=src.device)
+        _dev(sink, "sink", _U64, 1)
+        _check(lib.gleam_read_stream(_ptr(src), nbytes, _ptr(sink), hs))
     return sink
 
 
