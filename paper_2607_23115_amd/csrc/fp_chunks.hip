@@ -15,19 +15,20 @@
 // with this one). For blocks of 1 MiB and up the workgroup's LDS is padded past half
 // of the CU's 160 KiB, so each CU holds exactly one, and a grid of 4 per CU walks the
 // blocks. Smaller blocks keep one workgroup per item at normal occupancy: their
-// gathered and per-lane paths need the extra waves to hide latency.
+// gathered waves need the extra waves to hide latency.
 //
 // Memory path (the kernel is HBM-bound; XXH64 itself runs far above HBM rate).
-// A wave whose 32 leaves are full, contiguous and 16-byte aligned streams them with
-// non-temporal 16-byte loads in which 32 consecutive lanes read one 512-byte run of
-// one leaf (2 leaves per load instruction, 16 loads = 32 leaves x 512 B per stage).
-// Each stage goes through a per-wave LDS tile, 512 B per leaf, whose 32-byte stripes
-// are XOR-swizzled by the leaf index, so both the stores and each lane's 16-byte
-// reads of its own half-stripes are free of bank conflicts; the next stage's loads
-// are in flight while the current one is hashed. Waves of aligned leaves that are
-// not one contiguous full run (payload ends, small payloads) use the same tile with
-// per-instruction leaf addresses from a small LDS table; waves with a leaf that does not
-// start 16-byte aligned hash each leaf with its own lanes from 8-byte loads.
+// A wave whose 32 leaves are full and contiguous streams them with non-temporal
+// 16-byte loads in which 32 consecutive lanes read one 512-byte run of one leaf (2
+// leaves per load instruction, 16 loads = 32 leaves x 512 B per stage). Each stage goes
+// through a per-wave LDS tile, 512 B per leaf, whose 32-byte stripes are XOR-swizzled by
+// the leaf index, so both the stores and each lane's 16-byte reads of its own
+// half-stripes are free of bank conflicts; the next stage's loads are in flight while
+// the current one is hashed. Waves that are not one contiguous full run (payload ends,
+// small payloads) use the same tile with per-instruction leaf addresses from a small
+// LDS table. Every load covers 16 bytes of its own leaf from the leaf's start, at any
+// alignment (see load_stream16_any), so a leaf's bytes reach the tile in order and no
+// path shifts them.
 //
 // Tree: levels inside a wave's 32 leaves use cross-lane shuffles; the roots of
 // 32-leaf groups meet in LDS. Pairing by aligned position level by level is the same
@@ -38,6 +39,19 @@
 
 namespace gleam {
 namespace {
+
+// Streaming 16-byte load at any byte address. Under HSA, gfx950 runs with unaligned
+// access enabled (the compiler itself turns a byte-aligned 16-byte copy into one
+// global_load_dwordx4), so a leaf that does not start 16-byte aligned streams through
+// the same tile as an aligned one, each load covering 16 of its own bytes. Measured on
+// MI355X: a 4-byte aligned start streams like an aligned one; other starts cost the
+// memory pipeline more but still beat reading aligned chunks and shifting them in
+// registers.
+typedef u32x4 u32x4_any __attribute__((aligned(1)));
+__device__ __forceinline__ uint4 load_stream16_any(const uint8_t* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_any*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 constexpr int kLeavesPerWave = 32;
 constexpr int kRunLanes = 32;                     // lanes reading one contiguous run
@@ -163,46 +177,6 @@ __device__ __forceinline__ uint64_t finish_leaf(uint64_t v1, uint64_t v2, uint64
   return finish_leaf_words(v1, v2, v3, v4, p, len, W);
 }
 
-// One leaf of 0..4096 bytes at any alignment by the LPL lanes (2 or 4) that own it:
-// lane r of the group runs accumulators 4r/LPL .. 4(r+1)/LPL - 1 over the stripe words
-// (8-byte loads of the aligned words that hold the leaf's bytes; for a start that is not
-// 8-byte aligned each word is shifted together from two neighbours, both of which hold
-// leaf bytes, so no read touches another page), then the group's first lane gathers the
-// four accumulators and finishes the leaf.
-// Every lane of the wave must call this (it shuffles). Digest in the group's first lane.
-template <int LPL>
-__device__ uint64_t hash_leaf_group(const uint8_t* p, uint32_t len, int lane) {
-  constexpr int kAcc = 4 / LPL;  // accumulators per lane
-  const int r = lane & (LPL - 1);
-  const uintptr_t a = reinterpret_cast<uintptr_t>(p);
-  const uint32_t stripes = len >> 5;
-  uint64_t acc[kAcc];
-#pragma unroll
-  for (int m = 0; m < kAcc; ++m) {
-    const int k = r * kAcc + m;
-    acc[m] = k == 0 ? kP1 + kP2 : k == 1 ? kP2 : k == 2 ? 0ull : 0ull - kP1;
-  }
-  if (stripes) {
-    const uint64_t* q = reinterpret_cast<const uint64_t*>(a & ~(uintptr_t)7);
-    const uint32_t sh = (uint32_t)(a & 7) * 8;
-    for (uint32_t i = 0; i < stripes; ++i) {
-#pragma unroll
-      for (int m = 0; m < kAcc; ++m) {
-        const uint32_t j = 4 * i + r * kAcc + m;  // word j of the leaf
-        const uint64_t lo = q[j];
-        const uint64_t w = sh ? (lo >> sh) | (q[j + 1] << (64 - sh)) : lo;
-        acc[m] = xxh_round(acc[m], w);
-      }
-    }
-  }
-  const int g0 = lane & ~(LPL - 1);
-  uint64_t v[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) v[k] = shfl64(acc[k % kAcc], g0 + k / kAcc);
-  if (r != 0 || len == 0) return 0;
-  return finish_leaf(v[0], v[1], v[2], v[3], p, len);
-}
-
 // Lane roles shared by the streamed paths.
 struct Roles {
   int lm, lc;            // loader: leaf within the load instruction (0/1), 16-byte chunk (0..31)
@@ -229,7 +203,7 @@ __device__ __forceinline__ int tile_slot(const Roles& r, int k) {
   return l * kRun + (((r.lc >> 1) ^ (l & 7)) * 32) + (r.lc & 1) * 16;
 }
 
-// 32 full, contiguous, 16-byte aligned leaves from `base`; lane pair l hashes leaf l.
+// 32 full, contiguous leaves from `base` (any alignment); lane pair l hashes leaf l.
 // Returns the leaf digest in the even lane.
 __device__ uint64_t hash_wave_contiguous(const uint8_t* base, uint8_t* tile, int lane) {
   const Roles r = roles(tile, lane);
@@ -237,14 +211,14 @@ __device__ uint64_t hash_wave_contiguous(const uint8_t* base, uint8_t* tile, int
   uint64_t va = r.rp ? 0 : kP1 + kP2, vb = r.rp ? 0 - kP1 : kP2;
   uint4 R[kLoads];
 #pragma unroll
-  for (int k = 0; k < kLoads; ++k) R[k] = load_stream16(lp + k * 2 * 4096);
+  for (int k = 0; k < kLoads; ++k) R[k] = load_stream16_any(lp + k * 2 * 4096);
   for (int s = 0; s < kStages; ++s) {
 #pragma unroll
     for (int k = 0; k < kLoads; ++k) *reinterpret_cast<uint4*>(tile + tile_slot(r, k)) = R[k];
     wave_lds_sync();
     if (s + 1 < kStages) {
 #pragma unroll
-      for (int k = 0; k < kLoads; ++k) R[k] = load_stream16(lp + k * 2 * 4096 + (s + 1) * kRun);
+      for (int k = 0; k < kLoads; ++k) R[k] = load_stream16_any(lp + k * 2 * 4096 + (s + 1) * kRun);
     }
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
@@ -263,7 +237,7 @@ __device__ uint64_t hash_wave_contiguous(const uint8_t* base, uint8_t* tile, int
   return r.rp ? 0 : xxh_avalanche(xxh_converge(va, vb, pa, pb) + 4096);
 }
 
-// Any 32 leaves whose present ones start 16-byte aligned (lengths 0..4096, anywhere in
+// Any 32 leaves (lengths 0..4096, at any alignment, anywhere in
 // memory). Full stripes stream through the tile as above; the loader lanes find each
 // leaf's address and full-stripe chunk count in a small per-wave LDS table (kept out of
 // registers, which the streamed stage already fills); the wave runs as many stages as
@@ -288,7 +262,7 @@ __device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
 #pragma unroll
   for (int k = 0; k < kLoads; ++k) {
     const uint64_t* e = table + 2 * (2 * k + r.lm);
-    R[k] = (uint64_t)r.lc < e[1] ? load_stream16(reinterpret_cast<const uint8_t*>(e[0]) + r.lc * 16)
+    R[k] = (uint64_t)r.lc < e[1] ? load_stream16_any(reinterpret_cast<const uint8_t*>(e[0]) + r.lc * 16)
                                  : make_uint4(0, 0, 0, 0);
   }
   for (uint32_t s = 0; s < stages; ++s) {
@@ -300,7 +274,7 @@ __device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
 #pragma unroll
       for (int k = 0; k < kLoads; ++k) {
         const uint64_t* e = table + 2 * (2 * k + r.lm);
-        R[k] = chunk < e[1] ? load_stream16(reinterpret_cast<const uint8_t*>(e[0]) + chunk * 16)
+        R[k] = chunk < e[1] ? load_stream16_any(reinterpret_cast<const uint8_t*>(e[0]) + chunk * 16)
                             : make_uint4(0, 0, 0, 0);
       }
     }
@@ -324,106 +298,14 @@ __device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
   return finish_leaf_words(va, vb, pa, pb, lf.addr, lf.len, W);
 }
 
-// Bytes [d, d + 16) of the 32 bytes c0 || c1 (d in 0..15), as a 16-byte value.
-__device__ __forceinline__ uint4 shift_chunk(uint4 c0, uint4 c1, uint32_t d) {
-  const uint64_t w[4] = {lo64(c0), hi64(c0), lo64(c1), hi64(c1)};
-  uint64_t out[2];
-#pragma unroll
-  for (int m = 0; m < 2; ++m) {
-    const uint32_t b = d + 8 * m;  // first byte of output word m
-    const uint32_t i = b >> 3, sh = (b & 7) * 8;
-    const uint64_t lo = i == 0 ? w[0] : i == 1 ? w[1] : w[2];
-    const uint64_t hi = i == 0 ? w[1] : i == 1 ? w[2] : w[3];
-    out[m] = sh ? (lo >> sh) | (hi << (64 - sh)) : lo;
-  }
-  return make_uint4((uint32_t)out[0], (uint32_t)(out[0] >> 32), (uint32_t)out[1], (uint32_t)(out[1] >> 32));
-}
-
-// Any 32 leaves at any alignment: leaf l's bytes are read as the aligned 16-byte chunks
-// from (start rounded down to 16), every one of which holds leaf bytes. A stage holds
-// chunks 32s .. 32s + 31 of each leaf in the tile (as for aligned leaves) and chunk
-// 32s + 32 in a per-wave side area, so each lane can shift its half-stripes out of two
-// chunks by the leaf's start offset d. The table keeps {aligned address, chunks | d << 32}.
-__device__ uint64_t hash_wave_shifted(const Leaf& lf, uint8_t* tile, uint64_t* table, uint4* extra, int lane) {
-  const Roles r = roles(tile, lane);
-  const uint32_t stripes = lf.len >> 5;
-  const uintptr_t a = reinterpret_cast<uintptr_t>(lf.addr);
-  const uint32_t d = (uint32_t)(a & 15);
-  if ((lane & 1) == 0) {
-    table[lane] = a & ~(uintptr_t)15;
-    const uint64_t chunks = stripes ? (d + 32ull * stripes + 15) / 16 : 0;
-    table[lane + 1] = chunks | ((uint64_t)d << 32);
-  }
-  uint32_t longest = stripes;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) longest = max(longest, (uint32_t)__shfl_xor((int)longest, o, 64));
-  const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 15) / 16);
-  uint64_t W[5];
-  load_tail(lf.addr, r.rp ? 0u : lf.len, W);
-  wave_lds_sync();
-
-  uint64_t va = r.rp ? 0 : kP1 + kP2, vb = r.rp ? 0 - kP1 : kP2;
-  // extra-chunk loader: lanes 0..31 load chunk 32s + 32 of leaf `lane`
-  const uint64_t* ex = table + 2 * (lane & 31);
-  const bool ex_lane = lane < kLeavesPerWave;
-  uint4 R[kLoads], X;
-#pragma unroll
-  for (int k = 0; k < kLoads; ++k) {
-    const uint64_t* e = table + 2 * (2 * k + r.lm);
-    R[k] = (uint64_t)r.lc < (uint32_t)e[1] ? load_stream16(reinterpret_cast<const uint8_t*>(e[0]) + r.lc * 16)
-                                           : make_uint4(0, 0, 0, 0);
-  }
-  X = ex_lane && 32u < (uint32_t)ex[1] ? load_stream16(reinterpret_cast<const uint8_t*>(ex[0]) + 32 * 16)
-                                       : make_uint4(0, 0, 0, 0);
-  const uint8_t* rtile = tile + r.rl * kRun;  // the reader's leaf region
-  for (uint32_t s = 0; s < stages; ++s) {
-#pragma unroll
-    for (int k = 0; k < kLoads; ++k) *reinterpret_cast<uint4*>(tile + tile_slot(r, k)) = R[k];
-    if (ex_lane) extra[lane] = X;
-    wave_lds_sync();
-    if (s + 1 < stages) {
-      const uint64_t chunk = (uint64_t)(s + 1) * kRunLanes + r.lc;
-#pragma unroll
-      for (int k = 0; k < kLoads; ++k) {
-        const uint64_t* e = table + 2 * (2 * k + r.lm);
-        R[k] = chunk < (uint32_t)e[1] ? load_stream16(reinterpret_cast<const uint8_t*>(e[0]) + chunk * 16)
-                                      : make_uint4(0, 0, 0, 0);
-      }
-      const uint64_t xc = (uint64_t)(s + 2) * kRunLanes;
-      X = ex_lane && xc < (uint32_t)ex[1] ? load_stream16(reinterpret_cast<const uint8_t*>(ex[0]) + xc * 16)
-                                          : make_uint4(0, 0, 0, 0);
-    }
-    // half-stripe rp of stripe j = chunk 2j + rp of the stage shifted by d: chunks c, c + 1
-#pragma unroll 4
-    for (int j = 0; j < 16; ++j) {
-      const int c = 2 * j + r.rp;
-      const uint4 c0 = *reinterpret_cast<const uint4*>(rtile + ((((c >> 1) ^ r.rf) * 32) + (c & 1) * 16));
-      const int c1i = c + 1;
-      const uint4 c1 = c1i < 32 ? *reinterpret_cast<const uint4*>(rtile + ((((c1i >> 1) ^ r.rf) * 32) + (c1i & 1) * 16))
-                                : extra[r.rl];
-      const uint4 w = shift_chunk(c0, c1, d);
-      if (s * 16 + j < stripes) {
-        va = xxh_round(va, lo64(w));
-        vb = xxh_round(vb, hi64(w));
-      }
-    }
-    wave_lds_sync();
-  }
-  const uint64_t pa = shfl_xor64(va, 1), pb = shfl_xor64(vb, 1);
-  if (r.rp || lf.len == 0) return 0;
-  return finish_leaf_words(va, vb, pa, pb, lf.addr, lf.len, W);
-}
-
 // Digest of this lane pair's leaf, in the even lane.
-__device__ __forceinline__ uint64_t hash_slot(const Leaf& lf, uint8_t* tile, uint64_t* table, uint4* extra,
-                                              int lane) {
+__device__ __forceinline__ uint64_t hash_slot(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
   const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
   const uint64_t a0 = shfl64(addr, 0);
-  const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)(lane >> 1) * 4096 && (a0 & 15) == 0;
+  const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)(lane >> 1) * 4096;
   if (__all(contiguous)) return hash_wave_contiguous(reinterpret_cast<const uint8_t*>(uniform64(a0)), tile, lane);
   if (!__any(lf.len != 0)) return 0;
-  if (__all(lf.len == 0 || (addr & 15) == 0)) return hash_wave_gathered(lf, tile, table, lane);
-  return hash_wave_shifted(lf, tile, table, extra, lane);
+  return hash_wave_gathered(lf, tile, table, lane);
 }
 
 // Bottom-up tree over `count` roots in LDS (double-buffered), by one wave.
@@ -451,7 +333,6 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[W * kWaveLds + (kSolo ? kSoloPad : 0)];
   __shared__ uint64_t roots[2][kMaxRoots];
   __shared__ uint64_t tables[W][2 * kLeavesPerWave];
-  __shared__ uint4 extras[W][kLeavesPerWave];  // per-leaf 33rd chunk of a shifted stage
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   uint8_t* tile = lds + wave * kWaveLds;
@@ -470,7 +351,7 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
       const uint64_t g = slot >> L2;
       const uint32_t k = (uint32_t)(slot & (lpb - 1));
       const Leaf lf = locate_wave(a, wave_slot0 >> L2, g, k, lane);
-      const uint64_t d = hash_slot(lf, tile, table, extras[wave], lane);
+      const uint64_t d = hash_slot(lf, tile, table, lane);
       if (a.leaf_out && even && g < a.n_blocks) a.leaf_out[slot] = lf.len ? d : 0;
       const uint32_t G = lpb <= kLeavesPerWave ? lpb : (uint32_t)kLeavesPerWave;
       const uint32_t p = k & (G - 1);
@@ -509,7 +390,7 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
       for (uint32_t grp = 0; grp < groups; ++grp) {
         const uint32_t k = grp * GROUP + (uint32_t)wave * kLeavesPerWave + (lane >> 1);
         const Leaf lf = locate(a, g, k, s0);
-        const uint64_t d = hash_slot(lf, tile, table, extras[wave], lane);
+        const uint64_t d = hash_slot(lf, tile, table, lane);
         if (a.leaf_out && even) a.leaf_out[((uint64_t)g << L2) + k] = lf.len ? d : 0;
         const uint32_t before = k & ~(uint32_t)(kLeavesPerWave - 1);
         const uint32_t n = nleaf > before ? min(nleaf - before, (uint32_t)kLeavesPerWave) : 0u;
@@ -574,13 +455,13 @@ __device__ __forceinline__ uint64_t quad_rounds(uint64_t v, const uint8_t* tile,
   return v;
 }
 
-// 16 full, contiguous, 16-byte aligned leaves from `base`; digest in lane 4l of leaf l.
+// 16 full, contiguous leaves from `base` (any alignment); digest in lane 4l of leaf l.
 __device__ uint64_t hash_quad_contiguous(const uint8_t* base, uint8_t* tile, int lane) {
   const int lm = lane / 32, lc = lane % 32, rl = lane >> 2, ra = lane & 3;
   uint64_t v = quad_acc_init(ra);
   uint4 R[kQuadLoads];
 #pragma unroll
-  for (int k = 0; k < kQuadLoads; ++k) R[k] = load_stream16(base + quad_leaf(lm, k) * 4096 + quad_chunk(lc, k) * 16);
+  for (int k = 0; k < kQuadLoads; ++k) R[k] = load_stream16_any(base + quad_leaf(lm, k) * 4096 + quad_chunk(lc, k) * 16);
   for (int s = 0; s < kQuadStages; ++s) {
 #pragma unroll
     for (int k = 0; k < kQuadLoads; ++k) *reinterpret_cast<uint4*>(tile + quad_tile_slot(lm, lc, k)) = R[k];
@@ -588,7 +469,7 @@ __device__ uint64_t hash_quad_contiguous(const uint8_t* base, uint8_t* tile, int
     if (s + 1 < kQuadStages) {
 #pragma unroll
       for (int k = 0; k < kQuadLoads; ++k)
-        R[k] = load_stream16(base + quad_leaf(lm, k) * 4096 + (s + 1) * kQuadStage + quad_chunk(lc, k) * 16);
+        R[k] = load_stream16_any(base + quad_leaf(lm, k) * 4096 + (s + 1) * kQuadStage + quad_chunk(lc, k) * 16);
     }
     v = quad_rounds(v, tile, rl, ra, 32);
     wave_lds_sync();
@@ -598,7 +479,7 @@ __device__ uint64_t hash_quad_contiguous(const uint8_t* base, uint8_t* tile, int
   return ra ? 0 : xxh_avalanche(xxh_converge(v1, v2, v3, v4) + 4096);
 }
 
-// Any 16 leaves whose present ones start 16-byte aligned: full stripes through the tile
+// Any 16 leaves at any alignment: full stripes through the tile
 // (leaf addresses and full-stripe chunk counts in a per-wave LDS table), as many stages
 // as the longest leaf needs; lane 4l finishes leaf l's tail.
 __device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
@@ -621,7 +502,7 @@ __device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
   for (int k = 0; k < kQuadLoads; ++k) {
     const uint64_t* e = table + 2 * quad_leaf(lm, k);
     const uint64_t c = (uint64_t)quad_chunk(lc, k);
-    R[k] = c < e[1] ? load_stream16(reinterpret_cast<const uint8_t*>(e[0]) + c * 16) : make_uint4(0, 0, 0, 0);
+    R[k] = c < e[1] ? load_stream16_any(reinterpret_cast<const uint8_t*>(e[0]) + c * 16) : make_uint4(0, 0, 0, 0);
   }
   for (uint32_t s = 0; s < stages; ++s) {
 #pragma unroll
@@ -632,7 +513,7 @@ __device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
       for (int k = 0; k < kQuadLoads; ++k) {
         const uint64_t* e = table + 2 * quad_leaf(lm, k);
         const uint64_t c = (uint64_t)(s + 1) * 64 + quad_chunk(lc, k);
-        R[k] = c < e[1] ? load_stream16(reinterpret_cast<const uint8_t*>(e[0]) + c * 16) : make_uint4(0, 0, 0, 0);
+        R[k] = c < e[1] ? load_stream16_any(reinterpret_cast<const uint8_t*>(e[0]) + c * 16) : make_uint4(0, 0, 0, 0);
       }
     }
     const int left = (int)stripes - (int)(s * 32);
@@ -649,11 +530,10 @@ __device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
 __device__ __forceinline__ uint64_t hash_slot_quad(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
   const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
   const uint64_t a0 = shfl64(addr, 0);
-  const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)(lane >> 2) * 4096 && (a0 & 15) == 0;
+  const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)(lane >> 2) * 4096;
   if (__all(contiguous)) return hash_quad_contiguous(reinterpret_cast<const uint8_t*>(uniform64(a0)), tile, lane);
   if (!__any(lf.len != 0)) return 0;
-  if (__all(lf.len == 0 || (addr & 15) == 0)) return hash_quad_gathered(lf, tile, table, lane);
-  return hash_leaf_group<4>(lf.addr, lf.len, lane);
+  return hash_quad_gathered(lf, tile, table, lane);
 }
 
 // One workgroup of W waves per W * kQuadLeaves slots; LPB <= kQuadLeaves, so every wave

@@ -57,7 +57,7 @@ def test_digests_every_block_size(block):
     assert np.array_equal(gpu["leaves"], ref["leaves"])
 
 
-@pytest.mark.parametrize("skew", [1, 3, 8, 12])
+@pytest.mark.parametrize("skew", [1, 2, 3, 4, 8, 12])
 @pytest.mark.parametrize("block", [4096, 65536, 256 << 10, 1 << 20, 2 << 20, 16 << 20])
 def test_unaligned_payload_starts(skew, block):
     rng = np.random.default_rng(200 + skew + block.bit_length())
