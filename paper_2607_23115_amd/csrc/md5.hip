@@ -70,16 +70,18 @@ __global__ void md5_prefix_kernel(const uint64_t* seg_addr, const uint64_t* seg_
   const uint64_t len = seg_len[s];
   const uint32_t L = len < prefix ? (uint32_t)len : prefix;
   const uint8_t* p = reinterpret_cast<const uint8_t*>(seg_addr[s]);
-  const bool a4 = (reinterpret_cast<uintptr_t>(p) & 3) == 0;
   const uint32_t blocks = (L + 8) / 64 + 1;
   const uint64_t bits = (uint64_t)L * 8;
   uint32_t st[4] = {0x67452301u, 0xefcdab89u, 0x98badcfeu, 0x10325476u};
   for (uint32_t blk = 0; blk < blocks; ++blk) {
     const uint32_t base = blk * 64;
     uint32_t X[16];
-    if (a4 && base + 64 <= L) {
+    if (base + 64 <= L) {
+      // whole 64-byte block: 4-byte loads at any alignment (gfx950 under HSA runs with
+      // unaligned access enabled), each inside the prefix
+      typedef uint32_t u32_any __attribute__((aligned(1)));
 #pragma unroll
-      for (int w = 0; w < 16; ++w) X[w] = reinterpret_cast<const uint32_t*>(p + base)[w];
+      for (int w = 0; w < 16; ++w) X[w] = reinterpret_cast<const u32_any*>(p + base)[w];
     } else {
 #pragma unroll
       for (int w = 0; w < 16; ++w) {
