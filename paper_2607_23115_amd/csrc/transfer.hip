@@ -189,29 +189,28 @@ __global__ __launch_bounds__(kThreads) void plan_write_kernel(Geo geo, const uin
   }
 }
 
-// Copy len bytes with the whole workgroup: 16-byte non-temporal words when both ends
-// allow it (every byte is touched once), bytes otherwise.
+// Copy len bytes with the whole workgroup: 16-byte non-temporal words from either end's
+// start at any alignment (gfx950 under HSA runs with unaligned access enabled; each word
+// covers 16 bytes of the range, so every byte is touched once and none outside it), then
+// the last len mod 16 bytes one by one.
+typedef u32x4 u32x4_any __attribute__((aligned(1)));
 __device__ __forceinline__ void wg_copy(uint8_t* dst, const uint8_t* src, uint64_t len) {
-  if (((reinterpret_cast<uintptr_t>(dst) | reinterpret_cast<uintptr_t>(src)) & 15) == 0) {
-    const uint64_t words = len >> 4;
-    u32x4* d = reinterpret_cast<u32x4*>(dst);
-    const u32x4* s = reinterpret_cast<const u32x4*>(src);
-    uint64_t i = threadIdx.x;
-    for (; i + 3 * kThreads < words; i += 4 * kThreads) {
-      const u32x4 a = __builtin_nontemporal_load(s + i);
-      const u32x4 b = __builtin_nontemporal_load(s + i + kThreads);
-      const u32x4 c = __builtin_nontemporal_load(s + i + 2 * kThreads);
-      const u32x4 e = __builtin_nontemporal_load(s + i + 3 * kThreads);
-      __builtin_nontemporal_store(a, d + i);
-      __builtin_nontemporal_store(b, d + i + kThreads);
-      __builtin_nontemporal_store(c, d + i + 2 * kThreads);
-      __builtin_nontemporal_store(e, d + i + 3 * kThreads);
-    }
-    for (; i < words; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
-    for (uint64_t k = (words << 4) + threadIdx.x; k < len; k += kThreads) dst[k] = src[k];
-  } else {
-    for (uint64_t k = threadIdx.x; k < len; k += kThreads) dst[k] = src[k];
+  const uint64_t words = len >> 4;
+  u32x4_any* d = reinterpret_cast<u32x4_any*>(dst);
+  const u32x4_any* s = reinterpret_cast<const u32x4_any*>(src);
+  uint64_t i = threadIdx.x;
+  for (; i + 3 * kThreads < words; i += 4 * kThreads) {
+    const u32x4 a = __builtin_nontemporal_load(s + i);
+    const u32x4 b = __builtin_nontemporal_load(s + i + kThreads);
+    const u32x4 c = __builtin_nontemporal_load(s + i + 2 * kThreads);
+    const u32x4 e = __builtin_nontemporal_load(s + i + 3 * kThreads);
+    __builtin_nontemporal_store(a, d + i);
+    __builtin_nontemporal_store(b, d + i + kThreads);
+    __builtin_nontemporal_store(c, d + i + 2 * kThreads);
+    __builtin_nontemporal_store(e, d + i + 3 * kThreads);
   }
+  for (; i < words; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
+  for (uint64_t k = (words << 4) + threadIdx.x; k < len; k += kThreads) dst[k] = src[k];
 }
 
 // [at, at + len) lies inside [0, size), without overflow.
