@@ -95,8 +95,8 @@ enum {
  * host-to-device copy). Each payload is cut, from its first byte, into 4 KiB
  * leaves and blocks of block_bytes; a payload's last leaf and last block may be
  * short. Global block index g = blk_first[s] + j for block j of payload s.
- *   seg_addr  device u64[n_seg]    device address of payload s (any alignment; a
- *                                  4-byte aligned payload streams fastest)
+ *   seg_addr  device u64[n_seg]    device address of payload s (any alignment; 16-byte
+ *                                  aligned payloads stream fastest, then 4-byte aligned)
  *   seg_len   device u64[n_seg]    bytes of payload s (0 allowed)
  *   blk_first device u64[n_seg+1]  exclusive prefix of ceil(seg_len[s]/block_bytes);
  *                                  gleam_batch_geometry computes it
