@@ -251,6 +251,30 @@ def test_digests_do_not_depend_on_batch_position(block):
         assert np.array_equal(u64(g.fp_chunks(batch)), want[i]), f"alone: payload {i}"
 
 
+@pytest.mark.parametrize("block", [4096, 65536])
+@pytest.mark.parametrize("avg_slots", [55, 70])
+def test_large_batches_either_side_of_the_kernel_choice(block, avg_slots):
+    """Past 65,536 leaf slots, blocks of up to 64 KiB go to the four-lanes-per-leaf kernel
+    when payloads average at least 64 slots, else to the two-lanes one: batches of 1,400
+    payloads averaging about 55 or 70 slots (random tails, some empty payloads, a 3-byte skew);
+    every block and leaf digest equals the oracle's."""
+    rng = np.random.default_rng(5100 + avg_slots + block.bit_length())
+    n = 1400
+    leaves = rng.integers(avg_slots // 2, 3 * avg_slots // 2 + 1, n)
+    lens = leaves * 4096 - rng.integers(0, 4096, n)
+    lens[rng.choice(n, 20, replace=False)] = 0
+    payloads = [np.frombuffer(rng.bytes(int(m)), np.uint8) for m in lens]
+    arena, offs, blens = W.pack(payloads, align=256, skew=3)
+    batch = g.Batch.from_arena(to_device(arena), offs, blens, block)
+    slots = batch.n_blocks * batch.leaves_per_block
+    assert slots > 65536
+    say("kernel choice: slots per payload", slots / batch.n_seg, "block", block)
+    d, lv = g.fp_chunks(batch, with_leaves=True)
+    want, wleaves = oracle.batch_digests(payloads, block, with_leaves=True, threads=host_threads())
+    assert np.array_equal(u64(d), want)
+    assert np.array_equal(u64(lv), wleaves.reshape(-1))
+
+
 @pytest.mark.parametrize("skew", [0, 3, 16])
 def test_4k_blocks_past_the_small_batch_limit(skew):
     """4 KiB blocks past the small-batch kernel's 65,536 slots, every tail length: 80,000
