@@ -123,7 +123,7 @@ __device__ __forceinline__ Leaf locate_wave(const FpArgs& a, uint64_t g_first, u
 // XXH64 after the stripe loop: fold (or the short-input start), length, tail, avalanche.
 // The tail (the < 32 bytes after the last full stripe, at any address) lies in at most
 // five aligned 8-byte words, each holding tail bytes. load_tail reads them together (one
-// round trip, no byte loads; the streamed paths issue it before their stage loop, so it
+// round trip, no byte loads; the gathered paths issue it before their stage loop, so it
 // overlaps the first stage's loads); finish_leaf_words shifts the tail's own 8-byte
 // words out of adjacent pairs and runs the XXH64 tail steps in registers: whole words,
 // then a 4-byte step, then single bytes.
@@ -167,13 +167,6 @@ __device__ __forceinline__ uint64_t finish_leaf_words(uint64_t v1, uint64_t v2, 
     rest >>= 8;
   }
   return xxh_avalanche(h);
-}
-
-__device__ __forceinline__ uint64_t finish_leaf(uint64_t v1, uint64_t v2, uint64_t v3, uint64_t v4, const uint8_t* p,
-                                                uint32_t len) {
-  uint64_t W[5];
-  load_tail(p, len, W);
-  return finish_leaf_words(v1, v2, v3, v4, p, len, W);
 }
 
 // Lane roles shared by the streamed paths.
