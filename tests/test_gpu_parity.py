@@ -73,14 +73,15 @@ def test_unaligned_payload_starts(skew, block):
 
 @pytest.mark.parametrize("block", [4096, 65536, 1 << 20])
 def test_mixed_alignment_in_one_wave(block):
-    """Aligned and unaligned payloads side by side, so waves mix both kinds."""
+    """Payloads at 16-byte aligned, 8-byte, odd and 2-byte starts side by side, so waves
+    mix them."""
     rng = np.random.default_rng(250 + block.bit_length())
     payloads = make_payloads(rng, block, extra=[5000, 12000, 4096 * 3])
     lens = np.array([p.size for p in payloads], np.uint64)
     offs = np.zeros(len(payloads), np.uint64)
     pos = 0
     for i, n in enumerate(lens.tolist()):
-        start = ((pos + 255) // 256) * 256 + (8 if i % 3 == 1 else 0)
+        start = ((pos + 255) // 256) * 256 + (0, 8, 3, 2)[i % 4]
         offs[i] = start
         pos = start + n
     arena = np.zeros(pos + 512, np.uint8)
