@@ -188,7 +188,7 @@ __global__ __launch_bounds__(kThreads) void compact_tally_kernel(const uint8_t* 
 
 __global__ __launch_bounds__(kThreads) void compact_place_kernel(const uint8_t* status, uint64_t n, uint64_t tiles,
                                                                  const uint64_t* tile_counts, const uint64_t* deficits,
-                                                                 uint64_t n_def, uint64_t* miss_idx,
+                                                                 uint64_t n_parts, uint64_t* miss_idx,
                                                                  uint64_t* miss_count, uint64_t* miss_bytes,
                                                                  uint64_t block_bytes) {
   __shared__ uint32_t wave_sums[kThreads / 64];
@@ -209,7 +209,7 @@ __global__ __launch_bounds__(kThreads) void compact_place_kernel(const uint8_t* 
   if (blockIdx.x + 1 != tiles) return;
   uint64_t d = 0;
   if (miss_bytes)
-    for (uint64_t w = threadIdx.x; w < n_def; w += kThreads) d += deficits[w];
+    for (uint64_t w = threadIdx.x; w < n_parts; w += kThreads) d += deficits[w];
   d = block_sum64(d, wave_parts);
   if (threadIdx.x == 0) {
     const uint64_t count = before + total;
