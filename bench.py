@@ -30,7 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD public specification
-PROFILE_PMC = os.path.join(ROOT, "profiles", "fp_kernel_decoder7b_pmc.txt")
+PROFILE_PMC = {w: os.path.join(ROOT, "profiles", f"fp_kernel_{w}_pmc.txt") for w in ("decoder7b", "small_copies")}
 FP_SOURCE = os.path.join(ROOT, "paper_2607_23115_amd", "csrc", "fp_chunks.hip")
 
 
@@ -62,13 +62,15 @@ def source_digest() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def pmc_traffic(algo_bytes: int):
-    """HBM bytes per fingerprint launch from the committed counter summary, scaled by
-    the copy-kernel calibration in it; None if absent or taken on other source."""
-    if not os.path.exists(PROFILE_PMC):
+def pmc_traffic(workload: str):
+    """HBM bytes per fingerprint launch on this workload from its committed counter
+    summary, scaled by the copy-kernel calibration in it; None if there is none or it
+    was taken on other source."""
+    path = PROFILE_PMC.get(workload)
+    if path is None or not os.path.exists(path):
         return None
     kv = {}
-    with open(PROFILE_PMC) as f:
+    with open(path) as f:
         for line in f:
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
@@ -879,7 +881,7 @@ def main():
 
     algo_bytes = payload_bytes + 8 * n + 24 * batch.n_seg + 8 * (batch.n_seg + 1)
     achieved = algo_bytes / (fp_avg_ms * 1e-3) / 1e9
-    traffic = pmc_traffic(algo_bytes) if args.workload == "decoder7b" else None
+    traffic = pmc_traffic(args.workload)
     log(f"{desc}: {n} blocks, {miss_count} misses ({miss_bytes} bytes), fp {fp_avg_ms:.3f} ms "
         f"(min {min(fp_ms):.3f}, max {max(fp_ms):.3f}), step {ms_per_step:.3f} ms, cold {cold}, "
         f"read ceiling {read_gbs:.0f} GB/s")

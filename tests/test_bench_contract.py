@@ -22,23 +22,26 @@ def _summary(path, sha):
 
 def test_traffic_only_for_the_profiled_source(tmp_path, monkeypatch):
     p = tmp_path / "pmc.txt"
-    monkeypatch.setattr(bench, "PROFILE_PMC", str(p))
+    monkeypatch.setattr(bench, "PROFILE_PMC", {"decoder7b": str(p)})
     _summary(p, bench.source_digest())
-    assert bench.pmc_traffic(1) == int(1000.0 * 1024 * 2.0 + 10.0 * 1024 * 1.0)
+    assert bench.pmc_traffic("decoder7b") == int(1000.0 * 1024 * 2.0 + 10.0 * 1024 * 1.0)
+    assert bench.pmc_traffic("random16") is None  # no counter summary for that workload
     _summary(p, "0" * 16)
-    assert bench.pmc_traffic(1) is None
+    assert bench.pmc_traffic("decoder7b") is None
 
 
-def test_committed_profile_parses():
-    kv = {}
-    for line in open(bench.PROFILE_PMC):
-        if ":" in line and not line.startswith("#"):
-            k, v = line.split(":", 1)
-            kv[k.strip()] = v.strip()
-    for key in ("fp_chunks.hip sha256 prefix", "fp FETCH_SIZE KiB per dispatch", "fp WRITE_SIZE KiB per dispatch",
-                "copy fetch scale", "copy write scale"):
-        assert key in kv, key
-    float(kv["copy fetch scale"])
+def test_committed_profiles_parse():
+    for path in bench.PROFILE_PMC.values():
+        kv = {}
+        for line in open(path):
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+        for key in ("fp_chunks.hip sha256 prefix", "fp FETCH_SIZE KiB per dispatch",
+                    "fp WRITE_SIZE KiB per dispatch", "copy fetch scale", "copy write scale"):
+            assert key in kv, (path, key)
+        float(kv["fp FETCH_SIZE KiB per dispatch"])
+        float(kv["copy fetch scale"])
 
 
 def test_more_than_one_gpu_is_refused():
