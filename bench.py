@@ -38,12 +38,30 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def host_threads() -> int:
+def host_affinity() -> int:
+    """Cores this process may run on (sched_getaffinity)."""
     try:
-        n = len(os.sched_getaffinity(0))
+        return len(os.sched_getaffinity(0))
     except AttributeError:
-        n = os.cpu_count() or 1
-    return max(1, min(16, n))
+        return os.cpu_count() or 1
+
+
+def host_share():
+    """The host's CPU share for this job when the environment states one
+    (OMP_NUM_THREADS), else None."""
+    try:
+        v = int(os.environ.get("OMP_NUM_THREADS", ""))
+        return v if v > 0 else None
+    except ValueError:
+        return None
+
+
+def host_threads() -> int:
+    """Threads for the oracle: every core of the affinity mask, capped by a stated CPU
+    share (a shared host gives each GPU job its share of the cores)."""
+    n = host_affinity()
+    share = host_share()
+    return max(1, min(n, share) if share else n)
 
 
 def cpu_model() -> str:
@@ -225,6 +243,7 @@ def identify_path(args, g, torch, threads, batch, payloads, keep):
         oracle.identify_weights(rec, current, batch.block_bytes, region_first, threads=threads)
         dt = time.perf_counter() - t0
         cpu = {"value": round(payload_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+               "affinity": host_affinity(), "cpu_share": host_share(), "threads_used": threads,
                "sample": f"whole workload ({payload_bytes} bytes), one run {dt:.3f} s, {cpu_model()}"}
     out = {"metric": "payload GB/s for free-time weight identification (digest + compare), 1 MI355X",
            "value": round(payload_bytes / (ms * 1e-3) / 1e9, 2), "unit": "GB/s", "n_gpus": 1, "steps": K,
@@ -686,6 +705,7 @@ def run_cpu_baseline(payloads, block, threads, budget_bytes):
         times1.append(time.perf_counter() - t0)
     dt1 = float(np.median(times1))
     return {"value": round(total / dt / 1e9, 3), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "affinity": host_affinity(), "cpu_share": host_share(), "threads_used": threads,
             "sample": f"{len(sample)} of {len(payloads)} payloads ({total} bytes), median of 3 runs "
                       f"{dt:.3f} s, {cpu_model()}",
             "one_thread": {"value": round(one_total / dt1 / 1e9, 3), "unit": "GB/s",

@@ -25,7 +25,7 @@
  *   gleam_send_plan / gleam_pack_misses / gleam_restore_blocks -- the transfer
  *                          around the decision: what travels, packed, and rebuilt
  *   gleam_remap_*       -- the address-remap map of the weight-sharing layer: ranges
- *                          of client device addresses onto shareable positions (4.3)
+ *                          of client device addresses onto shareable positions (4.1.3)
  *   gleam_read_stream   -- calibration only: the measured HBM read ceiling
  *
  * Conventions for every entry point:
@@ -53,10 +53,21 @@
  *     not on each replay. The four exceptions sort or scan with rocPRIM, which also
  *     enqueues memsets; keep them out of captured graphs.
  *   - Device descriptor contents (seg_addr, seg_len, blk_first) are not read on
- *     the host. The caller guarantees they describe the batch; whatever they hold,
- *     kernels read payload memory only in aligned 16-byte units that contain at
- *     least one byte of [seg_addr[s], seg_addr[s] + seg_len[s]) (so never another
- *     page).
+ *     the host. The caller guarantees they describe the batch. Whatever they hold,
+ *     a kernel reads a payload P = [seg_addr[s], seg_addr[s] + seg_len[s]) only
+ *     with loads that lie inside P, or with aligned 8-byte loads that hold at least
+ *     one byte of P, so it never touches a page that holds no byte of P:
+ *       fingerprint (and identify): 16-byte loads at a leaf's own start + 16 i,
+ *         covering the leaf's whole 32-byte stripes; the tail (< 32 bytes) in the
+ *         aligned 8-byte words that hold it;
+ *       MD5 prefix: 4-byte loads at the payload start + 4 i over whole 64-byte
+ *         blocks of the prefix, then single bytes;
+ *       pack / restore: 16-byte loads and stores at a block's own start + 16 i,
+ *         then single bytes.
+ *     These loads keep the payload's alignment, so they are unaligned whenever the
+ *     payload is: the library relies on the unaligned global access that gfx950
+ *     runs with under ROCm (the HSA default). 16-byte aligned payloads stream
+ *     fastest, 4-byte aligned ones at about 85% of that rate, others at 65-70%.
  */
 #ifndef GLEAM_H
 #define GLEAM_H
@@ -374,12 +385,12 @@ gleam_status gleam_restore_blocks(const gleam_batch* dst, const gleam_send_recor
                                   void* stream);
 
 /*
- * Address-remap map (Sec. 4.3, weight sharing: two chunks written into one client
+ * Address-remap map (Sec. 4.1.3, Weight Chunk Sharing: two chunks written into one client
  * allocation may find their shareable copies in two different server allocations, so
  * a virtual memory layer maps client device addresses onto the actual shareable
- * positions; Sec. 6: each task gets a 1 TB virtual address space and the mappings are
- * kept in a red-black tree). Device pointers carried by remoted calls are translated
- * through it.
+ * positions; Appendix, Implementation Details, Virtual Memory Map: each task gets a
+ * 1 TB virtual address space and the mappings are kept in a red-black tree). Device
+ * pointers carried by remoted calls are translated through it.
  *
  * The map holds disjoint, non-empty intervals [start, start + length) of the 64-bit
  * address space, each with a target: address p inside one translates to

@@ -25,7 +25,7 @@ The oracle computes, per fixed-size block of each payload:
 
 The fingerprint is C (gleam_oracle.c) because the oracle must digest tens of GB;
 everything after it is numpy. remap.py holds the address-remap interval map of the
-weight-sharing layer (Sec. 4.3, Sec. 6).
+weight-sharing layer (Sec. 4.1.3; Appendix, Implementation Details, Virtual Memory Map).
 """
 
 from __future__ import annotations

@@ -3,13 +3,13 @@
 TEST INFRASTRUCTURE ONLY (the package docstring says who may use it). It shares no
 code with the GPU library.
 
-Gleam, Sec. 4.3 (weight sharing): two host-to-device chunks written into one client
-allocation may each find their shareable copy inside a different server allocation,
-so the server keeps a virtual memory layer that maps ranges of client device
-addresses onto the positions of those copies. Sec. 6 (virtual memory map): each task
-gets its own virtual address space of 1 TB, and the mappings are kept in a
-red-black tree; the calls whose arguments carry device pointers are translated
-through it.
+Gleam, Sec. 4.1.3 (Weight Chunk Sharing): two host-to-device chunks written into one
+client allocation may each find their shareable copy inside a different server
+allocation, so the server keeps a virtual memory layer that maps ranges of client device
+addresses onto the positions of those copies. Appendix, Implementation Details (Virtual
+Memory Map): each task gets its own virtual address space of 1 TB, and the mappings are
+kept in a red-black tree; the calls whose arguments carry device pointers are
+translated through it.
 
 Here the map is a set of disjoint, non-empty intervals [start, start + length), each
 with a target. A pointer p inside an interval translates to target + (p - start); a
@@ -83,22 +83,22 @@ class RemapMap:
         if rs.size and len(self):
             nz = rl > 0
             r_first, r_len = rs[nz], rl[nz]
-            # last address of [d, d + dlen), clipped at 2^64 - 1: d + (dlen - 1) passes the
-            # top exactly when dlen - 1 > (2^64 - 1) - d
-            top = np.uint64(_TOP)
-            over = (r_len - np.uint64(1)) > top - r_first
-            r_last = np.where(over, top, r_first + (r_len - np.uint64(1)))  # (the unused sum may wrap)
+            # last address of [d, d + dlen), clipped at the top of the 64-bit space
+            # (Python integers, so the sum cannot wrap)
+            r_last = _u64([min(d + n - 1, _TOP) for d, n in zip(r_first.tolist(), r_len.tolist())])
             if r_first.size:
+                # (an interval in the map never reaches past the top, so this cannot wrap)
                 last = self.start + (self.length - np.uint64(1))
                 keep = overlap_counts(self.start, last, r_first, r_last) == 0
         n_removed = int((~keep).sum())
         s_start, s_len, s_target = self.start[keep], self.length[keep], self.target[keep]
 
-        # 2. invalid additions
-        # (s + n > 2^64 - 1 is s > (2^64 - 1) - n, which cannot wrap in u64)
-        top = np.uint64(_TOP)
+        # 2. invalid additions: empty, or reaching past the top of the 64-bit space at
+        # either end (Python integers, so the sums cannot wrap)
         status = np.full(n_add, ADDED, np.uint8)
-        status[(a_l == 0) | (a_s > top - a_l) | (a_t > top - a_l)] = INVALID
+        for i, (s0, n, t0) in enumerate(zip(a_s.tolist(), a_l.tolist(), a_t.tolist())):
+            if n == 0 or s0 + n > _TOP or t0 + n > _TOP:
+                status[i] = INVALID
         valid = status == ADDED
 
         # 3. overlaps with survivors and with the other valid additions

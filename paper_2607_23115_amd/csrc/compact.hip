@@ -307,7 +307,9 @@ extern "C" gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, 
     return GLEAM_E_UNSUPPORTED;
   }
   hipStream_t s = (hipStream_t)stream;
-  if (n <= kSmallItems && (!d_miss_bytes || b->n_seg <= kSmallItems)) {
+  // (n == 0 always goes here: the tiled paths need at least one tile, and a batch of
+  // only empty payloads may be longer than kSmallItems)
+  if (n == 0 || (n <= kSmallItems && (!d_miss_bytes || b->n_seg <= kSmallItems))) {
     ShortBlocks sb{nullptr, nullptr, 0, 0, nullptr};
     if (d_miss_bytes) sb = ShortBlocks{b->seg_len, b->blk_first, b->n_seg, b->block_bytes, d_miss_bytes};
     hipLaunchKernelGGL(compact_small_kernel, dim3(1), dim3(kScanThreads), 0, s, d_status, n,

@@ -1,7 +1,8 @@
-// Address-remap interval map (Gleam Sec. 4.3: chunks written into one client allocation
-// may find their shareable copies in different server allocations, so a virtual memory
-// layer maps client device addresses onto those positions; Sec. 6: one 1 TB virtual
-// space per task, the mappings kept in a red-black tree).
+// Address-remap interval map (Gleam Sec. 4.1.3, Weight Chunk Sharing: chunks written into
+// one client allocation may find their shareable copies in different server allocations,
+// so a virtual memory layer maps client device addresses onto those positions; Appendix,
+// Implementation Details, Virtual Memory Map: one 1 TB virtual space per task, the
+// mappings kept in a red-black tree).
 //
 // The map is an array of disjoint intervals sorted by start, in caller-owned device
 // storage: [256-byte header: u64 count, fence stride, fence length][start x cap]

@@ -20,11 +20,16 @@ def say(*args) -> None:
 
 
 def host_threads() -> int:
+    """Oracle threads: the affinity mask, capped by the job's stated CPU share."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:
         n = os.cpu_count() or 1
-    return max(1, min(16, n))
+    try:
+        share = int(os.environ.get("OMP_NUM_THREADS", "0"))
+    except ValueError:
+        share = 0
+    return max(1, min(n, share) if share > 0 else n)
 
 
 def to_device(a: np.ndarray) -> torch.Tensor:

@@ -597,6 +597,19 @@ def test_empty_inputs():
     assert_same(gpu, oracle_path(payloads, 4096, oracle.Table()), "zero-length")
 
 
+def test_compaction_of_only_empty_payloads_beyond_small_path():
+    """70,000 zero-length payloads: no blocks, so no statuses, and the byte total is
+    wanted. The count and the byte total are still written (both 0)."""
+    batch = g.Batch(np.zeros(70_000, np.uint64), np.zeros(70_000, np.uint64), 65536)
+    assert batch.n_blocks == 0 and batch.n_seg > 65_536
+    say("compaction of 70,000 empty payloads")
+    status = torch.empty(1, dtype=torch.uint8, device="cuda")[:0]
+    counters = torch.full((2,), -1, dtype=torch.int64, device="cuda")
+    g.miss_compact(status, batch, counters=counters)
+    torch.cuda.synchronize()
+    assert u64(counters).tolist() == [0, 0]
+
+
 @pytest.mark.parametrize("n", [1_000, 10_000, 100_000])  # one-workgroup and grid lookups; both compactions
 def test_optional_outputs_absent(n):
     """Lookup without the ref output and compaction without a batch (no byte total) give

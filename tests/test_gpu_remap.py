@@ -1,5 +1,5 @@
-"""GPU parity of the address-remap map (Sec. 4.3 weight sharing; Sec. 6 virtual memory
-map): after every update the statuses, counts and exported intervals equal the
+"""GPU parity of the address-remap map (Sec. 4.1.3, Weight Chunk Sharing; Appendix,
+Implementation Details, Virtual Memory Map): after every update the statuses, counts and exported intervals equal the
 oracle's bit for bit, and so does the translation of every probed address."""
 
 import numpy as np
@@ -120,7 +120,7 @@ def test_full_leaves_the_map_unchanged():
 
 
 def test_paper_two_chunks_in_one_allocation():
-    """Sec. 4.3: two chunks of one client allocation map into two server allocations."""
+    """Sec. 4.1.3: two chunks of one client allocation map into two server allocations."""
     say("remap paper case")
     va = (3 << 40) + 0x4000
     pos1, pos2 = 0x7F00_0000_0000, 0x7F80_0000_1000

@@ -1,4 +1,5 @@
-"""Pins for the oracle's address-remap interval map (Gleam Sec. 4.3 and Sec. 6).
+"""Pins for the oracle's address-remap interval map (Gleam Sec. 4.1.3, Weight Chunk Sharing;
+Appendix, Implementation Details, Virtual Memory Map).
 
 The map's rules are pinned against a brute force that keeps every interval as the
 Python set of the addresses it covers, on an address space small enough to check
@@ -93,7 +94,7 @@ def test_random_updates_match_brute_force(seed):
 
 
 def test_paper_two_chunks_in_one_allocation():
-    """Sec. 4.3's case: two chunks written into one client allocation find their
+    """Sec. 4.1.3's case: two chunks written into one client allocation find their
     shareable copies in two different server allocations."""
     task, base = 3, 0x4000
     va = (task << 40) + base
