@@ -216,6 +216,24 @@ gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t* d_keys, ui
                                 uint64_t* d_ref, void* d_ws, size_t ws_bytes, void* stream);
 
 /*
+ * gleam_cache_lookup without a workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, hosts that forbid allocation). The
+ * same outputs as gleam_cache_lookup; the batch-dedup scratch table lives in a
+ * library-owned device array of 16 MiB + 256 B per GPU (held until the process ends),
+ * so n is at most gleam_cache_lookup_noalloc_max_keys() = 2^20. The call allocates
+ * nothing (its first call on a device looks up that device's array address).
+ * Every call on one GPU shares that GPU's array: calls that overlap on one GPU (on
+ * different streams, or from different threads) race and their outputs are undefined;
+ * order them on one stream. Each call clears what it uses (a fill kernel).
+ *   d_keys, d_status, d_ref   as for gleam_cache_lookup
+ * Errors: GLEAM_E_INVALID (null table, keys or status), GLEAM_E_UNSUPPORTED (n above
+ * 2^20), GLEAM_E_HIP. n == 0 is a no-op.
+ */
+size_t gleam_cache_lookup_noalloc_max_keys(void);
+gleam_status gleam_cache_lookup_noalloc(const gleam_cache* c, const uint64_t* d_keys, uint64_t n, uint8_t* d_status,
+                                        uint64_t* d_ref, void* stream);
+
+/*
  * The blocks whose bytes must still cross the network (Sec. 4.1.2: on a miss the
  * full chunk is sent).
  *   d_status      device u8[n] (as written by gleam_cache_lookup)

@@ -46,6 +46,7 @@ EXPORTS = (
     "gleam_cache_export", "gleam_cache_set_key_bound", "gleam_send_plan", "gleam_pack_misses",
     "gleam_restore_blocks", "gleam_read_stream", "gleam_remap_bytes", "gleam_remap_create", "gleam_remap_destroy",
     "gleam_remap_update_bytes", "gleam_remap_update", "gleam_remap_translate", "gleam_remap_export",
+    "gleam_cache_lookup_noalloc", "gleam_cache_lookup_noalloc_max_keys",
 )
 
 
@@ -77,6 +78,8 @@ def _load() -> ctypes.CDLL:
         "gleam_workspace_bytes": ([u64], sz),
         "gleam_cache_insert": ([vp, vp, vp, u64, vp, vp, sz, vp], st),
         "gleam_cache_lookup": ([vp, vp, u64, vp, vp, vp, sz, vp], st),
+        "gleam_cache_lookup_noalloc": ([vp, vp, u64, vp, vp, vp], st),
+        "gleam_cache_lookup_noalloc_max_keys": ([], sz),
         "gleam_miss_compact": ([vp, u64, ctypes.POINTER(_Batch), vp, vp, vp, vp, sz, vp], st),
         "gleam_identify_weights": ([ctypes.POINTER(_Batch), vp, vp, u64, vp, vp, vp, vp, sz, vp], st),
         "gleam_md5_prefix": ([ctypes.POINTER(_Batch), u32, u64, vp, vp, vp, vp], st),
@@ -180,6 +183,10 @@ def _on_stream(stream, device):
 
 def _u64_device(a: np.ndarray, device) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint64).view(np.int64)).to(device)
+
+
+def lookup_noalloc_max_keys() -> int:
+    return int(lib.gleam_cache_lookup_noalloc_max_keys())
 
 
 def workspace_bytes(n: int) -> int:
@@ -333,6 +340,18 @@ class Cache:
             _dev(ws, "ws", _U8)
             _check(lib.gleam_cache_lookup(self.handle, _ptr(keys), n, _ptr(status), _ptr(ref), _ptr(ws),
                                           ws.numel(), hs))
+        return status[:n], (ref[:n] if ref is not None else None)
+
+    def lookup_noalloc(self, keys: torch.Tensor, status: torch.Tensor, ref: torch.Tensor | None = None,
+                       stream=None):
+        """lookup() with the library's own scratch instead of a workspace (at most
+        lookup_noalloc_max_keys() keys; calls on one GPU must not overlap). The caller
+        passes the outputs, so nothing is allocated."""
+        n = keys.numel()
+        _dev(keys, "keys", _U64)
+        _dev(status, "status", _U8, n)
+        _dev(ref, "ref", _U64, n, optional=True)
+        _check(lib.gleam_cache_lookup_noalloc(self.handle, _ptr(keys), n, _ptr(status), _ptr(ref), _stream(stream)))
         return status[:n], (ref[:n] if ref is not None else None)
 
     # -- lifecycle ------------------------------------------------------------------ #

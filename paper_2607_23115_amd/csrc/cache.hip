@@ -15,6 +15,7 @@
 // ever holds. So a key's first index takes a slot with one compare-and-swap, and
 // only later duplicates need an atomicMin.
 
+#include <mutex>
 #include <new>
 
 #include "gleam_device.h"
@@ -441,6 +442,95 @@ extern "C" gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t*
   st = clear_scratch(d_ws, L, s);
   if (st != GLEAM_OK) return st;
   const ScratchRef sc = scratch_ref(d_ws, L);
+  const TableRef t = table_ref(c);
+  hipLaunchKernelGGL(lookup_probe_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s, t, sc, d_keys, n, d_status, d_ref);
+  if ((st = launch_status("lookup_probe_kernel")) != GLEAM_OK) return st;
+  hipLaunchKernelGGL(lookup_resolve_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s, sc, d_keys, n, d_status,
+                     d_ref);
+  return launch_status("lookup_resolve_kernel");
+}
+
+// ---- Lookup without a caller workspace ----------------------------------------------
+// For callers that cannot allocate device memory (code under HIP graph capture, tight
+// serving loops, hosts that forbid allocation): the dedup scratch table lives in a
+// file-scope device array instead of a workspace. Every call on a GPU shares that GPU's
+// copy, so overlapping calls on one GPU race. The array's device address is looked up
+// once per device with hipGetSymbolAddress; the host-side symbol is not a device address.
+namespace gleam {
+namespace {
+
+constexpr uint64_t kNoAllocMaxKeys = 1ull << 20;
+constexpr uint64_t kNoAllocSlots = 2 * kNoAllocMaxKeys;  // the workspace layout's cap for that n
+constexpr size_t kNoAllocBytes = kHeaderBytes + kNoAllocSlots * 8;  // 16 MiB + 256 B
+
+static __device__ __align__(256) uint8_t scratch[kNoAllocBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of this device's scratch array (looked up on the first call).
+gleam_status noalloc_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    set_error("hipGetDevice: %s", hipGetErrorString(e));
+    return GLEAM_E_HIP;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    set_error("gleam_cache_lookup_noalloc: device %d beyond the %d this library tracks", dev, kMaxDevices);
+    return GLEAM_E_UNSUPPORTED;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      set_error("hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+      return GLEAM_E_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return GLEAM_OK;
+}
+
+}  // namespace
+}  // namespace gleam
+
+extern "C" size_t gleam_cache_lookup_noalloc_max_keys(void) { return (size_t)gleam::kNoAllocMaxKeys; }
+
+extern "C" gleam_status gleam_cache_lookup_noalloc(const gleam_cache* c, const uint64_t* d_keys, uint64_t n,
+                                                   uint8_t* d_status, uint64_t* d_ref, void* stream) {
+  using namespace gleam;
+  clear_error();
+  if (!c) {
+    set_error("gleam_cache_lookup_noalloc: null table");
+    return GLEAM_E_INVALID;
+  }
+  if (n == 0) return GLEAM_OK;
+  if (!d_keys || !d_status) {
+    set_error("gleam_cache_lookup_noalloc: null keys or status");
+    return GLEAM_E_INVALID;
+  }
+  if (n > kNoAllocMaxKeys) {
+    set_error("gleam_cache_lookup_noalloc: %llu keys, at most %llu without a workspace (use gleam_cache_lookup)",
+              (unsigned long long)n, (unsigned long long)kNoAllocMaxKeys);
+    return GLEAM_E_UNSUPPORTED;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (n <= kSmallKeys) {  // the one-workgroup path dedups in LDS: no scratch at all
+    hipLaunchKernelGGL(lookup_small_kernel, dim3(1), dim3(kSmallThreads), 0, s, table_ref(c), d_keys, n, d_status,
+                       d_ref);
+    return launch_status("lookup_small_kernel");
+  }
+  void* ws = nullptr;
+  gleam_status st = noalloc_scratch(&ws);
+  if (st != GLEAM_OK) return st;
+  const WsLayout L = ws_layout(n);  // scratch_cap <= kNoAllocSlots for n <= kNoAllocMaxKeys
+  st = clear_scratch(ws, L, s);
+  if (st != GLEAM_OK) return st;
+  const ScratchRef sc = scratch_ref(ws, L);
   const TableRef t = table_ref(c);
   hipLaunchKernelGGL(lookup_probe_kernel, dim3(blocks_for(n)), dim3(kThreads), 0, s, t, sc, d_keys, n, d_status, d_ref);
   if ((st = launch_status("lookup_probe_kernel")) != GLEAM_OK) return st;

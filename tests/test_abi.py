@@ -134,6 +134,9 @@ def test_cache_create_validation():
 
 def test_lookup_insert_compact_validation():
     assert g.lib.gleam_cache_lookup(None, 256, 4, 256, None, 256, 1 << 20, None) == g.E_INVALID
+    # the workspace-free lookup: a null table is refused before anything touches a device
+    assert g.lib.gleam_cache_lookup_noalloc(None, 256, 4, 256, None, None) == g.E_INVALID
+    assert g.lookup_noalloc_max_keys() == 1 << 20
     assert g.lib.gleam_cache_insert(None, 256, 256, 4, None, 256, 1 << 20, None) == g.E_INVALID
     # compaction: null count, workspace too small or unaligned, bytes without a batch
     assert g.lib.gleam_miss_compact(256, 10, None, 256, None, None, 256, 1 << 20, None) == g.E_INVALID
