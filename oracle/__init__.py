@@ -382,6 +382,103 @@ def identify_weights(recorded_digests, current_payloads, block_bytes: int, regio
     return block_match, first_diff, region_weight
 
 
+def identify_leaves(recorded_leaf_digests, current_payloads, block_bytes: int, region_first, threads: int = 1):
+    """identify_weights at leaf granularity (Sec. 4.1.1's consistency check, located to
+    the first 4 KiB leaf that changed). The recorded leaf digests are laid out as
+    batch_digests(with_leaves=True) gives them: u64[n_blocks, block/leaf], slots past a
+    short block's last leaf 0.
+
+    Returns (leaf_match u8[n_blocks * block/leaf]: 1 where the recorded and current slot
+    agree, slots without a leaf included; first_diff_leaf u64[S] = index within the
+    payload of its first changed leaf or 2^64-1; region_weight u8[R] as in
+    identify_weights)."""
+    rec = np.asarray(recorded_leaf_digests, dtype=np.uint64).reshape(-1)
+    _, cur = batch_digests(current_payloads, block_bytes, with_leaves=True, threads=threads)
+    cur = cur.reshape(-1)
+    if cur.size != rec.size:
+        raise ValueError("recorded leaf digests do not match the payloads' geometry")
+    leaf_match = (cur == rec).astype(np.uint8)
+    per = block_bytes // LEAF_BYTES
+    lens = [_as_u8(p).size for p in current_payloads]
+    blk_first, _ = geometry(lens, block_bytes)
+    first_diff = np.full(len(lens), NO_DIFF, dtype=np.uint64)
+    for s in range(len(lens)):
+        # slot order within a payload is leaf order: block-major, then leaf
+        bad = np.flatnonzero(leaf_match[int(blk_first[s]) * per:int(blk_first[s + 1]) * per] == 0)
+        if bad.size:
+            first_diff[s] = bad[0]
+    rf = np.asarray(region_first, dtype=np.uint64).reshape(-1)
+    region_weight = np.zeros(rf.size - 1, dtype=np.uint8)
+    for r in range(rf.size - 1):
+        segs = first_diff[int(rf[r]):int(rf[r + 1])]
+        region_weight[r] = 1 if segs.size and (segs == NO_DIFF).all() else 0
+    return leaf_match, first_diff, region_weight
+
+
+FW_OK, FW_TOO_MANY, FW_INVALID = 0, 1, 2
+_TOP64 = (1 << 64) - 1
+
+
+def first_write_pieces(addr, length, region_first, max_writes: int | None = None):
+    """Sec. 4.1.1: where an address range is written several times, only the first
+    host-to-device write counts. Writes are listed in time order; the writes of
+    allocation r are [region_first[r], region_first[r+1]). A write owns the bytes of
+    [addr, addr + len) that no earlier write of its allocation covers; a piece is a
+    maximal run of bytes owned by one write.
+
+    Returns (piece_write u64[P], piece_offset u64[P] (from the write's start),
+    piece_len u64[P], region_piece_first u64[R+1], region_status u8[R]), pieces ordered
+    by allocation, then write, then address. An allocation with a write reaching past
+    the top of the 64-bit address space (addr + len > 2^64 - 1) is refused
+    (FW_INVALID, no pieces); with max_writes given, so is one with more writes than
+    that (FW_TOO_MANY).
+    """
+    a = [int(x) for x in np.asarray(addr, dtype=np.uint64).reshape(-1)]
+    n = [int(x) for x in np.asarray(length, dtype=np.uint64).reshape(-1)]
+    rf = [int(x) for x in np.asarray(region_first, dtype=np.uint64).reshape(-1)]
+    pw, po, pl = [], [], []
+    first = [0]
+    status = []
+    for r in range(len(rf) - 1):
+        w0, w1 = rf[r], rf[r + 1]
+        if any(a[j] + n[j] > _TOP64 for j in range(w0, w1)):
+            status.append(FW_INVALID)
+            first.append(len(pw))
+            continue
+        if max_writes is not None and w1 - w0 > max_writes:
+            status.append(FW_TOO_MANY)
+            first.append(len(pw))
+            continue
+        covered = []  # the union of the earlier writes: sorted, disjoint [lo, hi)
+        for j in range(w0, w1):
+            lo, hi = a[j], a[j] + n[j]
+            if lo == hi:
+                continue
+            # the gaps of `covered` inside [lo, hi), in address order
+            at = lo
+            for c_lo, c_hi in covered:
+                if c_hi <= at or c_lo >= hi:
+                    continue
+                if c_lo > at:
+                    pw.append(j), po.append(at - lo), pl.append(c_lo - at)
+                at = max(at, c_hi)
+            if at < hi:
+                pw.append(j), po.append(at - lo), pl.append(hi - at)
+            # merge [lo, hi) into the union
+            merged = []
+            for c_lo, c_hi in covered:
+                if c_hi < lo or c_lo > hi:
+                    merged.append((c_lo, c_hi))
+                else:
+                    lo, hi = min(lo, c_lo), max(hi, c_hi)
+            merged.append((lo, hi))
+            covered = sorted(merged)
+        status.append(FW_OK)
+        first.append(len(pw))
+    u = lambda v: np.array(v, dtype=np.uint64)
+    return u(pw), u(po), u(pl), u(first), np.array(status, dtype=np.uint8)
+
+
 # --------------------------------------------------------------------------- #
 # The paper's identifier: MD5 of a payload's first 1024 bits (Appendix discussion)
 # --------------------------------------------------------------------------- #
