@@ -9,7 +9,8 @@ of the base weights; the payload perturbs 3 of the 32 layers with a rank-16 upda
 so 1,158 blocks miss and 11,759 hit. Values are synthetic N(0, 0.02) (no checkpoint).
 
 One step = gleam_fp_chunks -> gleam_cache_lookup -> gleam_miss_compact over the whole
-batch, inputs already resident in HBM. Prints ONE JSON line.
+batch, inputs already resident in HBM (for a batch that gleam_detect runs as one kernel,
+one gleam_detect call, which writes the same outputs). Prints ONE JSON line.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload decoder7b]
 """
@@ -31,7 +32,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD public specification
 PROFILE_PMC = {w: os.path.join(ROOT, "profiles", f"fp_kernel_{w}_pmc.txt") for w in ("decoder7b", "small_copies")}
-FP_SOURCE = os.path.join(ROOT, "paper_2607_23115_amd", "csrc", "fp_chunks.hip")
+FP_SOURCES = [os.path.join(ROOT, "paper_2607_23115_amd", "csrc", f) for f in ("fp_core.h", "fp_chunks.hip")]
 
 
 def log(*a):
@@ -76,8 +77,12 @@ def cpu_model() -> str:
 
 
 def source_digest() -> str:
-    with open(FP_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """sha256 prefix of the fingerprint kernel's sources (fp_core.h, then fp_chunks.hip)."""
+    h = hashlib.sha256()
+    for path in FP_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def pmc_traffic(workload: str):
@@ -94,7 +99,7 @@ def pmc_traffic(workload: str):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip()
     try:
-        if kv.get("fp_chunks.hip sha256 prefix") != source_digest():
+        if kv.get("fingerprint source sha256 prefix") != source_digest():
             return None
         fetch = float(kv["fp FETCH_SIZE KiB per dispatch"]) * 1024 * float(kv["copy fetch scale"])
         write = float(kv["fp WRITE_SIZE KiB per dispatch"]) * 1024 * float(kv["copy write scale"])
@@ -318,9 +323,24 @@ def lifecycle_path(args, g, torch):
         table.touch(keys, epochs=epochs)
         torch.cuda.synchronize()
 
-    ev_ms, ex_ms = [], []
+    # erase of 1,000 present keys (cost follows the keys, not the 2^25 slots); they are
+    # put back (untimed, with their stamps) before export and eviction
+    pick = torch.randperm(n, generator=torch.Generator().manual_seed(6))[:1000].to("cuda")
+    er_keys, er_vals, er_ep = keys[pick].contiguous(), vals[pick].contiguous(), epochs[pick].contiguous()
+    er_ws = torch.empty(int(g.lib.gleam_cache_erase_bytes(1000)), dtype=torch.uint8, device="cuda")
+    ev_ms, ex_ms, er_ms = [], [], []
     for step in range(args.warmup + args.steps):
         restore()
+        e1, e2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e1.record()
+        er_counts = table.erase(er_keys, ws=er_ws)
+        e2.record()
+        torch.cuda.synchronize()
+        if [int(x) for x in g.as_u64(er_counts)] != [1000, n - 1000]:
+            raise SystemExit(f"erase counts wrong: {g.as_u64(er_counts)}")
+        table.set_key_bound(n - 1000)
+        table.insert(er_keys, er_vals, ws=ins_ws)
+        table.touch(er_keys, epochs=er_ep)
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         table.export(ws=ws)
@@ -334,6 +354,7 @@ def lifecycle_path(args, g, torch):
         if step >= args.warmup:
             ex_ms.append(a.elapsed_time(b))
             ev_ms.append(c.elapsed_time(d))
+            er_ms.append(e1.elapsed_time(e2))
     cnt = g.as_u64(counts)
     if int(cnt[0]) != n - n // 2 or int(cnt[1]) != n // 2:
         raise SystemExit(f"eviction counts wrong: {cnt}")
@@ -356,7 +377,9 @@ def lifecycle_path(args, g, torch):
            "vs_baseline": None, "dtype": "u64", "data": "synthetic",
            "config": {"workload": "20M random digests in 2^25 slots, random stamps, keep the 10M most recent",
                       "entries": n, "capacity": cap, "evict_ms": round(ev, 3), "export_ms": round(ex, 3),
-                      "export_M_entries_per_s": round(n / (ex * 1e-3) / 1e6, 1)},
+                      "export_M_entries_per_s": round(n / (ex * 1e-3) / 1e6, 1),
+                      "erase_1000_ms": {"median": round(float(np.median(er_ms)), 4), "min": round(min(er_ms), 4),
+                                        "max": round(max(er_ms), 4)}},
            "cpu_baseline": cpu}
     print(json.dumps(out), flush=True)
 
@@ -555,49 +578,82 @@ WORKLOADS = {"decoder7b": build_decoder7b, "random16": build_random16, "small_co
              "resnet50": build_resnet50, "large_bf16": build_large_bf16}
 
 
+def one_kernel_detect(batch) -> bool:
+    """Whether gleam_detect runs this batch as one kernel (blocks of at most 64 KiB, at
+    most 65,536 leaf slots and 4,096 blocks, as the library decides)."""
+    lpb = batch.block_bytes // 4096
+    return batch.n_blocks > 0 and lpb <= 16 and batch.n_blocks * lpb <= 65536 and batch.n_blocks <= 4096
+
+
 def per_buffer_leg(g, torch, batch, table, count, keep):
-    """The first `count` payloads, each as its own fingerprint -> lookup -> compaction
-    (descriptors, outputs and workspaces prepared before timing), against the same
-    payloads as one batched pass."""
+    """The first `count` payloads, each as its own call, against the same payloads as
+    one batched call. Every call's descriptors, outputs, workspace and ctypes arguments
+    are prepared before timing, and the timed loop calls the C ABI directly, so the
+    figure is the library's per-call cost (host enqueue and GPU), not the binding's.
+    Two per-call forms: gleam_detect (one call; one kernel for such a payload) and the
+    three calls gleam_fp_chunks -> gleam_cache_lookup -> gleam_miss_compact."""
+    import ctypes
+    lib = g.lib
     src = payload_tensor(keep)
     base = src.data_ptr()
     addr = batch.d_addr.cpu().numpy().view(np.uint64)[:count]
     lens = batch.host_len[:count]
-    singles = []
-    for a, n in zip(addr.tolist(), lens.tolist()):
-        b = g.Batch.from_arena(src, [a - base], [n], batch.block_bytes)
-        m = max(b.n_blocks, 1)
-        singles.append((b, torch.empty(m, dtype=torch.int64, device="cuda"),
-                        torch.empty(m, dtype=torch.uint8, device="cuda"), torch.empty(m, dtype=torch.int64, device="cuda"),
-                        torch.empty(m, dtype=torch.int64, device="cuda"), torch.zeros(2, dtype=torch.int64, device="cuda"),
-                        g.workspace(m)))
-    joint = g.Batch.from_arena(src, (addr - np.uint64(base)).astype(np.uint64), lens, batch.block_bytes)
-    nj = joint.n_blocks
-    jo = (torch.empty(nj, dtype=torch.int64, device="cuda"), torch.empty(nj, dtype=torch.uint8, device="cuda"),
-          torch.empty(nj, dtype=torch.int64, device="cuda"), torch.empty(nj, dtype=torch.int64, device="cuda"),
-          torch.zeros(2, dtype=torch.int64, device="cuda"), g.workspace(nj))
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    vp = ctypes.c_void_p
 
-    def one(b, d, st, ref, idx, cnt, ws):
-        g.fp_chunks(b, out=d)
-        table.lookup(d[:b.n_blocks], status=st, ref=ref, ws=ws)
-        g.miss_compact(st[:b.n_blocks], b, miss_idx=idx, counters=cnt, ws=ws)
+    def prepare(b):
+        o = g.Detect(b)
+        cb = ctypes.byref(b.c_struct())
+        n = b.n_blocks
+        det = (cb, table.handle, vp(o.digests.data_ptr()), vp(o.status.data_ptr()), vp(o.ref.data_ptr()),
+               vp(o.miss_idx.data_ptr()), vp(o.counters.data_ptr()), vp(o.counters.data_ptr() + 8),
+               vp(o.ws.data_ptr()), o.ws.numel(), stream)
+        fp = (cb, vp(o.digests.data_ptr()), None, stream)
+        lk = (table.handle, vp(o.digests.data_ptr()), n, vp(o.status.data_ptr()), vp(o.ref.data_ptr()),
+              vp(o.ws.data_ptr()), o.ws.numel(), stream)
+        cp = (vp(o.status.data_ptr()), n, cb, vp(o.miss_idx.data_ptr()), vp(o.counters.data_ptr()),
+              vp(o.counters.data_ptr() + 8), vp(o.ws.data_ptr()), o.ws.numel(), stream)
+        return b, o, det, fp, lk, cp
+
+    singles = [prepare(g.Batch.from_arena(src, [a - base], [n], batch.block_bytes))
+               for a, n in zip(addr.tolist(), lens.tolist())]
+    joint = prepare(g.Batch.from_arena(src, (addr - np.uint64(base)).astype(np.uint64), lens, batch.block_bytes))
+
+    def detect_call(x):
+        if lib.gleam_detect(*x[2]) != 0:
+            raise SystemExit(lib.gleam_last_error().decode())
+
+    def three_calls(x):
+        if lib.gleam_fp_chunks(*x[3]) or lib.gleam_cache_lookup(*x[4]) or lib.gleam_miss_compact(*x[5]):
+            raise SystemExit(lib.gleam_last_error().decode())
 
     def timed(fn):
         fn()
         torch.cuda.synchronize()
         a, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
         a.record()
         fn()
         e.record()
+        host = time.perf_counter() - t0
         torch.cuda.synchronize()
-        return a.elapsed_time(e)
+        return a.elapsed_time(e), host * 1e3
 
-    ms_each = timed(lambda: [one(*x) for x in singles])
-    ms_joint = timed(lambda: one(joint, *jo))
+    ms_det, host_det = timed(lambda: [detect_call(x) for x in singles])
+    ms_three, host_three = timed(lambda: [three_calls(x) for x in singles])
+    ms_joint, _ = timed(lambda: detect_call(joint))
+    # each separate call's digests equal the batched call's for its payload
+    nb = [x[0].n_blocks for x in singles]
+    if not torch.equal(torch.cat([x[1].digests[:m] for x, m in zip(singles, nb)]),
+                       joint[1].digests[:joint[0].n_blocks]):
+        raise SystemExit("per-buffer digests differ from the batched call's")
     nbytes = int(lens.sum())
-    return {"buffers": count, "bytes": nbytes, "separate_ms": round(ms_each, 4),
-            "separate_us_per_buffer": round(ms_each * 1e3 / count, 2),
-            "separate_gbs": round(nbytes / (ms_each * 1e-3) / 1e9, 2), "batched_ms": round(ms_joint, 4),
+    return {"buffers": count, "bytes": nbytes,
+            "detect_ms": round(ms_det, 4), "detect_us_per_buffer": round(ms_det * 1e3 / count, 2),
+            "detect_host_us_per_buffer": round(host_det * 1e3 / count, 2),
+            "three_calls_ms": round(ms_three, 4), "three_calls_us_per_buffer": round(ms_three * 1e3 / count, 2),
+            "three_calls_host_us_per_buffer": round(host_three * 1e3 / count, 2),
+            "separate_gbs": round(nbytes / (ms_det * 1e-3) / 1e9, 2), "batched_ms": round(ms_joint, 4),
             "batched_gbs": round(nbytes / (ms_joint * 1e-3) / 1e9, 2)}
 
 
@@ -742,6 +798,11 @@ def main():
     ap.add_argument("--pipeline", action="store_true",
                     help="detect path: overlap each batch's lookup and compaction (second stream) with the "
                          "next batch's fingerprint (double-buffered digests); every step still does all its work")
+    ap.add_argument("--call", default="auto", choices=["auto", "detect", "three"],
+                    help="detect path: how a step is issued. detect: one gleam_detect call; three: "
+                         "gleam_fp_chunks, gleam_cache_lookup, gleam_miss_compact; auto (default): "
+                         "gleam_detect where it runs as one kernel, else the three calls (the kernels "
+                         "gleam_detect would launch), so the fingerprint kernel can be timed on its own")
     ap.add_argument("--graph", action="store_true",
                     help="detect path: capture one step in a HIP graph and time K replays (cuts launch "
                          "overhead on small batches); the fp launch time then comes from an eager leg")
@@ -792,8 +853,19 @@ def main():
     miss_idx = torch.empty(n, dtype=torch.int64, device=dev)
     counters = torch.zeros(2, dtype=torch.int64, device=dev)
     ws = g.workspace(n, dev)
+    use_detect = args.call == "detect" or (args.call == "auto" and one_kernel_detect(batch))
+    det = g.Detect(batch)  # its own (prepared) workspace
+    det.digests, det.status, det.ref, det.miss_idx, det.counters = digests, status, ref, miss_idx, counters
+    timed_kernel = ("detect_small_kernel" if one_kernel_detect(batch) else "fp_kernel") if use_detect else "fp_kernel"
 
     def step(ev_a=None, ev_b=None):
+        if use_detect:  # events around the whole call (one kernel after a counter fill)
+            if ev_a is not None:
+                ev_a.record()
+            g.detect(batch, table, out=det)
+            if ev_b is not None:
+                ev_b.record()
+            return
         if ev_a is not None:
             ev_a.record()
         g.fp_chunks(batch, out=digests)
@@ -841,9 +913,12 @@ def main():
         c = g.as_u64(counters)
         if int(c[0]) != expect_miss:
             raise SystemExit(f"graph replay broke the planted truth: {int(c[0])} misses")
-        for a, b in ev_fp:  # eager fp launches for the kernel's own time
+        for a, b in ev_fp:  # eager launches for the kernel's own time
             a.record()
-            g.fp_chunks(batch, out=digests)
+            if use_detect:
+                g.detect(batch, table, out=det)
+            else:
+                g.fp_chunks(batch, out=digests)
             b.record()
         torch.cuda.synchronize()
     fp_ms = [a.elapsed_time(b) for a, b in ev_fp]
@@ -901,7 +976,7 @@ def main():
 
     algo_bytes = payload_bytes + 8 * n + 24 * batch.n_seg + 8 * (batch.n_seg + 1)
     achieved = algo_bytes / (fp_avg_ms * 1e-3) / 1e9
-    traffic = pmc_traffic(args.workload)
+    traffic = pmc_traffic(args.workload) if timed_kernel == "fp_kernel" else None
     log(f"{desc}: {n} blocks, {miss_count} misses ({miss_bytes} bytes), fp {fp_avg_ms:.3f} ms "
         f"(min {min(fp_ms):.3f}, max {max(fp_ms):.3f}), step {ms_per_step:.3f} ms, cold {cold}, "
         f"read ceiling {read_gbs:.0f} GB/s")
@@ -934,13 +1009,14 @@ def main():
                    "block_bytes": batch.block_bytes, "leaf_bytes": 4096, "misses": miss_count,
                    "miss_bytes": miss_bytes, "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
                    "launch": "hip_graph" if graph is not None else "eager",
+                   "call": "gleam_detect" if use_detect else "gleam_fp_chunks + gleam_cache_lookup + gleam_miss_compact",
                    "step_ms": {"median": round(float(np.median(warm_ms)), 4), "min": round(min(warm_ms), 4),
                                "max": round(max(warm_ms), 4)},
                    "cold": cold, "insert_ms": insert_ms, "pipelined": pipe, "per_buffer": per_buffer,
                    "truth": {"expected_misses": expect_miss, "misses": miss_count, "ok": True,
                              "check": "MISS count after the warm-up and after the timed steps equals the "
                                       "workload's planted truth; bit-exact parity is in tests/"}},
-        "roofline": {"bound": "hbm", "kernel": "fp_kernel", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "kernel": timed_kernel, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes": algo_bytes, "avg_launch_ms": round(fp_avg_ms, 4),
                      "measured_read_gbs": round(read_gbs, 1), "frac_of_measured": round(achieved / read_gbs, 4)},

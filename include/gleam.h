@@ -15,11 +15,14 @@
  *   gleam_cache_lookup  -- probe the resident identifier table; detect blocks
  *                          repeated inside the batch
  *   gleam_miss_compact  -- list the blocks whose bytes must still travel
+ *   gleam_detect        -- the three above in one call (one launch for a small batch)
  *   gleam_cache_insert  -- add identifiers to the table
  *   gleam_cache_touch / _evict / _erase / _export -- the table's lifecycle: last-use
  *                          stamps, LRU eviction, removal, the identifier set (4.1.3)
  *   gleam_identify_weights -- at free time, decide which allocations still hold
  *                          exactly what was written to them (Sec. 4.1.1)
+ *   gleam_identify_leaves  -- the same, located to the first changed 4 KiB leaf
+ *   gleam_first_writes  -- the first-write rule: the bytes each recorded write owns
  *   gleam_md5_prefix    -- the paper's own identifier (MD5 of a payload's first
  *                          1024 bits), as an ablation
  *   gleam_send_plan / gleam_pack_misses / gleam_restore_blocks -- the transfer
@@ -46,11 +49,11 @@
  *     error a negative status is returned and nothing has been enqueued. A HIP
  *     launch failure returns GLEAM_E_HIP; gleam_last_error() then holds the HIP
  *     message (thread-local).
- *   - HIP graph capture: every call except gleam_cache_evict, _erase, _export and
+ *   - HIP graph capture: every call except gleam_cache_evict, _export and
  *     gleam_remap_update enqueues kernel launches only (clears are fill kernels, not
  *     memsets), so a caller may capture it in a graph and replay it.
  *     gleam_cache_insert's host-side key bound grows once, when the call is captured,
- *     not on each replay. The four exceptions sort or scan with rocPRIM, which also
+ *     not on each replay. The three exceptions sort or scan with rocPRIM, which also
  *     enqueues memsets; keep them out of captured graphs.
  *   - Device descriptor contents (seg_addr, seg_len, blk_first) are not read on
  *     the host. The caller guarantees they describe the batch. Whatever they hold,
@@ -252,12 +255,47 @@ gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam
                                 void* stream);
 
 /*
+ * The whole decision for one batch in one call (Sec. 4.1.2: a chunk whose identifier the
+ * server holds sends only its hash and size; any other chunk sends its bytes). Writes
+ * exactly what gleam_fp_chunks, then gleam_cache_lookup, then gleam_miss_compact (with
+ * the batch, when d_miss_bytes is given) write, in one call:
+ *   b, c                  the batch and the table (only read)
+ *   d_digest              device u64[n_blocks]: block digests
+ *   d_status, d_ref       device u8[n_blocks] and nullable u64[n_blocks]: as for
+ *                         gleam_cache_lookup
+ *   d_miss_idx, d_miss_count, d_miss_bytes   as for gleam_miss_compact (d_miss_bytes
+ *                         nullable)
+ *   d_ws, ws_bytes        device workspace, 256-byte aligned,
+ *                         >= gleam_workspace_bytes(n_blocks), PREPARED: unlike the other
+ *                         calls' workspaces, it carries one word from call to call (an
+ *                         arrival counter at byte 128), which gleam_detect_ws_init sets
+ *                         and every gleam_detect call leaves set. Prepare a workspace once
+ *                         after allocating it, and again after any other use of its
+ *                         memory; calls that may overlap need separate workspaces.
+ * A small batch (blocks of at most 64 KiB, at most 65,536 leaf slots and 4,096 blocks:
+ * the latency-bound case, e.g. one copy of a few MB) runs as ONE kernel: every workgroup
+ * digests its leaves and arrives at the counter, and the last to arrive does the lookup
+ * and the compaction. A larger batch runs the three calls' kernels in order. Enqueues
+ * kernel launches only (graph-capturable). If the one-kernel path finds the workspace
+ * unprepared, it writes UINT64_MAX to *d_miss_count (and no statuses).
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED, GLEAM_E_HIP. An empty
+ * batch still sets the miss count (and bytes) to 0.
+ *
+ * gleam_detect_ws_init: prepare d_ws (device, 256-byte aligned, >= 256 bytes) for
+ * gleam_detect (one small kernel on `stream`). Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
+ */
+gleam_status gleam_detect(const gleam_batch* b, const gleam_cache* c, uint64_t* d_digest, uint8_t* d_status,
+                          uint64_t* d_ref, uint64_t* d_miss_idx, uint64_t* d_miss_count, uint64_t* d_miss_bytes,
+                          void* d_ws, size_t ws_bytes, void* stream);
+gleam_status gleam_detect_ws_init(void* d_ws, size_t ws_bytes, void* stream);
+
+/*
  * Table lifecycle (Sec. 4.1.3: identified weight chunks stay in a shared cache across
  * tasks and LRU eviction keeps it bounded; Sec. 4.1.2: at connect time the server sends
  * the identifiers it holds). Every entry has a last-use stamp (0 when inserted). These
  * calls must not overlap, on any stream, with other calls on the same table.
  *
- * gleam_cache_maint_bytes: device workspace bytes for evict, erase and export of this
+ * gleam_cache_maint_bytes: device workspace bytes for evict and export of this
  * table (0 for NULL, a table above 2^31 slots, or when the radix sort's storage query
  * fails; evict, erase and export then return GLEAM_E_HIP).
  *
@@ -271,8 +309,13 @@ gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam
  * (device u64[2]) receives {removed, live after}. The host key bound drops to `keep`.
  *
  * gleam_cache_erase: remove the given keys (device u64[n]) that are present; d_counts
- * (device u64[2]) receives {removed, live after}. The host bound is unchanged; lower
- * it with gleam_cache_set_key_bound once the live count has been read back.
+ * (device u64[2]) receives {removed, live after}. The cost follows the keys erased, not
+ * the capacity: each erased key's cluster (the run of occupied slots around it) is
+ * repaired in place, no tombstones remain, and the call enqueues kernels only (it may be
+ * captured in a graph). Its workspace: device, 256-byte aligned,
+ * >= gleam_cache_erase_bytes(n) (O(n); 0 for n above 2^36). The host bound is
+ * unchanged; lower it with gleam_cache_set_key_bound once the live count has been read
+ * back.
  *
  * gleam_cache_export: every entry sorted by key into device u64[capacity + 1] arrays
  * d_keys, d_vals and (nullable) d_stamps; *d_count (device u64[1]) = entries written.
@@ -282,15 +325,15 @@ gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam
  * gleam_cache_set_key_bound: lower the host key bound to n (a live count read back
  * from d_counts); raising it is refused.
  *
- * Workspace (evict, erase, export): device, 256-byte aligned,
- * >= gleam_cache_maint_bytes(c). Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE,
- * GLEAM_E_UNSUPPORTED, GLEAM_E_HIP.
+ * Workspace (evict, export): device, 256-byte aligned, >= gleam_cache_maint_bytes(c).
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED, GLEAM_E_HIP.
  */
 size_t gleam_cache_maint_bytes(const gleam_cache* c);
 gleam_status gleam_cache_touch(gleam_cache* c, const uint64_t* d_keys, uint64_t n, const uint64_t* d_epochs,
                                uint64_t epoch, uint64_t* d_n_touched, void* stream);
 gleam_status gleam_cache_evict(gleam_cache* c, uint64_t keep, uint64_t* d_evicted, uint64_t* d_counts, void* d_ws,
                                size_t ws_bytes, void* stream);
+size_t gleam_cache_erase_bytes(uint64_t n);
 gleam_status gleam_cache_erase(gleam_cache* c, const uint64_t* d_keys, uint64_t n, uint64_t* d_counts, void* d_ws,
                                size_t ws_bytes, void* stream);
 gleam_status gleam_cache_export(const gleam_cache* c, uint64_t* d_keys, uint64_t* d_vals, uint64_t* d_stamps,
@@ -322,6 +365,68 @@ gleam_status gleam_identify_weights(const gleam_batch* b, const uint64_t* d_reco
                                     const uint64_t* d_region_first, uint64_t n_regions,
                                     uint8_t* d_block_match, uint64_t* d_seg_first_diff,
                                     uint8_t* d_region_weight, void* d_ws, size_t ws_bytes, void* stream);
+
+/*
+ * gleam_identify_weights located to the leaf: the first changed 4 KiB leaf of each
+ * payload (Sec. 4.1.1's consistency check compares every recorded chunk byte with the
+ * current data; a leaf digest narrows a mismatch to 4 KiB).
+ *   b                  as for gleam_identify_weights
+ *   d_recorded_leaf    device u64[n_blocks * block_bytes/4096]: the leaf digests recorded
+ *                      at write time, as gleam_fp_chunks writes them (block-major, 0 in
+ *                      the slots past a short block's last leaf)
+ *   d_region_first     as for gleam_identify_weights
+ *   d_leaf_match       nullable device u8[n_blocks * block_bytes/4096]: 1 where the slot's
+ *                      recorded and current digests agree (slots without a leaf read 1)
+ *   d_seg_first_diff   nullable device u64[n_seg]: index, within its payload, of the first
+ *                      changed leaf (leaf k of block j is j * block_bytes/4096 + k);
+ *                      UINT64_MAX if none
+ *   d_region_weight    device u8[n_regions]: as for gleam_identify_weights (the verdicts
+ *                      agree: a block changed iff one of its leaves did)
+ *   d_ws, ws_bytes     device workspace, 256-byte aligned,
+ *                      >= gleam_workspace_bytes(n_blocks * block_bytes/4096 + n_seg)
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED, GLEAM_E_HIP.
+ */
+gleam_status gleam_identify_leaves(const gleam_batch* b, const uint64_t* d_recorded_leaf,
+                                   const uint64_t* d_region_first, uint64_t n_regions, uint8_t* d_leaf_match,
+                                   uint64_t* d_seg_first_diff, uint8_t* d_region_weight, void* d_ws,
+                                   size_t ws_bytes, void* stream);
+
+/*
+ * The first-write rule of weight identification (Sec. 4.1.1: where an address range is
+ * overwritten, only the first host-to-device write counts). The recorded writes are
+ * listed in time order, grouped by allocation: the writes of allocation r are
+ * [region_first[r], region_first[r+1]). A write owns the bytes of [addr, addr + len)
+ * that no earlier write of its allocation covers; a piece is a maximal run of bytes one
+ * write owns. Digesting each write's pieces from its payload when it lands (gleam_fp_chunks
+ * over a batch of the pieces at the payload: payload + offset) and the same pieces of the
+ * allocation at free time (the pieces at addr + offset), then gleam_identify_weights over
+ * the pieces with region_first = region_piece_first, checks every written byte against
+ * its first writer's byte.
+ *   d_addr, d_len        device u64[n_writes]: destination address and bytes of each write
+ *   d_region_first       device u64[n_regions+1]: non-decreasing, from 0 to n_writes
+ *   d_piece_write        device u64[2 * n_writes] output: the write owning piece p
+ *   d_piece_offset       device u64[2 * n_writes] output: its start minus the write's addr
+ *   d_piece_len          device u64[2 * n_writes] output: its bytes
+ *                        (pieces in order of allocation, write, then address; at most
+ *                        2 * n_writes - 1 of them)
+ *   d_region_piece_first device u64[n_regions+1] output: allocation r's pieces are
+ *                        [region_piece_first[r], region_piece_first[r+1]); the last entry
+ *                        is the piece count
+ *   d_region_status      nullable device u8[n_regions] output: GLEAM_FW_OK;
+ *                        GLEAM_FW_TOO_MANY (more than 2048 writes: no pieces);
+ *                        GLEAM_FW_INVALID (a write past the top of the address space, or
+ *                        a malformed region_first: no pieces)
+ *   d_ws, ws_bytes       device workspace, 256-byte aligned, >=
+ *                        gleam_first_writes_ws_bytes(n_writes, n_regions)
+ * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED (more than 2^36 writes or
+ * 2^31 allocations), GLEAM_E_HIP. gleam_first_writes_ws_bytes returns 0 beyond those.
+ */
+enum { GLEAM_FW_OK = 0, GLEAM_FW_TOO_MANY = 1, GLEAM_FW_INVALID = 2 };
+size_t gleam_first_writes_ws_bytes(uint64_t n_writes, uint64_t n_regions);
+gleam_status gleam_first_writes(const uint64_t* d_addr, const uint64_t* d_len, uint64_t n_writes,
+                                const uint64_t* d_region_first, uint64_t n_regions, uint64_t* d_piece_write,
+                                uint64_t* d_piece_offset, uint64_t* d_piece_len, uint64_t* d_region_piece_first,
+                                uint8_t* d_region_status, void* d_ws, size_t ws_bytes, void* stream);
 
 /*
  * The paper's own identifier (Appendix, discussion of hash cost and collisions): an MD5

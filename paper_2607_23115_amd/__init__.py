@@ -33,6 +33,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libgleam.so")
 
 OK, E_INVALID, E_CAPACITY, E_WORKSPACE, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+FW_OK, FW_TOO_MANY, FW_INVALID = 0, 1, 2
 MISS, HIT_CACHE, HIT_BATCH = 0, 1, 2
 REMAP_ADDED, REMAP_INVALID, REMAP_OVERLAP, REMAP_FULL = 0, 1, 2, 3
 UNMAPPED = (1 << 64) - 1
@@ -46,7 +47,9 @@ EXPORTS = (
     "gleam_cache_export", "gleam_cache_set_key_bound", "gleam_send_plan", "gleam_pack_misses",
     "gleam_restore_blocks", "gleam_read_stream", "gleam_remap_bytes", "gleam_remap_create", "gleam_remap_destroy",
     "gleam_remap_update_bytes", "gleam_remap_update", "gleam_remap_translate", "gleam_remap_export",
-    "gleam_cache_lookup_noalloc", "gleam_cache_lookup_noalloc_max_keys",
+    "gleam_cache_lookup_noalloc", "gleam_cache_lookup_noalloc_max_keys", "gleam_detect",
+    "gleam_detect_ws_init", "gleam_identify_leaves", "gleam_first_writes_ws_bytes", "gleam_first_writes",
+    "gleam_cache_erase_bytes",
 )
 
 
@@ -79,6 +82,11 @@ def _load() -> ctypes.CDLL:
         "gleam_cache_insert": ([vp, vp, vp, u64, vp, vp, sz, vp], st),
         "gleam_cache_lookup": ([vp, vp, u64, vp, vp, vp, sz, vp], st),
         "gleam_cache_lookup_noalloc": ([vp, vp, u64, vp, vp, vp], st),
+        "gleam_detect": ([ctypes.POINTER(_Batch), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], st),
+        "gleam_detect_ws_init": ([vp, sz, vp], st),
+        "gleam_identify_leaves": ([ctypes.POINTER(_Batch), vp, vp, u64, vp, vp, vp, vp, sz, vp], st),
+        "gleam_first_writes_ws_bytes": ([u64, u64], sz),
+        "gleam_first_writes": ([vp, vp, u64, vp, u64, vp, vp, vp, vp, vp, vp, sz, vp], st),
         "gleam_cache_lookup_noalloc_max_keys": ([], sz),
         "gleam_miss_compact": ([vp, u64, ctypes.POINTER(_Batch), vp, vp, vp, vp, sz, vp], st),
         "gleam_identify_weights": ([ctypes.POINTER(_Batch), vp, vp, u64, vp, vp, vp, vp, sz, vp], st),
@@ -87,6 +95,7 @@ def _load() -> ctypes.CDLL:
         "gleam_cache_touch": ([vp, vp, u64, vp, u64, vp, vp], st),
         "gleam_cache_evict": ([vp, u64, vp, vp, vp, sz, vp], st),
         "gleam_cache_erase": ([vp, vp, u64, vp, vp, sz, vp], st),
+        "gleam_cache_erase_bytes": ([u64], sz),
         "gleam_cache_export": ([vp, vp, vp, vp, vp, vp, sz, vp], st),
         "gleam_cache_set_key_bound": ([vp, u64], st),
         "gleam_send_plan": ([ctypes.POINTER(_Batch), vp, vp, vp, vp, vp, vp, sz, vp], st),
@@ -383,10 +392,15 @@ class Cache:
         return evicted, counts
 
     def erase(self, keys: torch.Tensor, ws: torch.Tensor | None = None, stream=None):
+        """Remove the given keys that are present: counts int64[2] = {removed, live after}."""
         _dev(keys, "keys", _U64)
         dev = self.storage.device
         with _on_stream(stream, dev) as hs:
-            ws = self.maint_workspace() if ws is None else ws
+            if ws is None:
+                nb = int(lib.gleam_cache_erase_bytes(keys.numel()))
+                if nb == 0:
+                    raise GleamError(E_UNSUPPORTED, "too many keys to erase at once")
+                ws = torch.empty(nb, dtype=torch.uint8, device=dev)
             counts = torch.empty(2, dtype=torch.int64, device=dev)
             _dev(ws, "ws", _U8)
             _check(lib.gleam_cache_erase(self.handle, _ptr(keys), keys.numel(), _ptr(counts), _ptr(ws), ws.numel(),
@@ -543,6 +557,45 @@ def miss_compact(status: torch.Tensor, batch: Batch | None = None, miss_idx: tor
     return miss_idx, counters
 
 
+class Detect:
+    """Outputs of detect calls on one batch (device tensors): digests, status, ref (or
+    None), miss_idx and counters = [miss_count, miss_bytes], plus the calls' workspace,
+    prepared once here with gleam_detect_ws_init (on `stream`)."""
+
+    def __init__(self, batch: Batch, want_ref: bool = True, device=None, stream=None):
+        dev = batch.d_first.device if device is None else device
+        n = max(batch.n_blocks, 1)
+        with _on_stream(stream, dev) as hs:
+            self.digests = torch.empty(n, dtype=torch.int64, device=dev)
+            self.status = torch.empty(n, dtype=torch.uint8, device=dev)
+            self.ref = torch.empty(n, dtype=torch.int64, device=dev) if want_ref else None
+            self.miss_idx = torch.empty(n, dtype=torch.int64, device=dev)
+            self.counters = torch.empty(2, dtype=torch.int64, device=dev)
+            self.ws = workspace(batch.n_blocks, dev)
+            _check(lib.gleam_detect_ws_init(_ptr(self.ws), self.ws.numel(), hs))
+
+
+def detect(batch: Batch, table: Cache, out: Detect | None = None, want_ref: bool = True, stream=None) -> Detect:
+    """fp_chunks -> lookup -> miss_compact in one library call (one kernel for a small
+    batch). Pass `out` (a Detect made for this batch, or for a larger one) to reuse its
+    tensors and workspace; calls that may overlap need separate Detects."""
+    dev = batch.d_first.device
+    n = batch.n_blocks
+    with _on_stream(stream, dev) as hs:
+        if out is None:
+            out = Detect(batch, want_ref, dev)
+        _dev(out.digests, "digests", _U64, n)
+        _dev(out.status, "status", _U8, n)
+        _dev(out.ref, "ref", _U64, n, optional=True)
+        _dev(out.miss_idx, "miss_idx", _U64, n)
+        _dev(out.counters, "counters", _U64, 2)
+        _dev(out.ws, "ws", _U8)
+        _check(lib.gleam_detect(ctypes.byref(batch.c_struct()), table.handle, _ptr(out.digests), _ptr(out.status),
+                                _ptr(out.ref), _ptr(out.miss_idx), _ptr(out.counters),
+                                ctypes.c_void_p(out.counters.data_ptr() + 8), _ptr(out.ws), out.ws.numel(), hs))
+    return out
+
+
 def identify_weights(batch: Batch, recorded: torch.Tensor, region_first, ws: torch.Tensor | None = None,
                      stream=None):
     """Free-time weight identification: (block_match u8[n_blocks], first_diff int64[n_seg],
@@ -564,6 +617,57 @@ def identify_weights(batch: Batch, recorded: torch.Tensor, region_first, ws: tor
                                           _ptr(block_match), _ptr(first_diff), _ptr(region_weight), _ptr(ws),
                                           ws.numel(), hs))
     return block_match[:batch.n_blocks], first_diff[:batch.n_seg], region_weight[:n_regions]
+
+
+def identify_leaves(batch: Batch, recorded_leaves: torch.Tensor, region_first, ws: torch.Tensor | None = None,
+                    stream=None):
+    """identify_weights at leaf granularity: (leaf_match u8[n_blocks * LPB], first_diff_leaf
+    int64[n_seg], region_weight u8[n_regions]) on the device. `recorded_leaves` holds the
+    leaf digests fp_chunks(with_leaves=True) gave when the payloads were written."""
+    dev = batch.d_first.device
+    n_slots = batch.n_blocks * batch.leaves_per_block
+    _dev(recorded_leaves, "recorded_leaves", _U64, n_slots)
+    with _on_stream(stream, dev) as hs:
+        rf = region_first if isinstance(region_first, torch.Tensor) else _u64_device(np.asarray(region_first), dev)
+        n_regions = rf.numel() - 1
+        leaf_match = torch.empty(max(n_slots, 1), dtype=torch.uint8, device=dev)
+        first_diff = torch.empty(max(batch.n_seg, 1), dtype=torch.int64, device=dev)
+        region_weight = torch.empty(max(n_regions, 1), dtype=torch.uint8, device=dev)
+        if ws is None:
+            ws = workspace(n_slots + batch.n_seg, dev)
+        _dev(rf, "region_first", _U64, 1)
+        _dev(ws, "ws", _U8)
+        _check(lib.gleam_identify_leaves(ctypes.byref(batch.c_struct()), _ptr(recorded_leaves), _ptr(rf), n_regions,
+                                         _ptr(leaf_match), _ptr(first_diff), _ptr(region_weight), _ptr(ws),
+                                         ws.numel(), hs))
+    return leaf_match[:n_slots], first_diff[:batch.n_seg], region_weight[:n_regions]
+
+
+def first_writes(addr, length, region_first, stream=None, device="cuda"):
+    """The first-write rule over recorded writes (time order, grouped by allocation):
+    (piece_write, piece_offset, piece_len, region_piece_first, region_status) device
+    tensors; the first region_piece_first[-1] pieces are valid."""
+    with _on_stream(stream, torch.device(device)) as hs:
+        d = [t if isinstance(t, torch.Tensor) else _u64_device(np.asarray(t), device)
+             for t in (addr, length, region_first)]
+        n, n_regions = d[0].numel(), d[2].numel() - 1
+        if d[1].numel() != n:
+            raise ValueError("addr and length differ in length")
+        for t, name in zip(d, ("addr", "length", "region_first")):
+            _dev(t, name, _U64)
+        cap = max(2 * n, 1)
+        pw = torch.empty(cap, dtype=torch.int64, device=device)
+        po = torch.empty(cap, dtype=torch.int64, device=device)
+        pl = torch.empty(cap, dtype=torch.int64, device=device)
+        first = torch.empty(n_regions + 1, dtype=torch.int64, device=device)
+        status = torch.empty(max(n_regions, 1), dtype=torch.uint8, device=device)
+        nb = int(lib.gleam_first_writes_ws_bytes(n, n_regions))
+        if nb == 0:
+            raise GleamError(E_UNSUPPORTED, "too many writes or allocations")
+        ws = torch.empty(nb, dtype=torch.uint8, device=device)
+        _check(lib.gleam_first_writes(_ptr(d[0]), _ptr(d[1]), n, _ptr(d[2]), n_regions, _ptr(pw), _ptr(po), _ptr(pl),
+                                      _ptr(first), _ptr(status), _ptr(ws), nb, hs))
+    return pw, po, pl, first, status[:n_regions]
 
 
 def md5_prefix(batch: Batch, prefix_bytes: int = 128, min_len: int = 1024, stream=None):

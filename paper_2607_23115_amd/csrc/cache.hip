@@ -20,6 +20,7 @@
 
 #include "gleam_device.h"
 #include "gleam_internal.h"
+#include "gleam_table.h"
 
 namespace gleam {
 namespace {
@@ -89,6 +90,7 @@ __global__ void insert_commit_kernel(TableRef t, ScratchRef sc, const uint64_t* 
     if (atomicCAS(ull(&t.hdr[0]), 0ull, 1ull) == 0ull) {
       t.hdr[1] = vals[i];
       atomicAdd(ull(n_new), 1ull);
+      atomicAdd(ull(&t.hdr[3]), 1ull);
     }
     return;
   }
@@ -99,6 +101,7 @@ __global__ void insert_commit_kernel(TableRef t, ScratchRef sc, const uint64_t* 
     if (prev == kEmpty) {
       slot[1] = vals[i];
       atomicAdd(ull(n_new), 1ull);
+      atomicAdd(ull(&t.hdr[3]), 1ull);
       return;
     }
     if (prev == k) return;  // already held: keep the existing value
@@ -139,26 +142,6 @@ __global__ void lookup_probe_kernel(TableRef t, ScratchRef sc, const uint64_t* k
     status[g] = 0xFF;
     scratch_mark(sc, keys, k, g);
   }
-}
-
-// Probe of the resident table for key k: (hit, value).
-__device__ __forceinline__ bool table_find(const TableRef& t, uint64_t k, uint64_t* val) {
-  if (k == kEmpty) {
-    *val = t.hdr[1];
-    return t.hdr[0] != 0;
-  }
-  uint64_t pos = slot_hash(k, t.shift);
-  for (uint64_t probe = 0; probe <= t.mask; ++probe) {
-    const uint4 e = *reinterpret_cast<const uint4*>(t.slots + 2 * pos);
-    const uint64_t key = lo64(e);
-    if (key == k) {
-      *val = hi64(e);
-      return true;
-    }
-    if (key == kEmpty) return false;
-    pos = (pos + 1) & t.mask;
-  }
-  return false;
 }
 
 // Lookups of up to kSmallKeys keys: one 1024-thread workgroup, with the dedup table in

@@ -36,6 +36,24 @@ __global__ void identify_compare_kernel(const uint64_t* current, const uint64_t*
   }
 }
 
+// Per leaf slot (slot = g * LPB + k): equal digests? Slots past a short block's last leaf
+// hold 0 on both sides, so they always agree. The first differing leaf of each payload by
+// atomicMin of its index within the payload, (g - blk_first[s]) * LPB + k.
+__global__ void identify_leaf_compare_kernel(const uint64_t* current, const uint64_t* recorded, uint64_t n_slots,
+                                             uint32_t lpb_log2, const uint64_t* blk_first, uint64_t n_seg,
+                                             uint8_t* leaf_match, uint64_t* first_diff) {
+  const uint64_t slot = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (slot >= n_slots) return;
+  const bool same = current[slot] == recorded[slot];
+  if (leaf_match) leaf_match[slot] = same ? 1 : 0;
+  if (!same) {
+    const uint64_t g = slot >> lpb_log2;
+    const uint64_t s = find_segment(blk_first, n_seg, g);
+    const uint64_t leaf = ((g - blk_first[s]) << lpb_log2) + (slot & ((1ull << lpb_log2) - 1));
+    atomicMin(reinterpret_cast<unsigned long long*>(&first_diff[s]), (unsigned long long)leaf);
+  }
+}
+
 // Per payload: a difference clears its allocation's weight flag.
 __global__ void identify_region_kernel(const uint64_t* first_diff, uint64_t n_seg, const uint64_t* region_first,
                                        uint64_t n_regions, uint8_t* region_weight) {
@@ -86,6 +104,49 @@ extern "C" gleam_status gleam_identify_weights(const gleam_batch* b, const uint6
   hipLaunchKernelGGL(identify_compare_kernel, dim3(grid_for(b->n_blocks)), dim3(kThreads), 0, s, current,
                      d_recorded, b->n_blocks, b->blk_first, b->n_seg, d_block_match, first_diff);
   if ((st = launch_status("identify_compare_kernel")) != GLEAM_OK) return st;
+  if (n_regions == 0) return GLEAM_OK;
+  hipLaunchKernelGGL(identify_region_kernel, dim3(grid_for(b->n_seg)), dim3(kThreads), 0, s, first_diff, b->n_seg,
+                     d_region_first, n_regions, d_region_weight);
+  return launch_status("identify_region_kernel");
+}
+
+extern "C" gleam_status gleam_identify_leaves(const gleam_batch* b, const uint64_t* d_recorded_leaf,
+                                              const uint64_t* d_region_first, uint64_t n_regions,
+                                              uint8_t* d_leaf_match, uint64_t* d_seg_first_diff,
+                                              uint8_t* d_region_weight, void* d_ws, size_t ws_bytes, void* stream) {
+  using namespace gleam;
+  clear_error();
+  gleam_status st = validate_batch(b, "gleam_identify_leaves");
+  if (st != GLEAM_OK) return st;
+  if ((b->n_blocks > 0 && !d_recorded_leaf) || (n_regions > 0 && (!d_region_first || !d_region_weight))) {
+    set_error("gleam_identify_leaves: null recorded leaf digests, region list or output");
+    return GLEAM_E_INVALID;
+  }
+  const uint32_t lpb_log2 = (uint32_t)(log2_exact(b->block_bytes) - 12);
+  const uint64_t n_slots = b->n_blocks << lpb_log2;  // n_blocks < 2^51 (validate_batch)
+  if (b->n_seg > 0x7fffffffull * kThreads || n_regions > 0x7fffffffull * kThreads ||
+      n_slots > 0x7fffffffull * kThreads) {
+    set_error("gleam_identify_leaves: more than 2^31 workgroups of leaf slots, payloads or regions");
+    return GLEAM_E_UNSUPPORTED;
+  }
+  const WsLayout L = ws_layout(n_slots + b->n_seg);
+  st = check_workspace(L, d_ws, ws_bytes, "gleam_identify_leaves");
+  if (st != GLEAM_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  // workspace: current leaf digests [n_slots], block digests [n_blocks], first_diff [n_seg]
+  // (16 * (n_slots + n_seg) bytes of scratch hold them)
+  uint64_t* cur_leaf = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(d_ws) + L.scratch_off);
+  uint64_t* cur_block = cur_leaf + n_slots;
+  uint64_t* first_diff = d_seg_first_diff ? d_seg_first_diff : cur_block + b->n_blocks;
+  const uint64_t init_n = b->n_seg > n_regions ? b->n_seg : n_regions;
+  hipLaunchKernelGGL(identify_init_kernel, dim3(grid_for(init_n, 4096)), dim3(kThreads), 0, s, first_diff, b->n_seg,
+                     d_region_first, n_regions, d_region_weight);
+  if ((st = launch_status("identify_init_kernel")) != GLEAM_OK) return st;
+  if (b->n_blocks == 0) return GLEAM_OK;
+  if ((st = launch_fp(b, cur_block, cur_leaf, s)) != GLEAM_OK) return st;
+  hipLaunchKernelGGL(identify_leaf_compare_kernel, dim3(grid_for(n_slots)), dim3(kThreads), 0, s, cur_leaf,
+                     d_recorded_leaf, n_slots, lpb_log2, b->blk_first, b->n_seg, d_leaf_match, first_diff);
+  if ((st = launch_status("identify_leaf_compare_kernel")) != GLEAM_OK) return st;
   if (n_regions == 0) return GLEAM_OK;
   hipLaunchKernelGGL(identify_region_kernel, dim3(grid_for(b->n_seg)), dim3(kThreads), 0, s, first_diff, b->n_seg,
                      d_region_first, n_regions, d_region_weight);

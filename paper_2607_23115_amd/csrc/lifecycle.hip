@@ -7,10 +7,21 @@
 //   erase   remove the given keys
 //   export  every entry, sorted by key (the identifier set, or a checkpoint)
 //
-// Evict and erase gather every slot into the workspace, then clear the table and
-// re-insert the survivors, so lookups and inserts never meet tombstones. The order
-// for eviction comes from three stable radix passes (key, then stamp, then a
-// live/empty bit), so it does not depend on where keys sit in the table.
+// Evict gathers every slot into the workspace, then clears the table and re-inserts the
+// survivors; the order for eviction comes from three stable radix passes (key, then
+// stamp, then a live/empty bit), so it does not depend on where keys sit in the table.
+//
+// Erase costs O(keys erased), not O(capacity), and leaves no tombstones: each erased key's
+// cluster (the run of occupied slots around it, bounded by empty slots; linear probing
+// never crosses an empty slot) is repaired by one thread. It empties the erased slots, then
+// re-inserts the cluster's other entries in cluster order, each at the first empty slot
+// from its home, which is never past its old slot, so the cluster stays a valid probe
+// sequence and other clusters are not touched. Clusters are found before any is repaired
+// (a kernel boundary apart), and each is repaired by exactly one thread (the first to
+// claim its start in a workspace set).
+//
+// The table header keeps the live-entry count (word 3): inserts add their new keys, erase
+// subtracts what it removed, evict sets it, so erase can report the count without a scan.
 
 #include <rocprim/device/device_radix_sort.hpp>
 
@@ -127,18 +138,6 @@ __global__ void touch_kernel(TableRef t, const uint64_t* keys, uint64_t n, const
   if (n_touched && (threadIdx.x & 63) == 0 && hit) atomicAdd(ull(n_touched), (unsigned long long)hit);
 }
 
-__global__ void erase_mark_kernel(TableRef t, const uint64_t* keys, uint64_t n, Entries e) {
-  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const uint64_t k = keys[i];
-  if (k == kEmpty) {
-    if (t.hdr[0]) e.flag[e.m - 1] = 1;
-    return;
-  }
-  const int64_t pos = find_slot(t, k);
-  if (pos >= 0) e.flag[pos] = 1;
-}
-
 // Copy every slot (and the kEmpty side slot) into the entry arrays; count live and
 // live-and-marked entries.
 __global__ void gather_kernel(TableRef t, Entries e) {
@@ -219,6 +218,7 @@ __global__ void evict_reinsert_kernel(TableRef t, Entries e, const uint64_t* per
   if (t0 == 0) {
     counts[0] = drop;
     counts[1] = live - drop;
+    t.hdr[3] = live - drop;
   }
   for (uint64_t i = t0; i < live; i += stride) {
     const uint64_t j = perm[i];
@@ -230,17 +230,137 @@ __global__ void evict_reinsert_kernel(TableRef t, Entries e, const uint64_t* per
   }
 }
 
-// Erase: every live, unmarked entry is re-inserted (slot order; placement does not
-// change any lookup result).
-__global__ void erase_reinsert_kernel(TableRef t, Entries e, uint64_t* counts) {
-  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  const uint64_t t0 = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t0 == 0) {
-    counts[0] = e.counters[1];
-    counts[1] = e.counters[0] - e.counters[1];
+// ---- erase: O(keys erased) ------------------------------------------------------------
+struct EraseWs {          // workspace of an erase of n keys
+  uint64_t* hdr;          // [0] entries removed, [1] clusters to repair
+  uint64_t* keyset;       // cap slots: index + 1 of an erased key (0 free); keys read back
+  uint64_t* starts;       // cap slots: cluster start + 1 (0 free)
+  uint64_t* leaders;      // n cluster starts, one per cluster
+  uint64_t mask;
+  int shift;
+};
+
+__device__ __forceinline__ bool in_keyset(const EraseWs& w, const uint64_t* keys, uint64_t k) {
+  uint64_t pos = slot_hash(k, w.shift);
+  for (uint64_t probe = 0; probe <= w.mask; ++probe) {
+    const uint64_t v = w.keyset[pos];
+    if (v == 0) return false;
+    if (keys[v - 1] == k) return true;
+    pos = (pos + 1) & w.mask;
   }
-  for (uint64_t i = t0; i < e.m; i += stride)
-    if (e.live[i] && !e.flag[i]) insert_entry(t, e.key[i], e.val[i], e.stamp[i]);
+  return false;
+}
+
+__global__ void erase_keyset_kernel(const uint64_t* keys, uint64_t n, EraseWs w) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n || keys[i] == kEmpty) return;
+  const uint64_t k = keys[i];
+  uint64_t pos = slot_hash(k, w.shift);
+  for (uint64_t probe = 0; probe <= w.mask; ++probe) {
+    const uint64_t prev = atomicCAS(ull(&w.keyset[pos]), 0ull, (unsigned long long)(i + 1));
+    if (prev == 0 || keys[prev - 1] == k) return;
+    pos = (pos + 1) & w.mask;
+  }
+}
+
+// Per erased key that is present: the start of its cluster, claimed once.
+__global__ void erase_find_kernel(TableRef t, const uint64_t* keys, uint64_t n, EraseWs w) {
+  const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const uint64_t k = keys[i];
+  if (k == kEmpty) {  // the header's side slot
+    if (atomicExch(ull(&t.hdr[0]), 0ull) == 1ull) {
+      t.hdr[2] = 0;
+      atomicAdd(ull(&w.hdr[0]), 1ull);
+    }
+    return;
+  }
+  const int64_t at = find_slot(t, k);
+  if (at < 0) return;
+  uint64_t c0 = (uint64_t)at;
+  for (uint64_t step = 0; step <= t.mask; ++step) {
+    const uint64_t before = (c0 - 1) & t.mask;
+    if (t.slots[2 * before] == kEmpty) break;
+    c0 = before;
+  }
+  uint64_t pos = slot_hash(c0, w.shift);
+  for (uint64_t probe = 0; probe <= w.mask; ++probe) {
+    const uint64_t prev = atomicCAS(ull(&w.starts[pos]), 0ull, (unsigned long long)(c0 + 1));
+    if (prev == 0) {
+      w.leaders[atomicAdd(ull(&w.hdr[1]), 1ull)] = c0;
+      return;
+    }
+    if (prev == c0 + 1) return;  // claimed by another key of this cluster
+    pos = (pos + 1) & w.mask;
+  }
+}
+
+// One thread per cluster: empty the erased slots, then re-insert the rest in cluster order.
+__global__ void erase_repair_kernel(TableRef t, const uint64_t* keys, uint64_t n, EraseWs w) {
+  const uint64_t clusters = w.hdr[1];
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t c = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; c < clusters && c < n; c += stride) {
+    const uint64_t c0 = w.leaders[c];
+    uint64_t len = 0, removed = 0;
+    for (uint64_t p = c0; len <= t.mask; p = (p + 1) & t.mask, ++len) {
+      const uint64_t k = t.slots[2 * p];
+      if (k == kEmpty) break;  // the cluster's end (slots emptied here lie behind)
+      if (in_keyset(w, keys, k)) {
+        t.slots[2 * p] = kEmpty;
+        t.stamps[p] = 0;
+        ++removed;
+      }
+    }
+    if (removed == 0) continue;
+    for (uint64_t i = 0; i < len; ++i) {
+      const uint64_t p = (c0 + i) & t.mask;
+      const uint64_t k = t.slots[2 * p];
+      if (k == kEmpty) continue;
+      uint64_t q = slot_hash(k, t.shift);
+      if (q == p) continue;  // at home: the first empty slot from its home is here
+      while (t.slots[2 * q] != kEmpty && q != p) q = (q + 1) & t.mask;
+      if (q == p) continue;  // no empty slot before it: stays
+      t.slots[2 * q] = k;
+      t.slots[2 * q + 1] = t.slots[2 * p + 1];
+      t.stamps[q] = t.stamps[p];
+      t.slots[2 * p] = kEmpty;
+      t.stamps[p] = 0;
+    }
+    atomicAdd(ull(&w.hdr[0]), (unsigned long long)removed);
+  }
+}
+
+__global__ void erase_finish_kernel(TableRef t, EraseWs w, uint64_t* counts) {
+  const uint64_t removed = w.hdr[0];
+  const uint64_t live = t.hdr[3] - removed;
+  t.hdr[3] = live;
+  counts[0] = removed;
+  counts[1] = live;
+}
+
+struct EraseLayout {
+  uint64_t cap;
+  size_t total;
+};
+
+EraseLayout erase_layout(uint64_t n) {
+  EraseLayout L;
+  L.cap = 64;
+  while (L.cap < 2 * n) L.cap <<= 1;
+  L.total = (kHeaderBytes + 16 * (size_t)L.cap + 8 * (size_t)n + 255) & ~(size_t)255;
+  return L;
+}
+
+EraseWs erase_ws(void* ws, const EraseLayout& L) {
+  uint8_t* b = static_cast<uint8_t*>(ws);
+  EraseWs w;
+  w.hdr = reinterpret_cast<uint64_t*>(b);
+  w.keyset = reinterpret_cast<uint64_t*>(b + kHeaderBytes);
+  w.starts = w.keyset + L.cap;
+  w.leaders = w.starts + L.cap;
+  w.mask = L.cap - 1;
+  w.shift = 64 - log2_exact(L.cap);
+  return w;
 }
 
 __global__ void export_kernel(Entries e, const uint64_t* perm, uint64_t* keys, uint64_t* vals, uint64_t* stamps,
@@ -376,35 +496,49 @@ extern "C" gleam_status gleam_cache_evict(gleam_cache* c, uint64_t keep, uint64_
   return GLEAM_OK;
 }
 
+extern "C" size_t gleam_cache_erase_bytes(uint64_t n) {
+  if (n > (1ull << 36)) return 0;
+  return gleam::erase_layout(n).total;
+}
+
 extern "C" gleam_status gleam_cache_erase(gleam_cache* c, const uint64_t* d_keys, uint64_t n, uint64_t* d_counts,
                                           void* d_ws, size_t ws_bytes, void* stream) {
   using namespace gleam;
   clear_error();
-  MaintLayout L;
-  gleam_status st = check_maint(c, d_ws, ws_bytes, "gleam_cache_erase", &L);
-  if (st != GLEAM_OK) return st;
-  if (!d_counts || (n > 0 && !d_keys)) {
-    set_error("gleam_cache_erase: null keys or counts");
+  if (!c || !d_counts || (n > 0 && !d_keys)) {
+    set_error("gleam_cache_erase: null table, keys or counts");
     return GLEAM_E_INVALID;
   }
-  if (n > 0x7fffffffull * kThreads) {
-    set_error("gleam_cache_erase: more than 2^31 workgroups of keys");
+  if (n > (1ull << 36) || n > 0x7fffffffull * kThreads) {
+    set_error("gleam_cache_erase: more than 2^36 keys");
     return GLEAM_E_UNSUPPORTED;
   }
+  const EraseLayout L = erase_layout(n);
+  if (!d_ws || !aligned256(d_ws)) {
+    set_error("gleam_cache_erase: workspace must be non-null and 256-byte aligned");
+    return GLEAM_E_INVALID;
+  }
+  if (ws_bytes < L.total) {
+    set_error("gleam_cache_erase: workspace of %zu bytes, %zu needed", ws_bytes, L.total);
+    return GLEAM_E_WORKSPACE;
+  }
   hipStream_t s = (hipStream_t)stream;
-  uint8_t* b = static_cast<uint8_t*>(d_ws);
-  const Entries e = entries_at(d_ws, L);
-  st = fill_u64(reinterpret_cast<uint64_t*>(b + L.flag), (L.m + 7) / 8, 0, s);
+  const EraseWs w = erase_ws(d_ws, L);
+  const TableRef t = table_ref(c);
+  // header and both sets to zero (a fill kernel, so the call can be captured in a graph)
+  gleam_status st = fill_u64(w.hdr, (kHeaderBytes + 16 * L.cap) / 8, 0, s);
   if (st != GLEAM_OK) return st;
   if (n > 0) {
-    hipLaunchKernelGGL(erase_mark_kernel, dim3((uint32_t)((n + kThreads - 1) / kThreads)), dim3(kThreads), 0, s,
-                       table_ref(c), d_keys, n, e);
-    if ((st = launch_status("erase_mark_kernel")) != GLEAM_OK) return st;
+    const dim3 grid((uint32_t)((n + kThreads - 1) / kThreads)), block(kThreads);
+    hipLaunchKernelGGL(erase_keyset_kernel, grid, block, 0, s, d_keys, n, w);
+    if ((st = launch_status("erase_keyset_kernel")) != GLEAM_OK) return st;
+    hipLaunchKernelGGL(erase_find_kernel, grid, block, 0, s, t, d_keys, n, w);
+    if ((st = launch_status("erase_find_kernel")) != GLEAM_OK) return st;
+    hipLaunchKernelGGL(erase_repair_kernel, dim3(grid_for(n)), block, 0, s, t, d_keys, n, w);
+    if ((st = launch_status("erase_repair_kernel")) != GLEAM_OK) return st;
   }
-  if ((st = gather(c, d_ws, L, s, false)) != GLEAM_OK) return st;
-  if ((st = clear_table(c, s)) != GLEAM_OK) return st;
-  hipLaunchKernelGGL(erase_reinsert_kernel, dim3(grid_for(L.m)), dim3(kThreads), 0, s, table_ref(c), e, d_counts);
-  return launch_status("erase_reinsert_kernel");
+  hipLaunchKernelGGL(erase_finish_kernel, dim3(1), dim3(1), 0, s, t, w, d_counts);
+  return launch_status("erase_finish_kernel");
 }
 
 extern "C" gleam_status gleam_cache_export(const gleam_cache* c, uint64_t* d_keys, uint64_t* d_vals,

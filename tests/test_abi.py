@@ -84,6 +84,22 @@ def test_fp_chunks_validation():
     assert _call_fp(_batch(n_seg=0, n_blocks=0), out=None) == g.OK
 
 
+def test_detect_validation():
+    det = g.lib.gleam_detect
+    ok = _batch(n_blocks=4)
+    # batch, table, outputs and workspace are checked before anything is enqueued
+    assert det(None, 256, 256, 256, None, 256, 256, None, 256, 1 << 20, None) == g.E_INVALID
+    assert det(ctypes.byref(_batch(leaf=512)), 256, 256, 256, None, 256, 256, None, 256, 1 << 20, None) == g.E_INVALID
+    assert det(ctypes.byref(ok), None, 256, 256, None, 256, 256, None, 256, 1 << 20, None) == g.E_INVALID
+    assert det(ctypes.byref(ok), 256, 256, 256, None, 256, None, None, 256, 1 << 20, None) == g.E_INVALID
+    assert det(ctypes.byref(ok), 256, None, 256, None, 256, 256, None, 256, 1 << 20, None) == g.E_INVALID
+    assert det(ctypes.byref(ok), 256, 256, None, None, 256, 256, None, 256, 1 << 20, None) == g.E_INVALID
+    assert det(ctypes.byref(ok), 256, 256, 256, None, None, 256, None, 256, 1 << 20, None) == g.E_INVALID
+    assert det(ctypes.byref(ok), 256, 256, 256, None, 256, 256, None, 256, 16, None) == g.E_WORKSPACE
+    assert det(ctypes.byref(ok), 256, 256, 256, None, 256, 256, None, 300, 1 << 20, None) == g.E_INVALID
+    assert g.lib.gleam_last_error() != b""
+
+
 def test_identify_validation():
     f = g.lib.gleam_identify_weights
     assert f(None, 256, 256, 1, None, None, 256, 256, 1 << 20, None) == g.E_INVALID

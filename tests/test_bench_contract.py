@@ -13,7 +13,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def _summary(path, sha):
     with open(path, "w") as f:
         f.write("# test summary\n")
-        f.write(f"fp_chunks.hip sha256 prefix: {sha}\n")
+        f.write(f"fingerprint source sha256 prefix: {sha}\n")
         f.write("fp FETCH_SIZE KiB per dispatch: 1000.0\n")
         f.write("fp WRITE_SIZE KiB per dispatch: 10.0\n")
         f.write("copy fetch scale: 2.0\n")
@@ -37,7 +37,7 @@ def test_committed_profiles_parse():
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip()
-        for key in ("fp_chunks.hip sha256 prefix", "fp FETCH_SIZE KiB per dispatch",
+        for key in ("fingerprint source sha256 prefix", "fp FETCH_SIZE KiB per dispatch",
                     "fp WRITE_SIZE KiB per dispatch", "copy fetch scale", "copy write scale"):
             assert key in kv, (path, key)
         float(kv["fp FETCH_SIZE KiB per dispatch"])

@@ -1,0 +1,215 @@
+"""GPU parity of the rest of free-time weight identification (Sec. 4.1.1):
+
+- gleam_first_writes: the pieces each recorded write owns (only the first write of an
+  address counts) equal the oracle's, piece for piece, with the per-allocation starts
+  and statuses, including the limits (2,048 writes per allocation, the top of the
+  address space);
+- the whole first-write check on the GPU: the pieces digested from the payloads as they
+  land, then from the allocations at free time, decide weights exactly as painting every
+  written byte with its first writer does;
+- gleam_identify_leaves: leaf matches, each payload's first changed leaf and the
+  allocations' verdicts equal the oracle's (at the full 7B-decoder size too)."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_23115_amd as g
+import workloads as W
+from gpu_util import host_threads, keys_to_device, say, to_device, u64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a visible GPU")
+    torch.cuda.init()
+
+
+def gpu_pieces(addr, length, region_first):
+    pw, po, pl, first, status = g.first_writes(np.asarray(addr, np.uint64), np.asarray(length, np.uint64),
+                                               np.asarray(region_first, np.uint64))
+    torch.cuda.synchronize()
+    first = u64(first)
+    n = int(first[-1])
+    return u64(pw)[:n], u64(po)[:n], u64(pl)[:n], first, status.cpu().numpy()
+
+
+def check_pieces(addr, length, region_first, what):
+    got = gpu_pieces(addr, length, region_first)
+    want = oracle.first_write_pieces(addr, length, region_first, max_writes=2048)
+    for a, b, name in zip(got, want, ("write", "offset", "length", "region first", "status")):
+        assert np.array_equal(a, b), f"{what}: {name} differs"
+    return got
+
+
+def random_log(rng, n_regions, max_writes, span):
+    addr, length, rf = [], [], [0]
+    for _ in range(n_regions):
+        k = int(rng.integers(0, max_writes + 1))
+        base = int(rng.integers(0, 2**40)) << 12
+        for _ in range(k):
+            u = rng.random()
+            if u < 0.05:
+                addr.append(base + int(rng.integers(0, span))), length.append(0)
+            elif u < 0.15 and len(addr) > rf[-1]:  # repeat an earlier write of this allocation
+                j = int(rng.integers(rf[-1], len(addr)))
+                addr.append(addr[j]), length.append(length[j])
+            else:
+                lo = int(rng.integers(0, span))
+                addr.append(base + lo), length.append(int(rng.integers(1, max(2, span // 4))))
+        rf.append(len(addr))
+    return addr, length, rf
+
+
+@pytest.mark.parametrize("seed,n_regions,max_writes,span", [(0, 1, 8, 100), (1, 50, 20, 1000), (2, 300, 60, 1 << 20),
+                                                             (3, 20, 400, 5000), (4, 4, 2048, 1 << 16)])
+def test_pieces_random_logs(seed, n_regions, max_writes, span):
+    rng = np.random.default_rng(7000 + seed)
+    addr, length, rf = random_log(rng, n_regions, max_writes, span)
+    say("first writes", seed, "writes", len(addr), "allocations", n_regions)
+    check_pieces(addr, length, rf, f"seed {seed}")
+
+
+def test_pieces_edges():
+    top = 2**64 - 1
+    # disjoint, nested, spanning, empty allocations, an allocation ending at the top of the
+    # address space, one past it, one with 2,048 writes and one with 2,049
+    addr = [0, 100, 50, 10, 40, 0, top - 9, top - 9, 5, 5]
+    length = [50, 10, 50, 10, 10, 60, 9, 10, 0, 0]
+    rf = [0, 3, 3, 6, 7, 8, 10]
+    nested = list(range(2048, 0, -1))  # each write starts one byte before the previous one
+    addr += nested
+    length += [4096] * 2048
+    rf.append(len(addr))
+    addr += list(range(2049))
+    length += [1] * 2049
+    rf.append(len(addr))
+    say("first writes edges")
+    _, _, _, _, status = check_pieces(addr, length, rf, "edges")
+    assert status.tolist() == [g.FW_OK, g.FW_OK, g.FW_OK, g.FW_OK, g.FW_INVALID, g.FW_OK, g.FW_OK, g.FW_TOO_MANY]
+
+
+def test_no_writes_and_no_allocations():
+    say("first writes empty")
+    pw, po, pl, first, status = gpu_pieces([], [], [0, 0, 0])
+    assert first.tolist() == [0, 0, 0] and status.tolist() == [0, 0]
+    pw, po, pl, first, status = gpu_pieces([], [], [0])
+    assert first.tolist() == [0]
+
+
+@pytest.mark.parametrize("block", [4096, 65536])
+def test_first_write_identification_end_to_end(block):
+    """Allocations on the device receive overlapping writes in order; at each write's
+    landing its owned pieces are digested from its payload, and at free time the same
+    pieces are digested from the allocation. The verdicts equal painting every written
+    byte with its first writer's byte and comparing with the allocation's bytes."""
+    rng = np.random.default_rng(7100 + block)
+    n_alloc = 24
+    sizes = [int(rng.integers(1, 40)) * 10_000 for _ in range(n_alloc)]
+    allocs = [torch.zeros(s, dtype=torch.uint8, device="cuda") for s in sizes]
+    writes = []  # (allocation, offset, payload bytes) in time order, grouped by allocation
+    rf = [0]
+    for a, size in enumerate(sizes):
+        for _ in range(int(rng.integers(0, 9))):
+            off = int(rng.integers(0, size))
+            n = int(rng.integers(0, size - off + 1))
+            if writes and writes[-1][0] == a and rng.random() < 0.3:  # the same bytes again
+                off, data = writes[-1][1], writes[-1][2]
+            else:
+                data = np.frombuffer(rng.bytes(n), np.uint8)
+            writes.append((a, off, data))
+        rf.append(len(writes))
+    # payloads as they arrive (the sources), and the allocations after every write
+    src, src_offs, src_lens = W.pack([w[2] for w in writes])
+    d_src = to_device(src)
+    for a, off, data in writes:
+        if data.size:
+            allocs[a][off:off + data.size] = to_device(data)
+    dst_addr = np.array([allocs[a].data_ptr() + off for a, off, _ in writes], np.uint64)
+    lens = np.array([w[2].size for w in writes], np.uint64)
+    say("first-write identification", block, "writes", len(writes))
+    pw, po, pl, first, status = gpu_pieces(dst_addr, lens, rf)
+    assert (status == g.FW_OK).all()
+    # recorded: the pieces of each payload, digested from the source bytes
+    rec_batch = g.Batch(np.uint64(d_src.data_ptr()) + src_offs[pw] + po, pl, block, keepalive=d_src)
+    recorded = g.fp_chunks(rec_batch).clone()
+    # later, in-place changes to some allocations
+    host_alloc = [t.cpu().numpy() for t in allocs]
+    for a in range(n_alloc):
+        if rng.random() < 0.3:
+            x = int(rng.integers(0, sizes[a]))
+            allocs[a][x] ^= 0x24
+            host_alloc[a][x] ^= 0x24
+    cur_batch = g.Batch(dst_addr[pw] + po, pl, block)
+    _, _, weight = g.identify_weights(cur_batch, recorded, first)
+    torch.cuda.synchronize()
+    # byte truth: every written byte equals its first writer's byte
+    expect = []
+    for a in range(n_alloc):
+        first_byte = {}
+        for w in reversed(range(rf[a], rf[a + 1])):
+            _, off, data = writes[w]
+            for i in range(data.size):
+                first_byte[off + i] = data[i]
+        ok = bool(first_byte) and all(host_alloc[a][x] == v for x, v in first_byte.items())
+        expect.append(1 if ok else 0)
+    assert weight.cpu().numpy().tolist() == expect
+    assert 0 < sum(expect) < n_alloc
+
+
+@pytest.mark.parametrize("block", [4096, 16384, 1 << 20])
+def test_identify_leaves_random_regions(block):
+    rng = np.random.default_rng(7200 + block.bit_length())
+    lens = [int(x) for x in rng.integers(0, 3 * block + 9000, 50)] + [0, 1, 4096, 4097, block]
+    rng.shuffle(lens)
+    written = [np.frombuffer(rng.bytes(n), np.uint8).copy() for n in lens]
+    current = [w.copy() for w in written]
+    for c in current:
+        if c.size and rng.random() < 0.3:
+            for _ in range(int(rng.integers(1, 3))):
+                c[int(rng.integers(0, c.size))] ^= 1 << int(rng.integers(0, 8))
+    cuts = sorted(set(int(x) for x in rng.integers(0, len(lens) + 1, 10)))
+    region_first = np.array([0] + cuts + [len(lens)], np.uint64)
+    _, rec_leaves = oracle.batch_digests(written, block, with_leaves=True)
+    arena, offs, lens_a = W.pack(current, skew=int(rng.integers(0, 8)))
+    batch = g.Batch.from_arena(to_device(arena), offs, lens_a, block)
+    say("identify leaves", block)
+    m, f, w = g.identify_leaves(batch, keys_to_device(rec_leaves.reshape(-1)), region_first)
+    torch.cuda.synchronize()
+    em, ef, ew = oracle.identify_leaves(rec_leaves, current, block, region_first)
+    assert np.array_equal(m.cpu().numpy(), em)
+    assert np.array_equal(u64(f), ef)
+    assert np.array_equal(w.cpu().numpy(), ew)
+
+
+@pytest.mark.timeout(900)
+def test_identify_leaves_decoder7b_full():
+    """The 13.5 GB decoder written as the base weights, 3 layers updated in place: the
+    first changed leaf of each updated matrix is its first leaf, and the verdicts are
+    the block-level ones."""
+    threads = host_threads()
+    dec = W.Decoder()
+    block = W.DECODER_BLOCK
+    say("identify leaves decoder7b generate")
+    arena, offs, lens = dec.arena(perturbed=True, threads=threads)
+    current = [arena[int(o):int(o) + int(n)] for o, n in zip(offs, lens)]
+    _, rec = oracle.batch_digests(current, block, with_leaves=True, threads=threads)
+    first = oracle.geometry(lens, block)[0]
+    for i in dec.perturbed:
+        _, lv = oracle.payload_digests(dec.base(i), block, with_leaves=True)
+        rec[int(first[i]):int(first[i + 1])] = lv
+    region_first = np.array([0] + [1 + 9 * l for l in range(33)] + [len(lens)], np.uint64)
+    batch = g.Batch.from_arena(to_device(arena), offs, lens, block)
+    say("identify leaves decoder7b gpu")
+    m, f, w = g.identify_leaves(batch, keys_to_device(rec.reshape(-1)), region_first)
+    torch.cuda.synchronize()
+    em, ef, ew = oracle.identify_leaves(rec, current, block, region_first, threads=threads)
+    assert np.array_equal(m.cpu().numpy(), em)
+    assert np.array_equal(u64(f), ef)
+    assert np.array_equal(w.cpu().numpy(), ew)
+    assert {r for r in range(ew.size) if ew[r] == 0} == {int(l) + 1 for l in dec.perturbed_layers}
+    assert all(u64(f)[i] == 0 for i in dec.perturbed)

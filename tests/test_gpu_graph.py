@@ -182,3 +182,91 @@ def test_graph_replays_the_other_capturable_calls():
             assert np.array_equal(got[k], eager[k]), f"replay {i}: {k}"
         g.fp_chunks(src, out=d)  # eager work between replays
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("which", ["random16", "resnet50"])
+def test_graph_replays_detect_one_kernel(which):
+    """gleam_detect (one kernel for these batches, its workspace counter re-armed by every
+    call) captured once: every replay equals the eager call and the three calls."""
+    if which == "random16":
+        payloads, block = [W.random16_payload()], W.RANDOM16_BLOCK
+    else:
+        payloads, block = W.resnet50_payloads(), W.RESNET_BLOCK
+    arena, offs, lens = W.pack(payloads)
+    d_arena = torch.from_numpy(arena).to("cuda")
+    batch = g.Batch.from_arena(d_arena, offs, lens, block)
+    table = g.Cache(1 << 12)
+    half = g.Batch.from_arena(d_arena, offs[: len(offs) // 2 + 1], lens[: len(lens) // 2 + 1], block)
+    table.insert(g.fp_chunks(half), torch.arange(half.n_blocks, dtype=torch.int64, device="cuda"))
+    ref = Path(batch, table)
+    ref.run()
+    eager = ref.snapshot()
+    out = g.Detect(batch)
+
+    def snap():
+        torch.cuda.synchronize()
+        c = u64(out.counters)
+        n = batch.n_blocks
+        return (u64(out.digests)[:n].copy(), out.status[:n].cpu().numpy().copy(), u64(out.ref)[:n].copy(),
+                u64(out.miss_idx)[:int(c[0])].copy(), c.copy())
+
+    say("graph detect", which, "eager")
+    g.detect(batch, table, out=out)
+    assert same(snap(), eager)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side), torch.cuda.graph(graph, stream=side):
+        g.detect(batch, table, out=out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for i in range(5):
+        say("graph detect", which, "replay", i)
+        for t in (out.digests, out.status, out.ref, out.miss_idx, out.counters):
+            t.fill_(-1 if t.dtype != torch.uint8 else 7)
+        graph.replay()
+        assert same(snap(), eager), f"replay {i}"
+        g.detect(batch, table, out=out)  # eager work between replays
+        assert same(snap(), eager)
+
+
+def test_graph_replays_erase():
+    """gleam_cache_erase captured once: each replay (after the keys are put back
+    eagerly) removes them again, with the oracle's counts and table."""
+    rng = np.random.default_rng(1400)
+    keys = rng.integers(0, 2**64, 3000, dtype=np.uint64, endpoint=False)
+    vals = rng.integers(0, 2**64, keys.size, dtype=np.uint64, endpoint=False)
+    table, ot = g.Cache(1 << 13, max_load=0.5), oracle.Table()
+    table.insert(torch.from_numpy(keys.view(np.int64)).to("cuda"), torch.from_numpy(vals.view(np.int64)).to("cuda"))
+    ot.insert(keys, vals)
+    erase = np.concatenate([keys[:400], rng.integers(0, 2**64, 50, dtype=np.uint64, endpoint=False)])
+    d_erase = torch.from_numpy(erase.view(np.int64)).to("cuda")
+    ws = torch.empty(int(g.lib.gleam_cache_erase_bytes(erase.size)), dtype=torch.uint8, device="cuda")
+    counts = torch.empty(2, dtype=torch.int64, device="cuda")
+    put_back = (torch.from_numpy(keys[:400].view(np.int64)).to("cuda"),
+                torch.from_numpy(vals[:400].view(np.int64)).to("cuda"))
+
+    def erase_call():
+        g._check(g.lib.gleam_cache_erase(table.handle, g._ptr(d_erase), erase.size, g._ptr(counts), g._ptr(ws),
+                                         ws.numel(), g._stream(None)))
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side), torch.cuda.graph(graph, stream=side):
+        erase_call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for i in range(3):
+        say("graph erase replay", i)
+        counts.fill_(-1)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert u64(counts).tolist() == [ot.erase(erase), len(ot)], f"replay {i}"
+        k, v, s, c = table.export()
+        torch.cuda.synchronize()
+        ek, ev, _ = ot.export()
+        assert np.array_equal(u64(k)[:int(c.item())], ek) and np.array_equal(u64(v)[:int(c.item())], ev)
+        table.set_key_bound(len(ot))
+        table.insert(*put_back)  # eager work between replays: the erased keys come back
+        ot.insert(keys[:400], vals[:400])

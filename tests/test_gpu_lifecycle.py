@@ -119,3 +119,77 @@ def test_maintenance_workspace_checked():
     assert e.value.status == g.E_WORKSPACE
     with pytest.raises(g.GleamError):
         table.set_key_bound(10)  # cannot raise the bound above 0
+
+
+GOLDEN = 0x9E3779B97F4A7C15
+GOLDEN_INV = pow(GOLDEN, -1, 1 << 64)
+
+
+def keys_at_homes(rng, homes, log2_cap):
+    """Keys whose table home slot (top log2_cap bits of key * GOLDEN) is the given one:
+    crowded homes make long clusters of linear probing."""
+    shift = 64 - log2_cap
+    out = []
+    for h in homes:
+        r = int(rng.integers(0, 1 << 62)) & ((1 << shift) - 1)
+        out.append((((int(h) << shift) | r) * GOLDEN_INV) % (1 << 64))
+    return np.array(out, np.uint64)
+
+
+def test_erase_long_clusters():
+    """Keys crowded onto a few home slots (clusters of hundreds of slots, wrapping past
+    the table's end), erased a few at a time: after each erase the export, counts and
+    lookups equal the oracle's."""
+    rng = np.random.default_rng(1002)
+    log2_cap = 12
+    homes = np.concatenate([rng.integers(0, 1 << log2_cap, 300), np.full(200, (1 << log2_cap) - 3),
+                            np.full(150, 17)])
+    keys = np.unique(keys_at_homes(rng, homes, log2_cap))
+    vals = rng.integers(0, 2**64, keys.size, dtype=np.uint64, endpoint=False)
+    table, ot = g.Cache(1 << log2_cap, max_load=0.5), oracle.Table()
+    table.insert(keys_to_device(keys), keys_to_device(vals))
+    ot.insert(keys, vals)
+    ep = rng.integers(1, 1000, keys.size, dtype=np.uint64)
+    table.touch(keys_to_device(keys), epochs=keys_to_device(ep))
+    ot.touch(keys, ep)
+    for rnd in range(6):
+        pick = keys[rng.random(keys.size) < 0.15]
+        absent = rng.integers(0, 2**64, 20, dtype=np.uint64, endpoint=False)
+        erase = np.concatenate([pick, absent, pick[:5]])  # repeats too
+        say("erase long clusters round", rnd, erase.size)
+        counts = table.erase(keys_to_device(erase))
+        torch.cuda.synchronize()
+        c = u64(counts)
+        assert int(c[0]) == ot.erase(erase) and int(c[1]) == len(ot)
+        assert_table(table, ot, f"round {rnd}")
+        probe = np.concatenate([keys, absent])
+        st, ref = table.lookup(keys_to_device(probe))
+        torch.cuda.synchronize()
+        est, eref = oracle.lookup(probe, ot)
+        assert np.array_equal(st.cpu().numpy(), est) and np.array_equal(u64(ref), eref)
+        # put half of them back, so later rounds erase from a changed layout
+        back = pick[::2]
+        bv = rng.integers(0, 2**64, back.size, dtype=np.uint64, endpoint=False)
+        table.set_key_bound(int(c[1]))
+        table.insert(keys_to_device(back), keys_to_device(bv))
+        ot.insert(back, bv)
+
+
+def test_erase_few_keys_from_large_table():
+    """1,000 present and 100 absent keys out of 2.5M entries in 2^22 slots."""
+    rng = np.random.default_rng(1003)
+    n = 2_500_000
+    keys = rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False)
+    vals = np.arange(n, dtype=np.uint64)
+    table, ot = g.Cache(1 << 22, max_load=0.65), oracle.Table()
+    say("erase large insert")
+    table.insert(keys_to_device(keys), keys_to_device(vals))
+    ot.insert(keys, vals)
+    erase = np.concatenate([keys[rng.choice(n, 1000, replace=False)],
+                            rng.integers(0, 2**64, 100, dtype=np.uint64, endpoint=False)])
+    say("erase large erase")
+    counts = table.erase(keys_to_device(erase))
+    torch.cuda.synchronize()
+    c = u64(counts)
+    assert int(c[0]) == ot.erase(erase) == 1000 and int(c[1]) == len(ot)
+    assert_table(table, ot, "after erase")
