@@ -266,28 +266,33 @@ gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam
  *   d_miss_idx, d_miss_count, d_miss_bytes   as for gleam_miss_compact (d_miss_bytes
  *                         nullable)
  *   d_ws, ws_bytes        device workspace, 256-byte aligned,
- *                         >= gleam_workspace_bytes(n_blocks), PREPARED: unlike the other
- *                         calls' workspaces, it carries one word from call to call (an
- *                         arrival counter at byte 128), which gleam_detect_ws_init sets
- *                         and every gleam_detect call leaves set. Prepare a workspace once
- *                         after allocating it, and again after any other use of its
- *                         memory; calls that may overlap need separate workspaces.
+ *                         >= gleam_detect_workspace_bytes(n_blocks), PREPARED: unlike the
+ *                         other calls' workspaces it carries one word from call to call (an
+ *                         arrival counter at byte 128), which gleam_detect_ws_init arms and
+ *                         every gleam_detect call leaves armed. Prepare a workspace once
+ *                         after allocating it, and again after any other use of its memory;
+ *                         a workspace sized for n blocks serves any smaller batch; calls
+ *                         that may overlap need separate workspaces.
  * A small batch (blocks of at most 64 KiB, at most 65,536 leaf slots and 4,096 blocks:
  * the latency-bound case, e.g. one copy of a few MB) runs as ONE kernel: every workgroup
- * digests its leaves and arrives at the counter, and the last to arrive does the lookup
- * and the compaction. A larger batch runs the three calls' kernels in order. Enqueues
- * kernel launches only (graph-capturable). If the one-kernel path finds the workspace
- * unprepared, it writes UINT64_MAX to *d_miss_count (and no statuses).
+ * digests its leaves and probes the table for them, then arrives at the counter, and the
+ * last to arrive resolves repeats inside the batch and compacts. A larger batch runs the
+ * three calls' kernels in order. Enqueues kernel launches only (graph-capturable). If the
+ * one-kernel path finds the workspace unprepared, it writes UINT64_MAX to *d_miss_count
+ * (statuses undefined).
  * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED, GLEAM_E_HIP. An empty
  * batch still sets the miss count (and bytes) to 0.
  *
  * gleam_detect_ws_init: prepare d_ws (device, 256-byte aligned, >= 256 bytes) for
- * gleam_detect (one small kernel on `stream`). Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
+ * gleam_detect (one small kernel on `stream`).
+ * gleam_detect_workspace_bytes: the workspace for batches of up to n_blocks blocks (0 for
+ * n_blocks above 2^40). Errors: GLEAM_E_INVALID, GLEAM_E_HIP.
  */
 gleam_status gleam_detect(const gleam_batch* b, const gleam_cache* c, uint64_t* d_digest, uint8_t* d_status,
                           uint64_t* d_ref, uint64_t* d_miss_idx, uint64_t* d_miss_count, uint64_t* d_miss_bytes,
                           void* d_ws, size_t ws_bytes, void* stream);
 gleam_status gleam_detect_ws_init(void* d_ws, size_t ws_bytes, void* stream);
+size_t gleam_detect_workspace_bytes(uint64_t n_blocks);
 
 /*
  * Table lifecycle (Sec. 4.1.3: identified weight chunks stay in a shared cache across

@@ -49,7 +49,7 @@ EXPORTS = (
     "gleam_remap_update_bytes", "gleam_remap_update", "gleam_remap_translate", "gleam_remap_export",
     "gleam_cache_lookup_noalloc", "gleam_cache_lookup_noalloc_max_keys", "gleam_detect",
     "gleam_detect_ws_init", "gleam_identify_leaves", "gleam_first_writes_ws_bytes", "gleam_first_writes",
-    "gleam_cache_erase_bytes",
+    "gleam_cache_erase_bytes", "gleam_detect_workspace_bytes",
 )
 
 
@@ -84,6 +84,7 @@ def _load() -> ctypes.CDLL:
         "gleam_cache_lookup_noalloc": ([vp, vp, u64, vp, vp, vp], st),
         "gleam_detect": ([ctypes.POINTER(_Batch), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], st),
         "gleam_detect_ws_init": ([vp, sz, vp], st),
+        "gleam_detect_workspace_bytes": ([u64], sz),
         "gleam_identify_leaves": ([ctypes.POINTER(_Batch), vp, vp, u64, vp, vp, vp, vp, sz, vp], st),
         "gleam_first_writes_ws_bytes": ([u64, u64], sz),
         "gleam_first_writes": ([vp, vp, u64, vp, u64, vp, vp, vp, vp, vp, vp, sz, vp], st),
@@ -571,7 +572,10 @@ class Detect:
             self.ref = torch.empty(n, dtype=torch.int64, device=dev) if want_ref else None
             self.miss_idx = torch.empty(n, dtype=torch.int64, device=dev)
             self.counters = torch.empty(2, dtype=torch.int64, device=dev)
-            self.ws = workspace(batch.n_blocks, dev)
+            nb = int(lib.gleam_detect_workspace_bytes(batch.n_blocks))
+            if nb == 0:
+                raise GleamError(E_UNSUPPORTED, "batch too large for a detect workspace")
+            self.ws = torch.empty(nb, dtype=torch.uint8, device=dev)
             _check(lib.gleam_detect_ws_init(_ptr(self.ws), self.ws.numel(), hs))
 
 

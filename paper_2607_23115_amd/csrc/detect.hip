@@ -45,6 +45,11 @@ struct DetectArgs {
   uint64_t* arrive;      // workspace: the armed arrival counter
 };
 
+// Workspace of gleam_detect: [256-byte header, word 16 the arrival counter][u32 per block:
+// its byte length (one-kernel path)]; larger batches use it as the three calls' workspace,
+// which leaves header word 16 alone. gleam_detect_ws_init arms the counter.
+size_t detect_own_bytes(uint64_t n) { return (kHeaderBytes + 4 * (size_t)n + 255) & ~(size_t)255; }
+
 // Exclusive scan of one value per thread over a workgroup of W waves; *total gets the sum.
 template <int W>
 __device__ __forceinline__ uint32_t wg_exclusive_scan(uint32_t x, uint32_t* wave_sums, uint32_t* total) {
@@ -216,6 +221,13 @@ __global__ void detect_arm_kernel(uint64_t* arrive) { *arrive = kArmed << 32; }
 }  // namespace
 }  // namespace gleam
 
+extern "C" size_t gleam_detect_workspace_bytes(uint64_t n_blocks) {
+  using namespace gleam;
+  if (n_blocks > kMaxWsItems) return 0;
+  const size_t own = detect_own_bytes(n_blocks), three = ws_layout(n_blocks).total;
+  return own > three ? own : three;
+}
+
 extern "C" gleam_status gleam_detect_ws_init(void* d_ws, size_t ws_bytes, void* stream) {
   using namespace gleam;
   clear_error();
@@ -246,12 +258,24 @@ extern "C" gleam_status gleam_detect(const gleam_batch* b, const gleam_cache* c,
     set_error("gleam_detect: null digest, status or miss list for a non-empty batch");
     return GLEAM_E_INVALID;
   }
-  const WsLayout L = ws_layout(n);
-  st = check_workspace(L, d_ws, ws_bytes, "gleam_detect");
-  if (st != GLEAM_OK) return st;
+  const size_t need = gleam_detect_workspace_bytes(n);
+  if (need == 0) {
+    set_error("gleam_detect: more than 2^40 blocks");
+    return GLEAM_E_UNSUPPORTED;
+  }
+  if (!d_ws || !aligned256(d_ws)) {
+    set_error("gleam_detect: workspace must be non-null and 256-byte aligned");
+    return GLEAM_E_INVALID;
+  }
+  if (ws_bytes < need) {
+    set_error("gleam_detect: workspace of %zu bytes, %zu needed", ws_bytes, need);
+    return GLEAM_E_WORKSPACE;
+  }
   hipStream_t s = (hipStream_t)stream;
   if (n == 0) return gleam_miss_compact(nullptr, 0, b, nullptr, d_miss_count, d_miss_bytes, d_ws, ws_bytes, stream);
 
+  uint8_t* ws = static_cast<uint8_t*>(d_ws);
+  uint64_t* hdr = reinterpret_cast<uint64_t*>(d_ws);
   const int lpb_log2 = log2_exact(b->block_bytes) - 12;
   const uint64_t lpb = 1ull << lpb_log2;
   const uint64_t slots = n * lpb;
@@ -260,7 +284,6 @@ extern "C" gleam_status gleam_detect(const gleam_batch* b, const gleam_cache* c,
     st = device_cu_count(&cus);
     if (st != GLEAM_OK) return st;
     const uint64_t waves = (slots + kQuadLeaves - 1) / kQuadLeaves;
-    uint64_t* hdr = reinterpret_cast<uint64_t*>(d_ws);
     DetectArgs a;
     a.fp = FpArgs{b->seg_addr, b->seg_len, b->blk_first, b->n_seg, n, d_digest, nullptr, (uint32_t)lpb_log2, waves};
     a.t = table_ref(c);
@@ -269,7 +292,7 @@ extern "C" gleam_status gleam_detect(const gleam_batch* b, const gleam_cache* c,
     a.miss_idx = d_miss_idx;
     a.miss_count = d_miss_count;
     a.miss_bytes = d_miss_bytes;
-    a.blen = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + L.scratch_off);  // 4n <= 8 * scratch_cap
+    a.blen = reinterpret_cast<uint32_t*>(ws + kHeaderBytes);
     a.arrive = hdr + kArriveWord;
     // one-wave workgroups while they spread the batch over more CUs (as in gleam_fp_chunks)
     // and the last one's 64 lanes hold at most 8 blocks each
@@ -280,6 +303,9 @@ extern "C" gleam_status gleam_detect(const gleam_batch* b, const gleam_cache* c,
     }
     return launch_status("detect_small_kernel");
   }
+  // larger batches: the three calls' kernels (measured faster than a fused pipeline, in
+  // which the fingerprint kernel's lanes probed the table and recorded their digests
+  // in the workspace: that kernel's workgroups waited for the atomics' round trips)
   st = launch_fp(b, d_digest, nullptr, s);
   if (st != GLEAM_OK) return st;
   st = gleam_cache_lookup(c, d_digest, n, d_status, d_ref, d_ws, ws_bytes, stream);

@@ -123,6 +123,7 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
   }
 }
 
+
 // One workgroup of W waves per W * kQuadLeaves slots; LPB <= kQuadLeaves, so every wave
 // holds whole blocks. W = 1 for the smallest batches (more CUs then share the loads; each
 // wave loads all its stages into LDS at once), 4 otherwise.
@@ -132,6 +133,7 @@ __global__ __launch_bounds__(64 * W) void fp_quad_kernel(FpArgs a) {
   __shared__ uint64_t tables[W][2 * kQuadLeaves];
   quad_pass<W, false, W == 1>(a, lds, tables, nullptr);
 }
+
 
 }  // namespace
 
@@ -205,6 +207,7 @@ gleam_status launch_fp(const gleam_batch* b, uint64_t* d_block_digest, uint64_t*
     hipLaunchKernelGGL(fp_kernel<false>, dim3((uint32_t)grid), dim3(kThreads), 0, stream, a);
   return launch_status("fp_kernel");
 }
+
 
 }  // namespace gleam
 

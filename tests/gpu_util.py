@@ -62,6 +62,19 @@ def run_path(batch: g.Batch, table: g.Cache, with_leaves: bool = False):
     return out
 
 
+def detect_path(batch: g.Batch, table: g.Cache, out: g.Detect | None = None):
+    """gleam_detect (one call: one kernel for small batches, three for large ones); host
+    copies of every output, as run_path returns them."""
+    res = g.detect(batch, table, out=out)
+    torch.cuda.synchronize()
+    n = batch.n_blocks
+    c = u64(res.counters)
+    o = {"digests": u64(res.digests)[:n], "status": res.status[:n].cpu().numpy(), "ref": u64(res.ref)[:n],
+         "miss_count": int(c[0]), "miss_bytes": int(c[1]), "leaves": None}
+    o["miss_idx"] = u64(res.miss_idx)[:o["miss_count"]]
+    return o
+
+
 def assert_same(gpu: dict, ref: dict, what: str = "") -> None:
     assert np.array_equal(gpu["digests"], ref["digests"]), f"{what}: digests differ"
     assert np.array_equal(gpu["status"], ref["status"]), f"{what}: status differs"

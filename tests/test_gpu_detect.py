@@ -202,3 +202,62 @@ def test_empty_batches():
         g.detect(batch, t, out=out)
         torch.cuda.synchronize()
         assert u64(out.counters).tolist() == [0, 0]
+
+
+def test_paths_alternate_on_one_workspace():
+    """One prepared workspace serves a three-kernel batch (planted repeats), a one-kernel
+    batch, then the first again: a dedup slot left behind by a call would show as a wrong
+    repeat or reference in the next."""
+    rng = np.random.default_rng(9700)
+    base = [np.frombuffer(rng.bytes(int(n)), np.uint8) for n in rng.integers(1, 60_000, 600)]
+    big = base + [base[i].copy() for i in rng.integers(0, len(base), 200)]  # repeats in the batch
+    arena, offs, lens = W.pack(big)
+    d_arena = to_device(arena)
+    b_big = g.Batch.from_arena(d_arena, offs, lens, 4096)
+    b_small = g.Batch.from_arena(d_arena, offs[:40], lens[:40], 4096)
+    assert b_big.n_blocks > 4096 and b_small.n_blocks <= 4096
+    t, ot = tables_from(big, 4096, range(0, 600, 7))
+    out = g.Detect(b_big)
+    for i, (b, p) in enumerate([(b_big, big), (b_small, big[:40]), (b_big, big), (b_big, big)]):
+        say("detect alternating", i, b.n_blocks)
+        got = detect_outputs(b, t, out=out)
+        want = oracle.run(p, 4096, ot, threads=host_threads())
+        for k in ("digests", "status", "ref", "miss_idx"):
+            assert np.array_equal(got[k], want[k]), f"call {i}: {k}"
+        assert (got["miss_count"], got["miss_bytes"]) == (want["miss_count"], want["miss_bytes"]), i
+
+
+def test_beyond_the_three_kernel_limit():
+    """2,100,000 blocks of 4 KiB (past 2,097,152: the three calls' kernels run) drawn from
+    4,000 distinct blocks, so most repeat; then a three-kernel batch on the same workspace."""
+    rng = np.random.default_rng(9800)
+    n_blk, per = 2_100_000, 100_000
+    pool = rng.integers(0, 256, (4000, 4096), dtype=np.uint8)
+    pick = rng.integers(0, pool.shape[0], n_blk)
+    arena = pool[pick].reshape(-1)
+    offs = np.arange(0, n_blk, per, dtype=np.uint64) * 4096
+    lens = np.full(offs.size, per * 4096, np.uint64)
+    lens[-1] = (n_blk - per * (offs.size - 1)) * 4096 - 123  # a short last block
+    payloads = [arena[int(o):int(o) + int(n)] for o, n in zip(offs, lens)]
+    d_arena = to_device(arena)
+    batch = g.Batch.from_arena(d_arena, offs, lens, 4096)
+    assert batch.n_blocks == n_blk
+    t, ot = g.Cache(1 << 13), oracle.Table()
+    keys = oracle.batch_digests([pool[i] for i in range(0, 4000, 3)], 4096)[0]
+    t.insert(keys_to_device(keys), keys_to_device(keys))
+    ot.insert(keys, keys)
+    out = g.Detect(batch)
+    say("detect past the three-kernel limit", n_blk)
+    got = detect_outputs(batch, t, out=out)
+    want = oracle.run(payloads, 4096, ot, threads=host_threads())
+    for k in ("digests", "status", "ref", "miss_idx"):
+        assert np.array_equal(got[k], want[k]), k
+    assert (got["miss_count"], got["miss_bytes"]) == (want["miss_count"], want["miss_bytes"])
+    sub_b = g.Batch.from_arena(d_arena, [offs[0], 4096 * 7], [9000 * 4096, 5000 * 4096 + 1], 4096)
+    say("detect after the limit, three kernels", sub_b.n_blocks)
+    got = detect_outputs(sub_b, t, out=out)
+    want = oracle.run([arena[:9000 * 4096], arena[4096 * 7:4096 * 7 + 5000 * 4096 + 1]], 4096, ot,
+                      threads=host_threads())
+    for k in ("digests", "status", "ref", "miss_idx"):
+        assert np.array_equal(got[k], want[k]), k
+    assert (got["miss_count"], got["miss_bytes"]) == (want["miss_count"], want["miss_bytes"])

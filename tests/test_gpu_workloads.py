@@ -13,7 +13,7 @@ import torch
 import oracle
 import paper_2607_23115_amd as g
 import workloads as W
-from gpu_util import assert_same, host_threads, keys_to_device, run_path, say, to_device
+from gpu_util import assert_same, detect_path, host_threads, keys_to_device, run_path, say, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -50,6 +50,7 @@ def test_resnet50_full():
     gpu = run_path(batch, gpu_table(1 << 12, keys, vals), with_leaves=True)
     ref = oracle.run(payloads, block, ot, threads=host_threads())
     assert_same(gpu, ref, "resnet50")
+    assert_same(detect_path(batch, gpu_table(1 << 12, keys, vals)), ref, "resnet50 detect")
     _, leaves = oracle.batch_digests(payloads, block, with_leaves=True, threads=host_threads())
     assert np.array_equal(gpu["leaves"], leaves)
     first = batch.host_first
@@ -68,6 +69,8 @@ def test_small_copies(skew, n):
     gpu = run_path(batch, g.Cache(1 << 10))
     ref = oracle.run(payloads, W.SMALL_BLOCK, oracle.Table(), threads=host_threads())
     assert_same(gpu, ref, "small copies")
+    say("small copies detect n", n, "skew", skew)
+    assert_same(detect_path(batch, g.Cache(1 << 10)), ref, "small copies detect")
     assert int((gpu["status"] == g.HIT_BATCH).sum()) == sc.targets.size
     assert gpu["miss_count"] == batch.n_blocks - sc.targets.size
 
@@ -100,6 +103,8 @@ def test_decoder7b_full():
     want = {"digests": digests, "status": status, "ref": ref, "miss_idx": midx, "miss_count": mcnt,
             "miss_bytes": mbytes}
     assert_same(gpu, want, "decoder7b")
+    say("decoder7b detect")
+    assert_same(detect_path(batch, gpu_table(1 << 15, base_digests, bidx)), want, "decoder7b detect")
     assert mcnt == 1158 and int((status == g.HIT_CACHE).sum()) == 11759
 
 
@@ -132,6 +137,8 @@ def test_large_bf16_40gb():
     want = {"digests": digests, "status": status, "ref": ref, "miss_idx": midx, "miss_count": mcnt,
             "miss_bytes": mbytes}
     assert_same(gpu, want, "large bf16")
+    say("large bf16 detect")
+    assert_same(detect_path(batch, table), want, "large bf16 detect")
     expect = np.zeros(n, np.uint8)
     expect[chosen] = g.HIT_CACHE
     assert np.array_equal(gpu["status"], expect)
