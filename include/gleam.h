@@ -49,12 +49,12 @@
  *     error a negative status is returned and nothing has been enqueued. A HIP
  *     launch failure returns GLEAM_E_HIP; gleam_last_error() then holds the HIP
  *     message (thread-local).
- *   - HIP graph capture: every call except gleam_cache_evict, _export and
- *     gleam_remap_update enqueues kernel launches only (clears are fill kernels, not
- *     memsets), so a caller may capture it in a graph and replay it.
- *     gleam_cache_insert's host-side key bound grows once, when the call is captured,
- *     not on each replay. The three exceptions sort or scan with rocPRIM, which also
- *     enqueues memsets; keep them out of captured graphs.
+ *   - HIP graph capture: every call except gleam_remap_update enqueues kernel launches
+ *     only (clears are fill kernels, not memsets), so a caller may capture it in a graph
+ *     and replay it. gleam_cache_insert's and gleam_cache_evict's host-side key bound
+ *     changes once, when the call is captured, not on each replay. gleam_remap_update
+ *     sorts and scans with rocPRIM, which also enqueues memsets; keep it out of captured
+ *     graphs.
  *   - Device descriptor contents (seg_addr, seg_len, blk_first) are not read on
  *     the host. The caller guarantees they describe the batch. Whatever they hold,
  *     a kernel reads a payload P = [seg_addr[s], seg_addr[s] + seg_len[s]) only
@@ -301,8 +301,7 @@ size_t gleam_detect_workspace_bytes(uint64_t n_blocks);
  * calls must not overlap, on any stream, with other calls on the same table.
  *
  * gleam_cache_maint_bytes: device workspace bytes for evict and export of this
- * table (0 for NULL, a table above 2^31 slots, or when the radix sort's storage query
- * fails; evict, erase and export then return GLEAM_E_HIP).
+ * table, about 64 bytes per slot (0 for NULL or a table above 2^31 slots).
  *
  * gleam_cache_touch: for every key present, stamp = max(stamp, epoch), the epoch being
  * d_epochs[i] (device u64[n]) or, when d_epochs is NULL, the scalar `epoch`.
@@ -324,6 +323,9 @@ size_t gleam_detect_workspace_bytes(uint64_t n_blocks);
  *
  * gleam_cache_export: every entry sorted by key into device u64[capacity + 1] arrays
  * d_keys, d_vals and (nullable) d_stamps; *d_count (device u64[1]) = entries written.
+ * Evict and export gather the live entries and order them with a radix sort of their
+ * own (kernels only), so both may be captured in a graph; their cost follows the
+ * capacity.
  * Re-inserting the exported pairs (and touching them with their stamps) rebuilds the
  * table: the export is also its checkpoint.
  *

@@ -7,9 +7,11 @@
 //   erase   remove the given keys
 //   export  every entry, sorted by key (the identifier set, or a checkpoint)
 //
-// Evict gathers every slot into the workspace, then clears the table and re-inserts the
-// survivors; the order for eviction comes from three stable radix passes (key, then
-// stamp, then a live/empty bit), so it does not depend on where keys sit in the table.
+// Evict and export gather the live entries into the workspace and order them with a
+// hand-written radix sort (radix_sort.h): by (stamp, key) for eviction, by key for export.
+// Both orders are of distinct keys, so they do not depend on where keys sit in the table.
+// Evict then clears the table and re-inserts the survivors. Every maintenance call
+// enqueues kernels only (fills are kernels too), so each may be captured in a HIP graph.
 //
 // Erase costs O(keys erased), not O(capacity), and leaves no tombstones: each erased key's
 // cluster (the run of occupied slots around it, bounded by empty slots; linear probing
@@ -23,10 +25,9 @@
 // The table header keeps the live-entry count (word 3): inserts add their new keys, erase
 // subtracts what it removed, evict sets it, so erase can report the count without a scan.
 
-#include <rocprim/device/device_radix_sort.hpp>
-
 #include "gleam_device.h"
 #include "gleam_internal.h"
+#include "radix_sort.h"
 
 namespace gleam {
 namespace {
@@ -34,20 +35,17 @@ namespace {
 constexpr int kThreads = 256;
 constexpr uint32_t kMaxGrid = 8192;
 
-struct Entries {  // gathered entries; m = capacity + 1, the last one is the key kEmpty
+struct Entries {  // the live entries, gathered in table-tile order (count in counters[0])
   uint64_t* key;
   uint64_t* val;
   uint64_t* stamp;
-  uint8_t* live;
-  uint8_t* flag;       // erase marks
-  uint64_t* counters;  // [0] live entries, [1] live entries marked for removal
-  uint64_t m;
+  uint64_t* counters;  // [0] live entries; [4..7] the sort's AND/OR words of (key, stamp)
+  uint64_t m;          // capacity + 1 (the last slot is the key kEmpty's header side slot)
 };
 
 struct MaintLayout {
   uint64_t m;
-  size_t counters, key, val, stamp, live, flag, k_a, k_b, i_a, i_b, sort_tmp, sort_bytes, total;
-  bool ok;  // the sort's temporary-storage queries succeeded
+  size_t counters, key, val, stamp, hi, lo, idx, sort, total;
 };
 
 MaintLayout maint_layout(uint64_t capacity) {
@@ -63,30 +61,28 @@ MaintLayout maint_layout(uint64_t capacity) {
   L.key = take(8 * L.m);
   L.val = take(8 * L.m);
   L.stamp = take(8 * L.m);
-  L.live = take(L.m);
-  L.flag = take(L.m);
-  L.k_a = take(8 * L.m);
-  L.k_b = take(8 * L.m);
-  L.i_a = take(8 * L.m);
-  L.i_b = take(8 * L.m);
-  size_t full = 0, one_bit = 0;
-  const hipError_t e_full = rocprim::radix_sort_pairs(nullptr, full, (const uint64_t*)nullptr, (uint64_t*)nullptr,
-                                                      (const uint64_t*)nullptr, (uint64_t*)nullptr, (size_t)L.m, 0, 64);
-  const hipError_t e_bit = rocprim::radix_sort_pairs(nullptr, one_bit, (const uint64_t*)nullptr, (uint64_t*)nullptr,
-                                                     (const uint64_t*)nullptr, (uint64_t*)nullptr, (size_t)L.m, 0, 1);
-  L.ok = e_full == hipSuccess && e_bit == hipSuccess;
-  L.sort_bytes = full > one_bit ? full : one_bit;
-  L.sort_tmp = take(L.sort_bytes);
+  L.hi = take(8 * L.m);  // the sort's keys and indices (its buffer a)
+  L.lo = take(8 * L.m);
+  L.idx = take(4 * L.m);
+  L.sort = take(sort_layout(L.m, 2).total);
   L.total = off;
   return L;
 }
 
 Entries entries_at(void* ws, const MaintLayout& L) {
   uint8_t* b = static_cast<uint8_t*>(ws);
-  return Entries{reinterpret_cast<uint64_t*>(b + L.key),   reinterpret_cast<uint64_t*>(b + L.val),
-                 reinterpret_cast<uint64_t*>(b + L.stamp), b + L.live,
-                 b + L.flag,                               reinterpret_cast<uint64_t*>(b + L.counters),
-                 L.m};
+  return Entries{reinterpret_cast<uint64_t*>(b + L.key), reinterpret_cast<uint64_t*>(b + L.val),
+                 reinterpret_cast<uint64_t*>(b + L.stamp), reinterpret_cast<uint64_t*>(b + L.counters), L.m};
+}
+
+SortBuf sort_a(void* ws, const MaintLayout& L, int words) {
+  uint8_t* b = static_cast<uint8_t*>(ws);
+  return SortBuf{words == 2 ? reinterpret_cast<uint64_t*>(b + L.hi) : nullptr, reinterpret_cast<uint64_t*>(b + L.lo),
+                 reinterpret_cast<uint32_t*>(b + L.idx)};
+}
+
+SortBuf sort_b(void* ws, const MaintLayout& L, int words) {
+  return sort_other(static_cast<uint8_t*>(ws) + L.sort, L.m, words);
 }
 
 uint32_t grid_for(uint64_t n) {
@@ -138,56 +134,106 @@ __global__ void touch_kernel(TableRef t, const uint64_t* keys, uint64_t n, const
   if (n_touched && (threadIdx.x & 63) == 0 && hit) atomicAdd(ull(n_touched), (unsigned long long)hit);
 }
 
-// Copy every slot (and the kEmpty side slot) into the entry arrays; count live and
-// live-and-marked entries.
-__global__ void gather_kernel(TableRef t, Entries e) {
-  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  uint64_t live = 0, marked = 0;
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < e.m; i += stride) {
-    uint64_t k, v, s;
-    bool is_live;
+__global__ void maint_init_kernel(uint64_t* counters) {
+  if (threadIdx.x < 8) counters[threadIdx.x] = (threadIdx.x == 4 || threadIdx.x == 6) ? ~0ull : 0ull;
+}
+
+// Each workgroup takes a tile of 4096 slots (the last tile also the kEmpty side slot),
+// counts its live entries, claims that many positions with one atomic, and writes the
+// entries there in slot order: to the entry arrays, and to the sort's buffer (key words
+// (stamp, key) or key; index = position). It also folds the AND and OR of the keys and
+// stamps into counters[4..7] (one atomic each per workgroup), from which the sort skips
+// the digits every entry shares.
+constexpr uint32_t kGatherItems = 16;
+constexpr uint64_t kGatherTile = (uint64_t)kThreads * kGatherItems;
+
+__global__ __launch_bounds__(kThreads) void gather_kernel(TableRef t, Entries e, SortBuf sb) {
+  __shared__ uint32_t wave_live[kThreads / 64];
+  __shared__ uint64_t tile_base;
+  __shared__ uint64_t fold[kThreads / 64][4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
+  const uint64_t first = (uint64_t)blockIdx.x * kGatherTile + (uint64_t)wave * 64 * kGatherItems + lane;
+  uint64_t key[kGatherItems], val[kGatherItems], mask[kGatherItems];
+  uint32_t live_n = 0;
+#pragma unroll
+  for (uint32_t r = 0; r < kGatherItems; ++r) {
+    const uint64_t i = first + 64ull * r;
+    bool live = false;
+    key[r] = kEmpty;
+    val[r] = 0;
     if (i + 1 < e.m) {
       const uint4 kv = *reinterpret_cast<const uint4*>(t.slots + 2 * i);
-      k = lo64(kv);
-      v = hi64(kv);
-      s = t.stamps[i];
-      is_live = k != kEmpty;
-    } else {
-      k = kEmpty;
-      v = t.hdr[1];
-      s = t.hdr[2];
-      is_live = t.hdr[0] != 0;
+      key[r] = lo64(kv);
+      val[r] = hi64(kv);
+      live = key[r] != kEmpty;
+    } else if (i + 1 == e.m) {
+      live = t.hdr[0] != 0;
+      val[r] = t.hdr[1];
     }
-    e.key[i] = k;
-    e.val[i] = v;
-    e.stamp[i] = s;
-    e.live[i] = is_live ? 1 : 0;
-    live += is_live ? 1 : 0;
-    marked += (is_live && e.flag[i]) ? 1 : 0;
+    mask[r] = __ballot(live);
+    live_n += (uint32_t)__popcll(mask[r]);
   }
-  live = wave_sum(live);
-  marked = wave_sum(marked);
-  if ((threadIdx.x & 63) == 0) {
-    if (live) atomicAdd(ull(&e.counters[0]), (unsigned long long)live);
-    if (marked) atomicAdd(ull(&e.counters[1]), (unsigned long long)marked);
+  if (lane == 0) wave_live[wave] = live_n;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t total = 0;
+    for (int w = 0; w < kThreads / 64; ++w) total += wave_live[w];
+    tile_base = total ? atomicAdd(ull(&e.counters[0]), (unsigned long long)total) : 0;
   }
-}
-
-__global__ void iota_kernel(uint64_t* out, uint64_t m) {
-  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += stride) out[i] = i;
-}
-
-__global__ void permute_kernel(const uint64_t* src, const uint64_t* perm, uint64_t* dst, uint64_t m) {
-  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += stride) dst[i] = src[perm[i]];
-}
-
-// 0 for live entries, 1 for empty slots (so a stable 1-bit pass puts live entries first).
-__global__ void empty_bit_kernel(const uint8_t* live, const uint64_t* perm, uint64_t* dst, uint64_t m) {
-  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < m; i += stride)
-    dst[i] = live[perm[i]] ? 0 : 1;
+  __syncthreads();
+  uint64_t at = tile_base;
+  for (int w = 0; w < wave; ++w) at += wave_live[w];
+  uint64_t and_k = ~0ull, or_k = 0, and_s = ~0ull, or_s = 0;
+#pragma unroll
+  for (uint32_t r = 0; r < kGatherItems; ++r) {
+    if ((mask[r] >> lane) & 1ull) {
+      const uint64_t i = first + 64ull * r;
+      const uint64_t s = i + 1 < e.m ? t.stamps[i] : t.hdr[2];
+      const uint64_t p = at + (uint64_t)__popcll(mask[r] & lt);
+      e.key[p] = key[r];
+      e.val[p] = val[r];
+      e.stamp[p] = s;
+      if (sb.hi) sb.hi[p] = s;
+      sb.lo[p] = key[r];
+      sb.idx[p] = (uint32_t)p;
+      and_k &= key[r];
+      or_k |= key[r];
+      and_s &= s;
+      or_s |= s;
+    }
+    at += (uint64_t)__popcll(mask[r]);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    and_k &= shfl_xor64(and_k, o);
+    or_k |= shfl_xor64(or_k, o);
+    and_s &= shfl_xor64(and_s, o);
+    or_s |= shfl_xor64(or_s, o);
+  }
+  if (lane == 0) {
+    fold[wave][0] = and_k;
+    fold[wave][1] = or_k;
+    fold[wave][2] = and_s;
+    fold[wave][3] = or_s;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t total = 0;
+    for (int w = 0; w < kThreads / 64; ++w) total += wave_live[w];
+    if (total) {
+      for (int w = 1; w < kThreads / 64; ++w) {
+        fold[0][0] &= fold[w][0];
+        fold[0][1] |= fold[w][1];
+        fold[0][2] &= fold[w][2];
+        fold[0][3] |= fold[w][3];
+      }
+      atomicAnd(ull(&e.counters[4]), (unsigned long long)fold[0][0]);
+      atomicOr(ull(&e.counters[5]), (unsigned long long)fold[0][1]);
+      atomicAnd(ull(&e.counters[6]), (unsigned long long)fold[0][2]);
+      atomicOr(ull(&e.counters[7]), (unsigned long long)fold[0][3]);
+    }
+  }
 }
 
 __device__ void insert_entry(const TableRef& t, uint64_t k, uint64_t v, uint64_t s) {
@@ -208,11 +254,16 @@ __device__ void insert_entry(const TableRef& t, uint64_t k, uint64_t v, uint64_t
   }
 }
 
-// Eviction: positions [0, E) of the (stamp, key) order go, [E, live) are re-inserted.
-__global__ void evict_reinsert_kernel(TableRef t, Entries e, const uint64_t* perm, uint64_t keep, uint64_t* evicted,
-                                      uint64_t* counts) {
+// Eviction: positions [0, E) of the (stamp, key) order go, the rest are re-inserted.
+// The evicted keys are read from the sorted keys; the survivors are re-inserted in
+// gather order (slot order within each tile, so neighbouring inserts touch neighbouring
+// slots), each kept when its (stamp, key) is not below the first survivor's. The pairs
+// are distinct, so that is exactly the sorted positions from E on.
+__global__ void evict_reinsert_kernel(TableRef t, Entries e, SortBuf a, SortBuf b, uint64_t keep,
+                                      uint64_t* evicted, uint64_t* counts) {
   const uint64_t live = e.counters[0];
   const uint64_t drop = live > keep ? live - keep : 0;
+  const SortBuf sorted = sort_result(a, b, e.counters + 4, 2);
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
   const uint64_t t0 = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t0 == 0) {
@@ -220,13 +271,16 @@ __global__ void evict_reinsert_kernel(TableRef t, Entries e, const uint64_t* per
     counts[1] = live - drop;
     t.hdr[3] = live - drop;
   }
+  if (drop == live) {
+    if (evicted)
+      for (uint64_t i = t0; i < drop; i += stride) evicted[i] = sorted.lo[i];
+    return;
+  }
+  const uint64_t min_s = sorted.hi[drop], min_k = sorted.lo[drop];
   for (uint64_t i = t0; i < live; i += stride) {
-    const uint64_t j = perm[i];
-    if (i < drop) {
-      if (evicted) evicted[i] = e.key[j];
-    } else {
-      insert_entry(t, e.key[j], e.val[j], e.stamp[j]);
-    }
+    if (evicted && i < drop) evicted[i] = sorted.lo[i];
+    const uint64_t s = e.stamp[i], k = e.key[i];
+    if (s > min_s || (s == min_s && k >= min_k)) insert_entry(t, k, e.val[i], s);
   }
 }
 
@@ -363,15 +417,16 @@ EraseWs erase_ws(void* ws, const EraseLayout& L) {
   return w;
 }
 
-__global__ void export_kernel(Entries e, const uint64_t* perm, uint64_t* keys, uint64_t* vals, uint64_t* stamps,
+__global__ void export_kernel(Entries e, SortBuf a, SortBuf b, uint64_t* keys, uint64_t* vals, uint64_t* stamps,
                               uint64_t* count) {
   const uint64_t live = e.counters[0];
+  const SortBuf sorted = sort_result(a, b, e.counters + 4, 1);
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
   const uint64_t t0 = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t0 == 0) *count = live;
   for (uint64_t i = t0; i < live; i += stride) {
-    const uint64_t j = perm[i];
-    keys[i] = e.key[j];
+    const uint64_t j = sorted.idx[i];
+    keys[i] = sorted.lo[i];
     vals[i] = e.val[j];
     if (stamps) stamps[i] = e.stamp[j];
   }
@@ -387,10 +442,6 @@ gleam_status check_maint(const gleam_cache* c, void* ws, size_t ws_bytes, const 
     return GLEAM_E_UNSUPPORTED;
   }
   *L = maint_layout(c->capacity);
-  if (!L->ok) {
-    set_error("%s: radix sort storage query failed", who);
-    return GLEAM_E_HIP;
-  }
   if (!ws || !aligned256(ws)) {
     set_error("%s: workspace must be non-null and 256-byte aligned", who);
     return GLEAM_E_INVALID;
@@ -402,26 +453,21 @@ gleam_status check_maint(const gleam_cache* c, void* ws, size_t ws_bytes, const 
   return GLEAM_OK;
 }
 
-// Reset counters and erase marks, then gather every entry.
-gleam_status gather(const gleam_cache* c, void* ws, const MaintLayout& L, hipStream_t s, bool clear_flags) {
+// Reset the live count and the AND/OR words, gather the live entries, and sort them:
+// by (stamp, key) for eviction (two key words), by key for export.
+gleam_status gather_sorted(const gleam_cache* c, void* ws, const MaintLayout& L, int words, hipStream_t s) {
   uint8_t* b = static_cast<uint8_t*>(ws);
-  gleam_status st = fill_u64(reinterpret_cast<uint64_t*>(b + L.counters), 4, 0, s);
-  if (st == GLEAM_OK && clear_flags) st = fill_u64(reinterpret_cast<uint64_t*>(b + L.flag), (L.m + 7) / 8, 0, s);
+  uint64_t* counters = reinterpret_cast<uint64_t*>(b + L.counters);
+  hipLaunchKernelGGL(maint_init_kernel, dim3(1), dim3(64), 0, s, counters);
+  gleam_status st = launch_status("maint_init_kernel");
   if (st != GLEAM_OK) return st;
-  hipLaunchKernelGGL(gather_kernel, dim3(grid_for(L.m)), dim3(kThreads), 0, s, table_ref(c), entries_at(ws, L));
-  return launch_status("gather_kernel");
-}
-
-gleam_status sort_pass(void* ws, const MaintLayout& L, const uint64_t* kin, uint64_t* kout, const uint64_t* vin,
-                       uint64_t* vout, unsigned end_bit, hipStream_t s) {
-  size_t bytes = L.sort_bytes;
-  const hipError_t e = rocprim::radix_sort_pairs(static_cast<uint8_t*>(ws) + L.sort_tmp, bytes, kin, kout, vin, vout,
-                                                 (size_t)L.m, 0, end_bit, s);
-  if (e != hipSuccess) {
-    set_error("radix sort: %s", hipGetErrorString(e));
-    return GLEAM_E_HIP;
-  }
-  return launch_status("radix sort");
+  const SortBuf a = sort_a(ws, L, words);
+  const uint32_t tiles = (uint32_t)((L.m + kGatherTile - 1) / kGatherTile);
+  hipLaunchKernelGGL(gather_kernel, dim3(tiles), dim3(kThreads), 0, s, table_ref(c), entries_at(ws, L), a);
+  if ((st = launch_status("gather_kernel")) != GLEAM_OK) return st;
+  // the key words' bits: (key, stamp) words are counters[4..7]; with one word the sort
+  // reads only the key's pair, with two the stamp's as the high word
+  return radix_sort_pairs(a, counters, counters + 4, L.m, words, b + L.sort, s);
 }
 
 }  // namespace
@@ -429,8 +475,7 @@ gleam_status sort_pass(void* ws, const MaintLayout& L, const uint64_t* kin, uint
 
 extern "C" size_t gleam_cache_maint_bytes(const gleam_cache* c) {
   if (!c || c->capacity > (1ull << 31)) return 0;
-  const gleam::MaintLayout L = gleam::maint_layout(c->capacity);
-  return L.ok ? L.total : 0;
+  return gleam::maint_layout(c->capacity).total;
 }
 
 extern "C" gleam_status gleam_cache_touch(gleam_cache* c, const uint64_t* d_keys, uint64_t n,
@@ -471,26 +516,10 @@ extern "C" gleam_status gleam_cache_evict(gleam_cache* c, uint64_t keep, uint64_
     return GLEAM_E_INVALID;
   }
   hipStream_t s = (hipStream_t)stream;
-  uint8_t* b = static_cast<uint8_t*>(d_ws);
-  const Entries e = entries_at(d_ws, L);
-  uint64_t* k_a = reinterpret_cast<uint64_t*>(b + L.k_a);
-  uint64_t* k_b = reinterpret_cast<uint64_t*>(b + L.k_b);
-  uint64_t* i_a = reinterpret_cast<uint64_t*>(b + L.i_a);
-  uint64_t* i_b = reinterpret_cast<uint64_t*>(b + L.i_b);
-  const dim3 grid(grid_for(L.m)), block(kThreads);
-  if ((st = gather(c, d_ws, L, s, true)) != GLEAM_OK) return st;
-  hipLaunchKernelGGL(iota_kernel, grid, block, 0, s, i_b, L.m);
-  if ((st = launch_status("iota_kernel")) != GLEAM_OK) return st;
-  // (stamp, key) order: by key, then stably by stamp, then live entries first
-  if ((st = sort_pass(d_ws, L, e.key, k_a, i_b, i_a, 64, s)) != GLEAM_OK) return st;
-  hipLaunchKernelGGL(permute_kernel, grid, block, 0, s, e.stamp, i_a, k_b, L.m);
-  if ((st = launch_status("permute_kernel")) != GLEAM_OK) return st;
-  if ((st = sort_pass(d_ws, L, k_b, k_a, i_a, i_b, 64, s)) != GLEAM_OK) return st;
-  hipLaunchKernelGGL(empty_bit_kernel, grid, block, 0, s, e.live, i_b, k_b, L.m);
-  if ((st = launch_status("empty_bit_kernel")) != GLEAM_OK) return st;
-  if ((st = sort_pass(d_ws, L, k_b, k_a, i_b, i_a, 1, s)) != GLEAM_OK) return st;
+  if ((st = gather_sorted(c, d_ws, L, 2, s)) != GLEAM_OK) return st;
   if ((st = clear_table(c, s)) != GLEAM_OK) return st;
-  hipLaunchKernelGGL(evict_reinsert_kernel, grid, block, 0, s, table_ref(c), e, i_a, keep, d_evicted, d_counts);
+  hipLaunchKernelGGL(evict_reinsert_kernel, dim3(grid_for(L.m)), dim3(kThreads), 0, s, table_ref(c),
+                     entries_at(d_ws, L), sort_a(d_ws, L, 2), sort_b(d_ws, L, 2), keep, d_evicted, d_counts);
   if ((st = launch_status("evict_reinsert_kernel")) != GLEAM_OK) return st;
   if (keep < c->key_bound) c->key_bound = keep;
   return GLEAM_OK;
@@ -554,21 +583,9 @@ extern "C" gleam_status gleam_cache_export(const gleam_cache* c, uint64_t* d_key
     return GLEAM_E_INVALID;
   }
   hipStream_t s = (hipStream_t)stream;
-  uint8_t* b = static_cast<uint8_t*>(d_ws);
-  const Entries e = entries_at(d_ws, L);
-  uint64_t* k_a = reinterpret_cast<uint64_t*>(b + L.k_a);
-  uint64_t* k_b = reinterpret_cast<uint64_t*>(b + L.k_b);
-  uint64_t* i_a = reinterpret_cast<uint64_t*>(b + L.i_a);
-  uint64_t* i_b = reinterpret_cast<uint64_t*>(b + L.i_b);
-  const dim3 grid(grid_for(L.m)), block(kThreads);
-  if ((st = gather(c, d_ws, L, s, true)) != GLEAM_OK) return st;
-  hipLaunchKernelGGL(iota_kernel, grid, block, 0, s, i_b, L.m);
-  if ((st = launch_status("iota_kernel")) != GLEAM_OK) return st;
-  if ((st = sort_pass(d_ws, L, e.key, k_a, i_b, i_a, 64, s)) != GLEAM_OK) return st;
-  hipLaunchKernelGGL(empty_bit_kernel, grid, block, 0, s, e.live, i_a, k_b, L.m);
-  if ((st = launch_status("empty_bit_kernel")) != GLEAM_OK) return st;
-  if ((st = sort_pass(d_ws, L, k_b, k_a, i_a, i_b, 1, s)) != GLEAM_OK) return st;
-  hipLaunchKernelGGL(export_kernel, grid, block, 0, s, e, i_b, d_keys, d_vals, d_stamps, d_count);
+  if ((st = gather_sorted(c, d_ws, L, 1, s)) != GLEAM_OK) return st;
+  hipLaunchKernelGGL(export_kernel, dim3(grid_for(L.m)), dim3(kThreads), 0, s, entries_at(d_ws, L),
+                     sort_a(d_ws, L, 1), sort_b(d_ws, L, 1), d_keys, d_vals, d_stamps, d_count);
   return launch_status("export_kernel");
 }
 

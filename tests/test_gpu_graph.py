@@ -1,5 +1,6 @@
 """Calls captured once in a HIP graph and replayed: the detect path (fingerprint ->
-lookup -> compaction), and identify, MD5 prefix, touch, send plan, pack and restore. Every
+lookup -> compaction), and identify, MD5 prefix, touch, send plan, pack and restore, and
+the table's erase, evict and export. Every
 replay equals an eager run, with eager work and synchronisations between replays, and a
 replay after the payload bytes change in place sees the new bytes. Every call is plain
 kernel launches (clears are fill kernels, nothing allocates device memory or syncs), so
@@ -270,3 +271,70 @@ def test_graph_replays_erase():
         table.set_key_bound(len(ot))
         table.insert(*put_back)  # eager work between replays: the erased keys come back
         ot.insert(keys[:400], vals[:400])
+
+
+def test_graph_replays_evict_and_export():
+    """gleam_cache_evict and gleam_cache_export captured once each: between replays new
+    keys are inserted and touched eagerly; every replay evicts the oracle's keys in its
+    order and exports the oracle's table."""
+    rng = np.random.default_rng(1500)
+    cap, keep = 1 << 14, 3000
+    table, ot = g.Cache(cap, max_load=0.7), oracle.Table()
+    ws = table.maint_workspace()
+    evicted = torch.empty(cap + 1, dtype=torch.int64, device="cuda")
+    counts = torch.empty(2, dtype=torch.int64, device="cuda")
+    ek = torch.empty(cap + 1, dtype=torch.int64, device="cuda")
+    ev, es, ec = torch.empty_like(ek), torch.empty_like(ek), torch.empty(1, dtype=torch.int64, device="cuda")
+
+    def grow(step):
+        keys = rng.integers(0, 2**64, 4000, dtype=np.uint64, endpoint=False)
+        if step == 0:
+            keys[:2] = [0, 2**64 - 1]
+        vals = rng.integers(0, 2**64, keys.size, dtype=np.uint64, endpoint=False)
+        table.insert(torch.from_numpy(keys.view(np.int64)).to("cuda"), torch.from_numpy(vals.view(np.int64)).to("cuda"))
+        ot.insert(keys, vals)
+        probe = np.concatenate([keys[::2], ot.export()[0][::7]])
+        ep = rng.integers(0, 2**64, probe.size, dtype=np.uint64, endpoint=False) >> np.uint64(step * 8)
+        ep[::5] = 17  # equal stamps: ties go by key
+        table.touch(torch.from_numpy(probe.view(np.int64)).to("cuda"), epochs=torch.from_numpy(ep.view(np.int64)).to("cuda"))
+        ot.touch(probe, ep)
+
+    def evict_call():
+        g._check(g.lib.gleam_cache_evict(table.handle, keep, g._ptr(evicted), g._ptr(counts), g._ptr(ws), ws.numel(),
+                                         g._stream(None)))
+
+    def export_call():
+        g._check(g.lib.gleam_cache_export(table.handle, g._ptr(ek), g._ptr(ev), g._ptr(es), g._ptr(ec), g._ptr(ws),
+                                          ws.numel(), g._stream(None)))
+
+    grow(0)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g_export, g_evict = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side), torch.cuda.graph(g_export, stream=side):
+        export_call()
+    with torch.cuda.stream(side), torch.cuda.graph(g_evict, stream=side):
+        evict_call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for i in range(4):
+        say("graph export/evict replay", i)
+        for t in (ek, ev, es, ec, evicted, counts):
+            t.fill_(-1)
+        g_export.replay()
+        torch.cuda.synchronize()
+        n = int(ec.item())
+        wk, wv, ws_ = ot.export()
+        assert n == wk.size, f"replay {i}: export count"
+        assert np.array_equal(u64(ek)[:n], wk) and np.array_equal(u64(ev)[:n], wv) and np.array_equal(u64(es)[:n], ws_)
+        g_evict.replay()
+        torch.cuda.synchronize()
+        want = ot.evict(keep)
+        assert u64(counts).tolist() == [want.size, len(ot)], f"replay {i}: evict counts"
+        assert np.array_equal(u64(evicted)[:want.size], want), f"replay {i}: eviction order"
+        k, v, s, c = table.export()  # eager export between replays
+        torch.cuda.synchronize()
+        wk, wv, ws_ = ot.export()
+        assert np.array_equal(u64(k)[:int(c.item())], wk) and np.array_equal(u64(s)[:int(c.item())], ws_)
+        table.set_key_bound(len(ot))  # a replay does not lower the host bound; the read-back count does
+        grow(i + 1)

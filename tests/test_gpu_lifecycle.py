@@ -193,3 +193,31 @@ def test_erase_few_keys_from_large_table():
     c = u64(counts)
     assert int(c[0]) == ot.erase(erase) == 1000 and int(c[1]) == len(ot)
     assert_table(table, ot, "after erase")
+
+
+def test_evict_full_width_stamps_and_export_order():
+    """Stamps spread over all 64 bits (every digit of the two-word sort key matters), the
+    keys 0 and 2^64-1 present, a table of several sort tiles: eviction order and export
+    equal the oracle's."""
+    rng = np.random.default_rng(1002)
+    n = 50_000
+    keys = rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False)
+    keys[:2] = [0, 2**64 - 1]
+    vals = rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False)
+    table, ot = g.Cache(1 << 17, max_load=0.5), oracle.Table()
+    table.insert(keys_to_device(keys), keys_to_device(vals))
+    ot.insert(keys, vals)
+    ep = rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False)
+    ep[::3] = ep[0]  # a third share one stamp
+    ep[1::7] >>= np.uint64(40)
+    table.touch(keys_to_device(keys), epochs=keys_to_device(ep))
+    ot.touch(keys, ep)
+    say("lifecycle full-width stamps")
+    assert_table(table, ot, "before evict")
+    for keep in (40_000, 12_345, 1, 0):
+        ev, counts = table.evict(keep)
+        torch.cuda.synchronize()
+        want = ot.evict(keep)
+        assert u64(counts).tolist() == [want.size, len(ot)]
+        assert np.array_equal(u64(ev)[:want.size], want)
+        assert_table(table, ot, f"after evict to {keep}")
