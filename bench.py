@@ -199,7 +199,9 @@ def build_resnet50(g, torch, threads):
 def build_large_bf16(g, torch, threads):
     import workloads as W
     ls = W.LargeSet()
+    log("large_bf16: generating the 40 GB arena on", threads, "threads")
     arena, offs, lens = ls.arena(threads=threads)
+    log("large_bf16: copying the arena to the device")
     d_arena = torch.from_numpy(arena).to("cuda")
     block = W.LARGE_BLOCK
     batch = g.Batch.from_arena(d_arena, offs, lens, block)
