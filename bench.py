@@ -608,6 +608,7 @@ def per_buffer_leg(g, torch, batch, table, count, keep):
     base = src.data_ptr()
     addr = batch.d_addr.cpu().numpy().view(np.uint64)[:count]
     lens = batch.host_len[:count]
+    count = int(addr.size)  # the batch may hold fewer payloads than asked for
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     vp = ctypes.c_void_p
 
