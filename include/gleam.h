@@ -49,12 +49,11 @@
  *     error a negative status is returned and nothing has been enqueued. A HIP
  *     launch failure returns GLEAM_E_HIP; gleam_last_error() then holds the HIP
  *     message (thread-local).
- *   - HIP graph capture: every call except gleam_remap_update enqueues kernel launches
- *     only (clears are fill kernels, not memsets), so a caller may capture it in a graph
- *     and replay it. gleam_cache_insert's and gleam_cache_evict's host-side key bound
- *     changes once, when the call is captured, not on each replay. gleam_remap_update
- *     sorts and scans with rocPRIM, which also enqueues memsets; keep it out of captured
- *     graphs.
+ *   - HIP graph capture: every call enqueues kernel launches only (clears are fill
+ *     kernels, not memsets; sorts and scans are the library's own kernels), so a caller
+ *     may capture it in a graph and replay it. gleam_cache_insert's and
+ *     gleam_cache_evict's host-side key bound changes once, when the call is captured,
+ *     not on each replay.
  *   - Device descriptor contents (seg_addr, seg_len, blk_first) are not read on
  *     the host. The caller guarantees they describe the batch. Whatever they hold,
  *     a kernel reads a payload P = [seg_addr[s], seg_addr[s] + seg_len[s]) only
@@ -559,8 +558,8 @@ gleam_status gleam_restore_blocks(const gleam_batch* dst, const gleam_send_recor
  * Every update passes over the whole capacity (survivors are marked and compacted)
  * whatever the count, plus a sort of the additions: size the capacity to the map.
  * Errors: GLEAM_E_INVALID, GLEAM_E_WORKSPACE, GLEAM_E_UNSUPPORTED (n_add or n_del
- * above 2^31), GLEAM_E_HIP. gleam_remap_update_bytes returns 0 for a NULL map, counts
- * above 2^31 or a failed rocPRIM storage query.
+ * above 2^31), GLEAM_E_HIP. gleam_remap_update_bytes returns 0 for a NULL map or counts
+ * above 2^31.
  *
  * gleam_remap_translate: d_out[i] (device u64[n]) = the translation of d_addr[i]
  * (device u64[n]). The map is only read. Errors: GLEAM_E_INVALID, GLEAM_E_HIP.

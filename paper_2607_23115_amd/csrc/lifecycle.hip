@@ -61,9 +61,9 @@ MaintLayout maint_layout(uint64_t capacity) {
   L.key = take(8 * L.m);
   L.val = take(8 * L.m);
   L.stamp = take(8 * L.m);
-  L.hi = take(8 * L.m);  // the sort's keys and indices (its buffer a)
-  L.lo = take(8 * L.m);
-  L.idx = take(4 * L.m);
+  L.hi = take(8 * sort_capacity(L.m));  // the sort's keys and indices (its buffer a)
+  L.lo = take(8 * sort_capacity(L.m));
+  L.idx = take(4 * sort_capacity(L.m));
   L.sort = take(sort_layout(L.m, 2).total);
   L.total = off;
   return L;
@@ -138,71 +138,76 @@ __global__ void maint_init_kernel(uint64_t* counters) {
   if (threadIdx.x < 8) counters[threadIdx.x] = (threadIdx.x == 4 || threadIdx.x == 6) ? ~0ull : 0ull;
 }
 
-// Each workgroup takes a tile of 4096 slots (the last tile also the kEmpty side slot),
-// counts its live entries, claims that many positions with one atomic, and writes the
-// entries there in slot order: to the entry arrays, and to the sort's buffer (key words
-// (stamp, key) or key; index = position). It also folds the AND and OR of the keys and
-// stamps into counters[4..7] (one atomic each per workgroup), from which the sort skips
-// the digits every entry shares.
+// Each workgroup takes tiles of 4096 slots in turn (the last tile also the kEmpty side
+// slot), counts a tile's live entries, claims that many positions with one atomic, and
+// writes the entries there in slot order: to the entry arrays, and to the sort's buffer
+// (key words (stamp, key) or key; index = position). It also folds the AND and OR of
+// the keys and stamps into counters[4..7], once per workgroup at the end, from which
+// the sort skips the digits every entry shares. The grid is capped so that those folds
+// (four atomics on four words per workgroup) stay few.
 constexpr uint32_t kGatherItems = 16;
 constexpr uint64_t kGatherTile = (uint64_t)kThreads * kGatherItems;
+constexpr uint32_t kGatherMaxGrid = 1024;
 
-__global__ __launch_bounds__(kThreads) void gather_kernel(TableRef t, Entries e, SortBuf sb) {
+__global__ __launch_bounds__(kThreads) void gather_kernel(TableRef t, Entries e, SortBuf sb, uint64_t tiles) {
   __shared__ uint32_t wave_live[kThreads / 64];
   __shared__ uint64_t tile_base;
   __shared__ uint64_t fold[kThreads / 64][4];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
-  const uint64_t first = (uint64_t)blockIdx.x * kGatherTile + (uint64_t)wave * 64 * kGatherItems + lane;
-  uint64_t key[kGatherItems], val[kGatherItems], mask[kGatherItems];
-  uint32_t live_n = 0;
-#pragma unroll
-  for (uint32_t r = 0; r < kGatherItems; ++r) {
-    const uint64_t i = first + 64ull * r;
-    bool live = false;
-    key[r] = kEmpty;
-    val[r] = 0;
-    if (i + 1 < e.m) {
-      const uint4 kv = *reinterpret_cast<const uint4*>(t.slots + 2 * i);
-      key[r] = lo64(kv);
-      val[r] = hi64(kv);
-      live = key[r] != kEmpty;
-    } else if (i + 1 == e.m) {
-      live = t.hdr[0] != 0;
-      val[r] = t.hdr[1];
-    }
-    mask[r] = __ballot(live);
-    live_n += (uint32_t)__popcll(mask[r]);
-  }
-  if (lane == 0) wave_live[wave] = live_n;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t total = 0;
-    for (int w = 0; w < kThreads / 64; ++w) total += wave_live[w];
-    tile_base = total ? atomicAdd(ull(&e.counters[0]), (unsigned long long)total) : 0;
-  }
-  __syncthreads();
-  uint64_t at = tile_base;
-  for (int w = 0; w < wave; ++w) at += wave_live[w];
   uint64_t and_k = ~0ull, or_k = 0, and_s = ~0ull, or_s = 0;
+  for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const uint64_t first = tile * kGatherTile + (uint64_t)wave * 64 * kGatherItems + lane;
+    uint64_t key[kGatherItems], val[kGatherItems], mask[kGatherItems];
+    uint32_t live_n = 0;
 #pragma unroll
-  for (uint32_t r = 0; r < kGatherItems; ++r) {
-    if ((mask[r] >> lane) & 1ull) {
+    for (uint32_t r = 0; r < kGatherItems; ++r) {
       const uint64_t i = first + 64ull * r;
-      const uint64_t s = i + 1 < e.m ? t.stamps[i] : t.hdr[2];
-      const uint64_t p = at + (uint64_t)__popcll(mask[r] & lt);
-      e.key[p] = key[r];
-      e.val[p] = val[r];
-      e.stamp[p] = s;
-      if (sb.hi) sb.hi[p] = s;
-      sb.lo[p] = key[r];
-      sb.idx[p] = (uint32_t)p;
-      and_k &= key[r];
-      or_k |= key[r];
-      and_s &= s;
-      or_s |= s;
+      bool live = false;
+      key[r] = kEmpty;
+      val[r] = 0;
+      if (i + 1 < e.m) {
+        const uint4 kv = *reinterpret_cast<const uint4*>(t.slots + 2 * i);
+        key[r] = lo64(kv);
+        val[r] = hi64(kv);
+        live = key[r] != kEmpty;
+      } else if (i + 1 == e.m) {
+        live = t.hdr[0] != 0;
+        val[r] = t.hdr[1];
+      }
+      mask[r] = __ballot(live);
+      live_n += (uint32_t)__popcll(mask[r]);
     }
-    at += (uint64_t)__popcll(mask[r]);
+    if (lane == 0) wave_live[wave] = live_n;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint32_t total = 0;
+      for (int w = 0; w < kThreads / 64; ++w) total += wave_live[w];
+      tile_base = total ? atomicAdd(ull(&e.counters[0]), (unsigned long long)total) : 0;
+    }
+    __syncthreads();
+    uint64_t at = tile_base;
+    for (int w = 0; w < wave; ++w) at += wave_live[w];
+#pragma unroll
+    for (uint32_t r = 0; r < kGatherItems; ++r) {
+      if ((mask[r] >> lane) & 1ull) {
+        const uint64_t i = first + 64ull * r;
+        const uint64_t s = i + 1 < e.m ? t.stamps[i] : t.hdr[2];
+        const uint64_t p = at + (uint64_t)__popcll(mask[r] & lt);
+        e.key[p] = key[r];
+        e.val[p] = val[r];
+        e.stamp[p] = s;
+        if (sb.hi) sb.hi[p] = s;
+        sb.lo[p] = key[r];
+        sb.idx[p] = (uint32_t)p;
+        and_k &= key[r];
+        or_k |= key[r];
+        and_s &= s;
+        or_s |= s;
+      }
+      at += (uint64_t)__popcll(mask[r]);
+    }
+    __syncthreads();  // wave_live and tile_base read before the next tile rewrites them
   }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) {
@@ -219,15 +224,13 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(TableRef t, Entries e,
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    uint32_t total = 0;
-    for (int w = 0; w < kThreads / 64; ++w) total += wave_live[w];
-    if (total) {
-      for (int w = 1; w < kThreads / 64; ++w) {
-        fold[0][0] &= fold[w][0];
-        fold[0][1] |= fold[w][1];
-        fold[0][2] &= fold[w][2];
-        fold[0][3] |= fold[w][3];
-      }
+    for (int w = 1; w < kThreads / 64; ++w) {
+      fold[0][0] &= fold[w][0];
+      fold[0][1] |= fold[w][1];
+      fold[0][2] &= fold[w][2];
+      fold[0][3] |= fold[w][3];
+    }
+    if (fold[0][0] != ~0ull || fold[0][1] != 0) {  // some live entry was seen (an all-ones key has OR != 0)
       atomicAnd(ull(&e.counters[4]), (unsigned long long)fold[0][0]);
       atomicOr(ull(&e.counters[5]), (unsigned long long)fold[0][1]);
       atomicAnd(ull(&e.counters[6]), (unsigned long long)fold[0][2]);
@@ -462,8 +465,9 @@ gleam_status gather_sorted(const gleam_cache* c, void* ws, const MaintLayout& L,
   gleam_status st = launch_status("maint_init_kernel");
   if (st != GLEAM_OK) return st;
   const SortBuf a = sort_a(ws, L, words);
-  const uint32_t tiles = (uint32_t)((L.m + kGatherTile - 1) / kGatherTile);
-  hipLaunchKernelGGL(gather_kernel, dim3(tiles), dim3(kThreads), 0, s, table_ref(c), entries_at(ws, L), a);
+  const uint64_t tiles = (L.m + kGatherTile - 1) / kGatherTile;
+  const uint32_t grid = (uint32_t)(tiles < kGatherMaxGrid ? tiles : kGatherMaxGrid);
+  hipLaunchKernelGGL(gather_kernel, dim3(grid), dim3(kThreads), 0, s, table_ref(c), entries_at(ws, L), a, tiles);
   if ((st = launch_status("gather_kernel")) != GLEAM_OK) return st;
   // the key words' bits: (key, stamp) words are counters[4..7]; with one word the sort
   // reads only the key's pair, with two the stamp's as the high word

@@ -1,6 +1,7 @@
 // Device-wide LSD radix sort of (key, index) pairs for the table's maintenance calls
-// (eviction order and export order), written for gfx950 so those calls enqueue kernels
-// only (no library sort, no memsets): a caller may capture them in a HIP graph.
+// (eviction order and export order) and the address map's update (removals and
+// additions by start), written for gfx950 so those calls enqueue kernels only (no
+// library sort, no memsets): a caller may capture them in a HIP graph.
 //
 // Keys are 64 or 128 bits (hi:lo), indices u32. Each pass sorts by one 8-bit digit,
 // stably, in three launches over 4096-element tiles:
@@ -18,8 +19,8 @@
 // return at once for such a pass, and the buffers' roles (which holds the input) follow
 // from how many passes before it were not skipped. Nothing is decided on the host, so
 // the launches are fixed and a graph of them replays correctly for any keys.
-// The sorted order of pairs with distinct keys does not depend on the input order; the
-// callers' keys are distinct (a table's keys, or (stamp, key) pairs).
+// The sort is stable: equal keys keep their input order (the address map's callers
+// number their entries in input order, so ties go to the lower index).
 #pragma once
 
 #include "gleam_device.h"
@@ -73,9 +74,17 @@ __global__ __launch_bounds__(kSortThreads) void sort_hist_kernel(SortBuf a, Sort
   h[threadIdx.x] = 0;
   __syncthreads();
   const uint64_t base = (uint64_t)blockIdx.x * kSortTile;
+  const uint64_t last = n ? n - 1 : 0;  // element 0 exists: the buffers hold n_max >= 1
+  uint64_t w[kSortItems];
+#pragma unroll
+  for (int r = 0; r < kSortItems; ++r) {  // unconditional (clamped) loads, issued together
+    const uint64_t i = base + (uint64_t)r * kSortThreads + threadIdx.x;
+    w[r] = word[i < last ? i : last];
+  }
+#pragma unroll
   for (int r = 0; r < kSortItems; ++r) {
     const uint64_t i = base + (uint64_t)r * kSortThreads + threadIdx.x;
-    if (i < n) atomicAdd(&h[(uint32_t)(word[i] >> sh) & 0xFFu], 1u);
+    if (i < n) atomicAdd(&h[(uint32_t)(w[r] >> sh) & 0xFFu], 1u);
   }
   __syncthreads();
   count[(uint64_t)threadIdx.x * tiles + blockIdx.x] = h[threadIdx.x];
@@ -168,12 +177,12 @@ __global__ __launch_bounds__(kSortThreads) void sort_scatter_kernel(SortBuf a, S
   uint64_t lo[kSortItems], hi[kSortItems];
   uint32_t ix[kSortItems], dg[kSortItems], pos[kSortItems];
 #pragma unroll
-  for (int r = 0; r < kSortItems; ++r) {
+  for (int r = 0; r < kSortItems; ++r) {  // unconditional (clamped) loads, issued together
     const uint32_t li = wave * kSortWaveSpan + r * 64 + lane;
-    const bool valid = li < in_tile;
-    lo[r] = valid ? in.lo[tile0 + li] : 0;
-    hi[r] = (kWords == 2 && valid) ? in.hi[tile0 + li] : 0;
-    ix[r] = valid ? in.idx[tile0 + li] : 0;
+    const uint64_t at = tile0 + (li < in_tile ? li : in_tile - 1);
+    lo[r] = in.lo[at];
+    hi[r] = kWords == 2 ? in.hi[at] : 0;
+    ix[r] = in.idx[at];
   }
   __syncthreads();  // run[] cleared
 
@@ -195,6 +204,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_scatter_kernel(SortBuf a, S
     dg[r] = d;
     pos[r] = prior + below;
     if (valid && below == 0) run[wave][d] = prior + (uint32_t)__popcll(peers);
+    wave_lds_sync();  // this round's counts before the next round's reads
   }
   __syncthreads();  // every wave's digit counts complete
 
@@ -257,6 +267,143 @@ __global__ __launch_bounds__(kSortThreads) void sort_scatter_kernel(SortBuf a, S
   }
 }
 
+// Sorts of at most kSortSmallMax elements run whole in one 1024-lane workgroup: every
+// pass in one launch instead of three launches per pass. Wave w owns elements
+// [w * 1024, (w + 1) * 1024), 16 per lane (element w * 1024 + 64 r + lane in round r).
+// A pass loads the digit word of the wave's share, ranks it stably with the same
+// ballots and a running per-digit count in the wave's own LDS row (so no barrier
+// between rounds), and turns the row totals into each wave's offset within each digit
+// and a scan over digits into each digit's first position. It then moves the elements
+// one word at a time through LDS: each lane reads its elements' word again (coalesced;
+// the share does not fit in registers beside the ranks) and places it at its sorted
+// position in LDS, and the workgroup writes LDS out in order, so the global stores
+// are coalesced (a single CU scattering 8-byte stores is slow). Passes alternate
+// between the two buffers through global memory, a workgroup barrier apart, and skip
+// exactly the passes the large sort skips, so the result is where sort_result() says.
+constexpr int kSortSmallThreads = 1024;
+constexpr int kSortSmallWaves = kSortSmallThreads / 64;
+constexpr uint32_t kSortSmallMax = (uint32_t)kSortSmallThreads * kSortItems;  // 16384
+
+// A lane's 16 elements first + 64 r of src, loaded without a guard (the buffers hold
+// sort_capacity(n_max) elements, a whole number of wave spans, so a wave that holds any
+// element may read its whole span), so that the loads issue together rather than as one
+// guarded round trip each. Elements past n are read but never used.
+template <typename T>
+__device__ __forceinline__ void small_share(const T* src, uint32_t first, T (&x)[kSortItems]) {
+#pragma unroll
+  for (int r = 0; r < kSortItems; ++r) x[r] = src[first + r * 64];
+}
+
+template <int kWords>
+__global__ __launch_bounds__(kSortSmallThreads) void sort_small_kernel(SortBuf a, SortBuf b, const uint64_t* n_dev,
+                                                                       const uint64_t* bits, uint64_t n_max) {
+  __shared__ uint32_t run[kSortSmallWaves][kDigits];  // per wave: digit counts, then offsets within each digit
+  __shared__ uint32_t dstart[kDigits];                 // each digit's first position
+  __shared__ uint32_t wsum[kDigits / 64];
+  __shared__ uint64_t xch[kSortSmallMax];              // one word of every element, in sorted order
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t lt_mask = lane ? (~0ull >> (64 - lane)) : 0ull;
+  const uint32_t span0 = (uint32_t)wave * kSortWaveSpan;
+  const uint64_t n_all = *n_dev;
+  const uint32_t n = (uint32_t)(n_all < n_max ? n_all : n_max);
+  if (n == 0) return;
+  const bool has = span0 < n;  // this wave's span holds elements (uniform over the wave)
+  SortBuf in = a, out = b;
+  for (uint32_t pass = 0; pass < 8u * kWords; ++pass) {
+    if (pass_trivial(bits, pass)) continue;  // uniform: every lane reads the same words
+
+    const uint32_t sh = (8 * pass) & 63;
+    const uint64_t* word = (kWords == 2 && pass >= 8) ? in.hi : in.lo;
+    for (int k = threadIdx.x; k < kSortSmallWaves * kDigits; k += kSortSmallThreads) (&run[0][0])[k] = 0;
+    uint32_t rank[kSortItems];  // (position within the wave's share of the digit) << 8 | digit
+    {
+      uint64_t w[kSortItems] = {};
+      if (has) small_share(word, span0 + lane, w);
+#pragma unroll
+      for (int r = 0; r < kSortItems; ++r) rank[r] = (uint32_t)(w[r] >> sh) & 0xFFu;
+    }
+    __syncthreads();  // run[] cleared
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+      const bool valid = span0 + r * 64 + lane < n;
+      const uint32_t d = rank[r];
+      uint64_t peers = __ballot(valid);
+#pragma unroll
+      for (int bit = 0; bit < 8; ++bit) {
+        const uint64_t ones = __ballot(valid && ((d >> bit) & 1u));
+        peers &= ((d >> bit) & 1u) ? ones : ~ones;
+      }
+      const uint32_t below = (uint32_t)__popcll(peers & lt_mask);
+      const uint32_t prior = run[wave][d];
+      rank[r] = (prior + below) << 8 | d;
+      if (valid && below == 0) run[wave][d] = prior + (uint32_t)__popcll(peers);
+      wave_lds_sync();  // this round's counts before the next round's reads
+    }
+    __syncthreads();  // every wave's digit counts complete
+    uint32_t tot = 0, incl = 0;
+    if (threadIdx.x < kDigits) {  // digit d = threadIdx.x: each wave's offset within d
+      const int d = threadIdx.x;
+      for (int w = 0; w < kSortSmallWaves; ++w) {
+        const uint32_t c = run[w][d];
+        run[w][d] = tot;
+        tot += c;
+      }
+      incl = tot;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(incl, o, 64);
+        if (lane >= o) incl += y;
+      }
+      if (lane == 63) wsum[wave] = incl;
+    }
+    __syncthreads();
+    if (threadIdx.x < kDigits) {
+      uint32_t before = 0;
+      for (int w = 0; w < wave; ++w) before += wsum[w];
+      dstart[threadIdx.x] = before + incl - tot;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {  // rank becomes the sorted position
+      const uint32_t d = rank[r] & 0xFFu;
+      rank[r] = dstart[d] + run[wave][d] + (rank[r] >> 8);
+    }
+    // move every element's words and index to its position through LDS, one array at a
+    // time, so that the global stores are in order
+    uint64_t x[kSortItems] = {};
+    uint32_t xi[kSortItems] = {};
+    if (has) {
+      small_share(in.lo, span0 + lane, x);
+      small_share(in.idx, span0 + lane, xi);
+    }
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r)
+      if (span0 + r * 64 + lane < n) xch[rank[r]] = x[r];
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < n; j += kSortSmallThreads) out.lo[j] = xch[j];
+    if (kWords == 2) {
+      if (has) small_share(in.hi, span0 + lane, x);
+      __syncthreads();  // xch read out before it is refilled
+#pragma unroll
+      for (int r = 0; r < kSortItems; ++r)
+        if (span0 + r * 64 + lane < n) xch[rank[r]] = x[r];
+      __syncthreads();
+      for (uint32_t j = threadIdx.x; j < n; j += kSortSmallThreads) out.hi[j] = xch[j];
+    }
+    __syncthreads();
+    uint32_t* xidx = reinterpret_cast<uint32_t*>(xch);
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r)
+      if (span0 + r * 64 + lane < n) xidx[rank[r]] = xi[r];
+    __syncthreads();
+    for (uint32_t j = threadIdx.x; j < n; j += kSortSmallThreads) out.idx[j] = xidx[j];
+    __syncthreads();  // this pass's stores visible to the workgroup before the next pass loads
+    const SortBuf t = in;
+    in = out;
+    out = t;
+  }
+}
+
 // Workspace of a sort of n elements with `words` 64-bit key words: the second key/index
 // buffer (b), the digit-major tile counts and the digit totals.
 struct SortLayout {
@@ -264,9 +411,16 @@ struct SortLayout {
   size_t hi, lo, idx, count, totals, total;
 };
 
-inline SortLayout sort_layout(uint64_t n, int words) {
+// Elements to allocate in each key/index buffer of a sort of at most n elements (the
+// caller's buffer a too): a one-workgroup sort reads whole wave spans.
+inline uint64_t sort_capacity(uint64_t n) {
+  return n <= kSortSmallMax ? (n + kSortWaveSpan - 1) / kSortWaveSpan * kSortWaveSpan : n;
+}
+
+inline SortLayout sort_layout(uint64_t n_max, int words) {
   SortLayout L;
-  L.tiles = (n + kSortTile - 1) / kSortTile;
+  const uint64_t n = sort_capacity(n_max);
+  L.tiles = (n_max + kSortTile - 1) / kSortTile;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -290,13 +444,22 @@ inline SortBuf sort_other(void* ws, uint64_t n_max, int words) {
 }
 
 // Sorts the first *n_dev (at most n_max, a device count the host does not read) pairs of
-// `a` (keys of `words` 64-bit words, 1 or 2; n_max below 2^32) by key, ascending.
+// `a` (keys of `words` 64-bit words, 1 or 2; n_max below 2^32) by key, ascending. Each
+// of a's arrays holds sort_capacity(n_max) elements.
 // `bits` (device u64[4], see pass_trivial) must describe those keys. The result is in `a`
 // or in the workspace's buffer (sort_other), as sort_result() tells on the device. Grids
 // are sized for n_max; tiles past *n_dev do nothing.
 inline gleam_status radix_sort_pairs(SortBuf a, const uint64_t* n_dev, const uint64_t* bits, uint64_t n_max,
                                      int words, void* ws, hipStream_t s) {
   if (n_max == 0) return GLEAM_OK;
+  if (n_max <= kSortSmallMax) {
+    const SortBuf b = sort_other(ws, n_max, words);
+    if (words == 2)
+      hipLaunchKernelGGL(sort_small_kernel<2>, dim3(1), dim3(kSortSmallThreads), 0, s, a, b, n_dev, bits, n_max);
+    else
+      hipLaunchKernelGGL(sort_small_kernel<1>, dim3(1), dim3(kSortSmallThreads), 0, s, a, b, n_dev, bits, n_max);
+    return launch_status("sort_small_kernel");
+  }
   const SortLayout L = sort_layout(n_max, words);
   uint8_t* p = static_cast<uint8_t*>(ws);
   const SortBuf b = sort_other(ws, n_max, words);

@@ -23,8 +23,8 @@
 //   1. removal ranges are sorted by start, with a running maximum of their last
 //      addresses, so one binary search tells whether an interval meets any of them;
 //      the survivors are compacted, in order, into the workspace (one scan);
-//   2. only the valid additions are sorted (rocPRIM radix sort; invalid ones take the
-//      key kNone and sort last);
+//   2. only the valid additions are sorted (the library's radix sort, radix_sort.h;
+//      invalid ones take the key kNone and sort last);
 //   3. an addition meets an earlier-starting addition iff the running maximum of ends
 //      just before it passes its start, a later-starting one iff the next start comes
 //      before its end, and a survivor iff the last survivor starting at or before its
@@ -37,11 +37,10 @@
 
 #include <new>
 
-#include <rocprim/device/device_radix_sort.hpp>
-#include <rocprim/device/device_scan.hpp>
-
+#include "device_scan.h"
 #include "gleam_device.h"
 #include "gleam_internal.h"
+#include "radix_sort.h"
 
 namespace gleam {
 namespace {
@@ -71,11 +70,11 @@ MapRef map_ref(const gleam_remap* m) {
 
 // Workspace of one update (cap = capacity, A = additions, R = removal ranges).
 struct UpdLayout {
+  size_t hdr;                                // [0] R, [1] A (the sorts' counts); [4..7] R's key bits, [8..11] A's
   size_t keep, kpos, s_start, s_et;         // cap: survivor flag, its scan, compacted survivors
-  size_t ka, kb, va, vb, aend, amax, acc, apos;  // A: sort keys/values, ends, running max, kept flag, scan
-  size_t rka, rkb, rva, rvb, rmax;          // R: removal ranges sorted by start, running max of last
-  size_t tmp, tmp_bytes, total;
-  bool ok;  // rocPRIM's storage queries succeeded
+  size_t ka, aidx, kb, vb, aend, amax, acc, apos;  // A: sort keys/indices, sorted keys/indices, ends, running max, kept flag, scan
+  size_t rka, ridx, rkb, rvb, rmax;         // R: sort keys/indices, sorted starts, their last addresses, running max
+  size_t sort, partial, total;              // the sort's second buffer and counts; the scans' tile totals
 };
 
 UpdLayout upd_layout(uint64_t cap, uint64_t n_add, uint64_t n_del) {
@@ -86,37 +85,28 @@ UpdLayout upd_layout(uint64_t cap, uint64_t n_add, uint64_t n_del) {
     off = (off + bytes + 255) & ~(size_t)255;
     return o;
   };
+  L.hdr = take(256);
   L.keep = take(8 * cap);
   L.kpos = take(8 * cap);
   L.s_start = take(8 * cap);
   L.s_et = take(16 * cap);
-  L.ka = take(8 * n_add);
+  L.ka = take(8 * sort_capacity(n_add));
+  L.aidx = take(4 * sort_capacity(n_add));
   L.kb = take(8 * n_add);
-  L.va = take(8 * n_add);
   L.vb = take(8 * n_add);
   L.aend = take(8 * n_add);
   L.amax = take(8 * n_add);
   L.acc = take(8 * n_add);
   L.apos = take(8 * n_add);
-  L.rka = take(8 * n_del);
+  L.rka = take(8 * sort_capacity(n_del));
+  L.ridx = take(4 * sort_capacity(n_del));
   L.rkb = take(8 * n_del);
-  L.rva = take(8 * n_del);
   L.rvb = take(8 * n_del);
   L.rmax = take(8 * n_del);
   const uint64_t ar = n_add > n_del ? n_add : n_del;
-  const uint64_t ca = cap > n_add ? cap : n_add;
-  size_t sort_b = 0, max_b = 0, sum_b = 0;
-  const hipError_t e1 = rocprim::radix_sort_pairs(nullptr, sort_b, (const uint64_t*)nullptr, (uint64_t*)nullptr,
-                                                  (const uint64_t*)nullptr, (uint64_t*)nullptr, (size_t)ar, 0, 64);
-  const hipError_t e2 = rocprim::inclusive_scan(nullptr, max_b, (const uint64_t*)nullptr, (uint64_t*)nullptr,
-                                                (size_t)ar, rocprim::maximum<uint64_t>());
-  const hipError_t e3 = rocprim::exclusive_scan(nullptr, sum_b, (const uint64_t*)nullptr, (uint64_t*)nullptr,
-                                                (uint64_t)0, (size_t)ca, rocprim::plus<uint64_t>());
-  L.ok = e1 == hipSuccess && e2 == hipSuccess && e3 == hipSuccess;
-  L.tmp_bytes = sort_b;
-  if (max_b > L.tmp_bytes) L.tmp_bytes = max_b;
-  if (sum_b > L.tmp_bytes) L.tmp_bytes = sum_b;
-  L.tmp = take(L.tmp_bytes);
+  const uint64_t most = cap > ar ? cap : ar;
+  L.sort = take(sort_layout(ar, 1).total);
+  L.partial = take(8 * scan_tiles(most));
   L.total = off;
   return L;
 }
@@ -124,6 +114,13 @@ UpdLayout upd_layout(uint64_t cap, uint64_t n_add, uint64_t n_del) {
 uint32_t grid_for(uint64_t n) {
   const uint64_t g = (n + kThreads - 1) / kThreads;
   return (uint32_t)(g == 0 ? 1 : (g < kMaxGrid ? g : kMaxGrid));
+}
+
+// Grid of a kernel that folds key bits with one pair of atomics per workgroup: few
+// enough workgroups that those atomics on two words do not queue behind each other.
+uint32_t fold_grid(uint64_t n) {
+  const uint32_t g = grid_for(n);
+  return g < 256 ? g : 256;
 }
 
 // Number of entries of the ascending keys[0, n) that are <= x (upper bound).
@@ -150,12 +147,63 @@ __device__ __forceinline__ uint64_t count_lt(const uint64_t* keys, uint64_t n, u
 
 // Removal ranges as sort key = first address, value = last address (clipped at 2^64 - 1);
 // an empty range takes the key kNone and is never found.
-__global__ void removal_prep_kernel(const uint64_t* d_start, const uint64_t* d_len, uint64_t r, uint64_t* key,
-                                    uint64_t* last) {
+// Counts of the two sorts and the AND/OR words of their keys (see radix_sort.h).
+__global__ void update_init_kernel(uint64_t* hdr, uint64_t r, uint64_t n_add) {
+  const int t = threadIdx.x;
+  if (t < 12) hdr[t] = t == 0 ? r : t == 1 ? n_add : (t == 4 || t == 8) ? ~0ull : 0ull;
+}
+
+// Fold a thread's AND/OR of keys into bits[0] (AND) and bits[1] (OR): one pair of
+// atomics per workgroup. Every thread of the workgroup calls it.
+__device__ void fold_key_bits(uint64_t and_k, uint64_t or_k, uint64_t* bits) {
+  __shared__ uint64_t fold[kThreads / 64][2];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    and_k &= shfl_xor64(and_k, o);
+    or_k |= shfl_xor64(or_k, o);
+  }
+  if (lane == 0) {
+    fold[wave][0] = and_k;
+    fold[wave][1] = or_k;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < kThreads / 64; ++w) {
+      and_k &= fold[w][0];
+      or_k |= fold[w][1];
+    }
+    atomicAnd(reinterpret_cast<unsigned long long*>(&bits[0]), (unsigned long long)and_k);
+    atomicOr(reinterpret_cast<unsigned long long*>(&bits[1]), (unsigned long long)or_k);
+  }
+}
+
+// Sort key of removal k: its start, or kNone for an empty range (it sorts last).
+__global__ __launch_bounds__(kThreads) void removal_prep_kernel(const uint64_t* d_start, const uint64_t* d_len,
+                                                                uint64_t r, uint64_t* key, uint32_t* idx,
+                                                                uint64_t* bits) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  uint64_t and_k = ~0ull, or_k = 0;
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < r; k += stride) {
+    const uint64_t s = d_len[k] ? d_start[k] : kNone;
+    key[k] = s;
+    idx[k] = (uint32_t)k;
+    and_k &= s;
+    or_k |= s;
+  }
+  fold_key_bits(and_k, or_k, bits);
+}
+
+// Sorted removals: start, and last address (the running maximum of these tells whether
+// any removal starting at or before an address reaches it).
+__global__ void removal_unpack_kernel(SortBuf a, SortBuf b, const uint64_t* bits, const uint64_t* d_start,
+                                      const uint64_t* d_len, uint64_t r, uint64_t* key, uint64_t* last) {
+  const SortBuf sorted = sort_result(a, b, bits, 1);
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
   for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < r; k += stride) {
-    const uint64_t s = d_start[k], n = d_len[k];
-    key[k] = n ? s : kNone;
+    const uint32_t j = sorted.idx[k];
+    const uint64_t s = d_start[j], n = d_len[j];
+    key[k] = sorted.lo[k];
     last[k] = n ? (n - 1 > kNone - s ? kNone : s + n - 1) : 0;
   }
 }
@@ -187,25 +235,39 @@ __global__ void compact_kernel(MapRef map, const uint64_t* keep, const uint64_t*
 }
 
 // Sort key of addition j: its start if valid, else kNone (status INVALID).
-__global__ void addition_prep_kernel(const uint64_t* a_start, const uint64_t* a_len, const uint64_t* a_target,
-                                     uint64_t n_add, uint8_t* status, uint64_t* key, uint64_t* val) {
+__global__ __launch_bounds__(kThreads) void addition_prep_kernel(const uint64_t* a_start, const uint64_t* a_len,
+                                                                 const uint64_t* a_target, uint64_t n_add,
+                                                                 uint8_t* status, uint64_t* key, uint32_t* idx,
+                                                                 uint64_t* bits) {
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  uint64_t and_k = ~0ull, or_k = 0;
   for (uint64_t j = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n_add; j += stride) {
     const uint64_t s = a_start[j], n = a_len[j], t = a_target[j];
     const bool valid = n != 0 && n <= kNone - s && n <= kNone - t;
     if (!valid && status) status[j] = GLEAM_REMAP_INVALID;
-    key[j] = valid ? s : kNone;
-    val[j] = j;
+    const uint64_t k = valid ? s : kNone;
+    key[j] = k;
+    idx[j] = (uint32_t)j;
+    and_k &= k;
+    or_k |= k;
   }
+  fold_key_bits(and_k, or_k, bits);
 }
 
-// End of each sorted addition; an invalid one ends at 0 (it sorts last, after every
-// valid one, so the running maximum of ends only ever sees real ends before it).
-__global__ void addition_end_kernel(const uint64_t* key, const uint64_t* val, const uint64_t* a_len, uint64_t n_add,
-                                    uint64_t* aend) {
+// Sorted additions: start, original index, and end; an invalid one ends at 0 (it sorts
+// last, after every valid one, so the running maximum of ends only ever sees real ends
+// before it).
+__global__ void addition_unpack_kernel(SortBuf a, SortBuf b, const uint64_t* bits, const uint64_t* a_len,
+                                       uint64_t n_add, uint64_t* key, uint64_t* val, uint64_t* aend) {
+  const SortBuf sorted = sort_result(a, b, bits, 1);
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n_add; k += stride)
-    aend[k] = key[k] == kNone ? 0 : key[k] + a_len[val[k]];
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n_add; k += stride) {
+    const uint64_t s = sorted.lo[k];
+    const uint32_t j = sorted.idx[k];
+    key[k] = s;
+    val[k] = j;
+    aend[k] = s == kNone ? 0 : s + a_len[j];
+  }
 }
 
 // Keep a valid addition that meets no other valid addition and no survivor.
@@ -234,8 +296,8 @@ __global__ void addition_classify_kernel(const uint64_t* key, const uint64_t* va
 
 // Batches of at most kSmall removals or additions (a task's allocations, its tensors) are
 // handled by one 1024-lane workgroup in LDS instead of the several launches of the
-// rocPRIM sort and scans: a bitonic sort of (key, index) pairs and Hillis-Steele scans
-// over at most 2048 entries.
+// device-wide sort and scans: a bitonic sort of (key, index) pairs and Hillis-Steele
+// scans over at most 2048 entries.
 constexpr int kSmallThreads = 1024;
 constexpr uint32_t kSmall = 2 * kSmallThreads;
 
@@ -577,8 +639,7 @@ extern "C" gleam_status gleam_remap_destroy(gleam_remap* m) {
 
 extern "C" size_t gleam_remap_update_bytes(const gleam_remap* m, uint64_t n_add, uint64_t n_del) {
   if (!m || n_add > gleam::kMaxCount || n_del > gleam::kMaxCount) return 0;
-  const gleam::UpdLayout L = gleam::upd_layout(m->capacity, n_add, n_del);
-  return L.ok ? L.total : 0;
+  return gleam::upd_layout(m->capacity, n_add, n_del).total;
 }
 
 extern "C" gleam_status gleam_remap_update(gleam_remap* m, const uint64_t* d_del_start, const uint64_t* d_del_len,
@@ -600,10 +661,6 @@ extern "C" gleam_status gleam_remap_update(gleam_remap* m, const uint64_t* d_del
     return GLEAM_E_UNSUPPORTED;
   }
   const UpdLayout L = upd_layout(m->capacity, n_add, n_del);
-  if (!L.ok) {
-    set_error("gleam_remap_update: rocPRIM storage query failed");
-    return GLEAM_E_HIP;
-  }
   if (!d_ws || !aligned256(d_ws)) {
     set_error("gleam_remap_update: workspace must be non-null and 256-byte aligned");
     return GLEAM_E_INVALID;
@@ -615,11 +672,14 @@ extern "C" gleam_status gleam_remap_update(gleam_remap* m, const uint64_t* d_del
   hipStream_t s = (hipStream_t)stream;
   uint8_t* b = static_cast<uint8_t*>(d_ws);
   auto at = [&](size_t off) { return reinterpret_cast<uint64_t*>(b + off); };
-  void* tmp = b + L.tmp;
-  size_t tmp_bytes;
+  uint64_t* hdr = at(L.hdr);
+  uint64_t* partial = at(L.partial);
+  void* sort_ws = b + L.sort;
   const MapRef map = map_ref(m);
   const uint64_t cap = m->capacity;
   gleam_status st;
+  hipLaunchKernelGGL(update_init_kernel, dim3(1), dim3(64), 0, s, hdr, n_del, n_add);
+  if ((st = launch_status("update_init_kernel")) != GLEAM_OK) return st;
 
   // 1. removals, survivors
   const uint64_t* rkey = nullptr;
@@ -631,30 +691,23 @@ extern "C" gleam_status gleam_remap_update(gleam_remap* m, const uint64_t* d_del
     rkey = at(L.rkb);
     rmax = at(L.rmax);
   } else if (n_del > 0) {
-    hipLaunchKernelGGL(removal_prep_kernel, dim3(grid_for(n_del)), dim3(kThreads), 0, s, d_del_start, d_del_len,
-                       n_del, at(L.rka), at(L.rva));
+    const SortBuf ra{nullptr, at(L.rka), reinterpret_cast<uint32_t*>(b + L.ridx)};
+    const SortBuf rb = sort_other(sort_ws, n_del, 1);
+    hipLaunchKernelGGL(removal_prep_kernel, dim3(fold_grid(n_del)), dim3(kThreads), 0, s, d_del_start, d_del_len,
+                       n_del, ra.lo, ra.idx, hdr + 4);
     if ((st = launch_status("removal_prep_kernel")) != GLEAM_OK) return st;
-    tmp_bytes = L.tmp_bytes;
-    st = hip_call(rocprim::radix_sort_pairs(tmp, tmp_bytes, at(L.rka), at(L.rkb), at(L.rva), at(L.rvb),
-                                            (size_t)n_del, 0, 64, s),
-                  "radix sort (removals)");
-    if (st != GLEAM_OK) return st;
-    tmp_bytes = L.tmp_bytes;
-    st = hip_call(rocprim::inclusive_scan(tmp, tmp_bytes, at(L.rvb), at(L.rmax), (size_t)n_del,
-                                          rocprim::maximum<uint64_t>(), s),
-                  "running maximum (removals)");
-    if (st != GLEAM_OK) return st;
+    if ((st = radix_sort_pairs(ra, hdr, hdr + 4, n_del, 1, sort_ws, s)) != GLEAM_OK) return st;
+    hipLaunchKernelGGL(removal_unpack_kernel, dim3(grid_for(n_del)), dim3(kThreads), 0, s, ra, rb, hdr + 4,
+                       d_del_start, d_del_len, n_del, at(L.rkb), at(L.rvb));
+    if ((st = launch_status("removal_unpack_kernel")) != GLEAM_OK) return st;
+    if ((st = device_scan<ScanMax, false>(at(L.rvb), at(L.rmax), n_del, partial, s)) != GLEAM_OK) return st;
     rkey = at(L.rkb);
     rmax = at(L.rmax);
   }
   const dim3 block(kThreads), gcap(grid_for(cap)), gadd(grid_for(n_add));
   hipLaunchKernelGGL(survive_kernel, gcap, block, 0, s, map, rkey, rmax, n_del, at(L.keep));
   if ((st = launch_status("survive_kernel")) != GLEAM_OK) return st;
-  tmp_bytes = L.tmp_bytes;
-  st = hip_call(rocprim::exclusive_scan(tmp, tmp_bytes, at(L.keep), at(L.kpos), (uint64_t)0, (size_t)cap,
-                                        rocprim::plus<uint64_t>(), s),
-                "scan (survivors)");
-  if (st != GLEAM_OK) return st;
+  if ((st = device_scan<ScanSum, true>(at(L.keep), at(L.kpos), cap, partial, s)) != GLEAM_OK) return st;
   hipLaunchKernelGGL(compact_kernel, gcap, block, 0, s, map, at(L.keep), at(L.kpos), at(L.s_start),
                      reinterpret_cast<ulonglong2*>(at(L.s_et)));
   if ((st = launch_status("compact_kernel")) != GLEAM_OK) return st;
@@ -667,30 +720,21 @@ extern "C" gleam_status gleam_remap_update(gleam_remap* m, const uint64_t* d_del
                        at(L.vb), at(L.aend), at(L.acc), at(L.apos));
     if ((st = launch_status("additions_small_kernel")) != GLEAM_OK) return st;
   } else if (n_add > 0) {
-    hipLaunchKernelGGL(addition_prep_kernel, gadd, block, 0, s, d_add_start, d_add_len, d_add_target, n_add,
-                       d_add_status, at(L.ka), at(L.va));
+    const SortBuf aa{nullptr, at(L.ka), reinterpret_cast<uint32_t*>(b + L.aidx)};
+    const SortBuf ab = sort_other(sort_ws, n_add, 1);
+    hipLaunchKernelGGL(addition_prep_kernel, dim3(fold_grid(n_add)), block, 0, s, d_add_start, d_add_len,
+                       d_add_target, n_add, d_add_status, aa.lo, aa.idx, hdr + 8);
     if ((st = launch_status("addition_prep_kernel")) != GLEAM_OK) return st;
-    tmp_bytes = L.tmp_bytes;
-    st = hip_call(rocprim::radix_sort_pairs(tmp, tmp_bytes, at(L.ka), at(L.kb), at(L.va), at(L.vb), (size_t)n_add,
-                                            0, 64, s),
-                  "radix sort (additions)");
-    if (st != GLEAM_OK) return st;
-    hipLaunchKernelGGL(addition_end_kernel, gadd, block, 0, s, at(L.kb), at(L.vb), d_add_len, n_add, at(L.aend));
-    if ((st = launch_status("addition_end_kernel")) != GLEAM_OK) return st;
-    tmp_bytes = L.tmp_bytes;
-    st = hip_call(rocprim::inclusive_scan(tmp, tmp_bytes, at(L.aend), at(L.amax), (size_t)n_add,
-                                          rocprim::maximum<uint64_t>(), s),
-                  "running maximum (additions)");
-    if (st != GLEAM_OK) return st;
+    if ((st = radix_sort_pairs(aa, hdr + 1, hdr + 8, n_add, 1, sort_ws, s)) != GLEAM_OK) return st;
+    hipLaunchKernelGGL(addition_unpack_kernel, gadd, block, 0, s, aa, ab, hdr + 8, d_add_len, n_add, at(L.kb),
+                       at(L.vb), at(L.aend));
+    if ((st = launch_status("addition_unpack_kernel")) != GLEAM_OK) return st;
+    if ((st = device_scan<ScanMax, false>(at(L.aend), at(L.amax), n_add, partial, s)) != GLEAM_OK) return st;
     hipLaunchKernelGGL(addition_classify_kernel, gadd, block, 0, s, at(L.kb), at(L.vb), at(L.aend), at(L.amax),
                        n_add, at(L.s_start), reinterpret_cast<const ulonglong2*>(at(L.s_et)), at(L.keep),
                        at(L.kpos), cap, d_add_status, at(L.acc));
     if ((st = launch_status("addition_classify_kernel")) != GLEAM_OK) return st;
-    tmp_bytes = L.tmp_bytes;
-    st = hip_call(rocprim::exclusive_scan(tmp, tmp_bytes, at(L.acc), at(L.apos), (uint64_t)0, (size_t)n_add,
-                                          rocprim::plus<uint64_t>(), s),
-                  "scan (additions)");
-    if (st != GLEAM_OK) return st;
+    if ((st = device_scan<ScanSum, true>(at(L.acc), at(L.apos), n_add, partial, s)) != GLEAM_OK) return st;
   }
 
   // 4. merge by rank into the storage (only if everything fits), then the header

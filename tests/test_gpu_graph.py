@@ -273,13 +273,15 @@ def test_graph_replays_erase():
         ot.insert(keys[:400], vals[:400])
 
 
-def test_graph_replays_evict_and_export():
+@pytest.mark.parametrize("cap", [1 << 13, 1 << 14])
+def test_graph_replays_evict_and_export(cap):
     """gleam_cache_evict and gleam_cache_export captured once each: between replays new
     keys are inserted and touched eagerly; every replay evicts the oracle's keys in its
-    order and exports the oracle's table."""
-    rng = np.random.default_rng(1500)
-    cap, keep = 1 << 14, 3000
-    table, ot = g.Cache(cap, max_load=0.7), oracle.Table()
+    order and exports the oracle's table. 2^13 slots sort in one workgroup, 2^14 (plus
+    the side slot) in tiles."""
+    rng = np.random.default_rng(1500 + cap)
+    keep = 3000
+    table, ot = g.Cache(cap, max_load=0.9), oracle.Table()
     ws = table.maint_workspace()
     evicted = torch.empty(cap + 1, dtype=torch.int64, device="cuda")
     counts = torch.empty(2, dtype=torch.int64, device="cuda")

@@ -195,16 +195,17 @@ def test_erase_few_keys_from_large_table():
     assert_table(table, ot, "after erase")
 
 
-def test_evict_full_width_stamps_and_export_order():
+@pytest.mark.parametrize("log2_cap,n,keeps", [(13, 5_000, (4_000, 1_234, 1, 0)),
+                                             (17, 50_000, (40_000, 12_345, 1, 0))])
+def test_evict_full_width_stamps_and_export_order(log2_cap, n, keeps):
     """Stamps spread over all 64 bits (every digit of the two-word sort key matters), the
-    keys 0 and 2^64-1 present, a table of several sort tiles: eviction order and export
-    equal the oracle's."""
-    rng = np.random.default_rng(1002)
-    n = 50_000
+    keys 0 and 2^64-1 present; a table the one-workgroup sort orders (2^13 slots) and one
+    of several sort tiles (2^17): eviction order and export equal the oracle's."""
+    rng = np.random.default_rng(1002 + log2_cap)
     keys = rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False)
     keys[:2] = [0, 2**64 - 1]
     vals = rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False)
-    table, ot = g.Cache(1 << 17, max_load=0.5), oracle.Table()
+    table, ot = g.Cache(1 << log2_cap, max_load=0.7), oracle.Table()
     table.insert(keys_to_device(keys), keys_to_device(vals))
     ot.insert(keys, vals)
     ep = rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False)
@@ -214,7 +215,7 @@ def test_evict_full_width_stamps_and_export_order():
     ot.touch(keys, ep)
     say("lifecycle full-width stamps")
     assert_table(table, ot, "before evict")
-    for keep in (40_000, 12_345, 1, 0):
+    for keep in keeps:
         ev, counts = table.evict(keep)
         torch.cuda.synchronize()
         want = ot.evict(keep)

@@ -179,7 +179,8 @@ def test_fence_strides(count):
     assert_translate(m, om, probes(om, rng, 10_000, 1 << 33), f"fence {count} shrunk")
 
 
-@pytest.mark.parametrize("n_add,n_del", [(1, 1), (2047, 2048), (2048, 2049), (2049, 5), (3000, 2047)])
+@pytest.mark.parametrize("n_add,n_del", [(1, 1), (2047, 2048), (2048, 2049), (2049, 5), (3000, 2047),
+                                         (16_384, 16_385), (16_385, 3)])
 def test_one_workgroup_and_batched_updates(n_add, n_del):
     """Batches of up to 2048 removals or additions run in one workgroup, larger ones
     through the radix sort and scans: both sides of the switch, with clashes, invalid
@@ -267,3 +268,55 @@ def test_binding_refusals():
     m.close()
     with pytest.raises(g.GleamError):
         m.translate(dev([1]))
+
+
+def test_update_replays_in_a_graph():
+    """gleam_remap_update with batches past the one-workgroup size (so through the radix
+    sort and scans) captured once: it clears a region and maps new intervals inside it,
+    so every replay gives the same map, whatever eager updates outside the region did in
+    between; statuses, counts, export and translation equal the oracle's each time."""
+    rng = np.random.default_rng(2400)
+    space, region = 1 << 24, (1 << 22, 1 << 23)
+    m, om = g.Remap(1 << 15), oremap.RemapMap(1 << 15)
+    n0 = 6000
+    base_s = np.sort(rng.choice(space // 256, n0, replace=False).astype(np.uint64)) * np.uint64(256)
+    update_both(m, om, add=(base_s, rng.integers(1, 256, n0, dtype=np.uint64),
+                            rng.integers(0, 1 << 60, n0, dtype=np.uint64)))
+    n_del, n_add = 3000, 2500
+    r_s = np.sort(rng.choice(np.arange(region[0], region[1], 1024, dtype=np.uint64), n_del, replace=False))
+    rem = (r_s, np.full(n_del, 1024, np.uint64))
+    a_s = rng.choice(r_s, n_add, replace=False) + rng.integers(0, 512, n_add, dtype=np.uint64)
+    add = (a_s, rng.integers(1, 256, n_add, dtype=np.uint64), rng.integers(0, 1 << 60, n_add, dtype=np.uint64))
+    d = [dev(x) for x in (*rem, *add)]
+    status = torch.empty(n_add, dtype=torch.uint8, device="cuda")
+    counts = torch.empty(4, dtype=torch.int64, device="cuda")
+    ws = m.update_workspace(n_add, n_del)
+
+    def update_call():
+        g._check(g.lib.gleam_remap_update(m.handle, g._ptr(d[0]), g._ptr(d[1]), n_del, g._ptr(d[2]), g._ptr(d[3]),
+                                          g._ptr(d[4]), n_add, g._ptr(status), g._ptr(counts), g._ptr(ws),
+                                          ws.numel(), g._stream(None)))
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side), torch.cuda.graph(graph, stream=side):
+        update_call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for k in range(3):
+        say("remap update graph replay", k)
+        status.fill_(0xEE)
+        counts.fill_(-1)
+        graph.replay()
+        torch.cuda.synchronize()
+        est, ecounts = om.update(*rem, *add)
+        assert np.array_equal(status.cpu().numpy(), est), f"replay {k}: statuses"
+        got = tuple(int(c) for c in u64(counts))
+        assert got[:len(ecounts)] == tuple(ecounts), f"replay {k}: counts"
+        assert_map(m, om, f"replay {k}")
+        assert_translate(m, om, probes(om, rng, 3000, space), f"replay {k}")
+        # eager work between replays, outside the region
+        out_s = rng.integers(region[1], space, 100, dtype=np.uint64)
+        update_both(m, om, rem=(out_s, np.full(100, 300, np.uint64)),
+                    add=(out_s + np.uint64(50), np.full(100, 10, np.uint64), np.full(100, k, np.uint64)))
