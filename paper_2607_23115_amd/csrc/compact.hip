@@ -27,14 +27,21 @@ constexpr int kScanThreads = 1024;
 constexpr int kSmallPerThread = 16;
 constexpr uint64_t kSmallItems = 1u << 16;  // single-workgroup path up to this many statuses
 
-__device__ __forceinline__ uint32_t count_misses(const uint8_t* status, uint64_t n, uint64_t first) {
-  uint32_t c = 0;
+// Bit e set: status first + e is a MISS (first + e < n). The loads are unconditional,
+// at indices clamped to the last status (n >= 1), so a thread's loads issue together: a
+// guarded load per status compiles to one round trip each.
+template <int kCount>
+__device__ __forceinline__ uint32_t miss_bits(const uint8_t* status, uint64_t n, uint64_t first) {
+  uint8_t v[kCount];
 #pragma unroll
-  for (int e = 0; e < kPerThread; ++e) {
+  for (int e = 0; e < kCount; ++e) {
     const uint64_t g = first + e;
-    c += (g < n && status[g] == GLEAM_MISS) ? 1u : 0u;
+    v[e] = status[g < n ? g : n - 1];
   }
-  return c;
+  uint32_t bits = 0;
+#pragma unroll
+  for (int e = 0; e < kCount; ++e) bits |= (first + e < n && v[e] == GLEAM_MISS) ? (1u << e) : 0u;
+  return bits;
 }
 
 __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x, int lane) {
@@ -70,7 +77,7 @@ __global__ __launch_bounds__(kThreads) void compact_count_kernel(const uint8_t* 
                                                                  uint64_t* tile_counts) {
   __shared__ uint32_t wave_sums[kThreads / 64];
   const uint64_t first = (uint64_t)blockIdx.x * kTileItems + (uint64_t)threadIdx.x * kPerThread;
-  const uint32_t c = count_misses(status, n, first);
+  const uint32_t c = (uint32_t)__builtin_popcount(miss_bits<kPerThread>(status, n, first));
   uint32_t total;
   block_exclusive_scan<kThreads / 64>(c, wave_sums, &total);
   if (threadIdx.x == 0) tile_counts[blockIdx.x] = total;
@@ -110,15 +117,11 @@ __global__ __launch_bounds__(kThreads) void compact_scatter_kernel(const uint8_t
                                                                    uint64_t* miss_idx, ShortBlocks sb) {
   __shared__ uint32_t wave_sums[kThreads / 64];
   const uint64_t first = (uint64_t)blockIdx.x * kTileItems + (uint64_t)threadIdx.x * kPerThread;
-  const uint32_t c = count_misses(status, n, first);
+  const uint32_t bits = miss_bits<kPerThread>(status, n, first);
   uint32_t total;
-  const uint32_t excl = block_exclusive_scan<kThreads / 64>(c, wave_sums, &total);
+  const uint32_t excl = block_exclusive_scan<kThreads / 64>((uint32_t)__builtin_popcount(bits), wave_sums, &total);
   uint64_t out = tile_offsets[blockIdx.x] + excl;
-#pragma unroll
-  for (int e = 0; e < kPerThread; ++e) {
-    const uint64_t g = first + e;
-    if (g < n && status[g] == GLEAM_MISS) miss_idx[out++] = g;
-  }
+  for (uint32_t m = bits; m; m &= m - 1) miss_idx[out++] = first + (uint64_t)__builtin_ctz(m);
   if (!sb.seg_len) return;
   // the grid strides over all payloads (a per-tile range would need a binary search of
   // blk_first: a chain of dependent reads)
@@ -170,7 +173,8 @@ __global__ __launch_bounds__(kThreads) void compact_tally_kernel(const uint8_t* 
   if (blockIdx.x < tiles) {
     const uint64_t first = (uint64_t)blockIdx.x * kTileItems + (uint64_t)threadIdx.x * kPerThread;
     uint32_t total;
-    block_exclusive_scan<kThreads / 64>(count_misses(status, n, first), wave_sums, &total);
+    block_exclusive_scan<kThreads / 64>((uint32_t)__builtin_popcount(miss_bits<kPerThread>(status, n, first)),
+                                        wave_sums, &total);
     if (threadIdx.x == 0) tile_counts[blockIdx.x] = total;
   }
   if (!sb.seg_len) return;
@@ -197,15 +201,11 @@ __global__ __launch_bounds__(kThreads) void compact_place_kernel(const uint8_t* 
   for (uint64_t t = threadIdx.x; t < blockIdx.x; t += kThreads) before += tile_counts[t];
   before = block_sum64(before, wave_parts);
   const uint64_t first = (uint64_t)blockIdx.x * kTileItems + (uint64_t)threadIdx.x * kPerThread;
-  const uint32_t c = count_misses(status, n, first);
+  const uint32_t bits = miss_bits<kPerThread>(status, n, first);
   uint32_t total;
-  const uint32_t excl = block_exclusive_scan<kThreads / 64>(c, wave_sums, &total);
+  const uint32_t excl = block_exclusive_scan<kThreads / 64>((uint32_t)__builtin_popcount(bits), wave_sums, &total);
   uint64_t out = before + excl;
-#pragma unroll
-  for (int e = 0; e < kPerThread; ++e) {
-    const uint64_t g = first + e;
-    if (g < n && status[g] == GLEAM_MISS) miss_idx[out++] = g;
-  }
+  for (uint32_t m = bits; m; m &= m - 1) miss_idx[out++] = first + (uint64_t)__builtin_ctz(m);
   if (blockIdx.x + 1 != tiles) return;
   uint64_t d = 0;
   if (miss_bytes)
@@ -238,12 +238,8 @@ __global__ __launch_bounds__(kScanThreads) void compact_small_kernel(const uint8
 #pragma unroll
       for (int e = 0; e < kSmallPerThread; ++e)
         bits |= ((w[e >> 2] >> (8 * (e & 3))) & 0xFFu) == GLEAM_MISS ? (1u << e) : 0u;
-    } else {
-#pragma unroll
-      for (int e = 0; e < kSmallPerThread; ++e) {
-        const uint64_t g = first + e;
-        bits |= (g < n && status[g] == GLEAM_MISS) ? (1u << e) : 0u;
-      }
+    } else if (first < n) {
+      bits = miss_bits<kSmallPerThread>(status, n, first);
     }
     uint32_t total;
     const uint32_t excl = block_exclusive_scan<kScanThreads / 64>((uint32_t)__builtin_popcount(bits), wave_sums,
