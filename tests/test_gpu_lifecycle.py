@@ -222,3 +222,34 @@ def test_evict_full_width_stamps_and_export_order(log2_cap, n, keeps):
         assert u64(counts).tolist() == [want.size, len(ot)]
         assert np.array_equal(u64(ev)[:want.size], want)
         assert_table(table, ot, f"after evict to {keep}")
+
+
+@pytest.mark.parametrize("log2_cap", [13, 14])
+def test_sort_skips_shared_digits(log2_cap):
+    """Keys that differ only in their top byte (seven of the export's eight digit passes
+    move nothing), all stamps equal (every stamp pass moves nothing), tables of 0, 1 and
+    2 entries (no pass moves anything): the orders still equal the oracle's, in the
+    one-workgroup sort (2^13 slots) and the tiled one (2^14 slots plus the side slot)."""
+    rng = np.random.default_rng(1003 + log2_cap)
+    base = np.uint64(0x0012_3456_789A_BCDE)
+    tops = rng.choice(256, 200, replace=False).astype(np.uint64)
+    cases = {"top byte": base | (tops << np.uint64(56)), "empty": np.zeros(0, np.uint64),
+             "one": np.array([7], np.uint64), "two": np.array([2**64 - 1, 0], np.uint64)}
+    for what, keys in cases.items():
+        say("lifecycle shared digits", log2_cap, what)
+        table, ot = g.Cache(1 << log2_cap, max_load=0.5), oracle.Table()
+        if keys.size:
+            vals = rng.integers(0, 2**64, keys.size, dtype=np.uint64, endpoint=False)
+            table.insert(keys_to_device(keys), keys_to_device(vals))
+            ot.insert(keys, vals)
+            ep = np.full(keys.size, 99, np.uint64)
+            table.touch(keys_to_device(keys), epochs=keys_to_device(ep))
+            ot.touch(keys, ep)
+        assert_table(table, ot, what)
+        keep = keys.size // 2
+        ev, counts = table.evict(keep)
+        torch.cuda.synchronize()
+        want = ot.evict(keep)
+        assert u64(counts).tolist() == [want.size, len(ot)], what
+        assert np.array_equal(u64(ev)[:want.size], want), what
+        assert_table(table, ot, f"{what} after evict")
