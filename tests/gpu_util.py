@@ -33,7 +33,10 @@ def host_threads() -> int:
 
 
 def to_device(a: np.ndarray) -> torch.Tensor:
-    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+    a = np.ascontiguousarray(a)
+    if not a.flags.writeable:  # torch warns on read-only arrays (e.g. views of bytes objects)
+        a = a.copy()
+    return torch.from_numpy(a).to("cuda")
 
 
 def u64(t: torch.Tensor) -> np.ndarray:
