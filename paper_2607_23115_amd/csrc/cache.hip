@@ -62,6 +62,38 @@ __device__ void scratch_mark(const ScratchRef& sc, const uint64_t* keys, uint64_
   }
 }
 
+// True for the lowest valid lane of the workgroup holding key k (lanes are in index
+// order, so that lane carries the workgroup's lowest index of k). Only those lanes mark
+// the device-wide scratch table: a batch of one repeated key (a zero-filled tensor)
+// would otherwise queue every thread's compare-and-swap on one word (measured: 262,144
+// equal keys took 3.2 ms, 18x their fingerprint). The check is an LDS table of lane
+// numbers, so it adds no device memory round trip. Every thread of the workgroup
+// (kThreads of them) calls it.
+constexpr int kBlockSlots = 2 * kThreads;  // power of two, load at most 1/2
+__device__ bool first_in_workgroup(uint64_t k, bool valid, uint64_t* bkeys, uint32_t* bslot) {
+  const uint32_t tid = threadIdx.x;
+  bkeys[tid] = k;
+  bslot[tid] = 0;
+  bslot[tid + kThreads] = 0;
+  __syncthreads();
+  uint32_t pos = 0;
+  if (valid) {
+    pos = (uint32_t)slot_hash(k, 64 - 9);
+    static_assert(kBlockSlots == 512, "slot_hash shift");
+    for (int probe = 0; probe < kBlockSlots; ++probe) {
+      const uint32_t prev = atomicCAS(&bslot[pos], 0u, tid + 1);
+      if (prev == 0) break;
+      if (bkeys[prev - 1] == k) {
+        atomicMin(&bslot[pos], tid + 1);
+        break;
+      }
+      pos = (pos + 1) & (kBlockSlots - 1);
+    }
+  }
+  __syncthreads();
+  return valid && bslot[pos] == tid + 1;
+}
+
 // Scratch: the lowest index recorded for key k = keys[g] (g was marked earlier).
 __device__ uint64_t scratch_min(const ScratchRef& sc, const uint64_t* keys, uint64_t k, uint64_t g) {
   if (k == kEmpty) return sc.hdr[0];
@@ -75,9 +107,13 @@ __device__ uint64_t scratch_min(const ScratchRef& sc, const uint64_t* keys, uint
   return ~0ull;
 }
 
-__global__ void insert_mark_kernel(ScratchRef sc, const uint64_t* keys, uint64_t n) {
+__global__ __launch_bounds__(kThreads) void insert_mark_kernel(ScratchRef sc, const uint64_t* keys, uint64_t n) {
+  __shared__ uint64_t bkeys[kThreads];
+  __shared__ uint32_t bslot[kBlockSlots];
   const uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) scratch_mark(sc, keys, keys[i], i);
+  const bool valid = i < n;
+  const uint64_t k = valid ? keys[i] : 0;
+  if (first_in_workgroup(k, valid, bkeys, bslot)) scratch_mark(sc, keys, k, i);
 }
 
 __global__ void insert_commit_kernel(TableRef t, ScratchRef sc, const uint64_t* keys, const uint64_t* vals,
@@ -110,12 +146,17 @@ __global__ void insert_commit_kernel(TableRef t, ScratchRef sc, const uint64_t* 
 }
 
 // Lookup pass 1: table probe. Hits are final; the rest are marked in the scratch
-// table and flagged 0xFF for pass 2.
-__global__ void lookup_probe_kernel(TableRef t, ScratchRef sc, const uint64_t* keys, uint64_t n, uint8_t* status,
-                                    uint64_t* ref) {
+// table (by the workgroup's lowest lane of each key) and flagged 0xFF for pass 2.
+__global__ __launch_bounds__(kThreads) void lookup_probe_kernel(TableRef t, ScratchRef sc, const uint64_t* keys,
+                                                                uint64_t n, uint8_t* status, uint64_t* ref) {
+  __shared__ uint64_t bkeys[kThreads];
+  __shared__ uint32_t bslot[kBlockSlots];
   const uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= n) return;
-  const uint64_t k = keys[g];
+  const bool valid = g < n;
+  const uint64_t k = valid ? keys[g] : 0;
+  // a repeat of a lower lane's key has that lane's table result: that lane marks
+  const bool marks = first_in_workgroup(k, valid, bkeys, bslot);
+  if (!valid) return;
   bool hit = false;
   uint64_t val = 0;
   if (k == kEmpty) {
@@ -140,7 +181,7 @@ __global__ void lookup_probe_kernel(TableRef t, ScratchRef sc, const uint64_t* k
     if (ref) ref[g] = val;
   } else {
     status[g] = 0xFF;
-    scratch_mark(sc, keys, k, g);
+    if (marks) scratch_mark(sc, keys, k, g);
   }
 }
 

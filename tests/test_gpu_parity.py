@@ -678,3 +678,64 @@ def test_binding_refuses_tensors_the_kernels_would_misread():
     with pytest.raises(ValueError):  # not contiguous
         g.Batch.from_arena(torch.zeros(64, 2, dtype=torch.uint8, device="cuda")[:, 0], [0], [8], 4096)
     assert g.Batch.from_arena(arena, [4000], [96], 4096).n_blocks == 1  # ends exactly at the end
+
+
+@pytest.mark.parametrize("layout", ["runs", "scattered", "special"])
+def test_lookup_and_insert_of_heavily_repeated_keys(layout):
+    """Batches dominated by one key, as zero-filled tensors make them: long runs of it
+    (lanes of one workgroup and of many), the same key scattered one per workgroup among
+    distinct keys, and the keys 0 and 2^64-1 repeated. Statuses, refs and insert counts
+    equal the oracle's, and the lookup of 262,144 equal keys stays within a small multiple
+    of the lookup of as many distinct keys (with one device-wide compare-and-swap per
+    key it took 36x as long)."""
+    rng = np.random.default_rng({"runs": 450, "scattered": 451, "special": 452}[layout])
+    n = 262_144
+    hot = np.uint64(0x5DEECE66D1234567)
+    keys = rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False)
+    if layout == "runs":
+        keys[:] = hot
+        keys[rng.integers(0, n, 300)] = rng.integers(0, 2**64, 300, dtype=np.uint64, endpoint=False)
+    elif layout == "scattered":
+        keys[::256] = hot
+        keys[7::512] = hot
+    else:
+        keys[: n // 2] = 2**64 - 1
+        keys[n // 2:] = 0
+    cached = np.array([keys[1], np.uint64(12345)], np.uint64)
+    table, ot = g.Cache(1 << 20, max_load=0.5), oracle.Table()
+    table.insert(keys_to_device(cached), keys_to_device(np.array([7, 8], np.uint64)))
+    ot.insert(cached, np.array([7, 8], np.uint64))
+    say("repeated keys", layout)
+    d = keys_to_device(keys)
+    status, ref = table.lookup(d)
+    torch.cuda.synchronize()
+    est, eref = oracle.lookup(keys, ot)
+    assert np.array_equal(status.cpu().numpy(), est)
+    assert np.array_equal(u64(ref), eref)
+    fresh, ofresh = g.Cache(1 << 20, max_load=0.5), oracle.Table()
+    vals = np.arange(n, dtype=np.uint64)
+    n_new = fresh.insert(d, keys_to_device(vals))
+    assert int(n_new.item()) == ofresh.insert(keys, vals)
+    k, v, _, c = fresh.export()
+    torch.cuda.synchronize()
+    ek, ev, _ = ofresh.export()
+    assert np.array_equal(u64(k)[:int(c.item())], ek) and np.array_equal(u64(v)[:int(c.item())], ev)
+    if layout == "runs":
+        distinct = keys_to_device(rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False))
+        ws = g.workspace(n)
+        st = torch.empty(n, dtype=torch.uint8, device="cuda")
+
+        def timed(x):
+            for _ in range(3):
+                table.lookup(x, status=st, ws=ws)
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(5):
+                table.lookup(x, status=st, ws=ws)
+            b.record()
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) / 5
+
+        t_hot, t_distinct = timed(d), timed(distinct)
+        assert t_hot < 4 * t_distinct + 0.05, (t_hot, t_distinct)
