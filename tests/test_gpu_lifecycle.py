@@ -253,3 +253,50 @@ def test_sort_skips_shared_digits(log2_cap):
         assert u64(counts).tolist() == [want.size, len(ot)], what
         assert np.array_equal(u64(ev)[:want.size], want), what
         assert_table(table, ot, f"{what} after evict")
+
+
+def test_touch_of_heavily_repeated_keys():
+    """262,144 copies of a few keys with distinct epochs, as the blocks of zero-filled
+    tensors give (runs, and one key scattered across workgroups): each stamp is the
+    largest epoch of its key's copies, the count is the oracle's, and the touch stays
+    within a small multiple of a touch of as many distinct keys (with one device-wide
+    atomic per copy it took 50x as long)."""
+    rng = np.random.default_rng(1004)
+    n = 262_144
+    hot = np.array([0x1234567, 0, 2**64 - 1, 99], np.uint64)
+    keys = np.full(n, hot[0], np.uint64)
+    keys[::256] = hot[1]
+    keys[5::512] = hot[2]
+    keys[n // 2: n // 2 + 1000] = hot[3]
+    table, ot = g.Cache(1 << 12, max_load=0.5), oracle.Table()
+    present = np.concatenate([hot[:3], np.array([7, 8], np.uint64)])
+    table.insert(keys_to_device(present), keys_to_device(np.arange(present.size, dtype=np.uint64)))
+    ot.insert(present, np.arange(present.size, dtype=np.uint64))
+    ep = rng.permutation(n).astype(np.uint64) + np.uint64(1)
+    say("touch repeated keys")
+    hit = table.touch(keys_to_device(keys), epochs=keys_to_device(ep))
+    torch.cuda.synchronize()
+    assert int(hit.item()) == ot.touch(keys, ep)
+    assert_table(table, ot, "after touch")
+    # timing against distinct keys (kernel time: epochs prepared beforehand)
+    dk = rng.integers(0, 2**63, n, dtype=np.uint64)
+    big = g.Cache(1 << 20, max_load=0.5)
+    d_dk, d_hot = keys_to_device(dk), keys_to_device(keys)
+    big.insert(d_dk, keys_to_device(np.arange(n, dtype=np.uint64)))
+    big.insert(keys_to_device(hot), keys_to_device(np.arange(hot.size, dtype=np.uint64)))
+    eps = [keys_to_device(ep + np.uint64(n * i)) for i in range(8)]
+
+    def timed(d):
+        for e in eps[:3]:
+            big.touch(d, epochs=e)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for e in eps[3:]:
+            big.touch(d, epochs=e)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / 5
+
+    t_hot, t_distinct = timed(d_hot), timed(d_dk)
+    assert t_hot < 4 * t_distinct + 0.05, (t_hot, t_distinct)
