@@ -22,18 +22,44 @@ __global__ void identify_init_kernel(uint64_t* first_diff, uint64_t n_seg, const
   for (uint64_t r = t; r < n_regions; r += stride) region_weight[r] = region_first[r + 1] > region_first[r] ? 1 : 0;
 }
 
+// first_diff[s] = min(first_diff[s], x) for the lanes with `differs`. When every such lane
+// of the wave lies in one payload (all but the waves at payload boundaries), the wave
+// takes the minimum itself and one lane issues the atomic: a payload whose blocks all changed
+// (a layer updated in place) would otherwise queue one atomic per block on its word
+// (262,144 leaves of one payload: 3.2 ms, 15x the comparison of unchanged leaves). Every
+// lane of the wave calls it.
+__device__ __forceinline__ void lower_first_diff(uint64_t* first_diff, uint64_t s, bool differs, uint64_t x) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t active = __ballot(differs);
+  const int leader = active ? __ffsll((unsigned long long)active) - 1 : 0;
+  const uint64_t s0 = shfl64(s, leader);
+  if (__ballot(differs && s != s0) == 0) {  // one payload for every differing lane
+    uint64_t m = differs ? x : ~0ull;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const uint64_t y = shfl_xor64(m, o);
+      m = y < m ? y : m;
+    }
+    if (lane == leader && m != ~0ull) atomicMin(reinterpret_cast<unsigned long long*>(&first_diff[s0]), m);
+  } else if (differs) {
+    atomicMin(reinterpret_cast<unsigned long long*>(&first_diff[s]), (unsigned long long)x);
+  }
+}
+
 // Per block: equal digests? The first differing block of each payload by atomicMin.
 __global__ void identify_compare_kernel(const uint64_t* current, const uint64_t* recorded, uint64_t n_blocks,
                                         const uint64_t* blk_first, uint64_t n_seg, uint8_t* block_match,
                                         uint64_t* first_diff) {
   const uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= n_blocks) return;
-  const bool same = current[g] == recorded[g];
-  if (block_match) block_match[g] = same ? 1 : 0;
+  const bool valid = g < n_blocks;
+  const bool same = !valid || current[g] == recorded[g];
+  if (valid && block_match) block_match[g] = same ? 1 : 0;
+  uint64_t s = 0, x = 0;
   if (!same) {
-    const uint64_t s = find_segment(blk_first, n_seg, g);
-    atomicMin(reinterpret_cast<unsigned long long*>(&first_diff[s]), (unsigned long long)(g - blk_first[s]));
+    s = find_segment(blk_first, n_seg, g);
+    x = g - blk_first[s];
   }
+  lower_first_diff(first_diff, s, !same, x);
 }
 
 // Per leaf slot (slot = g * LPB + k): equal digests? Slots past a short block's last leaf
@@ -43,15 +69,16 @@ __global__ void identify_leaf_compare_kernel(const uint64_t* current, const uint
                                              uint32_t lpb_log2, const uint64_t* blk_first, uint64_t n_seg,
                                              uint8_t* leaf_match, uint64_t* first_diff) {
   const uint64_t slot = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (slot >= n_slots) return;
-  const bool same = current[slot] == recorded[slot];
-  if (leaf_match) leaf_match[slot] = same ? 1 : 0;
+  const bool valid = slot < n_slots;
+  const bool same = !valid || current[slot] == recorded[slot];
+  if (valid && leaf_match) leaf_match[slot] = same ? 1 : 0;
+  uint64_t s = 0, leaf = 0;
   if (!same) {
     const uint64_t g = slot >> lpb_log2;
-    const uint64_t s = find_segment(blk_first, n_seg, g);
-    const uint64_t leaf = ((g - blk_first[s]) << lpb_log2) + (slot & ((1ull << lpb_log2) - 1));
-    atomicMin(reinterpret_cast<unsigned long long*>(&first_diff[s]), (unsigned long long)leaf);
+    s = find_segment(blk_first, n_seg, g);
+    leaf = ((g - blk_first[s]) << lpb_log2) + (slot & ((1ull << lpb_log2) - 1));
   }
+  lower_first_diff(first_diff, s, !same, leaf);
 }
 
 // Per payload: a difference clears its allocation's weight flag.

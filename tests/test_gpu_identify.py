@@ -95,3 +95,51 @@ def test_identify_decoder7b_full():
     bad_regions = {int(l) + 1 for l in dec.perturbed_layers}
     assert {r for r in range(w.size) if w[r] == 0} == bad_regions
     assert all(f[i] == 0 for i in dec.perturbed)
+
+
+@pytest.mark.parametrize("block", [4096, 1 << 20])
+def test_identify_payloads_changed_throughout(block):
+    """Payloads whose every leaf changed (a layer rewritten in place) next to unchanged and
+    partly changed ones, payload boundaries inside waves: leaf matches, first changed
+    leaves and verdicts equal the oracle's; and a 256 MiB payload changed throughout is
+    compared within a small multiple of the time of an unchanged one (with one atomic per
+    changed leaf on the payload's word it took 15x as long)."""
+    rng = np.random.default_rng(9100 + block.bit_length())
+    lens = [3 << 20, 5000, 1 << 20, 4096, 777, 2 << 20]
+    written = [np.frombuffer(rng.bytes(n), np.uint8).copy() for n in lens]
+    current = [np.frombuffer(rng.bytes(n), np.uint8).copy() if i % 2 == 0 else w.copy()
+               for i, (n, w) in enumerate(zip(lens, written))]
+    current[3][100] ^= 1
+    region_first = np.array([0, 2, 4, len(lens)], np.uint64)
+    _, rec = oracle.batch_digests(written, block, with_leaves=True)
+    arena, offs, lens_a = W.pack(current)
+    batch = g.Batch.from_arena(to_device(arena), offs, lens_a, block)
+    say("identify changed throughout", block)
+    m, f, w = g.identify_leaves(batch, keys_to_device(rec.reshape(-1)), region_first)
+    torch.cuda.synchronize()
+    em, ef, ew = oracle.identify_leaves(rec, current, block, region_first)
+    assert np.array_equal(m.cpu().numpy(), em)
+    assert np.array_equal(u64(f), ef)
+    assert np.array_equal(w.cpu().numpy(), ew)
+    if block != 4096:
+        return
+    big = torch.randint(0, 256, (256 << 20,), dtype=torch.uint8, device="cuda")
+    other = torch.randint(0, 256, (256 << 20,), dtype=torch.uint8, device="cuda")
+    cur = g.Batch.from_arena(big, [0], [big.numel()], block)
+    times = {}
+    for label, src in (("changed", other), ("same", big)):
+        rb = g.Batch.from_arena(src, [0], [src.numel()], block)
+        leaves = torch.empty(rb.n_blocks * rb.leaves_per_block, dtype=torch.int64, device="cuda")
+        g.fp_chunks(rb, leaf_out=leaves)
+        ws = g.workspace(leaves.numel() + 1)
+        for _ in range(3):
+            g.identify_leaves(cur, leaves, [0, 1], ws=ws)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(5):
+            g.identify_leaves(cur, leaves, [0, 1], ws=ws)
+        b.record()
+        torch.cuda.synchronize()
+        times[label] = a.elapsed_time(b) / 5
+    assert times["changed"] < 3 * times["same"] + 0.05, times
