@@ -209,16 +209,19 @@ __global__ __launch_bounds__(kSmallThreads) void lookup_small_kernel(TableRef t,
   uint32_t pending = 0;  // bit j: key j is not held by the table
   uint64_t k[kSmallPerThread];
   uint4 home[kSmallPerThread];
+  // all loads unconditional (keys at indices clamped to n - 1, n >= 1; slot 0 for a key
+  // that is out of range or kEmpty), so that a thread's loads issue together: guarded,
+  // they compiled to one round trip each
 #pragma unroll
   for (int j = 0; j < kSmallPerThread; ++j) {
     const uint64_t g = threadIdx.x + (uint64_t)j * kSmallThreads;
-    k[j] = g < n ? keys[g] : kEmpty;
+    const uint64_t kg = keys[g < n ? g : n - 1];
+    k[j] = g < n ? kg : kEmpty;
   }
 #pragma unroll
   for (int j = 0; j < kSmallPerThread; ++j) {
-    const uint64_t g = threadIdx.x + (uint64_t)j * kSmallThreads;
-    home[j] = make_uint4(0, 0, 0, 0);
-    if (g < n && k[j] != kEmpty) home[j] = *reinterpret_cast<const uint4*>(t.slots + 2 * slot_hash(k[j], t.shift));
+    const uint64_t pos = k[j] != kEmpty ? slot_hash(k[j], t.shift) : 0;
+    home[j] = *reinterpret_cast<const uint4*>(t.slots + 2 * pos);
   }
 #pragma unroll
   for (int j = 0; j < kSmallPerThread; ++j) {
