@@ -283,6 +283,98 @@ __global__ __launch_bounds__(kSmallThreads) void lookup_small_kernel(TableRef t,
   }
 }
 
+// Inserts of up to kSmallKeys keys: one 1024-thread workgroup, the dedup table in LDS as
+// in lookup_small_kernel, so one launch and no clear pass (the three-launch path costs
+// about 20 us whatever the size). The lowest index of each key inserts it; *n_new is
+// written once at the end.
+__global__ __launch_bounds__(kSmallThreads) void insert_small_kernel(TableRef t, const uint64_t* keys,
+                                                                     const uint64_t* vals, uint64_t n,
+                                                                     uint64_t* n_new) {
+  __shared__ uint32_t slots[kSmallSlots];
+  __shared__ uint32_t empty_min;  // lowest index of the key kEmpty
+  __shared__ uint32_t wave_new[kSmallThreads / 64];
+  for (uint32_t i = threadIdx.x; i < kSmallSlots; i += kSmallThreads) slots[i] = 0;
+  if (threadIdx.x == 0) empty_min = ~0u;
+  uint64_t k[kSmallPerThread];
+#pragma unroll
+  for (int j = 0; j < kSmallPerThread; ++j) {  // unconditional (clamped) loads, issued together
+    const uint64_t g = threadIdx.x + (uint64_t)j * kSmallThreads;
+    k[j] = keys[g < n ? g : n - 1];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kSmallPerThread; ++j) {
+    const uint64_t g = threadIdx.x + (uint64_t)j * kSmallThreads;
+    if (g >= n) continue;
+    if (k[j] == kEmpty) {
+      atomicMin(&empty_min, (uint32_t)g);
+      continue;
+    }
+    uint32_t pos = (uint32_t)slot_hash(k[j], kSmallShift);
+    for (uint32_t probe = 0; probe < kSmallSlots; ++probe) {
+      const uint32_t prev = atomicCAS(&slots[pos], 0u, (uint32_t)g + 1);
+      if (prev == 0) break;
+      if (keys[prev - 1] == k[j]) {
+        if (g + 1 < prev) atomicMin(&slots[pos], (uint32_t)g + 1);
+        break;
+      }
+      pos = (pos + 1) & (kSmallSlots - 1);
+    }
+  }
+  __syncthreads();
+  uint32_t added = 0;
+#pragma unroll
+  for (int j = 0; j < kSmallPerThread; ++j) {
+    const uint64_t g = threadIdx.x + (uint64_t)j * kSmallThreads;
+    if (g >= n) continue;
+    uint64_t g0 = g;
+    if (k[j] == kEmpty) {
+      g0 = empty_min;
+    } else {
+      uint32_t pos = (uint32_t)slot_hash(k[j], kSmallShift);
+      for (uint32_t probe = 0; probe < kSmallSlots; ++probe) {
+        const uint32_t v = slots[pos];
+        if (v == 0) break;
+        if (v - 1 == g || keys[v - 1] == k[j]) {
+          g0 = v - 1;
+          break;
+        }
+        pos = (pos + 1) & (kSmallSlots - 1);
+      }
+    }
+    if (g0 != g) continue;  // a lower index carries this key
+    if (k[j] == kEmpty) {
+      if (atomicCAS(ull(&t.hdr[0]), 0ull, 1ull) == 0ull) {
+        t.hdr[1] = vals[g];
+        ++added;
+      }
+      continue;
+    }
+    uint64_t pos = slot_hash(k[j], t.shift);
+    for (uint64_t probe = 0; probe <= t.mask; ++probe) {
+      uint64_t* slot = t.slots + 2 * pos;
+      const uint64_t prev = atomicCAS(ull(slot), (unsigned long long)kEmpty, (unsigned long long)k[j]);
+      if (prev == kEmpty) {
+        slot[1] = vals[g];
+        ++added;
+        break;
+      }
+      if (prev == k[j]) break;  // already held: keep the existing value
+      pos = (pos + 1) & t.mask;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) added += __shfl_xor(added, o, 64);
+  if ((threadIdx.x & 63) == 0) wave_new[threadIdx.x >> 6] = added;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t total = 0;
+    for (int w = 0; w < kSmallThreads / 64; ++w) total += wave_new[w];
+    if (n_new) *n_new = total;
+    if (total) atomicAdd(ull(&t.hdr[3]), (unsigned long long)total);
+  }
+}
+
 // Lookup pass 2: the earliest block with a digest is the MISS, later ones HIT_BATCH.
 __global__ void lookup_resolve_kernel(ScratchRef sc, const uint64_t* keys, uint64_t n, uint8_t* status,
                                       uint64_t* ref) {
@@ -424,6 +516,13 @@ extern "C" gleam_status gleam_cache_insert(gleam_cache* c, const uint64_t* d_key
     return GLEAM_E_CAPACITY;
   }
   hipStream_t s = (hipStream_t)stream;
+  if (n > 0 && n <= kSmallKeys) {
+    hipLaunchKernelGGL(insert_small_kernel, dim3(1), dim3(kSmallThreads), 0, s, table_ref(c), d_keys, d_vals, n,
+                       d_n_new);
+    if ((st = launch_status("insert_small_kernel")) != GLEAM_OK) return st;
+    c->key_bound += n;
+    return GLEAM_OK;
+  }
   st = clear_scratch(d_ws, L, s, d_n_new);
   uint64_t* counter = d_n_new ? d_n_new : reinterpret_cast<uint64_t*>(d_ws) + 1;
   if (st != GLEAM_OK) return st;
