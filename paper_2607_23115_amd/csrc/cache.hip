@@ -153,7 +153,11 @@ __global__ __launch_bounds__(kThreads) void lookup_probe_kernel(TableRef t, Scra
   __shared__ uint32_t bslot[kBlockSlots];
   const uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const bool valid = g < n;
-  const uint64_t k = valid ? keys[g] : 0;
+  const uint64_t kg = keys[valid ? g : n - 1];  // n >= 1; clamped so the load is unconditional
+  const uint64_t k = valid ? kg : 0;
+  // the home slot's read is issued before the workgroup's LDS pass, which hides under it
+  const uint64_t home = k != kEmpty ? slot_hash(k, t.shift) : 0;
+  const uint4 e0 = *reinterpret_cast<const uint4*>(t.slots + 2 * home);
   // a repeat of a lower lane's key has that lane's table result: that lane marks
   const bool marks = first_in_workgroup(k, valid, bkeys, bslot);
   if (!valid) return;
@@ -162,9 +166,12 @@ __global__ __launch_bounds__(kThreads) void lookup_probe_kernel(TableRef t, Scra
   if (k == kEmpty) {
     hit = t.hdr[0] != 0;
     val = t.hdr[1];
-  } else {
-    uint64_t pos = slot_hash(k, t.shift);
-    for (uint64_t probe = 0; probe <= t.mask; ++probe) {
+  } else if (lo64(e0) == k) {
+    hit = true;
+    val = hi64(e0);
+  } else if (lo64(e0) != kEmpty) {
+    uint64_t pos = (home + 1) & t.mask;
+    for (uint64_t probe = 1; probe <= t.mask; ++probe) {
       const uint4 e = *reinterpret_cast<const uint4*>(t.slots + 2 * pos);
       const uint64_t key = lo64(e);
       if (key == k) {
@@ -283,10 +290,13 @@ __global__ __launch_bounds__(kSmallThreads) void lookup_small_kernel(TableRef t,
   }
 }
 
-// Inserts of up to kSmallKeys keys: one 1024-thread workgroup, the dedup table in LDS as
-// in lookup_small_kernel, so one launch and no clear pass (the three-launch path costs
-// about 20 us whatever the size). The lowest index of each key inserts it; *n_new is
-// written once at the end.
+// Inserts of up to kSmallInsertKeys keys: one 1024-thread workgroup, the dedup table in
+// LDS as in lookup_small_kernel, so one launch and no clear pass. The lowest index of
+// each key inserts it; *n_new is written once at the end. GPU time on MI355X (this /
+// the three launches): 256 keys 6.4 us, 1,024 keys 10.2 us, 2,048 keys 15.1 us, 4,096
+// keys 38 us against about 20 us: past 2,048 keys one CU's chain of table
+// compare-and-swaps costs more than the launches it saves.
+constexpr uint64_t kSmallInsertKeys = 2048;
 __global__ __launch_bounds__(kSmallThreads) void insert_small_kernel(TableRef t, const uint64_t* keys,
                                                                      const uint64_t* vals, uint64_t n,
                                                                      uint64_t* n_new) {
@@ -516,7 +526,7 @@ extern "C" gleam_status gleam_cache_insert(gleam_cache* c, const uint64_t* d_key
     return GLEAM_E_CAPACITY;
   }
   hipStream_t s = (hipStream_t)stream;
-  if (n > 0 && n <= kSmallKeys) {
+  if (n > 0 && n <= kSmallInsertKeys) {
     hipLaunchKernelGGL(insert_small_kernel, dim3(1), dim3(kSmallThreads), 0, s, table_ref(c), d_keys, d_vals, n,
                        d_n_new);
     if ((st = launch_status("insert_small_kernel")) != GLEAM_OK) return st;
