@@ -221,7 +221,7 @@ gleam_status gleam_cache_lookup(const gleam_cache* c, const uint64_t* d_keys, ui
  * gleam_cache_lookup without a workspace, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, hosts that forbid allocation). The
  * same outputs as gleam_cache_lookup; the batch-dedup scratch table lives in a
- * library-owned device array of 16 MiB + 256 B per GPU (held until the process ends),
+ * library-owned device array of 32 MiB + 256 B per GPU (held until the process ends),
  * so n is at most gleam_cache_lookup_noalloc_max_keys() = 2^20. The call allocates
  * nothing (its first call on a device looks up that device's array address).
  * Every call on one GPU shares that GPU's array: calls that overlap on one GPU (on

@@ -75,7 +75,7 @@ WsLayout ws_layout(uint64_t n) {
     return L;
   }
   uint64_t cap = 64;
-  while (cap < 2 * n) cap <<= 1;
+  while (cap < 4 * n) cap <<= 1;
   L.scratch_cap = cap;
   L.scratch_off = kHeaderBytes;
   L.tiles = (n + kTileItems - 1) / kTileItems;
