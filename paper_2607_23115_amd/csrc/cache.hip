@@ -411,14 +411,18 @@ __global__ void scratch_clear_kernel(uint64_t* hdr, uint64_t* slots, uint64_t wo
   const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t < 4) hdr[t] = t == 0 ? ~0ull : 0ull;
   if (t == 4 && also_zero) *also_zero = 0;
-  for (uint64_t i = t; i < words; i += stride) slots[i] = ~0ull;
+  // 16-byte stores (the slot count is a power of two of at least 64, the slots start
+  // 256 bytes into a 256-byte aligned workspace)
+  uint4* s4 = reinterpret_cast<uint4*>(slots);
+  const uint4 ones = make_uint4(~0u, ~0u, ~0u, ~0u);
+  for (uint64_t i = t; i < words / 2; i += stride) s4[i] = ones;
 }
 
 gleam_status clear_scratch(void* ws, const WsLayout& L, hipStream_t stream, uint64_t* also_zero = nullptr) {
   uint64_t* hdr = reinterpret_cast<uint64_t*>(ws);
   uint64_t* slots = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + L.scratch_off);
   const uint64_t words = L.scratch_cap;
-  const uint64_t want = (words + kThreads - 1) / kThreads;
+  const uint64_t want = (words / 2 + kThreads - 1) / kThreads;
   const uint32_t grid = (uint32_t)(want < 2048 ? want : 2048);
   hipLaunchKernelGGL(scratch_clear_kernel, dim3(grid), dim3(kThreads), 0, stream, hdr, slots, words, also_zero);
   return launch_status("scratch_clear_kernel");
