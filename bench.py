@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, AMD public specification
 FIRST_LAUNCH_MS = None  # the process's first fingerprint launch over the workload (set by its builder)
+PRELOAD_MS = None  # host time of gleam_preload at start-up (the library's GPU code loaded)
 PROFILE_PMC = {w: os.path.join(ROOT, "profiles", f"fp_kernel_{w}_pmc.txt") for w in ("decoder7b", "small_copies")}
 FP_SOURCES = [os.path.join(ROOT, "paper_2607_23115_amd", "csrc", f) for f in ("fp_core.h", "fp_chunks.hip")]
 
@@ -839,6 +840,12 @@ def main():
     if args.copy_calibration:
         copy_calibration(torch)
         return
+    # a server loads the library's GPU code once at start-up; a model load's first
+    # fingerprint launch (config.first_fp_launch_ms) then pays only for its own work
+    global PRELOAD_MS
+    t0 = time.perf_counter()
+    g.preload()
+    PRELOAD_MS = round((time.perf_counter() - t0) * 1e3, 3)
 
     threads = host_threads()
     if args.path == "lifecycle":
@@ -1032,7 +1039,7 @@ def main():
                    "call": "gleam_detect" if use_detect else "gleam_fp_chunks + gleam_cache_lookup + gleam_miss_compact",
                    "step_ms": {"median": round(float(np.median(warm_ms)), 4), "min": round(min(warm_ms), 4),
                                "max": round(max(warm_ms), 4)},
-                   "cold": cold, "insert_ms": insert_ms, "first_fp_launch_ms": FIRST_LAUNCH_MS, "pipelined": pipe, "per_buffer": per_buffer,
+                   "cold": cold, "insert_ms": insert_ms, "first_fp_launch_ms": FIRST_LAUNCH_MS, "library_preload_ms": PRELOAD_MS, "pipelined": pipe, "per_buffer": per_buffer,
                    "truth": {"expected_misses": expect_miss, "misses": miss_count, "ok": True,
                              "check": "MISS count after the warm-up and after the timed steps equals the "
                                       "workload's planted truth; bit-exact parity is in tests/"}},

@@ -602,6 +602,16 @@ gleam_status gleam_remap_export(const gleam_remap* m, uint64_t* d_start, uint64_
 gleam_status gleam_read_stream(const void* d_src, uint64_t bytes, uint64_t* d_sink, void* stream);
 
 /* Static text for a status code. */
+/*
+ * gleam_preload: load the library's GPU code on the current device now rather than at
+ * each source file's first kernel launch, where the HIP runtime loads it lazily (about
+ * 0.8 ms of host time before the fingerprint's first launch on MI355X). For callers
+ * that want the first model load of a process to pay only for its own work: call once
+ * per device at start-up. Optional; without it the same loading happens on first use.
+ * Enqueues nothing. Errors: GLEAM_E_HIP (no usable device).
+ */
+gleam_status gleam_preload(void);
+
 const char* gleam_status_string(gleam_status s);
 
 /* Thread-local detail of the last error on this thread ("" if none). */

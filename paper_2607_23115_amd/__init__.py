@@ -49,7 +49,7 @@ EXPORTS = (
     "gleam_remap_update_bytes", "gleam_remap_update", "gleam_remap_translate", "gleam_remap_export",
     "gleam_cache_lookup_noalloc", "gleam_cache_lookup_noalloc_max_keys", "gleam_detect",
     "gleam_detect_ws_init", "gleam_identify_leaves", "gleam_first_writes_ws_bytes", "gleam_first_writes",
-    "gleam_cache_erase_bytes", "gleam_detect_workspace_bytes",
+    "gleam_cache_erase_bytes", "gleam_detect_workspace_bytes", "gleam_preload",
 )
 
 
@@ -111,6 +111,7 @@ def _load() -> ctypes.CDLL:
         "gleam_remap_translate": ([vp, vp, u64, vp, vp], st),
         "gleam_remap_export": ([vp, vp, vp, vp, vp, vp], st),
         "gleam_status_string": ([st], ctypes.c_char_p),
+        "gleam_preload": ([], st),
         "gleam_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sigs.items():
@@ -193,6 +194,13 @@ def _on_stream(stream, device):
 
 def _u64_device(a: np.ndarray, device) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint64).view(np.int64)).to(device)
+
+
+def preload(device="cuda") -> None:
+    """Load the library's GPU code on `device` now (gleam_preload), so that no later
+    call pays the lazy code-object load at its first launch."""
+    with torch.cuda.device(torch.device(device)):
+        _check(lib.gleam_preload())
 
 
 def lookup_noalloc_max_keys() -> int:

@@ -103,6 +103,22 @@ gleam_status check_workspace(const WsLayout& L, const void* ws, size_t ws_bytes,
 
 }  // namespace gleam
 
+extern "C" gleam_status gleam_preload(void) {
+  using namespace gleam;
+  clear_error();
+  hipError_t (*const loads[])() = {preload_fp_chunks, preload_cache,    preload_compact, preload_detect,
+                                   preload_identify,  preload_first_write, preload_md5,  preload_lifecycle,
+                                   preload_transfer,  preload_remap,    preload_calib};
+  for (auto load : loads) {
+    const hipError_t e = load();
+    if (e != hipSuccess) {
+      set_error("gleam_preload: %s", hipGetErrorString(e));
+      return GLEAM_E_HIP;
+    }
+  }
+  return GLEAM_OK;
+}
+
 extern "C" const char* gleam_status_string(gleam_status s) {
   switch (s) {
     case GLEAM_OK: return "ok";

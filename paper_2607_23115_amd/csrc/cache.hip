@@ -636,6 +636,12 @@ gleam_status noalloc_scratch(void** out) {
 }
 
 }  // namespace
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_cache() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&fill_kernel));
+}
+
 }  // namespace gleam
 
 extern "C" size_t gleam_cache_lookup_noalloc_max_keys(void) { return (size_t)gleam::kNoAllocMaxKeys; }

@@ -50,6 +50,12 @@ __global__ __launch_bounds__(kThreads) void read_stream_kernel(const uint8_t* sr
 }
 
 }  // namespace
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_calib() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&read_stream_kernel));
+}
+
 }  // namespace gleam
 
 extern "C" gleam_status gleam_read_stream(const void* d_src, uint64_t bytes, uint64_t* d_sink, void* stream) {

@@ -274,6 +274,12 @@ __global__ __launch_bounds__(kScanThreads) void compact_small_kernel(const uint8
 }
 
 }  // namespace
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_compact() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&compact_scan_kernel));
+}
+
 }  // namespace gleam
 
 extern "C" gleam_status gleam_miss_compact(const uint8_t* d_status, uint64_t n, const gleam_batch* b,

@@ -219,6 +219,12 @@ __global__ __launch_bounds__(64 * W) void detect_small_kernel(DetectArgs a) {
 __global__ void detect_arm_kernel(uint64_t* arrive) { *arrive = kArmed << 32; }
 
 }  // namespace
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_detect() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&detect_arm_kernel));
+}
+
 }  // namespace gleam
 
 extern "C" size_t gleam_detect_workspace_bytes(uint64_t n_blocks) {

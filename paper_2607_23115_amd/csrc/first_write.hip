@@ -279,6 +279,12 @@ __global__ void first_write_move_kernel(FwArgs a, const uint64_t* first, uint64_
 }
 
 }  // namespace
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_first_write() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&first_write_move_kernel));
+}
+
 }  // namespace gleam
 
 extern "C" size_t gleam_first_writes_ws_bytes(uint64_t n_writes, uint64_t n_regions) {

@@ -209,6 +209,12 @@ gleam_status launch_fp(const gleam_batch* b, uint64_t* d_block_digest, uint64_t*
 }
 
 
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_fp_chunks() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&fp_kernel<true>));
+}
+
 }  // namespace gleam
 
 extern "C" gleam_status gleam_fp_chunks(const gleam_batch* b, uint64_t* d_block_digest, uint64_t* d_leaf_digest,

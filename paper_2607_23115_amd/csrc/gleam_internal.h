@@ -85,4 +85,18 @@ gleam_status launch_fp(const gleam_batch* b, uint64_t* d_block_digest, uint64_t*
 // Fill n u64 words with value on stream (a kernel, so it can live in a captured graph).
 gleam_status fill_u64(uint64_t* p, uint64_t n, uint64_t value, hipStream_t stream);
 
+
+// Each source file's code-object preload (gleam_preload calls them all).
+hipError_t preload_cache();
+hipError_t preload_calib();
+hipError_t preload_compact();
+hipError_t preload_detect();
+hipError_t preload_first_write();
+hipError_t preload_fp_chunks();
+hipError_t preload_identify();
+hipError_t preload_lifecycle();
+hipError_t preload_md5();
+hipError_t preload_remap();
+hipError_t preload_transfer();
+
 }  // namespace gleam

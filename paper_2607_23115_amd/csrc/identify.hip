@@ -97,6 +97,12 @@ uint32_t grid_for(uint64_t n, uint64_t cap = 0x7fffffffull) {
 }
 
 }  // namespace
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_identify() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&identify_init_kernel));
+}
+
 }  // namespace gleam
 
 extern "C" gleam_status gleam_identify_weights(const gleam_batch* b, const uint64_t* d_recorded,

@@ -513,6 +513,12 @@ gleam_status gather_sorted(const gleam_cache* c, void* ws, const MaintLayout& L,
 }
 
 }  // namespace
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_lifecycle() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&maint_init_kernel));
+}
+
 }  // namespace gleam
 
 extern "C" size_t gleam_cache_maint_bytes(const gleam_cache* c) {

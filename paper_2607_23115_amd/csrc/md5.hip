@@ -110,6 +110,12 @@ __global__ void md5_prefix_kernel(const uint64_t* seg_addr, const uint64_t* seg_
 }
 
 }  // namespace
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_md5() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&md5_prefix_kernel));
+}
+
 }  // namespace gleam
 
 extern "C" gleam_status gleam_md5_prefix(const gleam_batch* b, uint32_t prefix_bytes, uint64_t min_len,

@@ -586,6 +586,12 @@ gleam_status hip_call(hipError_t e, const char* what) {
 }
 
 }  // namespace
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_remap() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&update_init_kernel));
+}
+
 }  // namespace gleam
 
 extern "C" size_t gleam_remap_bytes(uint64_t capacity) {

@@ -271,6 +271,12 @@ uint32_t copy_grid(uint64_t n) { return (uint32_t)(n < kMaxCopyGrid ? (n ? n : 1
 uint64_t chunks_per_block(uint32_t block_bytes) { return block_bytes > kChunk ? block_bytes / kChunk : 1; }
 
 }  // namespace
+// Loads this file's GPU code object on the current device (gleam_preload).
+hipError_t preload_transfer() {
+  hipFuncAttributes attr;
+  return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(&plan_scan_kernel));
+}
+
 }  // namespace gleam
 
 extern "C" gleam_status gleam_send_plan(const gleam_batch* b, const uint64_t* d_digest, const uint8_t* d_status,

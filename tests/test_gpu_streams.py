@@ -114,3 +114,17 @@ def test_binding_zeroed_counters_precede_the_kernel():
         _, ecnt, ebytes = oracle.compact(status, blen)
         assert u64(counters).tolist() == [ecnt, ebytes]
         assert u64(sink)[0] == want_sink
+
+
+def test_preload_then_calls_work():
+    """gleam_preload loads every source file's GPU code on the device; the calls work
+    after it as before, and calling it again is harmless."""
+    say("preload")
+    g.preload()
+    g.preload()
+    buf = torch.randint(0, 256, (1 << 20,), dtype=torch.uint8, device="cuda")
+    batch = g.Batch.from_arena(buf, [0], [buf.numel()], 65536)
+    d = g.fp_chunks(batch)
+    torch.cuda.synchronize()
+    want, _ = oracle.batch_digests([buf.cpu().numpy()], 65536)
+    assert np.array_equal(g.as_u64(d), want)
