@@ -601,7 +601,7 @@ namespace {
 
 constexpr uint64_t kNoAllocMaxKeys = 1ull << 20;
 constexpr uint64_t kNoAllocSlots = 4 * kNoAllocMaxKeys;  // the workspace layout's cap for that n
-constexpr size_t kNoAllocBytes = kHeaderBytes + kNoAllocSlots * 8;  // 16 MiB + 256 B
+constexpr size_t kNoAllocBytes = kHeaderBytes + kNoAllocSlots * 8;  // 32 MiB + 256 B
 
 static __device__ __align__(256) uint8_t scratch[kNoAllocBytes];
 

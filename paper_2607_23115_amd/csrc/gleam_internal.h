@@ -56,7 +56,7 @@ constexpr uint64_t kTileItems = 2048;  // statuses per compaction workgroup
 // Header u64 words: 0 = scratch min-index of the key kEmpty, 1 = new-key counter,
 // 2 = short-block byte deficit.
 struct WsLayout {
-  uint64_t scratch_cap;   // power of two >= max(64, 2n)
+  uint64_t scratch_cap;   // power of two >= max(64, 4n)
   size_t scratch_off;
   uint64_t tiles;
   size_t tiles_off;

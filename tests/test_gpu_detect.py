@@ -52,7 +52,7 @@ def check(batch, payloads, table, ot, what, want_ref=True):
     return got
 
 
-def tables_from(payloads, block, which):
+def tables_from(payloads, block, which, capacity=1 << 14):
     """A GPU table and an oracle table holding the digests of the payloads in `which`
     (computed by the oracle), with value = payload index."""
     keys, vals = [np.zeros(0, np.uint64)], [np.zeros(0, np.uint64)]
@@ -61,7 +61,7 @@ def tables_from(payloads, block, which):
         keys.append(d)
         vals.append(np.full(d.size, i, np.uint64))
     keys, vals = np.concatenate(keys), np.concatenate(vals)
-    t, ot = g.Cache(1 << 14), oracle.Table()
+    t, ot = g.Cache(capacity), oracle.Table()
     if keys.size:
         t.insert(keys_to_device(keys), keys_to_device(vals))
         ot.insert(keys, vals)
@@ -261,3 +261,28 @@ def test_beyond_the_three_kernel_limit():
     for k in ("digests", "status", "ref", "miss_idx"):
         assert np.array_equal(got[k], want[k]), k
     assert (got["miss_count"], got["miss_bytes"]) == (want["miss_count"], want["miss_bytes"])
+
+
+@pytest.mark.parametrize("block", [4096, 65536])
+def test_large_payloads_four_lanes(block):
+    """Past the one-kernel limits with payloads of at least 64 leaf slots on average (the
+    fingerprint then runs four lanes per leaf): 300 payloads of 0.5-1.5 MiB with short
+    last blocks, some blocks planted as copies of earlier ones."""
+    rng = np.random.default_rng(9900 + block)
+    sizes = rng.integers(1 << 19, 3 << 19, 300)
+    payloads = [bytearray(rng.bytes(int(n))) for n in sizes]
+    for _ in range(200):  # block-aligned copies of earlier blocks
+        i, j = sorted(rng.integers(0, len(payloads), 2))
+        bi = int(rng.integers(0, len(payloads[i]) // block))
+        bj = int(rng.integers(0, len(payloads[j]) // block))
+        if (i, bi) != (j, bj):
+            payloads[j][bj * block:(bj + 1) * block] = payloads[i][bi * block:(bi + 1) * block]
+    payloads = [np.frombuffer(bytes(p), np.uint8) for p in payloads]
+    arena, offs, lens = W.pack(payloads)
+    batch = g.Batch.from_arena(to_device(arena), offs, lens, block)
+    slots = batch.n_blocks * (block // 4096)
+    assert slots > 65536 and slots // 64 >= len(payloads)
+    t, ot = tables_from(payloads, block, range(0, len(payloads), 5), capacity=1 << 16)
+    say("detect large payloads", block, batch.n_blocks, "blocks")
+    got = check(batch, payloads, t, ot, f"large payloads, {block} blocks")
+    assert (got["status"] == g.HIT_BATCH).any()
