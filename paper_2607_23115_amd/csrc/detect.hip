@@ -107,7 +107,7 @@ __global__ __launch_bounds__(64 * W) void detect_small_kernel(DetectArgs a) {
   __shared__ uint64_t wave_bytes[W];
 
   // digests, block lengths, and each block's table probe
-  quad_pass<W, true, W == 1>(a.fp, lds, tables, a.blen, TableProbe{a.t, a.status, a.ref});
+  quad_pass<W, true, W == 1>(a.fp, blockIdx.x, lds, tables, a.blen, TableProbe{a.t, a.status, a.ref});
   // Arrive. Each thread waits for its own stores (digests, lengths, statuses) to
   // complete; after the barrier one release at device scope per workgroup writes them
   // back from this XCD's L2, and the arrival counts. (A device-scope fence in every wave

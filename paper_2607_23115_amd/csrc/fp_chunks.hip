@@ -8,7 +8,10 @@
 // block). Two lanes own one slot: the even lane keeps XXH64 accumulators 1 and 2, the
 // odd lane 3 and 4, so each lane runs two independent chains of 128 rounds and a
 // wave covers 32 leaves. A workgroup of 4 waves owns GROUP = 128 consecutive slots
-// (LPB <= GROUP), or one whole block walked GROUP slots at a time (LPB > GROUP).
+// (LPB <= GROUP), or one whole block walked GROUP slots at a time (LPB > GROUP). In a
+// large batch of blocks of up to 64 KiB, the last kQuadTailSlots slots go to workgroups
+// of four lanes per leaf (64 slots each, half the stages): the batch's last round of
+// workgroups, during which part of the GPU already idles, then ends sooner.
 //
 // Occupancy. HBM read rate on MI355X rises as fewer waves stream at once: one 4-wave
 // workgroup per CU reads faster than two or more (measured with plain read kernels and
@@ -41,6 +44,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kSoloPad = 24 << 10;  // takes the workgroup's LDS past 80 KiB: one per CU
+constexpr uint64_t kQuadTailSlots = 16384;
 
 template <bool kSolo>
 __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
@@ -56,6 +60,15 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
   const uint32_t L2 = a.lpb_log2;
   const uint32_t lpb = 1u << L2;
   const bool even = (lane & 1) == 0;
+
+  // The last slots of a batch of small blocks, past a.items groups: four lanes per leaf,
+  // W * kQuadLeaves slots per workgroup (see launch_fp).
+  if (!kSolo && blockIdx.x >= a.items) {
+    constexpr uint64_t kPerGroup = GROUP / (W * kQuadLeaves);
+    quad_pass<W, false>(a, a.items * kPerGroup + (blockIdx.x - a.items), lds,
+                        reinterpret_cast<uint64_t (*)[2 * kQuadLeaves]>(&tables[0][0]), nullptr);
+    return;
+  }
 
   // Persistent workgroups: a grid of a few workgroups per CU walks the work items.
   for (uint64_t item = blockIdx.x; item < a.items; item += gridDim.x) {
@@ -131,7 +144,7 @@ template <int W>
 __global__ __launch_bounds__(64 * W) void fp_quad_kernel(FpArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[W == 1 ? kQuadDirectLds : W * kQuadWaveLds];
   __shared__ uint64_t tables[W][2 * kQuadLeaves];
-  quad_pass<W, false, W == 1>(a, lds, tables, nullptr);
+  quad_pass<W, false, W == 1>(a, blockIdx.x, lds, tables, nullptr);
 }
 
 
@@ -184,11 +197,19 @@ gleam_status launch_fp(const gleam_batch* b, uint64_t* d_block_digest, uint64_t*
     return launch_status("fp_quad_kernel");
   }
   constexpr uint64_t group = (kThreads / 64) * kLeavesPerWave;
-  const uint64_t items = lpb <= group ? (b->n_blocks * lpb + group - 1) / group : b->n_blocks;
+  uint64_t items = lpb <= group ? (b->n_blocks * lpb + group - 1) / group : b->n_blocks;
   // 1 MiB blocks and up: one workgroup resident per CU, a grid of 4 per CU walking the
   // blocks. Smaller blocks: one workgroup per item (both measured best on MI355X).
   const bool solo = lpb >= 256;
   uint64_t grid = items;
+  // Blocks of up to 64 KiB in a batch of several rounds of workgroups: the last
+  // kQuadTailSlots slots (rounded to whole groups) run as workgroups of four lanes per
+  // leaf, which finish in half the time, so the GPU drains faster at the end.
+  if (lpb <= (uint64_t)kQuadLeaves && slots > 4 * kQuadTailSlots) {
+    items = (slots - kQuadTailSlots) / group;
+    const uint64_t quad_group = (kThreads / 64) * kQuadLeaves;
+    grid = items + (slots - items * group + quad_group - 1) / quad_group;
+  }
   if (solo) {
     int cus = 0;
     gleam_status st = device_cu_count(&cus);

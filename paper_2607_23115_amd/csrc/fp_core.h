@@ -515,8 +515,9 @@ __device__ __forceinline__ uint64_t hash_slot_quad_direct(const Leaf& lf, uint8_
   return hash_quad_gathered_direct(lf, tile, table, lane);
 }
 
-// The four-lanes-per-leaf pass of one workgroup of W waves over W * kQuadLeaves slots
-// (LPB <= kQuadLeaves, so every wave holds whole blocks): leaf digests (optional) and
+// The four-lanes-per-leaf pass of one workgroup of W waves over the W * kQuadLeaves slots
+// of group `group` (LPB <= kQuadLeaves, so every wave holds whole blocks): leaf digests
+// (optional) and
 // block digests. With kLen, the lane holding a block's last leaf also writes the
 // block's byte length to blen[g]. With kDirect (W = 1), `lds` holds kQuadDirectLds bytes
 // and aligned waves load every stage at once; otherwise kQuadWaveLds per wave.
@@ -531,15 +532,16 @@ struct NoProbe {
 };
 
 template <int W, bool kLen, bool kDirect = false, typename Probe = NoProbe>
-__device__ __forceinline__ void quad_pass(const FpArgs& a, uint8_t* lds, uint64_t (*tables)[2 * kQuadLeaves],
-                                          uint32_t* blen, const Probe& probe = Probe()) {
+__device__ __forceinline__ void quad_pass(const FpArgs& a, uint64_t group, uint8_t* lds,
+                                          uint64_t (*tables)[2 * kQuadLeaves], uint32_t* blen,
+                                          const Probe& probe = Probe()) {
   static_assert(!kDirect || W == 1, "the direct loads hold one wave's stages");
   constexpr uint64_t kQuadGroup = (uint64_t)W * kQuadLeaves;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const uint32_t L2 = a.lpb_log2;
   const uint32_t lpb = 1u << L2;
-  const uint64_t wave_slot0 = uniform64((uint64_t)blockIdx.x * kQuadGroup + (uint64_t)wave * kQuadLeaves);
+  const uint64_t wave_slot0 = uniform64(group * kQuadGroup + (uint64_t)wave * kQuadLeaves);
   const uint64_t slot = wave_slot0 + (lane >> 2);
   const uint64_t g = slot >> L2;
   const uint32_t k = (uint32_t)(slot & (lpb - 1));

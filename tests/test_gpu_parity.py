@@ -297,6 +297,24 @@ def test_4k_blocks_past_the_small_batch_limit(skew):
     assert np.array_equal(u64(lv), wleaves.reshape(-1))
 
 
+@pytest.mark.parametrize("block,skew", [(8192, 0), (16384, 5), (32768, 3)])
+def test_last_slots_four_lanes(block, skew):
+    """Past 65,536 leaf slots with small payloads, the two-lanes kernel hands the batch's
+    last 16,384 slots to workgroups of four lanes per leaf: 50,000 small copies (64 B to
+    24 KiB, planted repeats) in blocks of 2-8 leaves, so payloads straddle the hand-over;
+    every block and leaf digest equals the oracle's."""
+    sc = W.SmallCopies(n=50_000, lo=64, hi=24576, workload=41, skew=skew)
+    payloads = sc.payloads()
+    batch = g.Batch.from_arena(to_device(sc.arena), sc.offsets, sc.sizes, block)
+    slots = batch.n_blocks * batch.leaves_per_block
+    assert slots > 65536 and slots < 64 * batch.n_seg
+    say("last slots four lanes", block, "skew", skew, "slots", slots)
+    d, lv = g.fp_chunks(batch, with_leaves=True)
+    want, wleaves = oracle.batch_digests(payloads, block, with_leaves=True, threads=host_threads())
+    assert np.array_equal(u64(d), want)
+    assert np.array_equal(u64(lv), wleaves.reshape(-1))
+
+
 @pytest.mark.parametrize("seed", range(24))
 def test_randomized_batches(seed):
     """Seeded random batch geometries: block size 4 KiB..16 MiB, 1..4000 payloads whose
