@@ -286,3 +286,34 @@ def test_large_payloads_four_lanes(block):
     say("detect large payloads", block, batch.n_blocks, "blocks")
     got = check(batch, payloads, t, ot, f"large payloads, {block} blocks")
     assert (got["status"] == g.HIT_BATCH).any()
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_randomized_batches_detect(seed):
+    """Seeded random batches through gleam_detect, on both sides of its one-kernel limits:
+    block size 4-256 KiB, 1-3000 payloads of empty, tiny, leaf- and block-edge and
+    multi-block lengths, repeated payloads, an optional skew, a table holding a random part
+    of the digests; every output equals the oracle's and the three calls'."""
+    rng = np.random.default_rng(97_000 + seed)
+    block = 4096 << int(rng.integers(0, 7))
+    n = int(rng.choice([1, 9, 120, 900, 3000]))
+    edges = np.array([0, 1, 31, 32, 33, 4095, 4096, 4097, block - 1, block, block + 1, 2 * block + 17])
+    kind = rng.integers(0, 3, n)
+    lens = np.where(kind == 0, rng.choice(edges, n),
+                    np.where(kind == 1, rng.integers(0, 8192, n), rng.integers(0, 3 * block + 1, n)))
+    lens = np.minimum(lens, (96 << 20) // n)
+    payloads = [np.frombuffer(rng.bytes(int(m)), np.uint8) for m in lens]
+    for i in rng.integers(0, n, n // 8):
+        payloads[int(i)] = payloads[int(rng.integers(0, n))].copy()
+    skew = int(rng.choice([0, 0, 3, 8]))
+    arena, offs, blens = W.pack(payloads, align=256, skew=skew)
+    batch = g.Batch.from_arena(to_device(arena), offs, blens, block)
+    say("randomized detect", seed, "block", block, "payloads", n, "blocks", batch.n_blocks, "skew", skew)
+    dig, _ = oracle.batch_digests(payloads, block, threads=host_threads())
+    held = np.unique(dig[rng.random(dig.size) < 0.3]) if dig.size else np.zeros(0, np.uint64)
+    t, ot = g.Cache(1 << 16), oracle.Table()
+    if held.size:
+        vals = rng.integers(0, 2**63, held.size, dtype=np.uint64)
+        t.insert(keys_to_device(held), keys_to_device(vals))
+        ot.insert(held, vals)
+    check(batch, payloads, t, ot, f"seed {seed}")

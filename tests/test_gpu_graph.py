@@ -185,18 +185,22 @@ def test_graph_replays_the_other_capturable_calls():
         torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("which", ["random16", "resnet50"])
-def test_graph_replays_detect_one_kernel(which):
-    """gleam_detect (one kernel for these batches, its workspace counter re-armed by every
-    call) captured once: every replay equals the eager call and the three calls."""
+@pytest.mark.parametrize("which", ["random16", "resnet50", "small_copies_20k"])
+def test_graph_replays_detect(which):
+    """gleam_detect captured once: one kernel for the first two batches (its workspace
+    counter re-armed by every call), the three calls' kernels for 20k small copies with
+    planted repeats (scratch clear, probe, resolve, tally, place); every replay equals the
+    eager call and the three calls."""
     if which == "random16":
         payloads, block = [W.random16_payload()], W.RANDOM16_BLOCK
-    else:
+    elif which == "resnet50":
         payloads, block = W.resnet50_payloads(), W.RESNET_BLOCK
+    else:
+        payloads, block = W.SmallCopies(n=20_000).payloads(), W.SMALL_BLOCK
     arena, offs, lens = W.pack(payloads)
     d_arena = torch.from_numpy(arena).to("cuda")
     batch = g.Batch.from_arena(d_arena, offs, lens, block)
-    table = g.Cache(1 << 12)
+    table = g.Cache(1 << 17 if which == "small_copies_20k" else 1 << 12)
     half = g.Batch.from_arena(d_arena, offs[: len(offs) // 2 + 1], lens[: len(lens) // 2 + 1], block)
     table.insert(g.fp_chunks(half), torch.arange(half.n_blocks, dtype=torch.int64, device="cuda"))
     ref = Path(batch, table)
