@@ -231,6 +231,7 @@ def identify_path(args, g, torch, threads, batch, payloads, keep):
     n_regions = region_first.size - 1
     rf = torch.from_numpy(region_first.view(np.int64)).to("cuda")
     ws = g.workspace(batch.n_blocks + batch.n_seg)
+    settle = None if args.no_settle else settle_clock(g, torch, keep)
     for _ in range(args.warmup):
         g.identify_weights(batch, recorded, rf, ws=ws)
     torch.cuda.synchronize()
@@ -272,7 +273,8 @@ def identify_path(args, g, torch, threads, batch, payloads, keep):
                       "pct_of_hbm_peak": round(100 * payload_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
                       "call_ms": {"median": round(float(np.median(per_call)), 4), "min": round(min(per_call), 4),
                                   "max": round(max(per_call), 4)},
-                      "gbs_at_median": round(payload_bytes / (float(np.median(per_call)) * 1e-3) / 1e9, 2)},
+                      "gbs_at_median": round(payload_bytes / (float(np.median(per_call)) * 1e-3) / 1e9, 2),
+                      "clock_settle": None if settle is None else {"ms": settle[0], "read_launches": settle[1]}},
            "cpu_baseline": cpu}
     print(json.dumps(out), flush=True)
 
