@@ -279,6 +279,90 @@ def identify_path(args, g, torch, threads, batch, payloads, keep):
     print(json.dumps(out), flush=True)
 
 
+def block_lengths(batch):
+    """Host array of every block's byte length (the last block of a payload may be short)."""
+    first = batch.host_first.astype(np.int64)
+    lens = batch.host_len.astype(np.int64)
+    nb = np.diff(first)
+    out = np.full(batch.n_blocks, batch.block_bytes, dtype=np.int64)
+    last = first[1:][nb > 0] - 1
+    out[last] = lens[nb > 0] - (nb[nb > 0] - 1) * batch.block_bytes
+    return out
+
+
+def prefix_exposure(g, torch, batch, payloads, changed_frac=0.1, seed=2607):
+    """The paper's identifier (MD5 of a payload's first 128 bytes, keyed with the payload's
+    size; payloads of at most 1024 bytes get no entry) against the full-content block
+    digests, in two cases:
+    - reuse inside the batch, empty tables: a payload whose (prefix key, size) repeats an
+      earlier payload's would be restored from it (checked against its bytes); a block
+      whose digest repeats an earlier block's is HIT_BATCH;
+    - a reload after a partial update: `changed_frac` of the eligible payloads get one byte
+      flipped past their first 128 bytes, and the tables hold the first version's
+      identifiers. A prefix hit on a changed payload restores stale bytes; the block
+      digests send exactly the blocks holding a flipped byte (checked)."""
+    arena = batch.keepalive
+    offs = batch.d_addr.cpu().numpy().view(np.uint64).astype(np.int64) - arena.data_ptr()
+    lens = batch.host_len.astype(np.int64)
+    first = batch.host_first.astype(np.int64)
+    blen = block_lengths(batch)
+    n = batch.n_seg
+    # in-batch reuse
+    _, key, elig = g.md5_prefix(batch)
+    key = g.as_u64(key)
+    elig = elig.cpu().numpy().astype(bool)
+    seen, reused, reused_bytes, false_hits, false_bytes = {}, 0, 0, 0, 0
+    for i in np.flatnonzero(elig).tolist():
+        k = (int(key[i]), int(lens[i]))
+        if k not in seen:
+            seen[k] = i
+            continue
+        reused += 1
+        reused_bytes += int(lens[i])
+        if not np.array_equal(payloads[i], payloads[seen[k]]):
+            false_hits += 1
+            false_bytes += int(lens[i])
+    det = g.detect(batch, g.Cache(1 << 10))
+    st = det.status[:batch.n_blocks].cpu().numpy()
+    in_batch = {"prefix": {"eligible_payloads": int(elig.sum()), "reused_payloads": reused,
+                           "reused_bytes": reused_bytes, "false_hits": false_hits, "false_hit_bytes": false_bytes},
+                "blocks": {"hit_batch_blocks": int((st == g.HIT_BATCH).sum()),
+                           "saved_bytes": int(blen[st == g.HIT_BATCH].sum())}}
+    # reload after a partial update
+    rng = np.random.default_rng(seed)
+    cand = np.flatnonzero(elig)
+    changed = np.sort(rng.choice(cand, int(round(changed_frac * cand.size)), replace=False))
+    pos = np.array([int(rng.integers(128, int(lens[i]))) for i in changed.tolist()], dtype=np.int64)
+    arena2 = arena.clone()
+    where = torch.from_numpy(offs[changed] + pos).to(arena2.device)
+    arena2[where] = arena2[where] ^ 1
+    batch2 = g.Batch.from_arena(arena2, offs.astype(np.uint64), batch.host_len, batch.block_bytes)
+    _, key2, elig2 = g.md5_prefix(batch2)
+    key2 = g.as_u64(key2)
+    elig2 = elig2.cpu().numpy().astype(bool)
+    held = {(int(key[i]), int(lens[i])) for i in np.flatnonzero(elig).tolist()}
+    hit = np.array([bool(elig2[i]) and (int(key2[i]), int(lens[i])) in held for i in range(n)], dtype=bool)
+    is_changed = np.zeros(n, dtype=bool)
+    is_changed[changed] = True
+    digests = g.fp_chunks(batch)
+    cap = 1 << max(10, int(2 * batch.n_blocks - 1).bit_length())
+    btable = g.Cache(cap)
+    btable.insert(digests, torch.arange(batch.n_blocks, dtype=torch.int64, device=digests.device))
+    det2 = g.detect(batch2, btable)
+    st2 = det2.status[:batch.n_blocks].cpu().numpy()
+    want_miss = np.zeros(batch.n_blocks, dtype=bool)
+    want_miss[first[changed] + pos // batch.block_bytes] = True
+    if not np.array_equal(st2 == g.MISS, want_miss):
+        raise SystemExit("exposure: the block digests did not miss exactly the updated blocks")
+    reload = {"changed_payloads": int(changed.size),
+              "prefix": {"hits": int(hit.sum()), "stale_payloads": int((hit & is_changed).sum()),
+                         "stale_bytes": int(lens[hit & is_changed].sum()), "sent_bytes": int(lens[~hit].sum())},
+              "blocks": {"hits": int((st2 != g.MISS).sum()), "missed_blocks": int(want_miss.sum()),
+                         "stale_blocks": 0, "sent_bytes": int(blen[st2 == g.MISS].sum())}}
+    del arena2, batch2
+    return {"in_batch": in_batch, "reload_after_update": reload}
+
+
 def md5_path(args, g, torch, threads, batch, payloads, desc):
     """The paper's identifier (MD5 of each payload's first 1024 bits) over a workload's
     payloads: payloads per second; it reads at most 128 bytes of each."""
@@ -307,7 +391,8 @@ def md5_path(args, g, torch, threads, batch, payloads, desc):
            "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "u32", "data": "synthetic",
            "config": {"workload": desc, "payloads": batch.n_seg, "bytes_read": read,
-                      "payload_bytes": int(batch.host_len.sum())},
+                      "payload_bytes": int(batch.host_len.sum()),
+                      "exposure": prefix_exposure(g, torch, batch, payloads)},
            "cpu_baseline": cpu}
     print(json.dumps(out), flush=True)
 

@@ -49,3 +49,22 @@ def test_more_than_one_gpu_is_refused():
                          text=True, timeout=120)
     assert res.returncode == 2
     assert "one GPU" in res.stderr
+
+
+def test_block_lengths_follow_the_payload_geometry():
+    """The exposure figures weigh blocks by their byte lengths: full blocks, the short
+    last block of each payload, none for an empty payload."""
+
+    class B:  # the host-side fields of a Batch
+        pass
+
+    import numpy as np
+    b = B()
+    b.block_bytes = 4096
+    b.host_len = np.array([0, 1, 4096, 4097, 10000, 0, 8192], dtype=np.uint64)
+    nb = [(int(n) + 4095) // 4096 for n in b.host_len]
+    b.host_first = np.concatenate([[0], np.cumsum(nb)]).astype(np.uint64)
+    b.n_blocks = int(b.host_first[-1])
+    want = [1, 4096, 4096, 1, 4096, 4096, 1808, 4096, 4096]
+    assert bench.block_lengths(b).tolist() == want
+    assert int(bench.block_lengths(b).sum()) == int(b.host_len.sum())
