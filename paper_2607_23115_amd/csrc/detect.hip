@@ -100,14 +100,13 @@ __global__ __launch_bounds__(64 * W) void detect_small_kernel(DetectArgs a) {
   static_assert(kSlots >= 2 * kMax, "dedup table load at most 1/2");
   static_assert(16 * T >= (int)kMax, "one compaction round");
   __shared__ __attribute__((aligned(16))) uint8_t lds[W == 1 ? kQuadDirectLds : W * kQuadWaveLds];
-  __shared__ uint64_t tables[W][2 * kQuadLeaves];
   __shared__ __attribute__((aligned(16))) uint8_t st[kMax];
   __shared__ uint32_t last;
   __shared__ uint32_t wave_sums[W];
   __shared__ uint64_t wave_bytes[W];
 
   // digests, block lengths, and each block's table probe
-  quad_pass<W, true, W == 1>(a.fp, blockIdx.x, lds, tables, a.blen, TableProbe{a.t, a.status, a.ref});
+  quad_pass<W, true, W == 1>(a.fp, blockIdx.x, lds, a.blen, TableProbe{a.t, a.status, a.ref});
   // Arrive. Each thread waits for its own stores (digests, lengths, statuses) to
   // complete; after the barrier one release at device scope per workgroup writes them
   // back from this XCD's L2, and the arrival counts. (A device-scope fence in every wave

@@ -28,8 +28,9 @@
 // the leaf index, so both the stores and each lane's 16-byte reads of its own
 // half-stripes are free of bank conflicts; the next stage's loads are in flight while
 // the current one is hashed. Waves that are not one contiguous full run (payload ends,
-// small payloads) use the same tile with per-instruction leaf addresses from a small
-// LDS table. Every load covers 16 bytes of its own leaf from the leaf's start, at any
+// small payloads) use the same tile with per-instruction leaf addresses read from the
+// registers of the lanes that hash each leaf. Every load covers 16 bytes of its own leaf
+// from the leaf's start, at any
 // alignment (see load_stream16_any), so a leaf's bytes reach the tile in order and no
 // path shifts them.
 //
@@ -52,11 +53,9 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
   constexpr uint32_t GROUP = W * kLeavesPerWave;
   __shared__ __attribute__((aligned(16))) uint8_t lds[W * kWaveLds + (kSolo ? kSoloPad : 0)];
   __shared__ uint64_t roots[2][kMaxRoots];
-  __shared__ uint64_t tables[W][2 * kLeavesPerWave];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   uint8_t* tile = lds + wave * kWaveLds;
-  uint64_t* table = tables[wave];
   const uint32_t L2 = a.lpb_log2;
   const uint32_t lpb = 1u << L2;
   const bool even = (lane & 1) == 0;
@@ -65,8 +64,7 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
   // W * kQuadLeaves slots per workgroup (see launch_fp).
   if (!kSolo && blockIdx.x >= a.items) {
     constexpr uint64_t kPerGroup = GROUP / (W * kQuadLeaves);
-    quad_pass<W, false>(a, a.items * kPerGroup + (blockIdx.x - a.items), lds,
-                        reinterpret_cast<uint64_t (*)[2 * kQuadLeaves]>(&tables[0][0]), nullptr);
+    quad_pass<W, false>(a, a.items * kPerGroup + (blockIdx.x - a.items), lds, nullptr);
     return;
   }
 
@@ -80,7 +78,7 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
       const uint64_t g = slot >> L2;
       const uint32_t k = (uint32_t)(slot & (lpb - 1));
       const Leaf lf = locate_wave(a, wave_slot0 >> L2, g, k, lane);
-      const uint64_t d = hash_slot(lf, tile, table, lane);
+      const uint64_t d = hash_slot(lf, tile, lane);
       if (a.leaf_out && even && g < a.n_blocks) a.leaf_out[slot] = lf.len ? d : 0;
       const uint32_t G = lpb <= kLeavesPerWave ? lpb : (uint32_t)kLeavesPerWave;
       const uint32_t p = k & (G - 1);
@@ -119,7 +117,7 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
       for (uint32_t grp = 0; grp < groups; ++grp) {
         const uint32_t k = grp * GROUP + (uint32_t)wave * kLeavesPerWave + (lane >> 1);
         const Leaf lf = locate(a, g, k, s0);
-        const uint64_t d = hash_slot(lf, tile, table, lane);
+        const uint64_t d = hash_slot(lf, tile, lane);
         if (a.leaf_out && even) a.leaf_out[((uint64_t)g << L2) + k] = lf.len ? d : 0;
         const uint32_t before = k & ~(uint32_t)(kLeavesPerWave - 1);
         const uint32_t n = nleaf > before ? min(nleaf - before, (uint32_t)kLeavesPerWave) : 0u;
@@ -143,8 +141,7 @@ __global__ __launch_bounds__(kThreads) void fp_kernel(FpArgs a) {
 template <int W>
 __global__ __launch_bounds__(64 * W) void fp_quad_kernel(FpArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[W == 1 ? kQuadDirectLds : W * kQuadWaveLds];
-  __shared__ uint64_t tables[W][2 * kQuadLeaves];
-  quad_pass<W, false, W == 1>(a, blockIdx.x, lds, tables, nullptr);
+  quad_pass<W, false, W == 1>(a, blockIdx.x, lds, nullptr);
 }
 
 

@@ -18,9 +18,15 @@ namespace {
 // the same tile as an aligned one, each load covering 16 of its own bytes. Measured on
 // MI355X: a 4-byte aligned start streams at about 85% of the aligned rate, other starts
 // at 65-70%, both faster than reading aligned chunks and shifting them in registers.
+// The payload pointers are built from integer addresses, so the compiler cannot tell
+// their address space and would emit flat loads, which on gfx950 also count against the
+// LDS wait counter: a wait for the stage tile's LDS accesses would then wait for the
+// loads in flight too. The loads name the global address space instead.
 typedef u32x4 u32x4_any __attribute__((aligned(1)));
+typedef const __attribute__((address_space(1))) u32x4_any global_u32x4_any;
+typedef const __attribute__((address_space(1))) uint64_t global_u64;
 __device__ __forceinline__ uint4 load_stream16_any(const uint8_t* p) {
-  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_any*>(p));
+  const u32x4 v = __builtin_nontemporal_load((global_u32x4_any*)(p));
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
@@ -53,6 +59,13 @@ struct Leaf {
 __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// x as held by lane `src` (a constant after unrolling): a register read, no memory trip.
+__device__ __forceinline__ uint64_t lane64(uint64_t x, int src) {
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)x, src);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(x >> 32), src);
   return ((uint64_t)hi << 32) | lo;
 }
 
@@ -108,7 +121,7 @@ __device__ __forceinline__ void load_tail(const uint8_t* p, uint32_t len, uint64
   const uint64_t at = reinterpret_cast<uint64_t>(p) + (stripes << 5);
   const uint32_t lead = (uint32_t)(at & 7);
   const uint32_t words = tail ? (lead + tail + 7) >> 3 : 0;
-  const uint64_t* w = reinterpret_cast<const uint64_t*>(at - lead);
+  global_u64* w = (global_u64*)(at - lead);
 #pragma unroll
   for (int i = 0; i < 5; ++i) W[i] = (uint32_t)i < words ? w[i] : 0;
 }
@@ -202,46 +215,43 @@ __device__ uint64_t hash_wave_contiguous(const uint8_t* base, uint8_t* tile, int
 }
 
 // Any 32 leaves (lengths 0..4096, at any alignment, anywhere in
-// memory). Full stripes stream through the tile as above; the loader lanes find each
-// leaf's address and full-stripe chunk count in a small per-wave LDS table (kept out of
-// registers, which the streamed stage already fills); the wave runs as many stages as
-// its longest leaf needs; the even lane then finishes its leaf's tail directly.
-__device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
+// memory). Full stripes stream through the tile as above; for each load instruction the
+// loader lanes take their leaf's address and full-stripe chunk count from the lane pair
+// that hashes that leaf, by register reads (a table in LDS cost two dependent LDS round
+// trips per load); the wave runs as many stages as its longest leaf needs; the even lane
+// then finishes its leaf's tail directly.
+__device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, int lane) {
   const Roles r = roles(tile, lane);
   const uint32_t stripes = lf.len >> 5;
-  if ((lane & 1) == 0) {
-    table[lane] = reinterpret_cast<uint64_t>(lf.addr);  // entry of leaf lane / 2: {address, chunks}
-    table[lane + 1] = 2ull * stripes;
-  }
+  const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
+  const uint32_t chunks = 2 * stripes;  // 16-byte chunks in the leaf's whole stripes
   uint32_t longest = stripes;
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) longest = max(longest, (uint32_t)__shfl_xor((int)longest, o, 64));
   const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 15) / 16);
   uint64_t W[5];
   load_tail(lf.addr, r.rp ? 0u : lf.len, W);
-  wave_lds_sync();
 
+  // load instruction k: lanes 0-31 read leaf 2k (held by lanes 4k, 4k + 1), lanes 32-63
+  // leaf 2k + 1 (lanes 4k + 2, 4k + 3)
+  auto stage_loads = [&](uint4* R, uint64_t chunk) {
+#pragma unroll
+    for (int k = 0; k < kLoads; ++k) {
+      const uint64_t a0 = lane64(addr, 4 * k), a1 = lane64(addr, 4 * k + 2);
+      const uint32_t n0 = __builtin_amdgcn_readlane(chunks, 4 * k), n1 = __builtin_amdgcn_readlane(chunks, 4 * k + 2);
+      const uint64_t a = r.lm ? a1 : a0;
+      const uint32_t n = r.lm ? n1 : n0;
+      R[k] = chunk < n ? load_stream16_any(reinterpret_cast<const uint8_t*>(a) + chunk * 16) : make_uint4(0, 0, 0, 0);
+    }
+  };
   uint64_t va = r.rp ? 0 : kP1 + kP2, vb = r.rp ? 0 - kP1 : kP2;
   uint4 R[kLoads];
-#pragma unroll
-  for (int k = 0; k < kLoads; ++k) {
-    const uint64_t* e = table + 2 * (2 * k + r.lm);
-    R[k] = (uint64_t)r.lc < e[1] ? load_stream16_any(reinterpret_cast<const uint8_t*>(e[0]) + r.lc * 16)
-                                 : make_uint4(0, 0, 0, 0);
-  }
+  stage_loads(R, (uint64_t)r.lc);
   for (uint32_t s = 0; s < stages; ++s) {
 #pragma unroll
     for (int k = 0; k < kLoads; ++k) *reinterpret_cast<uint4*>(tile + tile_slot(r, k)) = R[k];
     wave_lds_sync();
-    if (s + 1 < stages) {
-      const uint64_t chunk = (uint64_t)(s + 1) * kRunLanes + r.lc;
-#pragma unroll
-      for (int k = 0; k < kLoads; ++k) {
-        const uint64_t* e = table + 2 * (2 * k + r.lm);
-        R[k] = chunk < e[1] ? load_stream16_any(reinterpret_cast<const uint8_t*>(e[0]) + chunk * 16)
-                            : make_uint4(0, 0, 0, 0);
-      }
-    }
+    if (s + 1 < stages) stage_loads(R, (uint64_t)(s + 1) * kRunLanes + r.lc);
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       uint4 D[8];
@@ -263,13 +273,13 @@ __device__ uint64_t hash_wave_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
 }
 
 // Digest of this lane pair's leaf, in the even lane.
-__device__ __forceinline__ uint64_t hash_slot(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
+__device__ __forceinline__ uint64_t hash_slot(const Leaf& lf, uint8_t* tile, int lane) {
   const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
   const uint64_t a0 = shfl64(addr, 0);
   const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)(lane >> 1) * 4096;
   if (__all(contiguous)) return hash_wave_contiguous(reinterpret_cast<const uint8_t*>(uniform64(a0)), tile, lane);
   if (!__any(lf.len != 0)) return 0;
-  return hash_wave_gathered(lf, tile, table, lane);
+  return hash_wave_gathered(lf, tile, lane);
 }
 
 // Bottom-up tree over `count` roots in LDS (double-buffered), by one wave.
@@ -367,43 +377,43 @@ __device__ uint64_t hash_quad_contiguous(const uint8_t* base, uint8_t* tile, int
   return ra ? 0 : xxh_avalanche(xxh_converge(v1, v2, v3, v4) + 4096);
 }
 
-// Any 16 leaves at any alignment: full stripes through the tile
-// (leaf addresses and full-stripe chunk counts in a per-wave LDS table), as many stages
-// as the longest leaf needs; lane 4l finishes leaf l's tail.
-__device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
+// Any 16 leaves at any alignment: full stripes through the tile, each load instruction's
+// leaf address and full-stripe chunk count read from the quad that hashes the leaf (as in
+// hash_wave_gathered), as many stages as the longest leaf needs; lane 4l finishes leaf
+// l's tail.
+__device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, int lane) {
   const int lm = lane / 32, lc = lane % 32, rl = lane >> 2, ra = lane & 3;
   const uint32_t stripes = lf.len >> 5;
-  if (ra == 0) {
-    table[2 * rl] = reinterpret_cast<uint64_t>(lf.addr);
-    table[2 * rl + 1] = 2ull * stripes;
-  }
+  const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
+  const uint32_t chunks = 2 * stripes;
   uint32_t longest = stripes;
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) longest = max(longest, (uint32_t)__shfl_xor((int)longest, o, 64));
   const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 31) / 32);
   uint64_t W[5];
   load_tail(lf.addr, ra ? 0u : lf.len, W);
-  wave_lds_sync();
+  // load instruction k: lanes 0-31 read leaf 2 (k mod 8) (held by lane 8 (k mod 8)),
+  // lanes 32-63 leaf 2 (k mod 8) + 1 (held by lane 8 (k mod 8) + 4)
+  auto stage_loads = [&](uint4* R, uint64_t stage_chunk) {
+#pragma unroll
+    for (int k = 0; k < kQuadLoads; ++k) {
+      const int h0 = 8 * (k & 7);
+      const uint64_t a0 = lane64(addr, h0), a1 = lane64(addr, h0 + 4);
+      const uint32_t n0 = __builtin_amdgcn_readlane(chunks, h0), n1 = __builtin_amdgcn_readlane(chunks, h0 + 4);
+      const uint64_t la = lm ? a1 : a0;
+      const uint32_t n = lm ? n1 : n0;
+      const uint64_t c = stage_chunk + (uint64_t)quad_chunk(lc, k);
+      R[k] = c < n ? load_stream16_any(reinterpret_cast<const uint8_t*>(la) + c * 16) : make_uint4(0, 0, 0, 0);
+    }
+  };
   uint64_t v = quad_acc_init(ra);
   uint4 R[kQuadLoads];
-#pragma unroll
-  for (int k = 0; k < kQuadLoads; ++k) {
-    const uint64_t* e = table + 2 * quad_leaf(lm, k);
-    const uint64_t c = (uint64_t)quad_chunk(lc, k);
-    R[k] = c < e[1] ? load_stream16_any(reinterpret_cast<const uint8_t*>(e[0]) + c * 16) : make_uint4(0, 0, 0, 0);
-  }
+  stage_loads(R, 0);
   for (uint32_t s = 0; s < stages; ++s) {
 #pragma unroll
     for (int k = 0; k < kQuadLoads; ++k) *reinterpret_cast<uint4*>(tile + quad_tile_slot(lm, lc, k)) = R[k];
     wave_lds_sync();
-    if (s + 1 < stages) {
-#pragma unroll
-      for (int k = 0; k < kQuadLoads; ++k) {
-        const uint64_t* e = table + 2 * quad_leaf(lm, k);
-        const uint64_t c = (uint64_t)(s + 1) * 64 + quad_chunk(lc, k);
-        R[k] = c < e[1] ? load_stream16_any(reinterpret_cast<const uint8_t*>(e[0]) + c * 16) : make_uint4(0, 0, 0, 0);
-      }
-    }
+    if (s + 1 < stages) stage_loads(R, (uint64_t)(s + 1) * 64);
     const int left = (int)stripes - (int)(s * 32);
     v = quad_rounds(v, tile, rl, ra, left < 0 ? 0 : (left > 32 ? 32 : left));
     wave_lds_sync();
@@ -415,13 +425,13 @@ __device__ uint64_t hash_quad_gathered(const Leaf& lf, uint8_t* tile, uint64_t* 
 }
 
 // Digest of this lane quad's leaf, in lane 4l.
-__device__ __forceinline__ uint64_t hash_slot_quad(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
+__device__ __forceinline__ uint64_t hash_slot_quad(const Leaf& lf, uint8_t* tile, int lane) {
   const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
   const uint64_t a0 = shfl64(addr, 0);
   const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)(lane >> 2) * 4096;
   if (__all(contiguous)) return hash_quad_contiguous(reinterpret_cast<const uint8_t*>(uniform64(a0)), tile, lane);
   if (!__any(lf.len != 0)) return 0;
-  return hash_quad_gathered(lf, tile, table, lane);
+  return hash_quad_gathered(lf, tile, lane);
 }
 
 // ---- One round trip per wave: every stage straight into LDS --------------------------
@@ -467,26 +477,25 @@ __device__ uint64_t hash_quad_contiguous_direct(const uint8_t* base, uint8_t* ti
 // Any 16 leaves at 16-byte aligned addresses: every stage the longest leaf needs, issued
 // together (a lane loads a chunk only if it lies in its leaf's whole stripes); lane 4l
 // finishes leaf l's tail.
-__device__ uint64_t hash_quad_gathered_direct(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
+__device__ uint64_t hash_quad_gathered_direct(const Leaf& lf, uint8_t* tile, int lane) {
   const int rl = lane >> 2, ra = lane & 3, t = lane >> 1, h = lane & 1;
   const uint32_t stripes = lf.len >> 5;
-  if (ra == 0) {
-    table[2 * rl] = reinterpret_cast<uint64_t>(lf.addr);
-    table[2 * rl + 1] = 2ull * stripes;
-  }
+  const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
+  const uint32_t chunks = 2 * stripes;
   uint32_t longest = stripes;
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) longest = max(longest, (uint32_t)__shfl_xor((int)longest, o, 64));
   const uint32_t stages = __builtin_amdgcn_readfirstlane((longest + 31) / 32);
   uint64_t W[5];
   load_tail(lf.addr, ra ? 0u : lf.len, W);
-  wave_lds_sync();
   for (uint32_t s = 0; s < stages; ++s) {
 #pragma unroll
     for (int l = 0; l < kQuadLeaves; ++l) {
-      const uint64_t* e = table + 2 * l;
+      // leaf l's address and chunk count, from lane 4l that hashes it (the same in every lane)
+      const uint64_t la = lane64(addr, 4 * l);
+      const uint32_t n = __builtin_amdgcn_readlane(chunks, 4 * l);
       const uint64_t c = (uint64_t)s * 64 + ((t ^ l) * 2) + h;  // chunk of leaf l for this lane
-      if (c < e[1]) load_lds16(reinterpret_cast<const uint8_t*>(e[0]) + c * 16, tile + s * kQuadWaveLds + l * kQuadStage);
+      if (c < n) load_lds16(reinterpret_cast<const uint8_t*>(la) + c * 16, tile + s * kQuadWaveLds + l * kQuadStage);
     }
   }
   __builtin_amdgcn_s_waitcnt(kWaitLoads);
@@ -504,15 +513,15 @@ __device__ uint64_t hash_quad_gathered_direct(const Leaf& lf, uint8_t* tile, uin
 
 // hash_slot_quad with a 64 KiB tile: the direct loads when every leaf of the wave is
 // 16-byte aligned, else the staged path.
-__device__ __forceinline__ uint64_t hash_slot_quad_direct(const Leaf& lf, uint8_t* tile, uint64_t* table, int lane) {
+__device__ __forceinline__ uint64_t hash_slot_quad_direct(const Leaf& lf, uint8_t* tile, int lane) {
   const uint64_t addr = reinterpret_cast<uint64_t>(lf.addr);
-  if (!__all((addr & 15) == 0 || lf.len == 0)) return hash_slot_quad(lf, tile, table, lane);
+  if (!__all((addr & 15) == 0 || lf.len == 0)) return hash_slot_quad(lf, tile, lane);
   const uint64_t a0 = shfl64(addr, 0);
   const bool contiguous = lf.len == 4096 && addr == a0 + (uint64_t)(lane >> 2) * 4096;
   if (__all(contiguous))
     return hash_quad_contiguous_direct(reinterpret_cast<const uint8_t*>(uniform64(a0)), tile, lane);
   if (!__any(lf.len != 0)) return 0;
-  return hash_quad_gathered_direct(lf, tile, table, lane);
+  return hash_quad_gathered_direct(lf, tile, lane);
 }
 
 // The four-lanes-per-leaf pass of one workgroup of W waves over the W * kQuadLeaves slots
@@ -532,8 +541,7 @@ struct NoProbe {
 };
 
 template <int W, bool kLen, bool kDirect = false, typename Probe = NoProbe>
-__device__ __forceinline__ void quad_pass(const FpArgs& a, uint64_t group, uint8_t* lds,
-                                          uint64_t (*tables)[2 * kQuadLeaves], uint32_t* blen,
+__device__ __forceinline__ void quad_pass(const FpArgs& a, uint64_t group, uint8_t* lds, uint32_t* blen,
                                           const Probe& probe = Probe()) {
   static_assert(!kDirect || W == 1, "the direct loads hold one wave's stages");
   constexpr uint64_t kQuadGroup = (uint64_t)W * kQuadLeaves;
@@ -546,8 +554,7 @@ __device__ __forceinline__ void quad_pass(const FpArgs& a, uint64_t group, uint8
   const uint64_t g = slot >> L2;
   const uint32_t k = (uint32_t)(slot & (lpb - 1));
   const Leaf lf = locate_wave(a, wave_slot0 >> L2, g, k, lane);
-  const uint64_t d = kDirect ? hash_slot_quad_direct(lf, lds, tables[0], lane)
-                             : hash_slot_quad(lf, lds + wave * kQuadWaveLds, tables[wave], lane);
+  const uint64_t d = kDirect ? hash_slot_quad_direct(lf, lds, lane) : hash_slot_quad(lf, lds + wave * kQuadWaveLds, lane);
   const bool head = (lane & 3) == 0;
   if (a.leaf_out && head && g < a.n_blocks) a.leaf_out[slot] = lf.len ? d : 0;
   if (kLen && head && g < a.n_blocks && lf.len && k + 1 == lf.blk_leaves) blen[g] = (k << 12) + lf.len;
