@@ -142,11 +142,12 @@ def build_decoder7b(g, torch, threads):
     global FIRST_LAUNCH_MS
     FIRST_LAUNCH_MS = round(e0.elapsed_time(e1), 4)
     table.insert(base_digests, torch.arange(base_batch.n_blocks, dtype=torch.int64, device="cuda"))
+    _, base_leaves = g.fp_chunks(base_batch, with_leaves=True)  # recorded leaf digests (identify leg)
     torch.cuda.synchronize()
     del d_side, base_batch, side
     global RECORDED
     RECORDED = (base_digests, np.array([0] + [1 + 9 * l for l in range(33)] + [len(lens)], np.uint64),
-                [dec.base(i) for i in dec.perturbed], list(dec.perturbed))
+                [dec.base(i) for i in dec.perturbed], list(dec.perturbed), base_leaves)
     first = batch.host_first
     expect_miss = int(sum(int(first[i + 1] - first[i]) for i in dec.perturbed))
     payloads = [arena[int(o):int(o) + int(n)] for o, n in zip(offs, lens)]
@@ -221,13 +222,13 @@ def build_large_bf16(g, torch, threads):
     return batch, table, payloads, batch.n_blocks - chosen.size, desc, d_arena
 
 
-RECORDED = None  # (recorded block digests, allocation boundaries, base tensors, their indices)
+RECORDED = None  # (recorded block digests, allocation boundaries, base tensors, their indices, recorded leaf digests)
 
 
 def identify_path(args, g, torch, threads, batch, payloads, keep):
     """Free-time weight identification over the 7B decoder: the digests recorded when the
     base weights were written vs. the device bytes now (3 layers updated in place)."""
-    recorded, region_first, base_tensors, base_idx = RECORDED
+    recorded, region_first, base_tensors, base_idx, recorded_leaves = RECORDED
     n_regions = region_first.size - 1
     rf = torch.from_numpy(region_first.view(np.int64)).to("cuda")
     ws = g.workspace(batch.n_blocks + batch.n_seg)
@@ -251,6 +252,21 @@ def identify_path(args, g, torch, threads, batch, payloads, keep):
     ms = start.elapsed_time(end) / K
     per_call = [evs[k].elapsed_time(evs[k + 1]) for k in range(K)]
     payload_bytes = int(batch.host_len.sum())
+    # the same check located to the leaf (gleam_identify_leaves), timed the same way
+    lws = g.workspace(batch.n_blocks * batch.leaves_per_block + batch.n_seg)
+    for _ in range(args.warmup):
+        g.identify_leaves(batch, recorded_leaves, rf, ws=lws)
+    torch.cuda.synchronize()
+    queue_ahead(g, torch, keep)
+    lstart, lend = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    lstart.record()
+    for _ in range(K):
+        lm, lf, lw = g.identify_leaves(batch, recorded_leaves, rf, ws=lws)
+    lend.record()
+    torch.cuda.synchronize()
+    if int(lw.sum().item()) != n_regions - 3:
+        raise SystemExit("leaf identification truth violated")
+    leaves_ms = lstart.elapsed_time(lend) / K
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -274,6 +290,8 @@ def identify_path(args, g, torch, threads, batch, payloads, keep):
                       "call_ms": {"median": round(float(np.median(per_call)), 4), "min": round(min(per_call), 4),
                                   "max": round(max(per_call), 4)},
                       "gbs_at_median": round(payload_bytes / (float(np.median(per_call)) * 1e-3) / 1e9, 2),
+                      "identify_leaves": {"ms_per_call": round(leaves_ms, 4),
+                                          "gbs": round(payload_bytes / (leaves_ms * 1e-3) / 1e9, 2)},
                       "clock_settle": None if settle is None else {"ms": settle[0], "read_launches": settle[1]}},
            "cpu_baseline": cpu}
     print(json.dumps(out), flush=True)
@@ -393,6 +411,53 @@ def md5_path(args, g, torch, threads, batch, payloads, desc):
            "config": {"workload": desc, "payloads": batch.n_seg, "bytes_read": read,
                       "payload_bytes": int(batch.host_len.sum()),
                       "exposure": prefix_exposure(g, torch, batch, payloads)},
+           "cpu_baseline": cpu}
+    print(json.dumps(out), flush=True)
+
+
+def first_writes_path(args, g, torch):
+    """The first-write rule of weight identification (Sec. 4.1.1: where an address range
+    is written several times only the first host-to-device write counts) over seeded
+    write logs of 4,096 allocations: recorded writes per second. Every piece of the GPU
+    result is checked against the oracle's, which is also the CPU baseline."""
+    import workloads as W
+    logs = W.WriteLogs()
+    n, n_alloc = int(logs.addr.size), logs.n_alloc
+    d_addr = torch.from_numpy(logs.addr.view(np.int64)).to("cuda")
+    d_len = torch.from_numpy(logs.length.view(np.int64)).to("cuda")
+    d_rf = torch.from_numpy(logs.region_first.view(np.int64)).to("cuda")
+    for _ in range(max(args.warmup, 1)):
+        out = g.first_writes(d_addr, d_len, d_rf)
+    torch.cuda.synchronize()
+    K = args.steps
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(K):
+        out = g.first_writes(d_addr, d_len, d_rf)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / K
+    import oracle
+    t0 = time.perf_counter()
+    want = oracle.first_write_pieces(logs.addr, logs.length, logs.region_first, max_writes=2048)
+    dt = time.perf_counter() - t0
+    pw, po, pl, first, status = out
+    first = g.as_u64(first)
+    p = int(first[-1])
+    got = (g.as_u64(pw)[:p], g.as_u64(po)[:p], g.as_u64(pl)[:p], first, status.cpu().numpy())
+    if not all(np.array_equal(a, b) for a, b in zip(got, want)):
+        raise SystemExit("first-write pieces differ from the oracle's")
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = {"value": round(n / dt / 1e6, 3), "unit": "M writes/s", "cores": 1, "kind": "oracle",
+               "sample": f"the whole log ({n} writes), one run {dt:.3f} s, {cpu_model()}"}
+    out = {"metric": "M recorded writes/s through the first-write rule (4,096 allocations, 1-64 writes each), 1 MI355X",
+           "value": round(n / (ms * 1e-3) / 1e6, 2), "unit": "M writes/s", "n_gpus": 1, "steps": K,
+           "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+           "config": {"workload": "4,096 allocations of 4 KiB-16 MiB, 1-64 recorded writes each (sub-ranges, "
+                                  "whole allocations, repeats)", "allocations": n_alloc, "writes": n, "pieces": p,
+                      "check": "every piece equals the oracle's"},
            "cpu_baseline": cpu}
     print(json.dumps(out), flush=True)
 
@@ -920,9 +985,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-gb", type=float, default=20.0)
     ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--path", default="detect", choices=["detect", "identify", "md5prefix", "lifecycle", "transfer", "remap"],
+    ap.add_argument("--path", default="detect", choices=["detect", "identify", "md5prefix", "lifecycle", "transfer", "remap",
+                                                          "first_writes"],
                     help="detect: fingerprint+lookup+compact (default); identify: free-time weight "
-                         "identification; md5prefix: the paper's MD5-of-first-1024-bits identifier")
+                         "identification (block and leaf level); md5prefix: the paper's MD5-of-first-1024-bits "
+                         "identifier and its exposure; lifecycle: evict/export/erase; transfer: send plan, "
+                         "packing and restore; remap: the address-remap map; first_writes: the first-write rule")
     ap.add_argument("--no-settle", action="store_true",
                     help="skip the untimed streaming reads that bring the engine clock to its steady "
                          "state before the warm-up")
@@ -967,6 +1035,9 @@ def main():
     PRELOAD_MS = round((time.perf_counter() - t0) * 1e3, 3)
 
     threads = host_threads()
+    if args.path == "first_writes":
+        first_writes_path(args, g, torch)
+        return
     if args.path == "lifecycle":
         lifecycle_path(args, g, torch)
         return

@@ -131,3 +131,27 @@ def test_large_set_truth_reduced():
     expect[chosen] = oracle.HIT_CACHE
     assert np.array_equal(res["status"], expect)
     assert np.array_equal(res["ref"][chosen], chosen.astype(np.uint64))
+
+
+def test_write_logs_recipe():
+    """The first-write logs: deterministic, grouped by allocation, every write inside its
+    allocation, and all three kinds of write present (sub-ranges, whole allocations,
+    repeats of an earlier write of the same allocation)."""
+    a = W.WriteLogs(n_alloc=300)
+    b = W.WriteLogs(n_alloc=300)
+    assert np.array_equal(a.addr, b.addr) and np.array_equal(a.length, b.length)
+    rf = a.region_first.astype(np.int64)
+    assert rf[0] == 0 and rf[-1] == a.addr.size and np.all(np.diff(rf) >= 1) and np.all(np.diff(rf) <= 64)
+    whole = repeats = 0
+    for r in range(300):
+        base = (r + 1) << 36
+        ad = a.addr[rf[r]:rf[r + 1]].astype(np.int64)
+        ln = a.length[rf[r]:rf[r + 1]].astype(np.int64)
+        size = int((ad + ln).max() - base)
+        assert np.all(ad >= base) and np.all(ad + ln <= base + (16 << 20))
+        seen = set()
+        for x, n in zip(ad.tolist(), ln.tolist()):
+            whole += x == base and n == size
+            repeats += (x, n) in seen
+            seen.add((x, n))
+    assert whole > 0 and repeats > 0

@@ -378,3 +378,42 @@ class RemapTasks:
         task = g.integers(0, self.n_tasks, n).astype(np.uint64)
         anywhere = (task << np.uint64(TASK_SPACE_BITS)) + g.integers(0, 1 << TASK_SPACE_BITS, n).astype(np.uint64)
         return np.where(inside, start[pick] + off, anywhere).astype(np.uint64)
+
+
+# --------------------------------------------------------------------------- #
+# Recorded host-to-device write logs of allocations (workload 7)
+# --------------------------------------------------------------------------- #
+class WriteLogs:
+    """`n_alloc` allocations, allocation r at (r + 1) << 36 with a size drawn log-uniform in
+    [4 KiB, 16 MiB], each receiving 1-64 recorded writes in time order: half of them a
+    uniformly drawn sub-range of the allocation, three in ten the whole allocation, two in
+    ten a repeat of an earlier write of the same allocation (the first write of an
+    allocation is never a repeat). Weight-like allocations (one write) and input-like ones
+    (the same range written again and again) both occur."""
+
+    def __init__(self, n_alloc: int = 4096, workload: int = 7, max_writes: int = 64):
+        g = rng(workload, PURPOSE_SELECT, 0)
+        sizes = np.floor(np.exp(g.uniform(math.log(4 * KiB), math.log(16 * MiB), n_alloc))).astype(np.int64)
+        counts = g.integers(1, max_writes + 1, n_alloc)
+        addr, length = [], []
+        first = [0]
+        for r in range(n_alloc):
+            base, size = (r + 1) << 36, int(sizes[r])
+            mine = []
+            for j in range(int(counts[r])):
+                u = g.random()
+                if u < 0.2 and mine:
+                    a, n = mine[int(g.integers(0, len(mine)))]
+                elif u < 0.5:
+                    a, n = base, size
+                else:
+                    lo, hi = sorted(int(x) for x in g.integers(0, size + 1, 2))
+                    a, n = base + lo, hi - lo
+                mine.append((a, n))
+            addr.extend(a for a, _ in mine)
+            length.extend(n for _, n in mine)
+            first.append(len(addr))
+        self.addr = np.array(addr, dtype=np.uint64)
+        self.length = np.array(length, dtype=np.uint64)
+        self.region_first = np.array(first, dtype=np.uint64)
+        self.n_alloc = n_alloc
