@@ -655,10 +655,28 @@ def identify_leaves(batch: Batch, recorded_leaves: torch.Tensor, region_first, w
     return leaf_match[:n_slots], first_diff[:batch.n_seg], region_weight[:n_regions]
 
 
-def first_writes(addr, length, region_first, stream=None, device="cuda"):
+def first_writes_outputs(n_writes: int, n_regions: int, device="cuda"):
+    """Output tensors for first_writes over n_writes writes of n_regions allocations:
+    (piece_write, piece_offset, piece_len, region_piece_first, region_status)."""
+    cap = max(2 * n_writes, 1)
+    return (torch.empty(cap, dtype=torch.int64, device=device), torch.empty(cap, dtype=torch.int64, device=device),
+            torch.empty(cap, dtype=torch.int64, device=device),
+            torch.empty(n_regions + 1, dtype=torch.int64, device=device),
+            torch.empty(max(n_regions, 1), dtype=torch.uint8, device=device))
+
+
+def first_writes_workspace(n_writes: int, n_regions: int, device="cuda") -> torch.Tensor:
+    nb = int(lib.gleam_first_writes_ws_bytes(n_writes, n_regions))
+    if nb == 0:
+        raise GleamError(E_UNSUPPORTED, "too many writes or allocations")
+    return torch.empty(nb, dtype=torch.uint8, device=device)
+
+
+def first_writes(addr, length, region_first, stream=None, device="cuda", out=None, ws=None):
     """The first-write rule over recorded writes (time order, grouped by allocation):
     (piece_write, piece_offset, piece_len, region_piece_first, region_status) device
-    tensors; the first region_piece_first[-1] pieces are valid."""
+    tensors; the first region_piece_first[-1] pieces are valid. `out` (from
+    first_writes_outputs) and `ws` (from first_writes_workspace) are reused when given."""
     with _on_stream(stream, torch.device(device)) as hs:
         d = [t if isinstance(t, torch.Tensor) else _u64_device(np.asarray(t), device)
              for t in (addr, length, region_first)]
@@ -667,18 +685,19 @@ def first_writes(addr, length, region_first, stream=None, device="cuda"):
             raise ValueError("addr and length differ in length")
         for t, name in zip(d, ("addr", "length", "region_first")):
             _dev(t, name, _U64)
+        if out is None:
+            out = first_writes_outputs(n, n_regions, device)
+        pw, po, pl, first, status = out
         cap = max(2 * n, 1)
-        pw = torch.empty(cap, dtype=torch.int64, device=device)
-        po = torch.empty(cap, dtype=torch.int64, device=device)
-        pl = torch.empty(cap, dtype=torch.int64, device=device)
-        first = torch.empty(n_regions + 1, dtype=torch.int64, device=device)
-        status = torch.empty(max(n_regions, 1), dtype=torch.uint8, device=device)
-        nb = int(lib.gleam_first_writes_ws_bytes(n, n_regions))
-        if nb == 0:
-            raise GleamError(E_UNSUPPORTED, "too many writes or allocations")
-        ws = torch.empty(nb, dtype=torch.uint8, device=device)
+        for t, name in ((pw, "piece_write"), (po, "piece_offset"), (pl, "piece_len")):
+            _dev(t, name, _U64, cap)
+        _dev(first, "region_piece_first", _U64, n_regions + 1)
+        _dev(status, "region_status", _U8, n_regions)
+        if ws is None:
+            ws = first_writes_workspace(n, n_regions, device)
+        _dev(ws, "ws", _U8)
         _check(lib.gleam_first_writes(_ptr(d[0]), _ptr(d[1]), n, _ptr(d[2]), n_regions, _ptr(pw), _ptr(po), _ptr(pl),
-                                      _ptr(first), _ptr(status), _ptr(ws), nb, hs))
+                                      _ptr(first), _ptr(status), _ptr(ws), ws.numel(), hs))
     return pw, po, pl, first, status[:n_regions]
 
 

@@ -6,7 +6,11 @@
 // and the same pieces of the allocation at free time, compares every written byte with
 // its first writer's byte (gleam_identify_weights over the pieces).
 //
-// One 1024-thread workgroup per allocation, all in LDS (up to kMaxWrites writes):
+// A call's allocations are cut into at most one chunk per CU, one 1024-thread workgroup
+// each. Its waves take the chunk's allocations of up to kSmallWrites writes (most of
+// them) one at a time, lane j holding write j, with the sorts and scans in registers
+// (cross-lane shuffles and ballots) and 3 KiB of LDS per wave; the whole workgroup then
+// takes the larger ones (up to kMaxWrites) in turn, in 136 KiB of LDS. Per allocation:
 //   1. the 2n write endpoints are sorted (bitonic) and made unique: boundaries B;
 //      consecutive boundaries delimit the elementary intervals;
 //   2. the first writer of each elementary interval is the least write index covering
@@ -15,8 +19,9 @@
 //      the least value on its path to the root (O(n log n) work, whatever the overlap);
 //   3. maximal runs of intervals with one first writer are the pieces; they are sorted
 //      by (write, address) with a second bitonic sort and written to the workspace.
-// A single-workgroup scan then gives each allocation's first piece, and a last pass
-// moves the pieces into the caller's dense arrays.
+// A second launch gives each allocation its first piece (the chunk sums before its chunk,
+// then a scan over the chunk) and moves the pieces into the caller's dense arrays, one
+// wave per allocation.
 
 #include "gleam_device.h"
 #include "gleam_internal.h"
@@ -25,9 +30,12 @@ namespace gleam {
 namespace {
 
 constexpr int kFwThreads = 1024;
+constexpr int kFwWaves = kFwThreads / 64;
 constexpr uint32_t kMaxWrites = 2048;
-constexpr uint32_t kMaxEnds = 2 * kMaxWrites;  // endpoints, boundaries, intervals
+constexpr uint32_t kSmallWrites = 64;     // the most one wave takes
+constexpr uint64_t kMaxChunks = 1024;     // workgroups of a call, at most
 constexpr uint32_t kNone = 0xFFFFFFFFu;
+constexpr uint64_t kDeferred = ~0ull;     // counts[r]: allocation r is left to the whole workgroup
 
 struct FwArgs {
   const uint64_t* addr;
@@ -48,12 +56,12 @@ __device__ __forceinline__ uint32_t p2_at_least(uint32_t x) {
   return p;
 }
 
-// Ascending bitonic sort of a[0, n), n a power of two, by the whole workgroup.
-template <typename T>
+// Ascending bitonic sort of a[0, n), n a power of two, by the whole workgroup of kT threads.
+template <int kT, typename T>
 __device__ void bitonic_sort(T* a, uint32_t n) {
   for (uint32_t k = 2; k <= n; k <<= 1) {
     for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-      for (uint32_t i = threadIdx.x; i < n; i += kFwThreads) {
+      for (uint32_t i = threadIdx.x; i < n; i += kT) {
         const uint32_t o = i ^ j;
         if (o > i) {
           const T x = a[i], y = a[o];
@@ -69,7 +77,9 @@ __device__ void bitonic_sort(T* a, uint32_t n) {
   }
 }
 
-// Exclusive scan of one value per thread over the workgroup; *total gets the sum.
+// Exclusive scan of one value per thread over the workgroup of kT threads; *total gets
+// the sum.
+template <int kT>
 __device__ uint32_t fw_scan(uint32_t x, uint32_t* wave_sums, uint32_t* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   uint32_t incl = x;
@@ -81,7 +91,7 @@ __device__ uint32_t fw_scan(uint32_t x, uint32_t* wave_sums, uint32_t* total) {
   if (lane == 63) wave_sums[wave] = incl;
   __syncthreads();
   uint32_t before = 0, sum = 0;
-  for (int w = 0; w < kFwThreads / 64; ++w) {
+  for (int w = 0; w < kT / 64; ++w) {
     const uint32_t s = wave_sums[w];
     before += w < wave ? s : 0u;
     sum += s;
@@ -102,48 +112,54 @@ __device__ __forceinline__ uint32_t lower_bound(const uint64_t* b, uint32_t m, u
   return lo;
 }
 
-__global__ __launch_bounds__(kFwThreads) void first_write_region_kernel(FwArgs a) {
-  __shared__ uint64_t ends[kMaxEnds];    // sorted endpoints
-  __shared__ uint64_t bounds[kMaxEnds];  // unique boundaries
-  __shared__ uint32_t tree[2 * kMaxEnds];
-  __shared__ uint32_t owner[kMaxEnds];   // first writer of each elementary interval
-  __shared__ uint32_t keys[kMaxEnds];    // pieces: (write << 12) | change-point rank
-  __shared__ uint16_t cps[kMaxEnds + 1]; // change points (interval index where a run starts)
-  __shared__ uint32_t wave_sums[kFwThreads / 64];
-  __shared__ uint32_t flag;
+// LDS of one allocation's pass for up to kMax writes.
+template <uint32_t kMax, int kT>
+struct FwLds {
+  static constexpr uint32_t kEnds = 2 * kMax;  // endpoints, boundaries, intervals
+  uint64_t ends[kEnds];    // sorted endpoints
+  uint64_t bounds[kEnds];  // unique boundaries
+  uint32_t tree[2 * kEnds];
+  uint32_t owner[kEnds];   // first writer of each elementary interval
+  uint32_t keys[kEnds];    // pieces: (write << 12) | change-point rank
+  uint16_t cps[kEnds + 1]; // change points (interval index where a run starts)
+  uint32_t wave_sums[kT / 64];
+  uint32_t flag;
+};
+
+// The pieces of allocation r, whose n = w1 - w0 writes (at most kMax) are valid, by the
+// whole workgroup of kT threads (4 kT >= 2 kMax). Returns their count.
+template <uint32_t kMax, int kT>
+__device__ uint32_t fw_region(const FwArgs& a, uint64_t r, uint64_t w0, uint64_t w1, FwLds<kMax, kT>& L) {
+  static_assert(4 * kT >= 2 * kMax, "four endpoints or intervals per thread");
+  uint64_t* ends = L.ends;
+  uint64_t* bounds = L.bounds;
+  uint32_t* tree = L.tree;
+  uint32_t* owner = L.owner;
+  uint32_t* keys = L.keys;
+  uint16_t* cps = L.cps;
+  uint32_t* wave_sums = L.wave_sums;
+  uint32_t& flag = L.flag;
   const uint32_t tid = threadIdx.x;
-  const uint64_t r = blockIdx.x;
-  const uint64_t w0 = a.region_first[r], w1 = a.region_first[r + 1];
-  uint8_t st = GLEAM_FW_OK;
-  if (w1 < w0 || w1 > a.n_writes) st = GLEAM_FW_INVALID;
-  else if (w1 - w0 > kMaxWrites) st = GLEAM_FW_TOO_MANY;
-  if (st != GLEAM_FW_OK) {  // uniform across the workgroup
-    if (tid == 0) {
-      a.counts[r] = 0;
-      if (a.status) a.status[r] = st;
-    }
-    return;
-  }
   const uint32_t n = (uint32_t)(w1 - w0);
   const uint32_t P = p2_at_least(n ? 2 * n : 2);
   if (tid == 0) flag = 0;
   __syncthreads();
-  for (uint32_t j = tid; j < n; j += kFwThreads) {
+  for (uint32_t j = tid; j < n; j += kT) {
     const uint64_t s = a.addr[w0 + j], l = a.len[w0 + j];
     if (l > ~0ull - s) atomicOr(&flag, 1u);  // past the top of the address space
     ends[2 * j] = s;
     ends[2 * j + 1] = s + l;
   }
-  for (uint32_t i = 2 * n + tid; i < P; i += kFwThreads) ends[i] = ~0ull;
+  for (uint32_t i = 2 * n + tid; i < P; i += kT) ends[i] = ~0ull;
   __syncthreads();
   if (flag) {
     if (tid == 0) {
       a.counts[r] = 0;
       if (a.status) a.status[r] = GLEAM_FW_INVALID;
     }
-    return;
+    return 0;
   }
-  bitonic_sort(ends, P);
+  bitonic_sort<kT>(ends, P);
 
   // unique boundaries: thread t takes ends[4t, 4t + 4)
   uint32_t total;
@@ -155,7 +171,7 @@ __global__ __launch_bounds__(kFwThreads) void first_write_region_kernel(FwArgs a
       f[e] = i < P && (i == 0 || ends[i] != ends[i - 1]);
       c += f[e];
     }
-    uint32_t at = fw_scan(c, wave_sums, &total);
+    uint32_t at = fw_scan<kT>(c, wave_sums, &total);
 #pragma unroll
     for (int e = 0; e < 4; ++e)
       if (f[e]) bounds[at++] = ends[4 * tid + e];
@@ -163,11 +179,11 @@ __global__ __launch_bounds__(kFwThreads) void first_write_region_kernel(FwArgs a
   const uint32_t M = total;        // boundaries
   const uint32_t E = M - 1;        // elementary intervals [bounds[i], bounds[i + 1])
   const uint32_t T2 = p2_at_least(E ? E : 1);
-  for (uint32_t i = tid; i < 2 * T2; i += kFwThreads) tree[i] = kNone;
+  for (uint32_t i = tid; i < 2 * T2; i += kT) tree[i] = kNone;
   __syncthreads();
 
   // every write min-updates the canonical nodes of its interval range
-  for (uint32_t j = tid; j < n; j += kFwThreads) {
+  for (uint32_t j = tid; j < n; j += kT) {
     const uint64_t s = a.addr[w0 + j], l = a.len[w0 + j];
     if (l == 0) continue;
     uint32_t lo = lower_bound(bounds, M, s) + T2, hi = lower_bound(bounds, M, s + l) + T2;
@@ -179,7 +195,7 @@ __global__ __launch_bounds__(kFwThreads) void first_write_region_kernel(FwArgs a
     }
   }
   __syncthreads();
-  for (uint32_t i = tid; i < E; i += kFwThreads) {
+  for (uint32_t i = tid; i < E; i += kT) {
     uint32_t m = kNone;
     for (uint32_t node = i + T2; node >= 1; node >>= 1) m = min(m, tree[node]);
     owner[i] = m;
@@ -195,7 +211,7 @@ __global__ __launch_bounds__(kFwThreads) void first_write_region_kernel(FwArgs a
       f[e] = i < E && (i == 0 || owner[i] != owner[i - 1]);
       c += f[e];
     }
-    uint32_t at = fw_scan(c, wave_sums, &total);
+    uint32_t at = fw_scan<kT>(c, wave_sums, &total);
 #pragma unroll
     for (int e = 0; e < 4; ++e)
       if (f[e]) cps[at++] = (uint16_t)(4 * tid + e);
@@ -204,19 +220,19 @@ __global__ __launch_bounds__(kFwThreads) void first_write_region_kernel(FwArgs a
   if (tid == 0) cps[K] = (uint16_t)E;
   __syncthreads();  // every change point written
   const uint32_t KP = p2_at_least(K ? K : 1);
-  for (uint32_t k = tid; k < KP; k += kFwThreads) {
+  for (uint32_t k = tid; k < KP; k += kT) {
     const uint32_t o = k < K ? owner[cps[k]] : kNone;
     keys[k] = o == kNone ? kNone : (o << 12) | k;
   }
   __syncthreads();
-  bitonic_sort(keys, KP);
+  bitonic_sort<kT>(keys, KP);
 
   // keys[0, pieces) are the owned runs, by (write, address)
   uint64_t* pw = a.pad_write + 2 * w0;
   uint64_t* po = a.pad_offset + 2 * w0;
   uint64_t* pl = a.pad_len + 2 * w0;
   uint32_t mine = 0;
-  for (uint32_t p = tid; p < KP; p += kFwThreads) {
+  for (uint32_t p = tid; p < KP; p += kT) {
     const uint32_t key = keys[p];
     if (key == kNone) continue;
     ++mine;
@@ -226,23 +242,280 @@ __global__ __launch_bounds__(kFwThreads) void first_write_region_kernel(FwArgs a
     po[p] = lo - a.addr[w0 + j];
     pl[p] = hi - lo;
   }
-  fw_scan(mine, wave_sums, &total);
+  fw_scan<kT>(mine, wave_sums, &total);
   if (tid == 0) {
     a.counts[r] = total;
     if (a.status) a.status[r] = GLEAM_FW_OK;
   }
+  return total;
 }
 
-// region_piece_first = exclusive prefix of the counts (and the total at [n_regions]).
-__global__ __launch_bounds__(kFwThreads) void first_write_scan_kernel(const uint64_t* counts, uint64_t n_regions,
-                                                                      uint64_t* first) {
-  __shared__ uint64_t wave_sums[kFwThreads / 64];
+// Ascending bitonic sort, in registers, of the wave's elements 2 lane + h < P (v0 holds
+// h = 0, v1 h = 1; P a power of two <= 128). Lanes at or past P / 2 exchange only among
+// themselves.
+template <typename T>
+__device__ __forceinline__ T wave_partner(T v, int m);
+template <>
+__device__ __forceinline__ uint64_t wave_partner<uint64_t>(uint64_t v, int m) { return shfl_xor64(v, m); }
+template <>
+__device__ __forceinline__ uint32_t wave_partner<uint32_t>(uint32_t v, int m) {
+  return (uint32_t)__shfl_xor((int)v, m, 64);
+}
+
+template <typename T>
+__device__ void wave_sort_pairs(T& v0, T& v1, uint32_t P) {
+  const uint32_t lane = threadIdx.x & 63;
+  for (uint32_t k = 2; k <= P; k <<= 1) {
+    const bool up = ((2 * lane) & k) == 0;  // the block of k elements this lane's pair sits in
+    for (uint32_t j = k >> 1; j >= 2; j >>= 1) {
+      const int m = (int)(j >> 1);  // element 2 lane + h pairs with 2 (lane ^ m) + h
+      const T p0 = wave_partner(v0, m), p1 = wave_partner(v1, m);
+      const bool keep_min = ((lane & m) == 0) == up;  // the lower index keeps the min going up
+      v0 = keep_min ? (p0 < v0 ? p0 : v0) : (p0 < v0 ? v0 : p0);
+      v1 = keep_min ? (p1 < v1 ? p1 : v1) : (p1 < v1 ? v1 : p1);
+    }
+    const T lo = v1 < v0 ? v1 : v0, hi = v1 < v0 ? v0 : v1;  // j = 1: the lane's own pair
+    v0 = up ? lo : hi;
+    v1 = up ? hi : lo;
+  }
+}
+
+// Number of elements of the ascending b[0, m) below x, and below y (m >= 1), the two
+// searches interleaved.
+__device__ __forceinline__ void count_below2(const uint64_t* b, uint32_t m, uint64_t x, uint64_t y, uint32_t& cx,
+                                             uint32_t& cy) {
+  uint32_t i = 0, j = 0;
+  for (uint32_t step = 1u << (31 - __clz(m)); step; step >>= 1) {
+    if (i + step <= m && b[i + step - 1] < x) i += step;
+    if (j + step <= m && b[j + step - 1] < y) j += step;
+  }
+  cx = i;
+  cy = j;
+}
+
+// LDS of the one-wave pass.
+struct FwWaveLds {
+  uint64_t bounds[2 * kSmallWrites];  // unique boundaries
+  uint32_t tree[4 * kSmallWrites];
+  uint32_t keys[2 * kSmallWrites];    // runs: (write << 8) | run rank, kNone when unowned
+  uint32_t cps[2 * kSmallWrites + 1]; // the interval each run starts at; cps[K] = E
+};
+
+// The pieces of allocation r, whose n <= kSmallWrites writes are in range, by one wave:
+// the steps of fw_region with lane j holding write j, each lane two endpoints, two
+// intervals and two runs (elements 2 lane and 2 lane + 1), so that sorts run on
+// shuffles and scans on ballots. Returns the piece count.
+__device__ uint32_t fw_wave(const FwArgs& a, uint64_t r, uint64_t w0, uint32_t n, FwWaveLds& L) {
+  const uint32_t lane = threadIdx.x & 63;
+  const uint64_t below = (1ull << lane) - 1;  // lanes under this one
+  uint64_t s = 0, l = 0;
+  if (lane < n) {
+    s = a.addr[w0 + lane];
+    l = a.len[w0 + lane];
+  }
+  if (__ballot(lane < n && l > ~0ull - s)) {  // past the top of the address space
+    if (lane == 0) {
+      a.counts[r] = 0;
+      if (a.status) a.status[r] = GLEAM_FW_INVALID;
+    }
+    return 0;
+  }
+  const uint32_t P = p2_at_least(n ? 2 * n : 2);
+  uint64_t v0 = lane < n ? s : ~0ull, v1 = lane < n ? s + l : ~0ull;
+  wave_sort_pairs(v0, v1, P);
+
+  // unique boundaries
+  const uint64_t before = shfl64(v1, lane ? (int)lane - 1 : 0);
+  const bool f0 = 2 * lane < P && (lane == 0 || v0 != before);
+  const bool f1 = 2 * lane + 1 < P && v1 != v0;
+  const uint64_t b0 = __ballot(f0), b1 = __ballot(f1);
+  const uint32_t at = (uint32_t)(__popcll(b0 & below) + __popcll(b1 & below));
+  if (f0) L.bounds[at] = v0;
+  if (f1) L.bounds[at + f0] = v1;
+  const uint32_t M = (uint32_t)(__popcll(b0) + __popcll(b1));
+  const uint32_t E = M - 1;
+  const uint32_t T2 = p2_at_least(E ? E : 1);
+  for (uint32_t i = lane; i < 2 * T2; i += 64) L.tree[i] = kNone;
+  wave_lds_sync();
+
+  // every write min-updates the canonical nodes of its interval range
+  if (lane < n && l != 0) {
+    uint32_t lo, hi;
+    count_below2(L.bounds, M, s, s + l, lo, hi);
+    lo += T2;
+    hi += T2;
+    while (lo < hi) {
+      if (lo & 1) atomicMin(&L.tree[lo++], lane);
+      if (hi & 1) atomicMin(&L.tree[--hi], lane);
+      lo >>= 1;
+      hi >>= 1;
+    }
+  }
+  wave_lds_sync();
+  uint32_t o0 = kNone, o1 = kNone;  // first writers of intervals 2 lane and 2 lane + 1
+  if (2 * lane < E) {
+    const bool two = 2 * lane + 1 < E;
+    for (uint32_t x = 2 * lane + T2, y = x + 1; x >= 1; x >>= 1, y >>= 1) {
+      o0 = min(o0, L.tree[x]);
+      if (two) o1 = min(o1, L.tree[y]);
+    }
+  }
+
+  // runs of one first writer
+  const uint32_t oprev = (uint32_t)__shfl((int)o1, lane ? (int)lane - 1 : 0, 64);
+  const bool c0 = 2 * lane < E && (lane == 0 || o0 != oprev);
+  const bool c1 = 2 * lane + 1 < E && o1 != o0;
+  const uint64_t q0 = __ballot(c0), q1 = __ballot(c1);
+  const uint32_t k0 = (uint32_t)(__popcll(q0 & below) + __popcll(q1 & below));
+  const uint32_t K = (uint32_t)(__popcll(q0) + __popcll(q1));
+  if (c0) {
+    L.cps[k0] = 2 * lane;
+    L.keys[k0] = o0 == kNone ? kNone : (o0 << 8) | k0;
+  }
+  if (c1) {
+    const uint32_t k = k0 + c0;
+    L.cps[k] = 2 * lane + 1;
+    L.keys[k] = o1 == kNone ? kNone : (o1 << 8) | k;
+  }
+  if (lane == 0) L.cps[K] = E;
+  wave_lds_sync();
+  uint32_t y0 = 2 * lane < K ? L.keys[2 * lane] : kNone, y1 = 2 * lane + 1 < K ? L.keys[2 * lane + 1] : kNone;
+  wave_sort_pairs(y0, y1, p2_at_least(K ? K : 1));
+
+  // the owned runs, by (write, address), are the first pieces elements
+  const uint32_t pieces = (uint32_t)(__popcll(__ballot(y0 != kNone)) + __popcll(__ballot(y1 != kNone)));
+  const uint64_t s0 = shfl64(s, y0 != kNone ? (int)(y0 >> 8) : 0);
+  const uint64_t s1 = shfl64(s, y1 != kNone ? (int)(y1 >> 8) : 0);
+  uint64_t* pw = a.pad_write + 2 * w0;
+  uint64_t* po = a.pad_offset + 2 * w0;
+  uint64_t* pl = a.pad_len + 2 * w0;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t y = h ? y1 : y0;
+    if (y == kNone) continue;
+    const uint32_t p = 2 * lane + h, k = y & 0xFFu;
+    const uint64_t lo = L.bounds[L.cps[k]], hi = L.bounds[L.cps[k + 1]];
+    pw[p] = w0 + (y >> 8);
+    po[p] = lo - (h ? s1 : s0);
+    pl[p] = hi - lo;
+  }
+  if (lane == 0) {
+    a.counts[r] = pieces;
+    if (a.status) a.status[r] = GLEAM_FW_OK;
+  }
+  return pieces;
+}
+
+// Allocation r's status when its write range is malformed or too long (else OK).
+__device__ __forceinline__ uint8_t fw_check(const FwArgs& a, uint64_t w0, uint64_t w1) {
+  if (w1 < w0 || w1 > a.n_writes) return GLEAM_FW_INVALID;
+  if (w1 - w0 > kMaxWrites) return GLEAM_FW_TOO_MANY;
+  return GLEAM_FW_OK;
+}
+
+// Allocation chunk b is [b chunk, min(n_regions, (b + 1) chunk)). Its workgroup's waves
+// take its allocations in turn, one each (those of more than kSmallWrites writes are
+// marked kDeferred); the whole workgroup then takes the marked ones one after another.
+// chunk_sum[b] gets the chunk's piece count.
+__global__ __launch_bounds__(kFwThreads) void first_write_kernel(FwArgs a, uint64_t chunk, uint64_t* chunk_sum) {
+  __shared__ union {
+    FwWaveLds wave[kFwWaves];
+    FwLds<kMaxWrites, kFwThreads> big;
+  } L;
+  __shared__ uint32_t marked[kFwThreads];
+  __shared__ uint32_t n_marked;
+  __shared__ uint64_t wave_pieces[kFwWaves];
+  const uint32_t wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const uint64_t r0 = (uint64_t)blockIdx.x * chunk;
+  const uint64_t r1 = r0 + chunk < a.n_regions ? r0 + chunk : a.n_regions;
+  uint64_t pieces = 0;  // this wave's
+  int deferred = 0;
+  for (uint64_t r = r0 + wave; r < r1; r += kFwWaves) {
+    const uint64_t w0 = a.region_first[r], w1 = a.region_first[r + 1];
+    const uint8_t st = fw_check(a, w0, w1);  // uniform across the wave
+    if (st == GLEAM_FW_OK && w1 - w0 > kSmallWrites) {
+      if (lane == 0) a.counts[r] = kDeferred;
+      deferred = 1;
+      continue;
+    }
+    if (st != GLEAM_FW_OK) {
+      if (lane == 0) {
+        a.counts[r] = 0;
+        if (a.status) a.status[r] = st;
+      }
+      continue;
+    }
+    wave_lds_sync();  // the previous allocation's LDS is no longer read
+    pieces += fw_wave(a, r, w0, (uint32_t)(w1 - w0), L.wave[wave]);
+  }
+  if (__syncthreads_or(deferred)) {
+    // rounds of kFwThreads allocations: each thread checks one, the marked ones are listed
+    for (uint64_t base = r0; base < r1; base += kFwThreads) {
+      if (threadIdx.x == 0) n_marked = 0;
+      __syncthreads();  // also: the previous round's list and LDS are no longer read
+      const uint64_t mine = base + threadIdx.x;
+      if (mine < r1 && a.counts[mine] == kDeferred) marked[atomicAdd(&n_marked, 1u)] = threadIdx.x;
+      __syncthreads();
+      const uint32_t m = n_marked;
+      for (uint32_t i = 0; i < m; ++i) {
+        const uint64_t r = base + marked[i];
+        __syncthreads();  // the previous allocation's LDS is no longer read
+        const uint32_t c = fw_region<kMaxWrites, kFwThreads>(a, r, a.region_first[r], a.region_first[r + 1], L.big);
+        if (wave == 0) pieces += c;  // counted once
+      }
+    }
+  }
+  if (lane == 0) wave_pieces[wave] = pieces;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t sum = 0;
+    for (int w = 0; w < kFwWaves; ++w) sum += wave_pieces[w];
+    chunk_sum[blockIdx.x] = sum;
+  }
+}
+
+// Sum over the workgroup, returned to every thread.
+__device__ uint64_t block_sum(uint64_t x, uint64_t* wave_sums) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint64_t carry = 0;
-  for (uint64_t base = 0; base < n_regions; base += kFwThreads) {
-    const uint64_t i = base + threadIdx.x;
-    const uint64_t x = i < n_regions ? counts[i] : 0;
-    uint64_t incl = x;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) x += shfl_xor64(x, d);
+  if (lane == 0) wave_sums[wave] = x;
+  __syncthreads();
+  uint64_t sum = 0;
+  for (int w = 0; w < kFwWaves; ++w) sum += wave_sums[w];
+  __syncthreads();
+  return sum;
+}
+
+// Chunk b (as in first_write_kernel): region_piece_first of its allocations (the pieces
+// of the chunks before it, then a scan of its counts in rounds of four per thread), and
+// their pieces moved from the workspace to the dense outputs, one wave per allocation and
+// one piece per lane (u64[2 n_writes] each: a well-formed region_first yields fewer
+// pieces; an ill-formed one, whose regions overlap, is cut at the end of the outputs).
+// The last workgroup writes the total at [n_regions].
+__global__ __launch_bounds__(kFwThreads) void first_write_move_kernel(FwArgs a, uint64_t chunk,
+                                                                      const uint64_t* chunk_sum, uint64_t* first,
+                                                                      uint64_t* out_write, uint64_t* out_offset,
+                                                                      uint64_t* out_len) {
+  constexpr uint32_t kRound = 4 * kFwThreads;
+  __shared__ uint64_t wave_sums[kFwWaves];
+  __shared__ uint64_t at[kRound];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t r0 = (uint64_t)blockIdx.x * chunk;
+  const uint64_t r1 = r0 + chunk < a.n_regions ? r0 + chunk : a.n_regions;
+  uint64_t x = 0;
+  for (uint32_t i = threadIdx.x; i < blockIdx.x; i += kFwThreads) x += chunk_sum[i];
+  uint64_t carry = block_sum(x, wave_sums);  // pieces of the chunks before this one
+  const uint64_t cap = 2 * a.n_writes;
+  for (uint64_t base = r0; base < r1; base += kRound) {
+    const uint64_t i0 = base + 4 * threadIdx.x;
+    uint64_t c[4], local = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      c[e] = i0 + e < r1 ? a.counts[i0 + e] : 0;
+      local += c[e];
+    }
+    uint64_t incl = local;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
       const uint64_t y = shfl64(incl, lane >= d ? lane - d : lane);
@@ -251,31 +524,33 @@ __global__ __launch_bounds__(kFwThreads) void first_write_scan_kernel(const uint
     if (lane == 63) wave_sums[wave] = incl;
     __syncthreads();
     uint64_t before = 0, sum = 0;
-    for (int w = 0; w < kFwThreads / 64; ++w) {
+    for (int w = 0; w < kFwWaves; ++w) {
       before += w < wave ? wave_sums[w] : 0;
       sum += wave_sums[w];
     }
-    __syncthreads();
-    if (i < n_regions) first[i] = carry + before + incl - x;
+    uint64_t p0 = carry + before + incl - local;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (i0 + e < r1) {
+        first[i0 + e] = p0;
+        at[4 * threadIdx.x + e] = p0;
+      }
+      p0 += c[e];
+    }
+    __syncthreads();  // every at[] written, wave_sums read
+    const uint64_t end = base + kRound < r1 ? base + kRound : r1;
+    for (uint64_t r = base + wave; r < end; r += kFwWaves) {
+      const uint64_t n = a.counts[r], o = at[r - base], src = 2 * a.region_first[r];
+      for (uint64_t p = lane; p < n && o + p < cap; p += 64) {
+        out_write[o + p] = a.pad_write[src + p];
+        out_offset[o + p] = a.pad_offset[src + p];
+        out_len[o + p] = a.pad_len[src + p];
+      }
+    }
     carry += sum;
+    __syncthreads();  // at[] is rewritten next round
   }
-  if (threadIdx.x == 0) first[n_regions] = carry;
-}
-
-// One thread per allocation moves its pieces from the workspace to the dense outputs
-// (u64[2 n_writes] each: a well-formed region_first yields fewer pieces; an ill-formed one,
-// whose regions overlap, is cut at the end of the outputs).
-__global__ void first_write_move_kernel(FwArgs a, const uint64_t* first, uint64_t* out_write,
-                                        uint64_t* out_offset, uint64_t* out_len) {
-  const uint64_t r = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= a.n_regions) return;
-  const uint64_t c = a.counts[r], w0 = a.region_first[r], at = first[r];
-  const uint64_t cap = 2 * a.n_writes;
-  for (uint64_t p = 0; p < c && at + p < cap; ++p) {
-    out_write[at + p] = a.pad_write[2 * w0 + p];
-    out_offset[at + p] = a.pad_offset[2 * w0 + p];
-    out_len[at + p] = a.pad_len[2 * w0 + p];
-  }
+  if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) first[a.n_regions] = carry;
 }
 
 }  // namespace
@@ -289,7 +564,7 @@ hipError_t preload_first_write() {
 
 extern "C" size_t gleam_first_writes_ws_bytes(uint64_t n_writes, uint64_t n_regions) {
   if (n_writes > (1ull << 36) || n_regions > (1ull << 36)) return 0;
-  const size_t b = gleam::kHeaderBytes + 8 * (size_t)n_regions + 48 * (size_t)n_writes;
+  const size_t b = gleam::kHeaderBytes + 8 * gleam::kMaxChunks + 8 * (size_t)n_regions + 48 * (size_t)n_writes;
   return (b + 255) & ~(size_t)255;
 }
 
@@ -326,21 +601,25 @@ extern "C" gleam_status gleam_first_writes(const uint64_t* d_addr, const uint64_
   a.n_writes = n_writes;
   a.region_first = d_region_first;
   a.n_regions = n_regions;
-  a.counts = reinterpret_cast<uint64_t*>(ws + kHeaderBytes);
+  uint64_t* chunk_sum = reinterpret_cast<uint64_t*>(ws + kHeaderBytes);
+  a.counts = chunk_sum + kMaxChunks;
   a.pad_write = a.counts + n_regions;
   a.pad_offset = a.pad_write + 2 * n_writes;
   a.pad_len = a.pad_offset + 2 * n_writes;
   a.status = d_region_status;
   gleam_status st;
+  int cus = 0;
+  if ((st = device_cu_count(&cus)) != GLEAM_OK) return st;
+  uint64_t wgs = (n_regions + kFwWaves - 1) / kFwWaves;
+  if (wgs > (uint64_t)cus) wgs = (uint64_t)cus;
+  if (wgs > kMaxChunks) wgs = kMaxChunks;
+  if (wgs == 0) wgs = 1;
+  const uint64_t chunk = (n_regions + wgs - 1) / wgs;
   if (n_regions > 0) {
-    hipLaunchKernelGGL(first_write_region_kernel, dim3((uint32_t)n_regions), dim3(kFwThreads), 0, s, a);
-    if ((st = launch_status("first_write_region_kernel")) != GLEAM_OK) return st;
+    hipLaunchKernelGGL(first_write_kernel, dim3((uint32_t)wgs), dim3(kFwThreads), 0, s, a, chunk, chunk_sum);
+    if ((st = launch_status("first_write_kernel")) != GLEAM_OK) return st;
   }
-  hipLaunchKernelGGL(first_write_scan_kernel, dim3(1), dim3(kFwThreads), 0, s, a.counts, n_regions,
-                     d_region_piece_first);
-  if ((st = launch_status("first_write_scan_kernel")) != GLEAM_OK) return st;
-  if (n_regions == 0) return GLEAM_OK;
-  hipLaunchKernelGGL(first_write_move_kernel, dim3((uint32_t)((n_regions + 255) / 256)), dim3(256), 0, s, a,
+  hipLaunchKernelGGL(first_write_move_kernel, dim3((uint32_t)wgs), dim3(kFwThreads), 0, s, a, chunk, chunk_sum,
                      d_region_piece_first, d_piece_write, d_piece_offset, d_piece_len);
   return launch_status("first_write_move_kernel");
 }

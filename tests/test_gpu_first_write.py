@@ -74,6 +74,73 @@ def test_pieces_random_logs(seed, n_regions, max_writes, span):
     check_pieces(addr, length, rf, f"seed {seed}")
 
 
+def test_pieces_one_wave_boundary():
+    """Allocations of 63, 64 and 65 writes (64 is the most a one-wave workgroup takes), each
+    also with a write past the top of the address space, between small ones."""
+    rng = np.random.default_rng(7100)
+    addr, length, rf = [], [], [0]
+    for k in (63, 64, 65, 1, 64, 65, 0, 63):
+        for bad in (False, True):
+            base = int(rng.integers(0, 2**40)) << 12
+            for j in range(k):
+                addr.append(base + int(rng.integers(0, 3000))), length.append(int(rng.integers(0, 700)))
+            if bad and k:
+                addr[-1], length[-1] = 2**64 - 5, 5 + int(rng.integers(1, 4))
+            rf.append(len(addr))
+    say("first writes one-wave boundary", "writes", len(addr))
+    *_, status = check_pieces(addr, length, rf, "one-wave boundary")
+    assert status.tolist() == [g.FW_OK, g.FW_INVALID] * 6 + [g.FW_OK, g.FW_OK, g.FW_OK, g.FW_INVALID]
+
+
+def test_pieces_many_large_allocations():
+    """Allocations of over 64 writes (more than one wave takes) in every chunk of a call,
+    so each workgroup takes several in turn (some refused, some small ones between them)."""
+    rng = np.random.default_rng(7200)
+    addr, length, rf = [], [], [0]
+    for r in range(600):
+        k = int(rng.integers(65, 90)) if r % 7 else int(rng.integers(0, 64))
+        a, l, _ = random_log_k(rng, k, 4000)
+        if r % 11 == 5 and k:
+            a[-1], l[-1] = 2**64 - 3, 4
+        addr += a
+        length += l
+        rf.append(len(addr))
+    say("first writes many large", "writes", len(addr))
+    check_pieces(addr, length, rf, "many large")
+
+
+def test_pieces_over_a_million_allocations():
+    """Over a million allocations: chunks of 4,116, so each wave takes about 257 in turn,
+    the larger ones are found in five rounds per chunk and each chunk's scan and move take
+    two rounds; most have zero to two writes, some over 64."""
+    rng = np.random.default_rng(7300)
+    n_regions = (1 << 20) + 5000
+    k = rng.integers(0, 3, size=n_regions)
+    big = rng.choice(n_regions, size=40, replace=False)
+    k[big] = rng.integers(65, 130, size=40)
+    rf = np.zeros(n_regions + 1, np.uint64)
+    rf[1:] = np.cumsum(k)
+    n = int(rf[-1])
+    region = np.repeat(np.arange(n_regions, dtype=np.uint64), k)
+    addr = (region << np.uint64(24)) + rng.integers(0, 5000, size=n).astype(np.uint64)
+    length = rng.integers(0, 3000, size=n).astype(np.uint64)
+    say("first writes", n_regions, "allocations", n, "writes")
+    check_pieces(addr, length, rf, "over a million allocations")
+
+
+def random_log_k(rng, k, span):
+    """One allocation of exactly k writes within [base, base + span)."""
+    base = int(rng.integers(0, 2**40)) << 12
+    addr, length = [], []
+    for _ in range(k):
+        if length and rng.random() < 0.1:
+            j = int(rng.integers(0, len(addr)))
+            addr.append(addr[j]), length.append(length[j])
+        else:
+            addr.append(base + int(rng.integers(0, span))), length.append(int(rng.integers(0, span // 3)))
+    return addr, length, [0, k]
+
+
 def test_pieces_edges():
     top = 2**64 - 1
     # disjoint, nested, spanning, empty allocations, an allocation ending at the top of the
@@ -91,6 +158,29 @@ def test_pieces_edges():
     say("first writes edges")
     _, _, _, _, status = check_pieces(addr, length, rf, "edges")
     assert status.tolist() == [g.FW_OK, g.FW_OK, g.FW_OK, g.FW_OK, g.FW_INVALID, g.FW_OK, g.FW_OK, g.FW_TOO_MANY]
+
+
+def test_reused_outputs_and_workspace():
+    """Calls sharing outputs and workspace (sized for the largest) give each log's pieces,
+    the later, smaller log too."""
+    rng = np.random.default_rng(7400)
+    logs = [random_log(rng, 400, 90, 1 << 16), random_log(rng, 37, 20, 3000)]
+    n = max(len(a) for a, _, _ in logs)
+    n_regions = max(len(rf) - 1 for _, _, rf in logs)
+    bufs = g.first_writes_outputs(n, n_regions)
+    ws = g.first_writes_workspace(n, n_regions)
+    for k, (addr, length, rf) in enumerate(logs):
+        say("first writes reused buffers", k, "writes", len(addr))
+        pw, po, pl, first, status = g.first_writes(np.asarray(addr, np.uint64), np.asarray(length, np.uint64),
+                                                   np.asarray(rf, np.uint64), out=bufs, ws=ws)
+        torch.cuda.synchronize()
+        want = oracle.first_write_pieces(addr, length, rf, max_writes=2048)
+        m = len(rf) - 1
+        first = u64(first)[:m + 1]
+        p = int(first[-1])
+        got = (u64(pw)[:p], u64(po)[:p], u64(pl)[:p], first, status.cpu().numpy()[:m])
+        for a, b, name in zip(got, want, ("write", "offset", "length", "region first", "status")):
+            assert np.array_equal(a, b), f"log {k}: {name} differs"
 
 
 def test_no_writes_and_no_allocations():
