@@ -250,34 +250,72 @@ __device__ uint32_t fw_region(const FwArgs& a, uint64_t r, uint64_t w0, uint64_t
   return total;
 }
 
-// Ascending bitonic sort, in registers, of the wave's elements 2 lane + h < P (v0 holds
-// h = 0, v1 h = 1; P a power of two <= 128). Lanes at or past P / 2 exchange only among
-// themselves.
-template <typename T>
-__device__ __forceinline__ T wave_partner(T v, int m);
-template <>
-__device__ __forceinline__ uint64_t wave_partner<uint64_t>(uint64_t v, int m) { return shfl_xor64(v, m); }
-template <>
-__device__ __forceinline__ uint32_t wave_partner<uint32_t>(uint32_t v, int m) {
-  return (uint32_t)__shfl_xor((int)v, m, 64);
+// The value lane ^ M holds (all 64 lanes active): DPP moves within rows of 16 lanes for
+// M = 1, 2 (quad permutes) and 8 (rotate by 8), swizzles within 32 lanes for 4 and 16,
+// and a permute through the LDS crossbar for 32.
+template <int M>
+__device__ __forceinline__ uint32_t xor_lanes32(uint32_t v) {
+  const int x = (int)v;
+  if constexpr (M == 1) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, true);  // quad_perm [1,0,3,2]
+  } else if constexpr (M == 2) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, true);  // quad_perm [2,3,0,1]
+  } else if constexpr (M == 8) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, x, 0x128, 0xF, 0xF, true);  // row_ror:8
+  } else if constexpr (M == 4 || M == 16) {
+    return (uint32_t)__builtin_amdgcn_ds_swizzle(x, (M << 10) | 0x1F);  // and 0x1F, xor M
+  } else {
+    return (uint32_t)__shfl_xor(x, M, 64);
+  }
 }
 
+template <int M>
+__device__ __forceinline__ uint64_t xor_lanes(uint64_t v) {
+  return ((uint64_t)xor_lanes32<M>((uint32_t)(v >> 32)) << 32) | xor_lanes32<M>((uint32_t)v);
+}
+template <int M>
+__device__ __forceinline__ uint32_t xor_lanes(uint32_t v) {
+  return xor_lanes32<M>(v);
+}
+
+// Bitonic merge steps of distance 2M, M / 2, ..., 2 over elements 2 lane + h: element
+// 2 lane + h pairs with 2 (lane ^ M) + h, and the lower index keeps the min going up.
+template <int M, typename T>
+__device__ __forceinline__ void wave_merge_steps(T& v0, T& v1, uint32_t lane, bool up) {
+  if constexpr (M >= 1) {
+    const T p0 = xor_lanes<M>(v0), p1 = xor_lanes<M>(v1);
+    const bool keep_min = ((lane & M) == 0) == up;
+    // take the partner's value when it is the one to keep (either, when equal)
+    if ((p0 < v0) == keep_min) v0 = p0;
+    if ((p1 < v1) == keep_min) v1 = p1;
+    wave_merge_steps<M / 2>(v0, v1, lane, up);
+  }
+}
+
+// One level of the bitonic sort: blocks of K elements, merged at distances K / 2 ... 1.
+template <int K, typename T>
+__device__ __forceinline__ void wave_sort_level(T& v0, T& v1, uint32_t lane) {
+  const bool up = ((2 * lane) & K) == 0;
+  wave_merge_steps<K / 4>(v0, v1, lane, up);
+  const bool swap = (v1 < v0) == up;  // distance 1: the lane's own pair
+  const T x0 = v0;
+  v0 = swap ? v1 : v0;
+  v1 = swap ? x0 : v1;
+}
+
+// Ascending bitonic sort, in registers, of the wave's elements 2 lane + h < P (v0 holds
+// h = 0, v1 h = 1; P a power of two <= 128, the same on every lane; all lanes active).
+// Lanes at or past P / 2 exchange only among themselves.
 template <typename T>
 __device__ void wave_sort_pairs(T& v0, T& v1, uint32_t P) {
   const uint32_t lane = threadIdx.x & 63;
-  for (uint32_t k = 2; k <= P; k <<= 1) {
-    const bool up = ((2 * lane) & k) == 0;  // the block of k elements this lane's pair sits in
-    for (uint32_t j = k >> 1; j >= 2; j >>= 1) {
-      const int m = (int)(j >> 1);  // element 2 lane + h pairs with 2 (lane ^ m) + h
-      const T p0 = wave_partner(v0, m), p1 = wave_partner(v1, m);
-      const bool keep_min = ((lane & m) == 0) == up;  // the lower index keeps the min going up
-      v0 = keep_min ? (p0 < v0 ? p0 : v0) : (p0 < v0 ? v0 : p0);
-      v1 = keep_min ? (p1 < v1 ? p1 : v1) : (p1 < v1 ? v1 : p1);
-    }
-    const T lo = v1 < v0 ? v1 : v0, hi = v1 < v0 ? v0 : v1;  // j = 1: the lane's own pair
-    v0 = up ? lo : hi;
-    v1 = up ? hi : lo;
-  }
+  if (P >= 2) wave_sort_level<2>(v0, v1, lane);
+  if (P >= 4) wave_sort_level<4>(v0, v1, lane);
+  if (P >= 8) wave_sort_level<8>(v0, v1, lane);
+  if (P >= 16) wave_sort_level<16>(v0, v1, lane);
+  if (P >= 32) wave_sort_level<32>(v0, v1, lane);
+  if (P >= 64) wave_sort_level<64>(v0, v1, lane);
+  if (P >= 128) wave_sort_level<128>(v0, v1, lane);
 }
 
 // Number of elements of the ascending b[0, m) below x, and below y (m >= 1), the two
@@ -499,21 +537,28 @@ __global__ __launch_bounds__(kFwThreads) void first_write_move_kernel(FwArgs a, 
                                                                       uint64_t* out_len) {
   constexpr uint32_t kRound = 4 * kFwThreads;
   __shared__ uint64_t wave_sums[kFwWaves];
-  __shared__ uint64_t at[kRound];
+  __shared__ uint64_t at[kRound];   // first piece, pieces and workspace start of each
+  __shared__ uint32_t cnt[kRound];  // allocation of the round
+  __shared__ uint64_t src_at[kRound];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t r0 = (uint64_t)blockIdx.x * chunk;
   const uint64_t r1 = r0 + chunk < a.n_regions ? r0 + chunk : a.n_regions;
-  uint64_t x = 0;
-  for (uint32_t i = threadIdx.x; i < blockIdx.x; i += kFwThreads) x += chunk_sum[i];
-  uint64_t carry = block_sum(x, wave_sums);  // pieces of the chunks before this one
+  uint64_t carry = 0;  // pieces before this round
   const uint64_t cap = 2 * a.n_writes;
   for (uint64_t base = r0; base < r1; base += kRound) {
+    // the round's counts and workspace starts, loaded with the chunk sums before them
     const uint64_t i0 = base + 4 * threadIdx.x;
     uint64_t c[4], local = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       c[e] = i0 + e < r1 ? a.counts[i0 + e] : 0;
+      if (i0 + e < r1) src_at[4 * threadIdx.x + e] = 2 * a.region_first[i0 + e];
       local += c[e];
+    }
+    if (base == r0) {  // first round: the pieces of the chunks before this one
+      uint64_t x = 0;
+      for (uint32_t i = threadIdx.x; i < blockIdx.x; i += kFwThreads) x += chunk_sum[i];
+      carry = block_sum(x, wave_sums);
     }
     uint64_t incl = local;
 #pragma unroll
@@ -534,13 +579,14 @@ __global__ __launch_bounds__(kFwThreads) void first_write_move_kernel(FwArgs a, 
       if (i0 + e < r1) {
         first[i0 + e] = p0;
         at[4 * threadIdx.x + e] = p0;
+        cnt[4 * threadIdx.x + e] = (uint32_t)c[e];
       }
       p0 += c[e];
     }
-    __syncthreads();  // every at[] written, wave_sums read
+    __syncthreads();  // every at[], cnt[] and src_at[] written, wave_sums read
     const uint64_t end = base + kRound < r1 ? base + kRound : r1;
     for (uint64_t r = base + wave; r < end; r += kFwWaves) {
-      const uint64_t n = a.counts[r], o = at[r - base], src = 2 * a.region_first[r];
+      const uint64_t n = cnt[r - base], o = at[r - base], src = src_at[r - base];
       for (uint64_t p = lane; p < n && o + p < cap; p += 64) {
         out_write[o + p] = a.pad_write[src + p];
         out_offset[o + p] = a.pad_offset[src + p];
@@ -549,6 +595,11 @@ __global__ __launch_bounds__(kFwThreads) void first_write_move_kernel(FwArgs a, 
     }
     carry += sum;
     __syncthreads();  // at[] is rewritten next round
+  }
+  if (r1 <= r0) {  // an empty chunk
+    uint64_t x = 0;
+    for (uint32_t i = threadIdx.x; i < blockIdx.x; i += kFwThreads) x += chunk_sum[i];
+    carry = block_sum(x, wave_sums);
   }
   if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) first[a.n_regions] = carry;
 }
@@ -615,6 +666,7 @@ extern "C" gleam_status gleam_first_writes(const uint64_t* d_addr, const uint64_
   if (wgs > kMaxChunks) wgs = kMaxChunks;
   if (wgs == 0) wgs = 1;
   const uint64_t chunk = (n_regions + wgs - 1) / wgs;
+  if (chunk > 0) wgs = (n_regions + chunk - 1) / chunk;  // no empty chunk
   if (n_regions > 0) {
     hipLaunchKernelGGL(first_write_kernel, dim3((uint32_t)wgs), dim3(kFwThreads), 0, s, a, chunk, chunk_sum);
     if ((st = launch_status("first_write_kernel")) != GLEAM_OK) return st;

@@ -66,7 +66,8 @@ def random_log(rng, n_regions, max_writes, span):
 
 
 @pytest.mark.parametrize("seed,n_regions,max_writes,span", [(0, 1, 8, 100), (1, 50, 20, 1000), (2, 300, 60, 1 << 20),
-                                                             (3, 20, 400, 5000), (4, 4, 2048, 1 << 16)])
+                                                             (3, 20, 400, 5000), (4, 4, 2048, 1 << 16),
+                                                             (5, 4097, 3, 1000), (6, 70_000, 2, 100)])
 def test_pieces_random_logs(seed, n_regions, max_writes, span):
     rng = np.random.default_rng(7000 + seed)
     addr, length, rf = random_log(rng, n_regions, max_writes, span)
