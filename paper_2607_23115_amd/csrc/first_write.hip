@@ -337,6 +337,7 @@ struct FwWaveLds {
   uint32_t tree[4 * kSmallWrites];
   uint32_t keys[2 * kSmallWrites];    // runs: (write << 8) | run rank, kNone when unowned
   uint32_t cps[2 * kSmallWrites + 1]; // the interval each run starts at; cps[K] = E
+  uint8_t rank[2 * kSmallWrites];     // boundary index of endpoint 2 j (start) and 2 j + 1 (end)
 };
 
 // The pieces of allocation r, whose n <= kSmallWrites writes are in range, by one wave:
@@ -359,17 +360,31 @@ __device__ uint32_t fw_wave(const FwArgs& a, uint64_t r, uint64_t w0, uint32_t n
     return 0;
   }
   const uint32_t P = p2_at_least(n ? 2 * n : 2);
-  uint64_t v0 = lane < n ? s : ~0ull, v1 = lane < n ? s + l : ~0ull;
+  // When every endpoint has the same top 7 bits (lane 0's), the sort keys carry the
+  // endpoint's number (2 j, or 2 j + 1 for an end) in their low 7 bits in place of them,
+  // so that each endpoint learns its boundary index without a search.
+  const uint64_t top = (uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(s >> 57));
+  const bool tagged = n > 0 && !__ballot(lane < n && ((s >> 57) != top || ((s + l) >> 57) != top));
+  const int sh = tagged ? 7 : 0;
+  const uint64_t tag = tagged ? 2 * lane : 0;
+  uint64_t v0 = lane < n ? (s << sh) | tag : ~0ull, v1 = lane < n ? ((s + l) << sh) | (tag + tagged) : ~0ull;
   wave_sort_pairs(v0, v1, P);
 
-  // unique boundaries
-  const uint64_t before = shfl64(v1, lane ? (int)lane - 1 : 0);
-  const bool f0 = 2 * lane < P && (lane == 0 || v0 != before);
-  const bool f1 = 2 * lane + 1 < P && v1 != v0;
+  // unique boundaries (compared without the endpoint numbers)
+  const uint64_t x0 = v0 >> sh, x1 = v1 >> sh;
+  const uint64_t before = shfl64(x1, lane ? (int)lane - 1 : 0);
+  const bool f0 = 2 * lane < P && (lane == 0 || x0 != before);
+  const bool f1 = 2 * lane + 1 < P && x1 != x0;
   const uint64_t b0 = __ballot(f0), b1 = __ballot(f1);
   const uint32_t at = (uint32_t)(__popcll(b0 & below) + __popcll(b1 & below));
-  if (f0) L.bounds[at] = v0;
-  if (f1) L.bounds[at + f0] = v1;
+  const uint64_t hi_bits = tagged ? top << 57 : 0;
+  if (f0) L.bounds[at] = hi_bits | x0;
+  if (f1) L.bounds[at + f0] = hi_bits | x1;
+  if (tagged) {  // padding (numbers past 2 n) aside
+    const uint32_t t0 = (uint32_t)(v0 & 127), t1 = (uint32_t)(v1 & 127);
+    if (t0 < 2 * n) L.rank[t0] = (uint8_t)(at + f0 - 1);
+    if (t1 < 2 * n) L.rank[t1] = (uint8_t)(at + f0 + f1 - 1);
+  }
   const uint32_t M = (uint32_t)(__popcll(b0) + __popcll(b1));
   const uint32_t E = M - 1;
   const uint32_t T2 = p2_at_least(E ? E : 1);
@@ -379,7 +394,12 @@ __device__ uint32_t fw_wave(const FwArgs& a, uint64_t r, uint64_t w0, uint32_t n
   // every write min-updates the canonical nodes of its interval range
   if (lane < n && l != 0) {
     uint32_t lo, hi;
-    count_below2(L.bounds, M, s, s + l, lo, hi);
+    if (tagged) {
+      lo = L.rank[2 * lane];
+      hi = L.rank[2 * lane + 1];
+    } else {
+      count_below2(L.bounds, M, s, s + l, lo, hi);
+    }
     lo += T2;
     hi += T2;
     while (lo < hi) {

@@ -93,6 +93,31 @@ def test_pieces_one_wave_boundary():
     assert status.tolist() == [g.FW_OK, g.FW_INVALID] * 6 + [g.FW_OK, g.FW_OK, g.FW_OK, g.FW_INVALID]
 
 
+def test_pieces_wide_address_spans():
+    """Allocations whose writes do not share their top 7 address bits (spread over the
+    whole 64-bit space, or straddling a multiple of 2^57), of one wave's size and larger,
+    beside ones that do."""
+    rng = np.random.default_rng(7500)
+    addr, length, rf = [], [], [0]
+    for k in (1, 5, 40, 64, 100, 64, 30):
+        for kind in ("spread", "straddle", "narrow"):
+            for _ in range(k):
+                if kind == "spread":
+                    a = int(rng.integers(0, 2**63)) * 2 + int(rng.integers(0, 2))
+                    n = int(rng.integers(0, min(2**62, 2**64 - 1 - a) + 1))
+                elif kind == "straddle":
+                    a = (5 << 57) - 3000 + int(rng.integers(0, 6000))
+                    n = int(rng.integers(0, 4000))
+                else:
+                    a = (9 << 57) + int(rng.integers(0, 6000))
+                    n = int(rng.integers(0, 4000))
+                addr.append(a), length.append(n)
+            rf.append(len(addr))
+    say("first writes wide spans", "writes", len(addr))
+    *_, status = check_pieces(addr, length, rf, "wide spans")
+    assert (status == g.FW_OK).all()
+
+
 def test_pieces_many_large_allocations():
     """Allocations of over 64 writes (more than one wave takes) in every chunk of a call,
     so each workgroup takes several in turn (some refused, some small ones between them)."""
