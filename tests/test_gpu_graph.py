@@ -1,6 +1,6 @@
 """Calls captured once in a HIP graph and replayed: the detect path (fingerprint ->
-lookup -> compaction), and identify, MD5 prefix, touch, send plan, pack and restore, and
-the table's erase, evict and export. Every
+lookup -> compaction), and identify, MD5 prefix, touch, send plan, pack and restore, the
+table's erase, evict and export, and the first-write rule. Every
 replay equals an eager run, with eager work and synchronisations between replays, and a
 replay after the payload bytes change in place sees the new bytes. Every call is plain
 kernel launches (clears are fill kernels, nothing allocates device memory or syncs), so
@@ -344,3 +344,58 @@ def test_graph_replays_evict_and_export(cap):
         assert np.array_equal(u64(k)[:int(c.item())], wk) and np.array_equal(u64(s)[:int(c.item())], ws_)
         table.set_key_bound(len(ot))  # a replay does not lower the host bound; the read-back count does
         grow(i + 1)
+
+
+def test_graph_replays_first_writes():
+    """gleam_first_writes captured once (its two launches): every replay, after the outputs
+    are scribbled over and an eager call on the same workspace, gives the oracle's pieces;
+    a replay after the write log changes in place gives the new log's pieces."""
+    logs = [W.WriteLogs(n_alloc=600, workload=11), W.WriteLogs(n_alloc=600, workload=12)]
+    n = max(int(l.addr.size) for l in logs)
+    d_addr = torch.zeros(n, dtype=torch.int64, device="cuda")
+    d_len = torch.zeros(n, dtype=torch.int64, device="cuda")
+    d_rf = torch.zeros(601, dtype=torch.int64, device="cuda")
+
+    def load(log):  # the log in place, padded with empty writes past its last allocation
+        m = int(log.addr.size)
+        d_addr.zero_(), d_len.zero_()
+        d_addr[:m].copy_(torch.from_numpy(log.addr.view(np.int64)))
+        d_len[:m].copy_(torch.from_numpy(log.length.view(np.int64)))
+        d_rf.copy_(torch.from_numpy(log.region_first.view(np.int64)))
+
+    def want(log):
+        return oracle.first_write_pieces(log.addr, log.length, log.region_first, max_writes=2048)
+
+    def got(out):
+        torch.cuda.synchronize()
+        pw, po, pl, first, status = out
+        first = u64(first)[:601]
+        p = int(first[-1])
+        return u64(pw)[:p], u64(po)[:p], u64(pl)[:p], first, status.cpu().numpy()[:600]
+
+    bufs = g.first_writes_outputs(n, 600)
+    ws = g.first_writes_workspace(n, 600)
+    other = g.first_writes_outputs(n, 600)
+    load(logs[0])
+    g.first_writes(d_addr, d_len, d_rf, out=bufs, ws=ws)  # first launch, outside the capture
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side), torch.cuda.graph(graph, stream=side):
+        g.first_writes(d_addr, d_len, d_rf, out=bufs, ws=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for i, log in enumerate([logs[0], logs[0], logs[1], logs[1], logs[0]]):
+        say("graph first writes replay", i)
+        load(log)
+        for t in bufs:
+            t.fill_(-1)
+        graph.replay()
+        w = want(log)
+        for a, b, name in zip(got(bufs), w, ("write", "offset", "length", "region first", "status")):
+            assert np.array_equal(a, b), f"replay {i}: {name}"
+        # eager work on the same workspace between replays
+        g.first_writes(d_addr, d_len, d_rf, out=other, ws=ws)
+        for a, b, name in zip(got(other), w, ("write", "offset", "length", "region first", "status")):
+            assert np.array_equal(a, b), f"eager after replay {i}: {name}"
