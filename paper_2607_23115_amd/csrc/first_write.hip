@@ -532,7 +532,10 @@ __global__ __launch_bounds__(kFwThreads) void first_write_kernel(FwArgs a, uint6
   }
 }
 
-// Sum over the workgroup, returned to every thread.
+constexpr int kMoveThreads = 256;
+constexpr int kMoveWaves = kMoveThreads / 64;
+
+// Sum over the workgroup of kMoveThreads, returned to every thread.
 __device__ uint64_t block_sum(uint64_t x, uint64_t* wave_sums) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
@@ -540,7 +543,7 @@ __device__ uint64_t block_sum(uint64_t x, uint64_t* wave_sums) {
   if (lane == 0) wave_sums[wave] = x;
   __syncthreads();
   uint64_t sum = 0;
-  for (int w = 0; w < kFwWaves; ++w) sum += wave_sums[w];
+  for (int w = 0; w < kMoveWaves; ++w) sum += wave_sums[w];
   __syncthreads();
   return sum;
 }
@@ -551,12 +554,12 @@ __device__ uint64_t block_sum(uint64_t x, uint64_t* wave_sums) {
 // one piece per lane (u64[2 n_writes] each: a well-formed region_first yields fewer
 // pieces; an ill-formed one, whose regions overlap, is cut at the end of the outputs).
 // The last workgroup writes the total at [n_regions].
-__global__ __launch_bounds__(kFwThreads) void first_write_move_kernel(FwArgs a, uint64_t chunk,
+__global__ __launch_bounds__(kMoveThreads) void first_write_move_kernel(FwArgs a, uint64_t chunk,
                                                                       const uint64_t* chunk_sum, uint64_t* first,
                                                                       uint64_t* out_write, uint64_t* out_offset,
                                                                       uint64_t* out_len) {
-  constexpr uint32_t kRound = 4 * kFwThreads;
-  __shared__ uint64_t wave_sums[kFwWaves];
+  constexpr uint32_t kRound = 4 * kMoveThreads;
+  __shared__ uint64_t wave_sums[kMoveWaves];
   __shared__ uint64_t at[kRound];   // first piece, pieces and workspace start of each
   __shared__ uint32_t cnt[kRound];  // allocation of the round
   __shared__ uint64_t src_at[kRound];
@@ -577,7 +580,7 @@ __global__ __launch_bounds__(kFwThreads) void first_write_move_kernel(FwArgs a, 
     }
     if (base == r0) {  // first round: the pieces of the chunks before this one
       uint64_t x = 0;
-      for (uint32_t i = threadIdx.x; i < blockIdx.x; i += kFwThreads) x += chunk_sum[i];
+      for (uint32_t i = threadIdx.x; i < blockIdx.x; i += kMoveThreads) x += chunk_sum[i];
       carry = block_sum(x, wave_sums);
     }
     uint64_t incl = local;
@@ -589,7 +592,7 @@ __global__ __launch_bounds__(kFwThreads) void first_write_move_kernel(FwArgs a, 
     if (lane == 63) wave_sums[wave] = incl;
     __syncthreads();
     uint64_t before = 0, sum = 0;
-    for (int w = 0; w < kFwWaves; ++w) {
+    for (int w = 0; w < kMoveWaves; ++w) {
       before += w < wave ? wave_sums[w] : 0;
       sum += wave_sums[w];
     }
@@ -605,7 +608,7 @@ __global__ __launch_bounds__(kFwThreads) void first_write_move_kernel(FwArgs a, 
     }
     __syncthreads();  // every at[], cnt[] and src_at[] written, wave_sums read
     const uint64_t end = base + kRound < r1 ? base + kRound : r1;
-    for (uint64_t r = base + wave; r < end; r += kFwWaves) {
+    for (uint64_t r = base + wave; r < end; r += kMoveWaves) {
       const uint64_t n = cnt[r - base], o = at[r - base], src = src_at[r - base];
       for (uint64_t p = lane; p < n && o + p < cap; p += 64) {
         out_write[o + p] = a.pad_write[src + p];
@@ -618,7 +621,7 @@ __global__ __launch_bounds__(kFwThreads) void first_write_move_kernel(FwArgs a, 
   }
   if (r1 <= r0) {  // an empty chunk
     uint64_t x = 0;
-    for (uint32_t i = threadIdx.x; i < blockIdx.x; i += kFwThreads) x += chunk_sum[i];
+    for (uint32_t i = threadIdx.x; i < blockIdx.x; i += kMoveThreads) x += chunk_sum[i];
     carry = block_sum(x, wave_sums);
   }
   if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) first[a.n_regions] = carry;
@@ -691,7 +694,7 @@ extern "C" gleam_status gleam_first_writes(const uint64_t* d_addr, const uint64_
     hipLaunchKernelGGL(first_write_kernel, dim3((uint32_t)wgs), dim3(kFwThreads), 0, s, a, chunk, chunk_sum);
     if ((st = launch_status("first_write_kernel")) != GLEAM_OK) return st;
   }
-  hipLaunchKernelGGL(first_write_move_kernel, dim3((uint32_t)wgs), dim3(kFwThreads), 0, s, a, chunk, chunk_sum,
+  hipLaunchKernelGGL(first_write_move_kernel, dim3((uint32_t)wgs), dim3(kMoveThreads), 0, s, a, chunk, chunk_sum,
                      d_region_piece_first, d_piece_write, d_piece_offset, d_piece_len);
   return launch_status("first_write_move_kernel");
 }

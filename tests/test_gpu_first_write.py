@@ -138,7 +138,7 @@ def test_pieces_many_large_allocations():
 def test_pieces_over_a_million_allocations():
     """Over a million allocations: chunks of 4,116, so each wave takes about 257 in turn,
     the larger ones are found in five rounds per chunk and each chunk's scan and move take
-    two rounds; most have zero to two writes, some over 64."""
+    five rounds; most have zero to two writes, some over 64."""
     rng = np.random.default_rng(7300)
     n_regions = (1 << 20) + 5000
     k = rng.integers(0, 3, size=n_regions)
