@@ -337,7 +337,6 @@ struct FwWaveLds {
   uint32_t tree[4 * kSmallWrites];
   uint32_t keys[2 * kSmallWrites];    // runs: (write << 8) | run rank, kNone when unowned
   uint32_t cps[2 * kSmallWrites + 1]; // the interval each run starts at; cps[K] = E
-  uint8_t rank[2 * kSmallWrites];     // boundary index of endpoint 2 j (start) and 2 j + 1 (end)
 };
 
 // The pieces of allocation r, whose n <= kSmallWrites writes are in range, by one wave:
@@ -362,7 +361,7 @@ __device__ uint32_t fw_wave(const FwArgs& a, uint64_t r, uint64_t w0, uint32_t n
   const uint32_t P = p2_at_least(n ? 2 * n : 2);
   // When every endpoint has the same top 7 bits (lane 0's), the sort keys carry the
   // endpoint's number (2 j, or 2 j + 1 for an end) in their low 7 bits in place of them,
-  // so that each endpoint learns its boundary index without a search.
+  // so that each sorted endpoint knows its write.
   const uint64_t top = (uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(s >> 57));
   const bool tagged = n > 0 && !__ballot(lane < n && ((s >> 57) != top || ((s + l) >> 57) != top));
   const int sh = tagged ? 7 : 0;
@@ -380,42 +379,54 @@ __device__ uint32_t fw_wave(const FwArgs& a, uint64_t r, uint64_t w0, uint32_t n
   const uint64_t hi_bits = tagged ? top << 57 : 0;
   if (f0) L.bounds[at] = hi_bits | x0;
   if (f1) L.bounds[at + f0] = hi_bits | x1;
-  if (tagged) {  // padding (numbers past 2 n) aside
-    const uint32_t t0 = (uint32_t)(v0 & 127), t1 = (uint32_t)(v1 & 127);
-    if (t0 < 2 * n) L.rank[t0] = (uint8_t)(at + f0 - 1);
-    if (t1 < 2 * n) L.rank[t1] = (uint8_t)(at + f0 + f1 - 1);
-  }
   const uint32_t M = (uint32_t)(__popcll(b0) + __popcll(b1));
   const uint32_t E = M - 1;
-  const uint32_t T2 = p2_at_least(E ? E : 1);
-  for (uint32_t i = lane; i < 2 * T2; i += 64) L.tree[i] = kNone;
-  wave_lds_sync();
-
-  // every write min-updates the canonical nodes of its interval range
-  if (lane < n && l != 0) {
-    uint32_t lo, hi;
-    if (tagged) {
-      lo = L.rank[2 * lane];
-      hi = L.rank[2 * lane + 1];
-    } else {
-      count_below2(L.bounds, M, s, s + l, lo, hi);
-    }
-    lo += T2;
-    hi += T2;
-    while (lo < hi) {
-      if (lo & 1) atomicMin(&L.tree[lo++], lane);
-      if (hi & 1) atomicMin(&L.tree[--hi], lane);
-      lo >>= 1;
-      hi >>= 1;
-    }
-  }
-  wave_lds_sync();
   uint32_t o0 = kNone, o1 = kNone;  // first writers of intervals 2 lane and 2 lane + 1
-  if (2 * lane < E) {
-    const bool two = 2 * lane + 1 < E;
-    for (uint32_t x = 2 * lane + T2, y = x + 1; x >= 1; x >>= 1, y >>= 1) {
-      o0 = min(o0, L.tree[x]);
-      if (two) o1 = min(o1, L.tree[y]);
+  if (tagged) {
+    // Each sorted endpoint toggles its write's bit; the XOR of the toggles up to the last
+    // endpoint at boundary i is the set of writes covering interval i (a zero-length
+    // write toggles twice there), and its lowest bit is the first writer.
+    const uint32_t t0 = (uint32_t)(v0 & 127), t1 = (uint32_t)(v1 & 127);  // padding: >= 2 n
+    const uint64_t bit0 = t0 < 2 * n ? 1ull << (t0 >> 1) : 0, bit1 = t1 < 2 * n ? 1ull << (t1 >> 1) : 0;
+    uint64_t incl = bit0 ^ bit1;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint64_t y = shfl64(incl, lane >= (uint32_t)d ? (int)lane - d : (int)lane);
+      if (lane >= (uint32_t)d) incl ^= y;
+    }
+    const uint64_t cover0 = incl ^ bit1, cover1 = incl;  // through elements 2 lane, 2 lane + 1
+    const bool next_new = __shfl((int)f0, lane < 63 ? (int)lane + 1 : 63, 64) != 0;
+    const uint32_t i0 = at + f0 - 1, i1 = at + f0 + f1 - 1;  // their boundary indexes
+    const bool last0 = 2 * lane < P && f1, last1 = 2 * lane + 1 < P && (2 * lane + 2 >= P || next_new);
+    if (last0 && i0 < E) L.tree[i0] = cover0 ? (uint32_t)__builtin_ctzll(cover0) : kNone;
+    if (last1 && i1 < E) L.tree[i1] = cover1 ? (uint32_t)__builtin_ctzll(cover1) : kNone;
+    wave_lds_sync();
+    if (2 * lane < E) o0 = L.tree[2 * lane];
+    if (2 * lane + 1 < E) o1 = L.tree[2 * lane + 1];
+  } else {
+    // every write min-updates the canonical nodes of its interval range in a segment tree
+    const uint32_t T2 = p2_at_least(E ? E : 1);
+    for (uint32_t i = lane; i < 2 * T2; i += 64) L.tree[i] = kNone;
+    wave_lds_sync();
+    if (lane < n && l != 0) {
+      uint32_t lo, hi;
+      count_below2(L.bounds, M, s, s + l, lo, hi);
+      lo += T2;
+      hi += T2;
+      while (lo < hi) {
+        if (lo & 1) atomicMin(&L.tree[lo++], lane);
+        if (hi & 1) atomicMin(&L.tree[--hi], lane);
+        lo >>= 1;
+        hi >>= 1;
+      }
+    }
+    wave_lds_sync();
+    if (2 * lane < E) {
+      const bool two = 2 * lane + 1 < E;
+      for (uint32_t x = 2 * lane + T2, y = x + 1; x >= 1; x >>= 1, y >>= 1) {
+        o0 = min(o0, L.tree[x]);
+        if (two) o1 = min(o1, L.tree[y]);
+      }
     }
   }
 
