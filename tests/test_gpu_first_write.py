@@ -93,6 +93,32 @@ def test_pieces_one_wave_boundary():
     assert status.tolist() == [g.FW_OK, g.FW_INVALID] * 6 + [g.FW_OK, g.FW_OK, g.FW_OK, g.FW_INVALID]
 
 
+def test_pieces_one_wave_shapes():
+    """Allocations of at most 64 writes in the shapes that stress the one-wave pass: 64
+    nested writes (each one byte wider on the left), 64 identical writes, 64 touching
+    writes end to start, 64 zero-length writes at one address, zero-length writes at the
+    ends of others, writes growing and then shrinking around one point, and a write at the
+    top of the address space."""
+    top = 2**64 - 1
+    logs = [
+        ([1000 - j for j in range(64)], [100 + j for j in range(64)]),
+        ([5000] * 64, [300] * 64),
+        ([10_000 + 7 * j for j in range(64)], [7] * 64),
+        ([777] * 64, [0] * 64),
+        ([100, 100, 200, 200, 150], [100, 0, 0, 50, 0]),
+        ([500 - j for j in range(32)] + [470 + j for j in range(32)], [2 * j + 1 for j in range(32)] + [40 - j for j in range(32)]),
+        ([top - 100, top - 50, top - 100], [100, 50, 10]),
+    ]
+    addr, length, rf = [], [], [0]
+    for a, l in logs:
+        addr += a
+        length += l
+        rf.append(len(addr))
+    say("first writes one-wave shapes")
+    *_, status = check_pieces(addr, length, rf, "one-wave shapes")
+    assert (status == g.FW_OK).all()
+
+
 def test_pieces_wide_address_spans():
     """Allocations whose writes do not share their top 7 address bits (spread over the
     whole 64-bit space, or straddling a multiple of 2^57), of one wave's size and larger,
