@@ -17,6 +17,8 @@
 //      it: every write min-updates the O(log) canonical nodes of a segment tree over the
 //      elementary intervals that make up its range, and an interval's first writer is
 //      the least value on its path to the root (O(n log n) work, whatever the overlap);
+//      a wave whose sorted endpoints know their writes (n <= 64) instead XOR-scans the
+//      writes' bits along them: the set covering each interval, whose lowest bit it is;
 //   3. maximal runs of intervals with one first writer are the pieces; they are sorted
 //      by (write, address) with a second bitonic sort and written to the workspace.
 // A second launch gives each allocation its first piece (the chunk sums before its chunk,
