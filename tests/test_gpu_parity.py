@@ -483,6 +483,42 @@ def test_dedup_collisions_with_duplicates(n_keys, repeats, filler):
     assert np.array_equal(st2.cpu().numpy(), est2) and np.array_equal(u64(ref2), eref2)
 
 
+@pytest.mark.parametrize("kind", ["one_partition", "one_key", "two_partitions_with_hits"])
+def test_lookup_skewed_keys(kind):
+    """Lookups of 9,000-16,384 keys (the three-launch path) with skewed keys: 16,384
+    distinct keys that agree in bits 40-43, one key repeated 16,384 times, and keys
+    drawn from two such groups with half of them cached and repeats, against the
+    oracle."""
+    rng = np.random.default_rng(870)
+    n = 16_384
+    if kind == "one_partition":
+        keys = rng.integers(0, 2**64, n, dtype=np.uint64, endpoint=False)
+        keys = (keys & ~np.uint64(0xF << 40)) | np.uint64(7 << 40)
+        keys = np.unique(keys)[:n]
+        keys = keys[rng.permutation(keys.size)]
+        cached = keys[: keys.size // 4]
+    elif kind == "one_key":
+        keys = np.full(n, 0x123456789ABCDEF0, np.uint64)
+        cached = np.zeros(0, np.uint64)
+    else:
+        pool = rng.integers(0, 2**64, 3000, dtype=np.uint64, endpoint=False)
+        pool = (pool & ~np.uint64(0xF << 40)) | (np.uint64(3 << 40) * (pool & np.uint64(1)).astype(np.uint64))
+        pool = np.concatenate([pool, np.array([0, 2**64 - 1], np.uint64)])
+        keys = pool[rng.integers(0, pool.size, 9000)]
+        cached = pool[rng.choice(pool.size, pool.size // 2, replace=False)]
+    cvals = rng.integers(0, 2**64, cached.size, dtype=np.uint64, endpoint=False)
+    say("lookup skewed keys", kind, keys.size)
+    table, ot = g.Cache(1 << 15), oracle.Table()
+    if cached.size:
+        table.insert(keys_to_device(cached), keys_to_device(cvals))
+        ot.insert(cached, cvals)
+    status, ref = table.lookup(keys_to_device(keys))
+    torch.cuda.synchronize()
+    est, eref = oracle.lookup(keys, ot)
+    assert np.array_equal(status.cpu().numpy(), est)
+    assert np.array_equal(u64(ref), eref)
+
+
 @pytest.mark.parametrize("n", [4_095, 4_096, 4_097, 16_384, 16_385])
 def test_lookup_at_single_workgroup_limit(n):
     rng = np.random.default_rng(850 + n)
